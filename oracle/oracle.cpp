@@ -1,0 +1,383 @@
+// Reference oracle for batched prefix matching and queue signals.
+//
+// TEST INFRASTRUCTURE ONLY. Nothing in the product library links, loads or
+// calls this file; only the tests, the smoke check and the benchmark's CPU
+// baseline leg use it. It shares no code, header or table with the HIP path.
+//
+// It is a deliberately plain, slow, pointer-based implementation of what the
+// paper defines, written for a reader to check by eye:
+//
+//  * The engine's prefix cache is a radix tree of cached token sequences with
+//    children keyed by the first token of their edge (Sec. 2, RadixCache;
+//    App. A implementation details: children keyed by first edge token).
+//  * LPM hit length of a waiting request: the longest prefix of its prompt
+//    that is present in the cache, where a partially matched edge still
+//    counts (Alg. 1: h = d + delta, MatchInRadix returns matched edge tokens).
+//    The engine caches whole blocks of B tokens, so h = B * floor(m / B).
+//  * Pending demand of cache node c: the number of waiting requests whose walk
+//    enters c, i.e. whose prompt agrees with the node's path beyond the
+//    parent's depth. This is the per-path pending count the eviction score
+//    reads along a cached block's ancestors (Eq. 2).
+//  * Pending radix tree over the queue with a per-node pending_count; a
+//    request's cluster is the deepest node on its path with count >= 2 and
+//    the cluster size is that count (Sec. 3.1, App. A.3). A cluster counts
+//    only if its depth reaches the threshold T; otherwise the request is a
+//    singleton (id -1, size 1). Cluster id = smallest arrival index among the
+//    requests whose cluster is that same node.
+//
+// Build: g++ -O2 -std=c++17 -shared -fPIC oracle.cpp -o liboracle.so
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <vector>
+
+namespace {
+
+struct Node {
+  std::vector<int32_t> edge;        // tokens on the edge from the parent into this node
+  int64_t depth = 0;                // tokens from the root to the end of this edge
+  Node* parent = nullptr;
+  std::map<int32_t, Node*> kids;    // keyed by the first token of the child's edge
+  int64_t input_index = -1;         // index in a tree description, if built from one
+  int32_t canon = -1;               // canonical preorder id
+};
+
+struct Tree {
+  Node* root = nullptr;
+  std::vector<Node*> nodes;         // every node, owned here
+  std::vector<Node*> by_canon;      // canonical preorder
+};
+
+Node* new_node(Tree* t) {
+  Node* n = new Node();
+  t->nodes.push_back(n);
+  return n;
+}
+
+void free_tree(Tree* t) {
+  for (Node* n : t->nodes) delete n;
+  delete t;
+}
+
+// Canonical ids: depth-first preorder, children visited by ascending first
+// token (signed comparison, which is std::map's order for int32_t keys).
+void number_preorder(Tree* t) {
+  t->by_canon.clear();
+  std::vector<Node*> stack{t->root};
+  while (!stack.empty()) {
+    Node* n = stack.back();
+    stack.pop_back();
+    n->canon = (int32_t)t->by_canon.size();
+    t->by_canon.push_back(n);
+    for (auto it = n->kids.rbegin(); it != n->kids.rend(); ++it) stack.push_back(it->second);
+  }
+}
+
+// Textbook radix-tree insertion: descend along matching edges, split an edge
+// where the sequence diverges from it or ends inside it, and hang the rest of
+// the sequence as a new leaf. Nodes are the root, branch points and
+// sequence ends.
+void insert_sequence(Tree* t, const int32_t* s, int64_t len) {
+  Node* node = t->root;
+  int64_t i = 0;
+  while (i < len) {
+    auto it = node->kids.find(s[i]);
+    if (it == node->kids.end()) {
+      Node* leaf = new_node(t);
+      leaf->edge.assign(s + i, s + len);
+      leaf->parent = node;
+      leaf->depth = node->depth + (len - i);
+      node->kids[s[i]] = leaf;
+      return;
+    }
+    Node* child = it->second;
+    int64_t k = 0;
+    int64_t elen = (int64_t)child->edge.size();
+    while (k < elen && i + k < len && child->edge[k] == s[i + k]) ++k;
+    if (k < elen) {
+      // split child's edge after k tokens
+      Node* mid = new_node(t);
+      mid->edge.assign(child->edge.begin(), child->edge.begin() + k);
+      mid->parent = node;
+      mid->depth = node->depth + k;
+      child->edge.erase(child->edge.begin(), child->edge.begin() + k);
+      child->parent = mid;
+      mid->kids[child->edge[0]] = child;
+      node->kids[s[i]] = mid;
+      if (i + k < len) {
+        Node* leaf = new_node(t);
+        leaf->edge.assign(s + i + k, s + len);
+        leaf->parent = mid;
+        leaf->depth = mid->depth + (len - i - k);
+        mid->kids[s[i + k]] = leaf;
+      }
+      return;
+    }
+    i += k;
+    node = child;
+  }
+}
+
+// Per-request walk: from the root, look the next prompt token up among the
+// current node's children, enter that child, compare its edge token by
+// token, and stop at the first mismatch, at the end of the prompt, or when
+// no child starts with the next token.
+struct WalkResult {
+  int64_t matched;
+  Node* last;
+};
+
+WalkResult walk(const Tree* t, const int32_t* p, int64_t len) {
+  Node* c = t->root;
+  int64_t d = 0;
+  while (d < len) {
+    auto it = c->kids.find(p[d]);
+    if (it == c->kids.end()) break;
+    c = it->second;
+    int64_t e = (int64_t)c->edge.size();
+    int64_t k = 0;
+    while (k < e && d + k < len && c->edge[k] == p[d + k]) ++k;
+    d += k;
+    if (k < e) break;
+  }
+  return {d, c};
+}
+
+// Pending radix tree over the queue. Edges are views into the caller's
+// prompt buffer, which outlives the tree.
+struct PNode {
+  const int32_t* edge = nullptr;
+  int64_t elen = 0;
+  int64_t depth = 0;
+  int64_t pending_count = 0;
+  std::map<int32_t, PNode*> kids;
+};
+
+struct PendingTree {
+  PNode* root = nullptr;
+  std::vector<PNode*> nodes;
+  ~PendingTree() {
+    for (PNode* n : nodes) delete n;
+  }
+  PNode* make() {
+    PNode* n = new PNode();
+    nodes.push_back(n);
+    return n;
+  }
+};
+
+// Insert a prompt, splitting at divergence and at the prompt's end, and add
+// one to pending_count on every node of its path (root included).
+// Returns the node where the prompt terminates.
+PNode* pending_insert(PendingTree* T, const int32_t* s, int64_t len) {
+  std::vector<PNode*> path{T->root};
+  PNode* node = T->root;
+  int64_t i = 0;
+  PNode* end = nullptr;
+  while (end == nullptr) {
+    if (i == len) {
+      end = node;
+      break;
+    }
+    auto it = node->kids.find(s[i]);
+    if (it == node->kids.end()) {
+      PNode* leaf = T->make();
+      leaf->edge = s + i;
+      leaf->elen = len - i;
+      leaf->depth = node->depth + leaf->elen;
+      node->kids[s[i]] = leaf;
+      path.push_back(leaf);
+      end = leaf;
+      break;
+    }
+    PNode* child = it->second;
+    int64_t k = 0;
+    while (k < child->elen && i + k < len && child->edge[k] == s[i + k]) ++k;
+    if (k < child->elen) {
+      PNode* mid = T->make();
+      mid->edge = child->edge;
+      mid->elen = k;
+      mid->depth = node->depth + k;
+      mid->pending_count = child->pending_count;
+      child->edge += k;
+      child->elen -= k;
+      mid->kids[child->edge[0]] = child;
+      node->kids[s[i]] = mid;
+      node = mid;
+      i += k;
+      path.push_back(mid);
+      continue;
+    }
+    i += k;
+    node = child;
+    path.push_back(node);
+  }
+  for (PNode* n : path) n->pending_count += 1;
+  return end;
+}
+
+}  // namespace
+
+extern "C" {
+
+typedef struct Tree oracle_tree;
+
+// Tree from a description: node i has parent[i] (-1 for the single root) and
+// edge edge_tokens[edge_offsets[i] : edge_offsets[i+1]]. Returns NULL if the
+// description is not a valid radix tree: not exactly one root, root edge not
+// empty, an empty non-root edge, a parent index out of range, two siblings
+// with the same first token, or a node not reachable from the root (cycle).
+oracle_tree* oracle_tree_from_description(int64_t num_nodes, const int32_t* parent,
+                                          const int64_t* edge_offsets, const int32_t* edge_tokens) {
+  if (num_nodes < 1) return nullptr;
+  Tree* t = new Tree();
+  std::vector<Node*> by_input(num_nodes);
+  for (int64_t i = 0; i < num_nodes; ++i) {
+    Node* n = new_node(t);
+    n->input_index = i;
+    if (edge_offsets[i + 1] < edge_offsets[i]) { free_tree(t); return nullptr; }
+    n->edge.assign(edge_tokens + edge_offsets[i], edge_tokens + edge_offsets[i + 1]);
+    by_input[i] = n;
+  }
+  int64_t roots = 0;
+  for (int64_t i = 0; i < num_nodes; ++i) {
+    Node* n = by_input[i];
+    if (parent[i] == -1) {
+      ++roots;
+      t->root = n;
+      if (!n->edge.empty()) { free_tree(t); return nullptr; }
+      continue;
+    }
+    if (parent[i] < 0 || parent[i] >= num_nodes || parent[i] == i || n->edge.empty()) {
+      free_tree(t);
+      return nullptr;
+    }
+    Node* p = by_input[parent[i]];
+    if (p->kids.count(n->edge[0])) { free_tree(t); return nullptr; }
+    p->kids[n->edge[0]] = n;
+    n->parent = p;
+  }
+  if (roots != 1) { free_tree(t); return nullptr; }
+  // depths and reachability from the root
+  int64_t seen = 0;
+  std::vector<Node*> stack{t->root};
+  while (!stack.empty()) {
+    Node* n = stack.back();
+    stack.pop_back();
+    ++seen;
+    n->depth = (n->parent ? n->parent->depth : 0) + (int64_t)n->edge.size();
+    for (auto& kv : n->kids) stack.push_back(kv.second);
+  }
+  if (seen != num_nodes) { free_tree(t); return nullptr; }
+  number_preorder(t);
+  return t;
+}
+
+// Tree from raw cached sequences (packed tokens + offsets[num_seqs+1]).
+oracle_tree* oracle_tree_from_sequences(const int32_t* tokens, const int64_t* offsets, int64_t num_seqs) {
+  Tree* t = new Tree();
+  t->root = new_node(t);
+  for (int64_t s = 0; s < num_seqs; ++s)
+    insert_sequence(t, tokens + offsets[s], offsets[s + 1] - offsets[s]);
+  number_preorder(t);
+  return t;
+}
+
+void oracle_tree_free(oracle_tree* t) {
+  if (t) free_tree(t);
+}
+
+int64_t oracle_tree_num_nodes(const oracle_tree* t) { return (int64_t)t->by_canon.size(); }
+
+int64_t oracle_tree_num_edge_tokens(const oracle_tree* t) {
+  int64_t s = 0;
+  for (Node* n : t->by_canon) s += (int64_t)n->edge.size();
+  return s;
+}
+
+// Canonical description: node ids are preorder ids; parent_out[num_nodes],
+// depth_out[num_nodes], edge_offsets_out[num_nodes+1], edge_tokens_out[total].
+// Any output may be NULL.
+void oracle_tree_export(const oracle_tree* t, int32_t* parent_out, int64_t* depth_out,
+                        int64_t* edge_offsets_out, int32_t* edge_tokens_out) {
+  int64_t pos = 0;
+  for (size_t i = 0; i < t->by_canon.size(); ++i) {
+    const Node* n = t->by_canon[i];
+    if (parent_out) parent_out[i] = n->parent ? n->parent->canon : -1;
+    if (depth_out) depth_out[i] = n->depth;
+    if (edge_offsets_out) edge_offsets_out[i] = pos;
+    if (edge_tokens_out && !n->edge.empty())
+      std::memcpy(edge_tokens_out + pos, n->edge.data(), n->edge.size() * sizeof(int32_t));
+    pos += (int64_t)n->edge.size();
+  }
+  if (edge_offsets_out) edge_offsets_out[t->by_canon.size()] = pos;
+}
+
+// For trees built from a description: canon_out[input index] = canonical id.
+void oracle_tree_canonical_ids(const oracle_tree* t, int32_t* canon_out) {
+  for (const Node* n : t->by_canon)
+    if (n->input_index >= 0) canon_out[n->input_index] = n->canon;
+}
+
+// LPM for every request: m_out = matched prompt tokens, h_out = block-floored
+// hit, last_out = canonical id of the last node the walk entered (root = 0).
+void oracle_lpm(const oracle_tree* t, int64_t n, const int32_t* tokens, const int64_t* offsets,
+                int32_t block_size, int64_t* m_out, int64_t* h_out, int32_t* last_out) {
+  for (int64_t r = 0; r < n; ++r) {
+    WalkResult w = walk(t, tokens + offsets[r], offsets[r + 1] - offsets[r]);
+    if (m_out) m_out[r] = w.matched;
+    if (h_out) h_out[r] = block_size * (w.matched / block_size);
+    if (last_out) last_out[r] = w.last->canon;
+  }
+}
+
+// Demand per canonical node: for each request, climb from its last node to
+// the root adding one at every node on the way.
+void oracle_demand(const oracle_tree* t, int64_t n, const int32_t* last_node, int64_t* demand_out) {
+  size_t nn = t->by_canon.size();
+  for (size_t i = 0; i < nn; ++i) demand_out[i] = 0;
+  for (int64_t r = 0; r < n; ++r)
+    for (const Node* c = t->by_canon[last_node[r]]; c != nullptr; c = c->parent) demand_out[c->canon] += 1;
+}
+
+// Queue signals from the pending radix tree: share_out[r] = depth of the
+// deepest node on r's path with pending_count >= 2 (0 when there is none),
+// and cluster id / size per the threshold rule.
+void oracle_clusters(int64_t n, const int32_t* tokens, const int64_t* offsets, int64_t threshold,
+                     int64_t* share_out, int64_t* cluster_id_out, int64_t* cluster_size_out) {
+  PendingTree T;
+  T.root = T.make();
+  for (int64_t r = 0; r < n; ++r) pending_insert(&T, tokens + offsets[r], offsets[r + 1] - offsets[r]);
+  std::vector<PNode*> cluster(n, nullptr);
+  for (int64_t r = 0; r < n; ++r) {
+    const int32_t* p = tokens + offsets[r];
+    int64_t len = offsets[r + 1] - offsets[r];
+    // walk r's own path through the pending tree; every edge matches fully
+    PNode* node = T.root;
+    PNode* deepest = (node->pending_count >= 2) ? node : nullptr;
+    int64_t d = 0;
+    while (d < len) {
+      PNode* child = node->kids.at(p[d]);
+      d += child->elen;
+      node = child;
+      if (node->pending_count >= 2) deepest = node;
+    }
+    int64_t share = deepest ? deepest->depth : 0;
+    share_out[r] = share;
+    cluster[r] = (deepest && share >= threshold) ? deepest : nullptr;
+  }
+  std::map<PNode*, int64_t> smallest_member;
+  for (int64_t r = 0; r < n; ++r)
+    if (cluster[r] && !smallest_member.count(cluster[r])) smallest_member[cluster[r]] = r;
+  for (int64_t r = 0; r < n; ++r) {
+    if (cluster[r]) {
+      cluster_id_out[r] = smallest_member[cluster[r]];
+      cluster_size_out[r] = cluster[r]->pending_count;
+    } else {
+      cluster_id_out[r] = -1;
+      cluster_size_out[r] = 1;
+    }
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+"""Literal evaluation of the definitions, for tiny inputs only.
+
+Pure-Python loops over every cached node path and every pair of prompts,
+with no tree walk at all. These pin the oracle: they share nothing with it
+but the definitions.
+
+Definitions (p_r = prompt r, P(c) = token string from the root to the end
+of cache node c, LCP = longest common prefix length):
+  m_r          = max_c LCP(p_r, P(c))                          (Alg. 1: d + delta)
+  h_r          = B * floor(m_r / B)                            (whole cached blocks)
+  last_node_r  = deepest c with LCP(p_r, P(c)) > |P(parent c)|  (root: parent depth -1)
+  demand[c]    = #{r : LCP(p_r, P(c)) > |P(parent c)|}           (Eq. 2 pending count)
+  share_r      = max_{r' != r} LCP(p_r, p_r')                  (Sec. 3.1 deepest node with count >= 2)
+  share_r >= T: size = #{r' : LCP(p_r, p_r') >= share_r},
+                id   = min{r' : share_r' = share_r and LCP(p_r, p_r') >= share_r}
+  otherwise:    id = -1, size = 1
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def lcp(a, b) -> int:
+    k = 0
+    n = min(len(a), len(b))
+    while k < n and a[k] == b[k]:
+        k += 1
+    return k
+
+
+def seqs_of(tokens, offsets):
+    return [tuple(int(x) for x in tokens[offsets[i]:offsets[i + 1]]) for i in range(len(offsets) - 1)]
+
+
+def nodes_from_sequences(seqs):
+    """Node strings of the compressed trie of `seqs`: the empty string, every
+    sequence, and every prefix followed by two or more distinct tokens."""
+    follow = {}
+    for s in seqs:
+        for k in range(len(s)):
+            follow.setdefault(s[:k], set()).add(s[k])
+    nodes = {()}
+    nodes.update(seqs)
+    nodes.update(x for x, nxt in follow.items() if len(nxt) >= 2)
+    return sorted(nodes)       # lexicographic order == canonical preorder
+
+
+def nodes_from_description(parent, edge_offsets, edge_tokens):
+    """Node strings of a described tree, plus input index -> canonical id."""
+    n = len(parent)
+    memo = {}
+
+    def path(i):
+        if i in memo:
+            return memo[i]
+        e = tuple(int(x) for x in edge_tokens[edge_offsets[i]:edge_offsets[i + 1]])
+        s = e if parent[i] < 0 else path(int(parent[i])) + e
+        memo[i] = s
+        return s
+
+    strings = [path(i) for i in range(n)]
+    order = sorted(strings)
+    rank = {s: i for i, s in enumerate(order)}
+    return order, np.array([rank[s] for s in strings], dtype=np.int32)
+
+
+def parent_depth(nodes):
+    """|P(parent c)| for every node string; -1 for the root."""
+    nodeset = set(nodes)
+    out = []
+    for s in nodes:
+        if len(s) == 0:
+            out.append(-1)
+            continue
+        k = len(s) - 1
+        while s[:k] not in nodeset:
+            k -= 1
+        out.append(k)
+    return out
+
+
+def lpm_and_demand(nodes, prompts, block):
+    pd = parent_depth(nodes)
+    m, h, last = [], [], []
+    demand = [0] * len(nodes)
+    for p in prompts:
+        ls = [lcp(p, s) for s in nodes]
+        entered = [c for c in range(len(nodes)) if ls[c] > pd[c]]     # the root always qualifies
+        for c in entered:
+            demand[c] += 1
+        best = max(ls)
+        m.append(best)
+        h.append(block * (best // block))
+        last.append(max(entered, key=lambda c: len(nodes[c])))
+    return np.array(m), np.array(h), np.array(last), np.array(demand)
+
+
+def clusters(prompts, threshold):
+    n = len(prompts)
+    L = [[lcp(prompts[a], prompts[b]) for b in range(n)] for a in range(n)]
+    share = [max([L[r][q] for q in range(n) if q != r], default=0) for r in range(n)]
+    cid, size = [], []
+    for r in range(n):
+        s = share[r]
+        if s >= threshold:
+            size.append(sum(1 for q in range(n) if L[r][q] >= s))
+            cid.append(min(q for q in range(n) if share[q] == s and L[r][q] >= s))
+        else:
+            size.append(1)
+            cid.append(-1)
+    return np.array(share), np.array(cid), np.array(size)

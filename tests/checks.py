@@ -1,0 +1,71 @@
+"""Invariants that hold for any correct output, at any size.
+
+Used on the oracle's outputs (to pin it) and on the GPU's outputs (beside
+element-wise parity). Node ids are canonical preorder ids.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def subtree_end(parent: np.ndarray) -> np.ndarray:
+    """Preorder ids: subtree(c) = [c, end[c])."""
+    n = len(parent)
+    size = np.ones(n, dtype=np.int64)
+    for c in range(n - 1, 0, -1):
+        size[parent[c]] += size[c]
+    return np.arange(n, dtype=np.int64) + size
+
+
+def check_lpm(w, parent, depth, m, h, last):
+    lens = w.lengths
+    B = w.block_size
+    m = np.asarray(m, dtype=np.int64)
+    h = np.asarray(h, dtype=np.int64)
+    last = np.asarray(last, dtype=np.int64)
+    assert np.all(h >= 0) and np.all(h <= m) and np.all(m <= lens)
+    assert np.all(h % B == 0) and np.array_equal(h, B * (m // B))
+    at_root = last == 0
+    assert np.all(m[at_root] == 0)
+    nr = ~at_root
+    pdep = depth[parent[last[nr]]]
+    assert np.all(pdep < m[nr]) and np.all(m[nr] <= depth[last[nr]])
+
+
+def check_demand(n, parent, last, demand):
+    demand = np.asarray(demand, dtype=np.int64)
+    nn = len(parent)
+    assert demand[0] == n
+    assert np.all(demand[1:] <= demand[parent[1:]])
+    child_sum = np.zeros(nn, dtype=np.int64)
+    np.add.at(child_sum, parent[1:], demand[1:])
+    assert np.all(child_sum <= demand)
+    # demand[c] = number of requests whose last node lies in subtree(c)
+    end = subtree_end(parent)
+    s = np.sort(np.asarray(last, dtype=np.int64))
+    expect = np.searchsorted(s, end, side="left") - np.searchsorted(s, np.arange(nn), side="left")
+    assert np.array_equal(demand, expect)
+
+
+def check_clusters(w, cid, csz, lcp_fn=None):
+    cid = np.asarray(cid, dtype=np.int64)
+    csz = np.asarray(csz, dtype=np.int64)
+    n = w.n
+    r = np.arange(n)
+    single = cid == -1
+    assert np.all(csz[single] == 1)
+    inc = ~single
+    assert np.all(cid[inc] <= r[inc]) and np.all(cid[inc] >= 0)
+    assert np.all(cid[cid[inc]] == cid[inc])            # the id's owner is its own id
+    assert np.all(csz[inc] >= 2)
+    ids, counts = np.unique(cid[inc], return_counts=True)
+    sizes = csz[ids]
+    assert np.all(sizes >= counts)
+    assert np.array_equal(csz[inc], csz[cid[inc]])       # one size per cluster
+    # members of one id agree with each other beyond the threshold
+    for q in np.nonzero(inc)[0]:
+        a = w.prompt(int(q))
+        b = w.prompt(int(cid[q]))
+        k = min(len(a), len(b), w.threshold)
+        assert len(a) >= w.threshold and len(b) >= w.threshold
+        assert np.array_equal(a[:k], b[:k])

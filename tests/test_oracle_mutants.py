@@ -1,0 +1,49 @@
+"""Plant plausible mistakes in a copy of the oracle and check that the pins
+in test_oracle.py catch every one of them (each mutant must fail a pin)."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.cpp")
+
+MUTANTS = {
+    "walk_continues_after_partial_edge": ("    d += k;\n    if (k < e) break;", "    d += k;"),
+    "walk_counts_whole_edge": ("    d += k;\n    if (k < e) break;", "    d += e;\n    if (k < e) break;"),
+    "hit_rounds_up": ("block_size * (w.matched / block_size)",
+                      "block_size * ((w.matched + block_size - 1) / block_size)"),
+    "demand_skips_root": ("c != nullptr; c = c->parent", "c->parent != nullptr; c = c->parent"),
+    "split_forgets_counts": ("mid->pending_count = child->pending_count;", "mid->pending_count = 0;"),
+    "cluster_accepts_count_one": ("if (node->pending_count >= 2) deepest = node;",
+                                  "if (node->pending_count >= 1) deepest = node;"),
+    "threshold_strict": ("share >= threshold", "share > threshold"),
+    "id_is_largest_member": ("if (cluster[r] && !smallest_member.count(cluster[r])) smallest_member[cluster[r]] = r;",
+                             "if (cluster[r]) smallest_member[cluster[r]] = r;"),
+    "children_in_descending_order": ("for (auto it = n->kids.rbegin(); it != n->kids.rend(); ++it)",
+                                     "for (auto it = n->kids.begin(); it != n->kids.end(); ++it)"),
+    "split_depth_off_by_one": ("      mid->depth = node->depth + k;\n      child->edge.erase",
+                               "      mid->depth = node->depth + k + 1;\n      child->edge.erase"),
+    "reachability_check_dropped": ("if (seen != num_nodes) { free_tree(t); return nullptr; }", ""),
+    "last_node_is_parent_on_partial": ("  return {d, c};", "  return {d, (c->parent && d < c->depth) ? c->parent : c};"),
+}
+
+PINS = "brute_force or worked or unary or invalid or tiny or agentic"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    mutant = tmp_path / "oracle_mutant.cpp"
+    mutant.write_text(src.replace(old, new))
+    lib = O.build(force=True, src=str(mutant), out=str(tmp_path / "liboracle_mutant.so"))
+    env = dict(os.environ, PEEK_ORACLE_LIB=lib)
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle.py"), "-k", PINS],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
