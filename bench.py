@@ -1,0 +1,199 @@
+"""Benchmark of the hot path on one MI355X.
+
+A step is one pass of the whole hot path over a resident batch: batched LPM
+of every waiting request against the flattened cache tree (peek_lpm_batch),
+then per-node demand and prefix-sharing clusters (peek_queue_signals). The
+workload is the scale queue: 65536 prompts (60% RAG-shaped, 30% agentic,
+10% random) against a cache tree of about one million nodes. The cache is
+built once (not timed); prompts and cache are resident in HBM before the
+timed region starts.
+
+Prints one JSON line (rank 0). See --help for flags.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LPM queries/sec + achieved HBM GB/s (% of peak), N=64K queue on 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def walk_algorithmic_bytes(lengths, m, last, demand, exp):
+    """Bytes the LPM walk must move: the prompt up to and including the first
+    mismatch, the distinct cache edge tokens it compares, one 32-byte node
+    record plus child probe per distinct node entered, offsets and outputs."""
+    n = len(lengths)
+    prompt = 4 * int(np.minimum(lengths, m + 1).sum())
+    depth = exp["depth"].astype(np.int64)
+    elen = exp["edge_len"].astype(np.int64)
+    parent = exp["parent"].astype(np.int64)
+    entered = demand > 0
+    entered[0] = False
+    # nodes passed through completely by at least one request
+    last_cnt = np.bincount(last, minlength=len(depth))
+    full = entered & (demand > last_cnt)
+    compared = np.where(full, elen, 0)
+    # nodes where some walk stopped: tokens compared up to the mismatch
+    stop = last > 0
+    lc = last[stop]
+    dp = depth[parent[lc]]
+    part = np.minimum(elen[lc], m[stop] - dp + 1)
+    part_max = np.zeros(len(depth), dtype=np.int64)
+    np.maximum.at(part_max, lc, part)
+    compared = np.maximum(compared, np.where(entered, part_max, 0))
+    edge_bytes = 4 * int(compared.sum())
+    node_bytes = 32 * int(entered.sum())
+    io_bytes = 8 * (n + 1) + 4 * 3 * n
+    return prompt + edge_bytes + node_bytes + io_bytes, {
+        "prompt_bytes": prompt, "edge_bytes": edge_bytes, "node_bytes": node_bytes, "io_bytes": io_bytes}
+
+
+def cpu_baseline(w, budget_s: float):
+    import oracle as O
+    O.build(force=False)
+    t0 = time.perf_counter()
+    tree = O.cache_tree_of(w)
+    ingest = time.perf_counter() - t0
+    reps, total = 0, 0.0
+    while total < budget_s or reps == 0:
+        t = time.perf_counter()
+        l = O.lpm(tree, w.tokens, w.offsets, w.block_size)
+        O.demand(tree, l.last_node)
+        O.clusters(w.tokens, w.offsets, w.threshold)
+        total += time.perf_counter() - t
+        reps += 1
+    return {"value": w.n * reps / total, "unit": "LPM queries/s", "cores": 1, "kind": "oracle",
+            "sample": f"whole scale queue ({w.n} requests): LPM + demand + clusters, single thread, "
+                      f"{reps} passes in {total:.1f} s; cache-tree ingest {ingest:.1f} s not counted",
+            "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="scale")
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this hot path is built and measured on a single MI355X "
+              "(multi-GPU sharding is described in the design notes, not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import peek_workloads as W
+    from paper_2607_02525_amd import peek_cache_export
+    from paper_2607_02525_amd.runner import HotPath
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    w = W.make(args.config, args.seed)
+    log(f"workload {w.name} n={w.n} tokens={len(w.tokens)} generated in {time.perf_counter() - t0:.1f}s")
+    t0 = time.perf_counter()
+    if w.cache_tree is not None:
+        hp = HotPath.from_description(*w.cache_tree)
+    else:
+        hp = HotPath.from_sequences(*w.cache_sequences)
+    build_s = time.perf_counter() - t0
+    stats = hp.cache.stats()
+    log(f"cache built in {build_s:.1f}s: {stats}")
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        hp.step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        a, b, c = ev[i]
+        a.record(stream)
+        hp.lpm()
+        b.record(stream)
+        hp.signals()
+        c.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    lpm_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    sig_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (lpm {lpm_ms.mean():.3f} ms, signals {sig_ms.mean():.3f} ms)")
+
+    res = hp.results()
+    exp = peek_cache_export(hp.cache)
+    b_alg, parts = walk_algorithmic_bytes(w.lengths.astype(np.int64), res["match_len"].astype(np.int64),
+                                          res["last_node"].astype(np.int64), res["demand"].astype(np.int64), exp)
+    lpm_avg_s = float(lpm_ms.mean()) / 1e3
+    achieved = b_alg / lpm_avg_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_lpm_walk", "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
+                "avg_launch_ms": round(float(lpm_ms.mean()), 4), "min_launch_ms": round(float(lpm_ms.min()), 4)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the oracle on the host for cpu_baseline")
+        cpu = cpu_baseline(w, args.cpu_budget)
+
+    out = {
+        "metric": METRIC,
+        "value": round(w.n / (ms_per_step / 1e3), 1),
+        "unit": "LPM queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.n} prompts ({len(w.tokens)} tokens), cache tree "
+                               f"{stats['num_nodes']} nodes / {stats['num_edge_tokens']} edge tokens, "
+                               f"block {w.block_size}, cluster threshold {w.threshold}, seed {w.seed}",
+                   "queue": w.n, "parallelism": "single GPU"},
+        "lpm_queries_per_s": round(w.n / lpm_avg_s, 1),
+        "lpm_ms": round(float(lpm_ms.mean()), 4),
+        "signals_ms": round(float(sig_ms.mean()), 4),
+        "cache_build_s": round(build_s, 2),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,180 @@
+/*
+ * peek.h - batched longest-prefix match of a waiting queue against a KV
+ * prefix-cache radix tree, plus the queue-side signals derived from it,
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * The problem (PEEK, Sec. 3.1 and Alg. 1): for every waiting request r,
+ * find the LPM hit length H[r] of its prompt against the engine's radix
+ * cache, where a partially matched edge still counts (Alg. 1: h = d + delta
+ * with delta the matched tokens of an edge). Engines cache whole blocks of B
+ * tokens, so the reported hit is h = B * floor(m / B) with m the raw match.
+ * The same queue yields its prefix-sharing clusters (Sec. 3.1: the deepest
+ * pending-tree node with pending_count >= 2 on a request's path, its count
+ * being the cluster size) and the per-cache-node pending demand read by the
+ * eviction score (Eq. 2).
+ *
+ * Conventions for every call:
+ *  - Plain C ABI; no exceptions cross it; nothing aborts the process.
+ *  - Errors return a negative peek_status; peek_last_error() then describes
+ *    the failure for the calling thread. Outputs are not written on error.
+ *  - "d_" pointers are device memory on the current HIP device, owned by the
+ *    caller, and must stay valid until `stream` has executed the call. Host
+ *    pointers are read before the call returns and may be freed afterwards.
+ *  - `stream` is a hipStream_t (NULL = the default stream). GPU work is
+ *    enqueued on it; calls do not synchronize it unless stated.
+ *  - Token ids are opaque int32 values compared for equality; child order
+ *    uses signed comparison.
+ *  - A prompt set is packed: request r's prompt is
+ *    d_tokens[d_offsets[r] : d_offsets[r+1]], offsets int64, non-decreasing.
+ *    Offsets and tokens live on the device, so they are preconditions the
+ *    library does not re-check. Each prompt must be shorter than 2^29 tokens.
+ */
+#ifndef PEEK_H
+#define PEEK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PEEK_ABI_VERSION 1
+
+typedef enum peek_status {
+  PEEK_OK = 0,
+  PEEK_ERR_INVALID_ARGUMENT = -1,    /* null pointer, negative size, bad parameter */
+  PEEK_ERR_INVALID_TREE = -2,        /* tree description is not a radix tree */
+  PEEK_ERR_OUT_OF_MEMORY = -3,       /* host or device allocation failed */
+  PEEK_ERR_DEVICE = -4,              /* a HIP call failed; message names it */
+  PEEK_ERR_WORKSPACE_TOO_SMALL = -5, /* see peek_queue_signals_workspace */
+  PEEK_ERR_UNSUPPORTED_DEVICE = -6   /* current device is not gfx950 */
+} peek_status;
+
+/* Opaque handle: a cache tree flattened into device memory. Immutable after
+ * build, so concurrent calls on different streams may share it. */
+typedef struct peek_cache peek_cache;
+
+int32_t peek_abi_version(void);
+
+/* Description of the most recent failure on the calling thread (never NULL;
+ * empty after success). Valid until the thread's next peek_ call. */
+const char* peek_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Cache tree description (host).
+ *
+ * A tree of num_nodes nodes: node i has parent parent[i] (-1 for exactly one
+ * root) and the edge label edge_tokens[edge_offsets[i] : edge_offsets[i+1]].
+ * The root's edge is empty; every other edge is non-empty; siblings have
+ * distinct first tokens (SGLang's RadixCache keys children by the first edge
+ * token, App. A implementation details); every node is reachable from the
+ * root. Unary nodes are allowed and kept.
+ *
+ * Canonical node ids: depth-first preorder from the root (id 0), children
+ * visited by ascending first token. Every device output that names a node
+ * (last_node, demand) uses canonical ids, so results do not depend on how
+ * the caller numbered its nodes.
+ * ---------------------------------------------------------------------- */
+
+/* Validates a description and writes canon_id[i] = canonical id of input
+ * node i (host only; no GPU needed). PEEK_ERR_INVALID_TREE if invalid. */
+peek_status peek_tree_canonical_ids(int32_t num_nodes, const int32_t* parent,
+                                    const int64_t* edge_offsets, const int32_t* edge_tokens,
+                                    int32_t* canon_id);
+
+/* Builds the compressed radix tree of raw cached sequences (host only).
+ * Sequence s is tokens[offsets[s] : offsets[s+1]]. Nodes are the root,
+ * every branch point and every sequence end; the output description is in
+ * canonical order (node i has canonical id i). The three output arrays are
+ * allocated by the library; release each with peek_free_host. */
+peek_status peek_tree_from_sequences(const int32_t* tokens, const int64_t* offsets, int64_t num_seqs,
+                                     int32_t* num_nodes_out, int32_t** parent_out,
+                                     int64_t** edge_offsets_out, int32_t** edge_tokens_out);
+void peek_free_host(void* p);
+
+/* ------------------------------------------------------------------------
+ * peek_cache_build: validate a host description, renumber it canonically,
+ * and upload it as CSR arrays to the current device (the engine's prefix
+ * cache, Sec. 2, flattened for the device). Host arrays are copied; the call
+ * waits for the upload to finish before returning. On success *out owns all
+ * device memory of the cache. canon_id (host, nullable) receives
+ * canon_id[i] = canonical id of input node i, so demand[] can be mapped back
+ * to the caller's nodes. Errors: INVALID_ARGUMENT, INVALID_TREE,
+ * OUT_OF_MEMORY, DEVICE, UNSUPPORTED_DEVICE; *out is left untouched.
+ * ---------------------------------------------------------------------- */
+peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
+                             const int32_t* edge_tokens, void* stream, peek_cache** out,
+                             int32_t* canon_id);
+
+/* Any output pointer may be NULL. max_depth is the longest root-to-node
+ * path in tokens; device_bytes the device memory the handle owns. */
+peek_status peek_cache_stats(const peek_cache* cache, int64_t* num_nodes, int64_t* num_edge_tokens,
+                             int32_t* max_fanout, int64_t* max_depth, int64_t* device_bytes);
+
+/* Host copies of the canonical node table (each output nullable, length
+ * num_nodes): parent id, depth at the end of the edge, edge length,
+ * preorder end of the subtree (subtree(c) = [c, subtree_end[c])). */
+peek_status peek_cache_export(const peek_cache* cache, int32_t* parent, int32_t* depth,
+                              int32_t* edge_len, int32_t* subtree_end);
+
+/* Frees the handle and its device memory (NULL is a no-op). The caller must
+ * ensure no enqueued work still uses it. */
+peek_status peek_cache_free(peek_cache* cache);
+
+/* ------------------------------------------------------------------------
+ * peek_lpm_batch: LPM hit of every waiting request (Alg. 1 ENSURE clause:
+ * H[r] for every waiting request r; MatchInRadix counts partial edges).
+ *
+ * For request r with prompt p:
+ *   match_len[r] = m = max over cached paths P(c) of LCP(p, P(c))
+ *   h[r]         = block_size * floor(m / block_size)
+ *   last_node[r] = canonical id of the deepest node c the walk enters, i.e.
+ *                  with LCP(p, P(c)) > depth(parent(c)); 0 if none.
+ * d_h is required; d_last_node and d_match_len may be NULL. All outputs are
+ * int32[n]. n = 0 is a no-op. Asynchronous on `stream`; no workspace.
+ * Errors: INVALID_ARGUMENT (n < 0, block_size < 1, null cache/pointers,
+ * cache built on another device), DEVICE.
+ * ---------------------------------------------------------------------- */
+peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
+                           const int64_t* d_offsets, int32_t block_size, int32_t* d_h,
+                           int32_t* d_last_node, int32_t* d_match_len, void* stream);
+
+/* ------------------------------------------------------------------------
+ * peek_queue_signals: prefix-sharing clusters of the waiting queue and the
+ * pending demand of every cache node (Sec. 3.1, App. A.3, Eq. 2).
+ *
+ * Demand (when d_demand != NULL; needs cache and d_last_node from
+ * peek_lpm_batch on the same prompts):
+ *   d_demand[c] = number of requests whose walk enters cache node c
+ *               = #{r : last_node[r] in subtree(c)}; int32[num_nodes],
+ *                 canonical ids; d_demand[0] = n.
+ * Clusters (when d_cluster_id or d_cluster_size != NULL; need d_tokens,
+ * d_offsets; the cache is not used):
+ *   share_r = max over r' != r of LCP(p_r, p_r')   (0 when n = 1)
+ *   if share_r >= threshold:
+ *     cluster_size[r] = #{r' : LCP(p_r, p_r') >= share_r}   (pending_count)
+ *     cluster_id[r]   = min{r' : share_r' = share_r and LCP(p_r, p_r') >= share_r}
+ *   else cluster_id[r] = -1, cluster_size[r] = 1 (in no cluster).
+ * Request indices are positions in the submitted batch (arrival order).
+ *
+ * Scratch comes only from d_workspace (device, 256-byte aligned, at least
+ * peek_queue_signals_workspace(n, num_nodes) bytes); the library allocates
+ * nothing here. The cluster pass refines a sort in rounds and synchronizes
+ * `stream` once per round to read a device flag, so this call returns after
+ * the stream has finished its work. threshold >= 1.
+ * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
+ * ---------------------------------------------------------------------- */
+size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes);
+
+peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
+                               const int64_t* d_offsets, const int32_t* d_last_node,
+                               int32_t threshold, int32_t* d_cluster_id, int32_t* d_cluster_size,
+                               int32_t* d_demand, void* d_workspace, size_t workspace_bytes,
+                               void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PEEK_H */

@@ -1,0 +1,214 @@
+"""Python binding of libpeek (include/peek.h): batched longest-prefix match of
+a waiting queue against a KV prefix-cache radix tree, plus the queue signals
+(prefix-sharing clusters and per-cache-node pending demand), on MI355X.
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+Device arrays are torch tensors on the current HIP device (torch is used for
+device memory and streams); host arrays are numpy. Each function has the
+name of the C entry point it calls and raises PeekError on failure. There is
+no CPU fallback: importing this module fails if libpeek.so is not built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpeek.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_02525_amd.build` "
+                      "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+PEEK_OK = 0
+PEEK_ERR_INVALID_ARGUMENT = -1
+PEEK_ERR_INVALID_TREE = -2
+PEEK_ERR_OUT_OF_MEMORY = -3
+PEEK_ERR_DEVICE = -4
+PEEK_ERR_WORKSPACE_TOO_SMALL = -5
+PEEK_ERR_UNSUPPORTED_DEVICE = -6
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_vp = ctypes.c_void_p
+
+# (name, restype, argtypes) of every exported symbol in include/peek.h
+EXPORTS = [
+    ("peek_abi_version", ctypes.c_int32, []),
+    ("peek_last_error", ctypes.c_char_p, []),
+    ("peek_tree_canonical_ids", ctypes.c_int, [ctypes.c_int32, _i32p, _i64p, _i32p, _i32p]),
+    ("peek_tree_from_sequences", ctypes.c_int,
+     [_i32p, _i64p, ctypes.c_int64, _i32p, ctypes.POINTER(_i32p), ctypes.POINTER(_i64p), ctypes.POINTER(_i32p)]),
+    ("peek_free_host", None, [_vp]),
+    ("peek_cache_build", ctypes.c_int, [ctypes.c_int32, _i32p, _i64p, _i32p, _vp, ctypes.POINTER(_vp), _i32p]),
+    ("peek_cache_stats", ctypes.c_int, [_vp, _i64p, _i64p, _i32p, _i64p, _i64p]),
+    ("peek_cache_export", ctypes.c_int, [_vp, _i32p, _i32p, _i32p, _i32p]),
+    ("peek_cache_free", ctypes.c_int, [_vp]),
+    ("peek_lpm_batch", ctypes.c_int, [_vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp]),
+    ("peek_queue_signals_workspace", ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
+    ("peek_queue_signals", ctypes.c_int,
+     [_vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+]
+
+for _name, _res, _args in EXPORTS:
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+class PeekError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"peek status {status}: {message}")
+        self.status = status
+
+
+def peek_last_error() -> str:
+    return (_lib.peek_last_error() or b"").decode()
+
+
+def peek_abi_version() -> int:
+    return int(_lib.peek_abi_version())
+
+
+def _check(status: int):
+    if status != PEEK_OK:
+        raise PeekError(status, peek_last_error())
+
+
+def _np32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _np64(a):
+    return np.ascontiguousarray(a, dtype=np.int64)
+
+
+def _p32(a):
+    return a.ctypes.data_as(_i32p) if a is not None and a.size else (None if a is None else
+                                                                      np.zeros(1, np.int32).ctypes.data_as(_i32p))
+
+
+def _dptr(t):
+    """Device pointer of a torch tensor (or None)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def peek_tree_canonical_ids(parent, edge_offsets, edge_tokens) -> np.ndarray:
+    parent, edge_offsets, edge_tokens = _np32(parent), _np64(edge_offsets), _np32(edge_tokens)
+    out = np.empty(len(parent), dtype=np.int32)
+    keep = edge_tokens if edge_tokens.size else np.zeros(1, np.int32)
+    _check(_lib.peek_tree_canonical_ids(len(parent), parent.ctypes.data_as(_i32p), edge_offsets.ctypes.data_as(_i64p),
+                                        keep.ctypes.data_as(_i32p), out.ctypes.data_as(_i32p)))
+    return out
+
+
+def peek_tree_from_sequences(tokens, offsets):
+    """Raw cached sequences -> canonical tree description (parent, edge_offsets, edge_tokens)."""
+    tokens, offsets = _np32(tokens), _np64(offsets)
+    keep = tokens if tokens.size else np.zeros(1, np.int32)
+    nn = ctypes.c_int32()
+    P, O, T = _i32p(), _i64p(), _i32p()
+    _check(_lib.peek_tree_from_sequences(keep.ctypes.data_as(_i32p), offsets.ctypes.data_as(_i64p),
+                                         len(offsets) - 1, ctypes.byref(nn), ctypes.byref(P), ctypes.byref(O),
+                                         ctypes.byref(T)))
+    try:
+        n = nn.value
+        parent = np.ctypeslib.as_array(P, shape=(n,)).copy()
+        eoff = np.ctypeslib.as_array(O, shape=(n + 1,)).copy()
+        etok = np.ctypeslib.as_array(T, shape=(max(1, int(eoff[-1])),)).copy()[:int(eoff[-1])]
+    finally:
+        for p in (P, O, T):
+            _lib.peek_free_host(ctypes.cast(p, _vp))
+    return parent, eoff, etok
+
+
+class Cache:
+    """Owns a peek_cache handle (device CSR of a cache tree)."""
+
+    def __init__(self, handle: int):
+        self.handle = ctypes.c_void_p(handle)
+
+    def free(self):
+        if self.handle:
+            _check(_lib.peek_cache_free(self.handle))
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            if self.handle:
+                _lib.peek_cache_free(self.handle)
+        except Exception:
+            pass
+
+    def stats(self) -> dict:
+        return peek_cache_stats(self)
+
+
+def peek_cache_build(parent, edge_offsets, edge_tokens, stream=None):
+    """Host tree description -> (Cache, canon_id[int32, num_nodes])."""
+    parent, edge_offsets, edge_tokens = _np32(parent), _np64(edge_offsets), _np32(edge_tokens)
+    keep = edge_tokens if edge_tokens.size else np.zeros(1, np.int32)
+    canon = np.empty(len(parent), dtype=np.int32)
+    out = ctypes.c_void_p()
+    _check(_lib.peek_cache_build(len(parent), parent.ctypes.data_as(_i32p), edge_offsets.ctypes.data_as(_i64p),
+                                 keep.ctypes.data_as(_i32p), _stream(stream), ctypes.byref(out),
+                                 canon.ctypes.data_as(_i32p)))
+    return Cache(out.value), canon
+
+
+def peek_cache_stats(cache: Cache) -> dict:
+    nn, et, md, db = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    mf = ctypes.c_int32()
+    _check(_lib.peek_cache_stats(cache.handle, ctypes.byref(nn), ctypes.byref(et), ctypes.byref(mf),
+                                 ctypes.byref(md), ctypes.byref(db)))
+    return {"num_nodes": nn.value, "num_edge_tokens": et.value, "max_fanout": mf.value,
+            "max_depth": md.value, "device_bytes": db.value}
+
+
+def peek_cache_export(cache: Cache) -> dict:
+    n = peek_cache_stats(cache)["num_nodes"]
+    out = {k: np.empty(n, dtype=np.int32) for k in ("parent", "depth", "edge_len", "subtree_end")}
+    _check(_lib.peek_cache_export(cache.handle, *(out[k].ctypes.data_as(_i32p)
+                                                  for k in ("parent", "depth", "edge_len", "subtree_end"))))
+    return out
+
+
+def peek_cache_free(cache: Cache):
+    cache.free()
+
+
+def peek_lpm_batch(cache: Cache, tokens, offsets, block_size: int, h, last_node=None, match_len=None,
+                   stream=None):
+    """tokens int32[*], offsets int64[n+1], outputs int32[n]: all torch tensors on the device."""
+    n = int(offsets.shape[0]) - 1
+    _check(_lib.peek_lpm_batch(cache.handle, n, _dptr(tokens), _dptr(offsets), int(block_size), _dptr(h),
+                               _dptr(last_node), _dptr(match_len), _stream(stream)))
+
+
+def peek_queue_signals_workspace(n: int, num_nodes: int) -> int:
+    return int(_lib.peek_queue_signals_workspace(int(n), int(num_nodes)))
+
+
+def peek_queue_signals(cache, tokens, offsets, last_node, threshold: int, cluster_id, cluster_size, demand,
+                       workspace, stream=None):
+    """cluster_id/cluster_size int32[n], demand int32[num_nodes], workspace uint8 tensor; torch tensors."""
+    n = int(offsets.shape[0]) - 1
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(_lib.peek_queue_signals(None if cache is None else cache.handle, n, _dptr(tokens), _dptr(offsets),
+                                   _dptr(last_node), int(threshold), _dptr(cluster_id), _dptr(cluster_size),
+                                   _dptr(demand), _dptr(workspace), ws_bytes, _stream(stream)))

@@ -1,0 +1,508 @@
+// Host side of libpeek: error reporting, tree validation and canonical
+// flattening, the sequences-to-tree helper, and the C ABI entry points.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "peek_internal.h"
+
+namespace peek {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+peek_status fail(peek_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+namespace {
+
+// Validated, canonically renumbered tree ready for upload.
+struct Flat {
+  std::vector<int32_t> canon;      // input index -> canonical id
+  std::vector<NodeRec> recs;       // canonical order
+  std::vector<int32_t> child_tok;  // per-parent child tables, parents in canonical order
+  std::vector<int32_t> child_id;
+  std::vector<int32_t> pool;       // edge labels, each edge padded to a multiple of 4 tokens
+  int64_t edge_tokens = 0;
+  int32_t max_fanout = 0;
+  int64_t max_depth = 0;
+};
+
+constexpr int64_t kPoolTailPad = 64;   // tokens of zero padding after the last edge
+
+// Validates the description and computes canonical ids. When `out_full`
+// is set it also builds the node records, child tables and edge pool.
+peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eoff,
+                    const int32_t* etok, Flat* f, bool out_full) {
+  if (num_nodes < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "num_nodes must be >= 1 (got %d)", num_nodes);
+  if (!parent || !eoff) return fail(PEEK_ERR_INVALID_ARGUMENT, "parent and edge_offsets must not be NULL");
+  if (eoff[0] < 0) return fail(PEEK_ERR_INVALID_TREE, "edge_offsets[0] is negative");
+  for (int32_t i = 0; i < num_nodes; ++i)
+    if (eoff[i + 1] < eoff[i]) return fail(PEEK_ERR_INVALID_TREE, "edge_offsets decrease at node %d", i);
+  if (eoff[num_nodes] > eoff[0] && !etok)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "edge_tokens is NULL but edges are not empty");
+
+  int32_t root = -1;
+  std::vector<int32_t> nkids(num_nodes + 1, 0);
+  for (int32_t i = 0; i < num_nodes; ++i) {
+    const int32_t p = parent[i];
+    const int64_t len = eoff[i + 1] - eoff[i];
+    if (p == -1) {
+      if (root != -1) return fail(PEEK_ERR_INVALID_TREE, "more than one root (nodes %d and %d)", root, i);
+      if (len != 0) return fail(PEEK_ERR_INVALID_TREE, "root edge must be empty (node %d has %lld tokens)", i, (long long)len);
+      root = i;
+      continue;
+    }
+    if (p < 0 || p >= num_nodes || p == i)
+      return fail(PEEK_ERR_INVALID_TREE, "node %d has invalid parent %d", i, p);
+    if (len <= 0) return fail(PEEK_ERR_INVALID_TREE, "non-root node %d has an empty edge", i);
+    if (len > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "edge of node %d is too long", i);
+    nkids[p + 1] += 1;
+  }
+  if (root == -1) return fail(PEEK_ERR_INVALID_TREE, "no root (a node with parent -1)");
+
+  // children grouped per parent (counting sort), then ordered by first token
+  std::vector<int32_t> kbeg(num_nodes + 1, 0);
+  for (int32_t i = 0; i < num_nodes; ++i) kbeg[i + 1] = kbeg[i] + nkids[i + 1];
+  std::vector<int32_t> kids(num_nodes > 0 ? num_nodes - 1 : 0);
+  {
+    std::vector<int32_t> fill(kbeg.begin(), kbeg.end() - 1);
+    for (int32_t i = 0; i < num_nodes; ++i)
+      if (parent[i] != -1) kids[fill[parent[i]]++] = i;
+  }
+  auto first_tok = [&](int32_t c) { return etok[eoff[c]]; };
+  int32_t max_fanout = 0;
+  for (int32_t v = 0; v < num_nodes; ++v) {
+    int32_t* b = kids.data() + kbeg[v];
+    int32_t* e = kids.data() + kbeg[v + 1];
+    std::sort(b, e, [&](int32_t x, int32_t y) { return first_tok(x) < first_tok(y); });
+    for (int32_t* q = b + 1; q < e; ++q)
+      if (first_tok(q[-1]) == first_tok(q[0]))
+        return fail(PEEK_ERR_INVALID_TREE, "siblings %d and %d (parent %d) share first token %d", q[-1], q[0], v,
+                    first_tok(q[0]));
+    max_fanout = std::max<int32_t>(max_fanout, (int32_t)(e - b));
+  }
+
+  // depth-first preorder from the root, children by ascending first token
+  std::vector<int32_t> order;
+  order.reserve(num_nodes);
+  std::vector<int64_t> depth_in(num_nodes, -1);
+  {
+    std::vector<int32_t> stack{root};
+    depth_in[root] = 0;
+    while (!stack.empty()) {
+      const int32_t v = stack.back();
+      stack.pop_back();
+      order.push_back(v);
+      for (int32_t q = kbeg[v + 1] - 1; q >= kbeg[v]; --q) {
+        const int32_t c = kids[q];
+        depth_in[c] = depth_in[v] + (eoff[c + 1] - eoff[c]);
+        stack.push_back(c);
+      }
+    }
+  }
+  if ((int32_t)order.size() != num_nodes)
+    return fail(PEEK_ERR_INVALID_TREE, "%d of %d nodes are not reachable from the root (cycle)",
+                num_nodes - (int32_t)order.size(), num_nodes);
+
+  f->canon.assign(num_nodes, -1);
+  for (int32_t c = 0; c < num_nodes; ++c) f->canon[order[c]] = c;
+  f->max_fanout = max_fanout;
+  f->max_depth = 0;
+  for (int32_t i = 0; i < num_nodes; ++i) f->max_depth = std::max(f->max_depth, depth_in[i]);
+  if (f->max_depth > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "tree deeper than 2^31-1 tokens");
+  f->edge_tokens = eoff[num_nodes] - eoff[0];
+  if (!out_full) return PEEK_OK;
+
+  // subtree sizes: in preorder every child comes after its parent
+  std::vector<int32_t> size(num_nodes, 1);
+  for (int32_t c = num_nodes - 1; c > 0; --c) size[f->canon[parent[order[c]]]] += size[c];
+
+  int64_t pool_len = 0;
+  for (int32_t c = 0; c < num_nodes; ++c) {
+    const int64_t len = eoff[order[c] + 1] - eoff[order[c]];
+    pool_len += (len + 3) & ~int64_t(3);
+  }
+  pool_len += kPoolTailPad;
+  try {
+    f->recs.resize(num_nodes);
+    f->child_tok.resize(std::max<int32_t>(1, num_nodes - 1));
+    f->child_id.resize(std::max<int32_t>(1, num_nodes - 1));
+    f->pool.assign(pool_len, 0);
+  } catch (const std::bad_alloc&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation for the flattened tree failed");
+  }
+  int64_t pos = 0;
+  int32_t ct = 0;
+  for (int32_t c = 0; c < num_nodes; ++c) {
+    const int32_t v = order[c];
+    const int64_t len = eoff[v + 1] - eoff[v];
+    NodeRec& r = f->recs[c];
+    r.edge_off = pos;
+    r.edge_len = (int32_t)len;
+    r.depth = (int32_t)depth_in[v];
+    r.child_beg = ct;
+    r.n_child = kbeg[v + 1] - kbeg[v];
+    r.parent = parent[v] == -1 ? -1 : f->canon[parent[v]];
+    r.subtree_end = c + size[c];
+    if (len) std::memcpy(f->pool.data() + pos, etok + eoff[v], len * sizeof(int32_t));
+    pos += (len + 3) & ~int64_t(3);
+    for (int32_t q = kbeg[v]; q < kbeg[v + 1]; ++q) {
+      f->child_tok[ct] = first_tok(kids[q]);
+      f->child_id[ct] = f->canon[kids[q]];
+      ++ct;
+    }
+  }
+  return PEEK_OK;
+}
+
+peek_status check_device(int* dev_out) {
+  int dev = 0;
+  PEEK_HIP_TRY(hipGetDevice(&dev));
+  hipDeviceProp_t prop;
+  PEEK_HIP_TRY(hipGetDeviceProperties(&prop, dev));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(PEEK_ERR_UNSUPPORTED_DEVICE, "device %d is %s; this library is built for gfx950 only", dev,
+                prop.gcnArchName);
+  *dev_out = dev;
+  return PEEK_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Lexicographic order of two token strings (signed tokens; a proper prefix first).
+struct SeqRef {
+  const int32_t* p;
+  int64_t len;
+};
+
+bool seq_less(const SeqRef& a, const SeqRef& b) {
+  const int64_t n = std::min(a.len, b.len);
+  for (int64_t k = 0; k < n; ++k)
+    if (a.p[k] != b.p[k]) return a.p[k] < b.p[k];
+  return a.len < b.len;
+}
+
+int64_t seq_lcp(const SeqRef& a, const SeqRef& b) {
+  const int64_t n = std::min(a.len, b.len);
+  int64_t k = 0;
+  while (k < n && a.p[k] == b.p[k]) ++k;
+  return k;
+}
+
+}  // namespace
+}  // namespace peek
+
+using namespace peek;
+
+extern "C" {
+
+int32_t peek_abi_version(void) { return PEEK_ABI_VERSION; }
+
+const char* peek_last_error(void) { return g_last_error.c_str(); }
+
+peek_status peek_tree_canonical_ids(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
+                                    const int32_t* edge_tokens, int32_t* canon_id) {
+  clear_error();
+  if (!canon_id) return fail(PEEK_ERR_INVALID_ARGUMENT, "canon_id must not be NULL");
+  Flat f;
+  peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, false);
+  if (s != PEEK_OK) return s;
+  std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
+  return PEEK_OK;
+}
+
+void peek_free_host(void* p) { std::free(p); }
+
+// Compressed trie of raw sequences, built from their lexicographic order:
+// consecutive sorted sequences share a prefix of length lcp, so a stack of
+// the current root-to-leaf path (depths strictly increasing) is unwound to
+// that depth, a branch node is inserted there if none exists, and the new
+// sequence hangs below as a leaf. Every node keeps one witness sequence
+// that passes through it; its edge is witness[depth(parent) : depth].
+peek_status peek_tree_from_sequences(const int32_t* tokens, const int64_t* offsets, int64_t num_seqs,
+                                     int32_t* num_nodes_out, int32_t** parent_out,
+                                     int64_t** edge_offsets_out, int32_t** edge_tokens_out) {
+  clear_error();
+  if (num_seqs < 0 || !offsets || !num_nodes_out || !parent_out || !edge_offsets_out || !edge_tokens_out)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "invalid arguments to peek_tree_from_sequences");
+  if (offsets[num_seqs] > offsets[0] && !tokens) return fail(PEEK_ERR_INVALID_ARGUMENT, "tokens is NULL");
+  std::vector<SeqRef> seqs;
+  seqs.reserve(num_seqs);
+  for (int64_t s = 0; s < num_seqs; ++s) {
+    if (offsets[s + 1] < offsets[s]) return fail(PEEK_ERR_INVALID_ARGUMENT, "offsets decrease at %lld", (long long)s);
+    seqs.push_back({tokens + offsets[s], offsets[s + 1] - offsets[s]});
+  }
+  std::sort(seqs.begin(), seqs.end(), seq_less);
+
+  struct TNode {
+    int64_t depth;
+    int32_t parent;
+    int32_t witness;   // index into seqs
+  };
+  std::vector<TNode> nodes{{0, -1, -1}};
+  std::vector<int32_t> stack{0};
+  int32_t prev = -1;
+  for (int32_t i = 0; i < (int32_t)seqs.size(); ++i) {
+    const SeqRef& s = seqs[i];
+    if (s.len == 0) continue;                       // ends at the root
+    int64_t l = 0;
+    if (prev >= 0) {
+      l = seq_lcp(seqs[prev], s);
+      if (l == s.len && l == seqs[prev].len) continue;   // duplicate
+    }
+    int32_t popped = -1;
+    while (nodes[stack.back()].depth > l) {
+      popped = stack.back();
+      stack.pop_back();
+    }
+    if (nodes[stack.back()].depth < l) {
+      // branch point inside the edge into `popped`
+      TNode b{l, stack.back(), i};
+      nodes.push_back(b);
+      const int32_t bid = (int32_t)nodes.size() - 1;
+      nodes[popped].parent = bid;
+      stack.push_back(bid);
+    }
+    if (s.len > l) {
+      nodes.push_back({s.len, stack.back(), i});
+      stack.push_back((int32_t)nodes.size() - 1);
+    }
+    prev = i;
+  }
+  if (nodes.size() > (size_t)INT32_MAX) return fail(PEEK_ERR_INVALID_ARGUMENT, "too many nodes");
+  const int32_t nn = (int32_t)nodes.size();
+  int64_t total = 0;
+  for (int32_t v = 1; v < nn; ++v) total += nodes[v].depth - nodes[nodes[v].parent].depth;
+  std::vector<int32_t> par(nn);
+  std::vector<int64_t> eoff(nn + 1);
+  std::vector<int32_t> etok(std::max<int64_t>(total, 1));
+  int64_t pos = 0;
+  for (int32_t v = 0; v < nn; ++v) {
+    par[v] = nodes[v].parent;
+    eoff[v] = pos;
+    if (v > 0) {
+      const int64_t d0 = nodes[nodes[v].parent].depth;
+      const SeqRef& w = seqs[nodes[v].witness];
+      std::memcpy(etok.data() + pos, w.p + d0, sizeof(int32_t) * (nodes[v].depth - d0));
+      pos += nodes[v].depth - d0;
+    }
+  }
+  eoff[nn] = pos;
+  // emit in canonical order
+  Flat f;
+  peek_status st = flatten(nn, par.data(), eoff.data(), etok.data(), &f, false);
+  if (st != PEEK_OK) return fail(PEEK_ERR_INVALID_TREE, "internal: built tree is invalid: %s", g_last_error.c_str());
+  std::vector<int32_t> order(nn);
+  for (int32_t v = 0; v < nn; ++v) order[f.canon[v]] = v;
+  int32_t* P = (int32_t*)std::malloc(sizeof(int32_t) * nn);
+  int64_t* O = (int64_t*)std::malloc(sizeof(int64_t) * (nn + 1));
+  int32_t* T = (int32_t*)std::malloc(sizeof(int32_t) * std::max<int64_t>(total, 1));
+  if (!P || !O || !T) {
+    std::free(P);
+    std::free(O);
+    std::free(T);
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  int64_t q = 0;
+  for (int32_t c = 0; c < nn; ++c) {
+    const int32_t v = order[c];
+    P[c] = par[v] == -1 ? -1 : f.canon[par[v]];
+    O[c] = q;
+    const int64_t len = eoff[v + 1] - eoff[v];
+    if (len) std::memcpy(T + q, etok.data() + eoff[v], sizeof(int32_t) * len);
+    q += len;
+  }
+  O[nn] = q;
+  *num_nodes_out = nn;
+  *parent_out = P;
+  *edge_offsets_out = O;
+  *edge_tokens_out = T;
+  return PEEK_OK;
+}
+
+peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
+                             const int32_t* edge_tokens, void* stream, peek_cache** out, int32_t* canon_id) {
+  clear_error();
+  if (!out) return fail(PEEK_ERR_INVALID_ARGUMENT, "out must not be NULL");
+  Flat f;
+  peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, true);
+  if (s != PEEK_OK) return s;
+  int dev = 0;
+  s = check_device(&dev);
+  if (s != PEEK_OK) return s;
+
+  const size_t b_nodes = align256(sizeof(NodeRec) * (size_t)num_nodes);
+  const size_t b_ctok = align256(sizeof(int32_t) * f.child_tok.size());
+  const size_t b_cid = align256(sizeof(int32_t) * f.child_id.size());
+  const size_t b_pool = align256(sizeof(int32_t) * f.pool.size());
+  const size_t total = b_nodes + b_ctok + b_cid + b_pool;
+  void* base = nullptr;
+  hipError_t e = hipMalloc(&base, total);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
+  }
+  char* p = (char*)base;
+  hipStream_t st = (hipStream_t)stream;
+  const hipError_t e1 = hipMemcpyAsync(p, f.recs.data(), sizeof(NodeRec) * num_nodes, hipMemcpyHostToDevice, st);
+  const hipError_t e2 = hipMemcpyAsync(p + b_nodes, f.child_tok.data(), sizeof(int32_t) * f.child_tok.size(),
+                                       hipMemcpyHostToDevice, st);
+  const hipError_t e3 = hipMemcpyAsync(p + b_nodes + b_ctok, f.child_id.data(), sizeof(int32_t) * f.child_id.size(),
+                                       hipMemcpyHostToDevice, st);
+  const hipError_t e4 = hipMemcpyAsync(p + b_nodes + b_ctok + b_cid, f.pool.data(), sizeof(int32_t) * f.pool.size(),
+                                       hipMemcpyHostToDevice, st);
+  const hipError_t e5 = hipStreamSynchronize(st);
+  for (hipError_t ee : {e1, e2, e3, e4, e5}) {
+    if (ee != hipSuccess) {
+      (void)hipFree(base);
+      return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(ee));
+    }
+  }
+  peek_cache* c = new (std::nothrow) peek_cache();
+  if (!c) {
+    (void)hipFree(base);
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  c->device = dev;
+  c->num_nodes = num_nodes;
+  c->num_edge_tokens = f.edge_tokens;
+  c->pool_tokens = (int64_t)f.pool.size();
+  c->max_fanout = f.max_fanout;
+  c->max_depth = f.max_depth;
+  c->device_bytes = (int64_t)total;
+  c->d_base = base;
+  c->tree.nodes = (const NodeRec*)p;
+  c->tree.child_tok = (const int32_t*)(p + b_nodes);
+  c->tree.child_id = (const int32_t*)(p + b_nodes + b_ctok);
+  c->tree.pool = (const int32_t*)(p + b_nodes + b_ctok + b_cid);
+  c->tree.num_nodes = num_nodes;
+  if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
+  *out = c;
+  return PEEK_OK;
+}
+
+peek_status peek_cache_stats(const peek_cache* c, int64_t* num_nodes, int64_t* num_edge_tokens, int32_t* max_fanout,
+                             int64_t* max_depth, int64_t* device_bytes) {
+  clear_error();
+  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+  if (num_nodes) *num_nodes = c->num_nodes;
+  if (num_edge_tokens) *num_edge_tokens = c->num_edge_tokens;
+  if (max_fanout) *max_fanout = c->max_fanout;
+  if (max_depth) *max_depth = c->max_depth;
+  if (device_bytes) *device_bytes = c->device_bytes;
+  return PEEK_OK;
+}
+
+peek_status peek_cache_export(const peek_cache* c, int32_t* parent, int32_t* depth, int32_t* edge_len,
+                              int32_t* subtree_end) {
+  clear_error();
+  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+  std::vector<NodeRec> recs(c->num_nodes);
+  PEEK_HIP_TRY(hipMemcpy(recs.data(), c->tree.nodes, sizeof(NodeRec) * c->num_nodes, hipMemcpyDeviceToHost));
+  for (int32_t i = 0; i < c->num_nodes; ++i) {
+    if (parent) parent[i] = recs[i].parent;
+    if (depth) depth[i] = recs[i].depth;
+    if (edge_len) edge_len[i] = recs[i].edge_len;
+    if (subtree_end) subtree_end[i] = recs[i].subtree_end;
+  }
+  return PEEK_OK;
+}
+
+peek_status peek_cache_free(peek_cache* c) {
+  clear_error();
+  if (!c) return PEEK_OK;
+  hipError_t e = hipFree(c->d_base);
+  delete c;
+  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
+  return PEEK_OK;
+}
+
+static peek_status check_same_device(const peek_cache* c) {
+  int dev = 0;
+  PEEK_HIP_TRY(hipGetDevice(&dev));
+  if (dev != c->device)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "cache lives on device %d but device %d is current", c->device, dev);
+  return PEEK_OK;
+}
+
+peek_status peek_lpm_batch(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                           int32_t block_size, int32_t* d_h, int32_t* d_last_node, int32_t* d_match_len,
+                           void* stream) {
+  clear_error();
+  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+  if (block_size < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "block_size must be >= 1 (got %d)", block_size);
+  if (n == 0) return PEEK_OK;
+  if (!d_tokens || !d_offsets || !d_h)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h must not be NULL");
+  peek_status s = check_same_device(c);
+  if (s != PEEK_OK) return s;
+  hipError_t e = launch_lpm_walk(c->tree, n, d_tokens, d_offsets, block_size, d_h, d_last_node, d_match_len,
+                                 (hipStream_t)stream);
+  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "lpm walk launch failed: %s", hipGetErrorString(e));
+  return PEEK_OK;
+}
+
+size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes) {
+  if (n < 0 || num_nodes < 0) return 0;
+  return signals_workspace_bytes(n, num_nodes);
+}
+
+peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                               const int32_t* d_last_node, int32_t threshold, int32_t* d_cluster_id,
+                               int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
+                               size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+  if (threshold < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "threshold must be >= 1 (got %d)", threshold);
+  const bool want_demand = d_demand != nullptr;
+  const bool want_clusters = d_cluster_id != nullptr || d_cluster_size != nullptr;
+  if (want_clusters && (!d_cluster_id || !d_cluster_size))
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_cluster_id and d_cluster_size must both be given");
+  if (want_demand && !c) return fail(PEEK_ERR_INVALID_ARGUMENT, "demand needs the cache");
+  if (want_demand && n > 0 && !d_last_node) return fail(PEEK_ERR_INVALID_ARGUMENT, "demand needs d_last_node");
+  if (want_clusters && n > 0 && (!d_tokens || !d_offsets))
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "clusters need d_tokens and d_offsets");
+  const int64_t nn = c ? c->num_nodes : 0;
+  const size_t need = signals_workspace_bytes(n, nn);
+  if ((want_demand || want_clusters) && need > 0) {
+    if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
+    if (workspace_bytes < need)
+      return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+    if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+  }
+  if (c) {
+    peek_status s = check_same_device(c);
+    if (s != PEEK_OK) return s;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  if (want_demand) {
+    peek_status s = run_demand(c->tree, n, d_last_node, d_demand, d_workspace, workspace_bytes, st);
+    if (s != PEEK_OK) return s;
+  }
+  if (want_clusters && n > 0) {
+    peek_status s = run_clusters(n, d_tokens, d_offsets, threshold, d_cluster_id, d_cluster_size, nn, d_workspace,
+                                 workspace_bytes, st);
+    if (s != PEEK_OK) return s;
+  }
+  return PEEK_OK;
+}
+
+}  // extern "C"

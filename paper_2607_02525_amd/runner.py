@@ -1,0 +1,76 @@
+"""One pass of the whole hot path over a resident batch: LPM of every request,
+then demand and clusters, with device buffers allocated once up front.
+
+    hp = HotPath.from_description(parent, edge_offsets, edge_tokens)    # or from_sequences
+    hp.load_queue(tokens, offsets, block_size=16, threshold=256)         # numpy -> HBM
+    hp.step()                                                           # enqueue on the current stream
+    out = hp.results()                                                  # numpy copies
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (Cache, peek_cache_build, peek_cache_stats, peek_lpm_batch, peek_queue_signals,
+               peek_queue_signals_workspace, peek_tree_from_sequences)
+
+
+class HotPath:
+    def __init__(self, cache: Cache, canon_id: np.ndarray, device=None):
+        self.cache = cache
+        self.canon_id = canon_id
+        self.device = torch.device("cuda") if device is None else torch.device(device)
+        self.num_nodes = peek_cache_stats(cache)["num_nodes"]
+        self.n = 0
+
+    @classmethod
+    def from_description(cls, parent, edge_offsets, edge_tokens, device=None):
+        cache, canon = peek_cache_build(parent, edge_offsets, edge_tokens)
+        return cls(cache, canon, device)
+
+    @classmethod
+    def from_sequences(cls, tokens, offsets, device=None):
+        return cls.from_description(*peek_tree_from_sequences(tokens, offsets), device=device)
+
+    def load_queue(self, tokens, offsets, block_size: int, threshold: int):
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+        self.n = int(offsets.shape[0] - 1)
+        self.block_size = int(block_size)
+        self.threshold = int(threshold)
+        dev = self.device
+        self.d_tokens = torch.from_numpy(tokens if tokens.size else np.zeros(1, np.int32)).to(dev)
+        self.d_offsets = torch.from_numpy(offsets).to(dev)
+        n = max(self.n, 1)
+        self.d_h = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_last = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_m = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_cid = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_csz = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_demand = torch.empty(self.num_nodes, dtype=torch.int32, device=dev)
+        ws = peek_queue_signals_workspace(self.n, self.num_nodes)
+        self.d_ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
+
+    def lpm(self, stream=None):
+        peek_lpm_batch(self.cache, self.d_tokens, self.d_offsets, self.block_size, self.d_h, self.d_last, self.d_m,
+                       stream=stream)
+
+    def signals(self, stream=None):
+        peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last, self.threshold, self.d_cid,
+                           self.d_csz, self.d_demand, self.d_ws, stream=stream)
+
+    def step(self, stream=None):
+        self.lpm(stream)
+        self.signals(stream)
+
+    def results(self) -> dict:
+        torch.cuda.synchronize(self.device)
+        n = self.n
+        return {
+            "h": self.d_h[:n].cpu().numpy(),
+            "last_node": self.d_last[:n].cpu().numpy(),
+            "match_len": self.d_m[:n].cpu().numpy(),
+            "cluster_id": self.d_cid[:n].cpu().numpy(),
+            "cluster_size": self.d_csz[:n].cpu().numpy(),
+            "demand": self.d_demand.cpu().numpy(),
+        }

@@ -1,0 +1,142 @@
+"""Host-only checks of the C ABI library: it loads, exports every symbol the
+header declares, validates trees, numbers nodes canonically, builds trees
+from sequences, and rejects bad arguments before touching a GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2607_02525_amd as P
+import peek_workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "peek.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(peek_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 11
+    out = subprocess.run(["nm", "-D", "--defined-only", P.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (peek_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+    bound = {name for name, _, _ in P.EXPORTS}
+    assert set(names) == bound
+
+
+def test_library_is_built_for_gfx950_only():
+    blob = open(P.LIB_PATH, "rb").read()
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa--(gfx\w+)", blob))
+    assert targets == {b"gfx950"}
+
+
+def test_abi_version():
+    assert P.peek_abi_version() == 1
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_canonical_ids_match_the_oracle(seed):
+    w = W.random_tree_case(seed, n_nodes=60, n=4, vocab=7, max_edge=4)
+    ours = P.peek_tree_canonical_ids(*w.cache_tree)
+    theirs = O.Tree.from_description(*w.cache_tree).canonical_ids(len(w.cache_tree[0]))
+    assert np.array_equal(ours, theirs)
+
+
+def _desc(parent, edges):
+    tok, off = W.pack([np.asarray(e, dtype=np.int32) for e in edges])
+    return np.asarray(parent, dtype=np.int32), off, tok
+
+
+@pytest.mark.parametrize("parent,edges", [
+    ([-1, 0, 0], [[], [1, 2], [1, 3]]),
+    ([-1, 0, 0], [[], [1], []]),
+    ([-1, -1], [[], []]),
+    ([0, 0], [[1], [2]]),
+    ([-1, 2, 1], [[], [1], [2]]),
+    ([-1, 5], [[], [1]]),
+    ([-1, 0], [[4], [1]]),
+])
+def test_invalid_trees_are_rejected(parent, edges):
+    with pytest.raises(P.PeekError) as e:
+        P.peek_tree_canonical_ids(*_desc(parent, edges))
+    assert e.value.status == P.PEEK_ERR_INVALID_TREE
+    assert P.peek_last_error()
+
+
+def test_signed_token_order_and_extremes():
+    # children ordered by signed first token: INT32_MIN < -1 < 0 < INT32_MAX
+    lo, hi = np.iinfo(np.int32).min, np.iinfo(np.int32).max
+    parent, off, tok = _desc([-1, 0, 0, 0, 0], [[], [hi, 1], [0], [lo], [-1, 5]])
+    assert list(P.peek_tree_canonical_ids(parent, off, tok)) == [0, 4, 3, 1, 2]
+
+
+def _same_tree(a, b):
+    pa, oa, ta = a
+    pb, ob, tb = b
+    return np.array_equal(pa, pb) and np.array_equal(oa, ob) and np.array_equal(ta, tb)
+
+
+@pytest.mark.parametrize("seed,vocab", [(s, v) for s in range(8) for v in (2, 3, 50)])
+def test_tree_from_sequences_matches_the_oracle(seed, vocab):
+    w = W.random_case(seed, n=5, n_cached=30, vocab=vocab, max_len=30)
+    ours = P.peek_tree_from_sequences(*w.cache_sequences)
+    par, depth, eoff, etok = O.Tree.from_sequences(*w.cache_sequences).export()
+    assert _same_tree(ours, (par, eoff, etok))
+
+
+@pytest.mark.parametrize("name", ["tiny", "rag", "agentic", "nosharing"])
+def test_tree_from_sequences_on_workload_caches(name):
+    w = W.make(name, 42)
+    ours = P.peek_tree_from_sequences(*w.cache_sequences)
+    par, depth, eoff, etok = O.Tree.from_sequences(*w.cache_sequences).export()
+    assert _same_tree(ours, (par, eoff, etok))
+
+
+def test_tree_from_sequences_edge_cases():
+    # no sequences, only empty ones, duplicates, a prefix of another
+    for seqs in ([], [[]], [[], []], [[1, 2], [1, 2]], [[1, 2, 3], [1, 2]], [[5], [5, 6], [5, 6, 7]]):
+        tok, off = W.pack([np.asarray(s, np.int32) for s in seqs])
+        ours = P.peek_tree_from_sequences(tok, off)
+        par, depth, eoff, etok = O.Tree.from_sequences(tok, off).export()
+        assert _same_tree(ours, (par, eoff, etok)), seqs
+
+
+def test_argument_errors_before_any_gpu_work():
+    lib = P._lib
+    # NULL cache
+    assert lib.peek_lpm_batch(None, 1, None, None, 16, None, None, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "NULL" in P.peek_last_error()
+    assert lib.peek_cache_stats(None, None, None, None, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_cache_free(None) == P.PEEK_OK
+    # threshold < 1, n < 0, mismatched cluster outputs
+    assert lib.peek_queue_signals(None, 4, None, None, None, 0, None, None, None, None, 0, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_queue_signals(None, -1, None, None, None, 8, None, None, None, None, 0, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.peek_queue_signals(None, 4, fake, fake, None, 8, fake, None, None, None, 0, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+    # workspace too small for the cluster pass (checked before any launch)
+    need = P.peek_queue_signals_workspace(4, 0)
+    assert need > 0
+    assert lib.peek_queue_signals(None, 4, fake, fake, None, 8, fake, fake, None, fake, need - 1, None) \
+        == P.PEEK_ERR_WORKSPACE_TOO_SMALL
+    # demand without a cache
+    assert lib.peek_queue_signals(None, 4, fake, fake, fake, 8, None, None, fake, fake, need, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+
+
+def test_workspace_grows_with_the_queue_and_the_cache():
+    a = P.peek_queue_signals_workspace(1000, 10)
+    assert P.peek_queue_signals_workspace(2000, 10) > a
+    assert P.peek_queue_signals_workspace(1000, 100000) > a
+    assert P.peek_queue_signals_workspace(-1, 0) == 0

@@ -1,0 +1,157 @@
+"""GPU parity: every output of the HIP path against the oracle, element by
+element and bit-exact (all outputs are integers), on the five workload
+configurations, randomized small cases and adversarial shapes."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+import peek_workloads as W
+from tests import checks
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _hot():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_02525_amd.runner import HotPath
+    return HotPath
+
+
+def gpu_run(w, repeat=1):
+    HotPath = _hot()
+    print(f"[gpu] {w.name} seed={w.seed} n={w.n} tokens={len(w.tokens)}", flush=True)
+    if w.cache_tree is not None:
+        hp = HotPath.from_description(*w.cache_tree)
+    else:
+        hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    outs = []
+    for _ in range(repeat):
+        hp.step()
+        outs.append(hp.results())
+    return hp, outs
+
+
+def assert_parity(w, res, s):
+    assert np.array_equal(res["match_len"], s.lpm.m), "match_len"
+    assert np.array_equal(res["h"], s.lpm.h), "h"
+    assert np.array_equal(res["last_node"], s.lpm.last_node), "last_node"
+    assert np.array_equal(res["demand"], s.demand), "demand"
+    assert np.array_equal(res["cluster_id"], s.clusters.cluster_id), "cluster_id"
+    assert np.array_equal(res["cluster_size"], s.clusters.cluster_size), "cluster_size"
+
+
+def run_and_compare(w, repeat=1):
+    s = O.run(w)
+    hp, outs = gpu_run(w, repeat)
+    for res in outs:
+        assert_parity(w, res, s)
+    return hp, outs[0], s
+
+
+@pytest.mark.parametrize("name", ["tiny", "rag", "agentic", "nosharing"])
+@pytest.mark.parametrize("seed", W.PAPER_SEEDS)
+def test_configs_bit_exact(name, seed):
+    w = W.make(name, seed)
+    hp, res, s = run_and_compare(w)
+    parent, depth, _, _ = s.tree.export()
+    checks.check_lpm(w, parent, depth, res["match_len"], res["h"], res["last_node"])
+    checks.check_demand(w.n, parent, res["last_node"], res["demand"])
+
+
+def test_scale_bit_exact_full_size():
+    w = W.make("scale", 42)
+    hp, res, s = run_and_compare(w, repeat=2)
+    parent, depth, _, _ = s.tree.export()
+    checks.check_lpm(w, parent, depth, res["match_len"], res["h"], res["last_node"])
+    checks.check_demand(w.n, parent, res["last_node"], res["demand"])
+    exp = hp.cache.stats()
+    assert exp["num_nodes"] == s.tree.num_nodes
+
+
+@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("vocab,B,T", [(2, 1, 1), (3, 2, 2), (4, 4, 8), (32000, 16, 4)])
+def test_random_sequence_cases(seed, vocab, B, T):
+    w = W.random_case(seed * 13 + vocab, n=40, n_cached=24, vocab=vocab, max_len=80, block_size=B, threshold=T)
+    run_and_compare(w)
+
+
+@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("vocab,fan", [(3, None), (6, 1), (200, None), (90, 70)])
+def test_random_described_trees(seed, vocab, fan):
+    w = W.random_tree_case(seed, n_nodes=400 if fan != 1 else 60, n=64, vocab=vocab, max_edge=300,
+                           block_size=16, threshold=8, max_fanout=fan)
+    run_and_compare(w)
+
+
+def _w(prompts, cached=None, tree=None, B=16, T=4, name="adv"):
+    tok, off = W.pack([np.asarray(p, np.int32) for p in prompts])
+    if tree is not None:
+        return W.Workload(name, 0, tok, off, B, T, cache_tree=tree)
+    ctok, coff = W.pack([np.asarray(c, np.int32) for c in (cached or [])])
+    return W.Workload(name, 0, tok, off, B, T, cache_sequences=(ctok, coff))
+
+
+def test_empty_prompts_and_empty_cache():
+    run_and_compare(_w([[], [1, 2, 3], [], [1, 2, 3, 4]], cached=[]))
+    run_and_compare(_w([[], []], cached=[[1, 2]]))
+
+
+def test_single_request():
+    run_and_compare(_w([[7] * 100], cached=[[7] * 40]))
+
+
+def test_identical_and_prefix_prompts():
+    base = list(range(1, 600))
+    prompts = [base, base, base[:300], base[:300], base[:17], base + [9], base[:299] + [5]]
+    run_and_compare(_w(prompts, cached=[base[:250], base[:600]], T=16))
+
+
+def test_block_boundaries():
+    base = list(range(1000, 1200))
+    prompts = [base[:k] + [1] for k in (15, 16, 17, 31, 32, 33, 63, 64, 65)]
+    run_and_compare(_w(prompts, cached=[base], B=16))
+
+
+def test_extreme_token_values():
+    lo, hi = int(np.iinfo(np.int32).min), int(np.iinfo(np.int32).max)
+    cached = [[lo, hi, 0, -1] * 100, [hi, lo] * 50, [-1, 0, 1], [0, lo]]
+    prompts = [[lo, hi, 0, -1] * 80 + [hi], [hi, lo] * 60, [-1, 0, 2], [0, lo, lo], [lo], [hi]]
+    run_and_compare(_w(prompts, cached=cached))
+
+
+def test_fanout_64_65_and_large():
+    rng = np.random.default_rng(5)
+    for fan in (1, 63, 64, 65, 129, 4096, 20000):
+        firsts = rng.choice(10**6, size=fan, replace=False)
+        cached = [[int(f)] + list(range(50)) for f in firsts]
+        picks = rng.choice(firsts, size=min(fan, 300), replace=False)
+        prompts = [[int(f)] + list(range(60)) for f in picks] + [[-5, 1], [10**7, 2]]
+        run_and_compare(_w(prompts, cached=cached, T=8))
+
+
+def test_deep_chain_beyond_64k_tokens():
+    rng = np.random.default_rng(6)
+    long = rng.integers(0, 128256, size=70000, dtype=np.int32).tolist()
+    cuts = [16 * k for k in (300, 1500, 4000, 4375)]
+    cached = [long[:c] for c in cuts]
+    prompts = [long[:69000], long[:70000], long[:66000] + [5], long[:100]]
+    run_and_compare(_w(prompts, cached=cached, T=256))
+
+
+def test_many_requests_not_multiple_of_the_block():
+    w = W.random_case(77, n=1001, n_cached=300, vocab=3, max_len=120, block_size=4, threshold=5)
+    run_and_compare(w)
+
+
+def test_repeated_runs_are_identical():
+    w = W.make("agentic", 142)
+    s = O.run(w)
+    hp, outs = gpu_run(w, repeat=3)
+    for res in outs:
+        assert_parity(w, res, s)
