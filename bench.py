@@ -100,6 +100,8 @@ def main():
     ap.add_argument("--seed", type=int, default=42)
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device-to-device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this hot path is built and measured on a single MI355X "
@@ -162,6 +164,15 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                 "kernel": "k_lpm_walk", "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
                 "avg_launch_ms": round(float(lpm_ms.mean()), 4), "min_launch_ms": round(float(lpm_ms.min()), 4)}
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration copy: 3 x 1 GiB device-to-device")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -27,7 +27,7 @@
  *  - A prompt set is packed: request r's prompt is
  *    d_tokens[d_offsets[r] : d_offsets[r+1]], offsets int64, non-decreasing.
  *    Offsets and tokens live on the device, so they are preconditions the
- *    library does not re-check. Each prompt must be shorter than 2^29 tokens.
+ *    library does not re-check. Each prompt must be shorter than 2^31 tokens.
  */
 #ifndef PEEK_H
 #define PEEK_H
@@ -144,13 +144,12 @@ peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_
  * peek_queue_signals: prefix-sharing clusters of the waiting queue and the
  * pending demand of every cache node (Sec. 3.1, App. A.3, Eq. 2).
  *
- * Demand (when d_demand != NULL; needs cache and d_last_node from
- * peek_lpm_batch on the same prompts):
+ * Demand (when d_demand != NULL; needs the cache and d_last_node):
  *   d_demand[c] = number of requests whose walk enters cache node c
  *               = #{r : last_node[r] in subtree(c)}; int32[num_nodes],
  *                 canonical ids; d_demand[0] = n.
- * Clusters (when d_cluster_id or d_cluster_size != NULL; need d_tokens,
- * d_offsets; the cache is not used):
+ * Clusters (when d_cluster_id and d_cluster_size != NULL; need d_tokens and
+ * d_offsets):
  *   share_r = max over r' != r of LCP(p_r, p_r')   (0 when n = 1)
  *   if share_r >= threshold:
  *     cluster_size[r] = #{r' : LCP(p_r, p_r') >= share_r}   (pending_count)
@@ -158,20 +157,27 @@ peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_
  *   else cluster_id[r] = -1, cluster_size[r] = 1 (in no cluster).
  * Request indices are positions in the submitted batch (arrival order).
  *
+ * d_last_node and d_match_len, when given, must be the outputs of
+ * peek_lpm_batch for the same prompts and cache. The cluster pass then
+ * starts from the prefixes the walk already proved shared and does not read
+ * them again; with either pointer NULL (or no cache) it starts from scratch.
+ * The results are the same either way.
+ *
  * Scratch comes only from d_workspace (device, 256-byte aligned, at least
- * peek_queue_signals_workspace(n, num_nodes) bytes); the library allocates
- * nothing here. The cluster pass refines a sort in rounds and synchronizes
- * `stream` once per round to read a device flag, so this call returns after
- * the stream has finished its work. threshold >= 1.
+ * peek_queue_signals_workspace(n, num_nodes) bytes, num_nodes = 0 without a
+ * cache); the library allocates nothing here. The cluster pass refines a
+ * sort in rounds and synchronizes `stream` once per round to read a device
+ * flag, so this call returns after the stream has finished its work.
+ * threshold >= 1.
  * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
  * ---------------------------------------------------------------------- */
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes);
 
 peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
                                const int64_t* d_offsets, const int32_t* d_last_node,
-                               int32_t threshold, int32_t* d_cluster_id, int32_t* d_cluster_size,
-                               int32_t* d_demand, void* d_workspace, size_t workspace_bytes,
-                               void* stream);
+                               const int32_t* d_match_len, int32_t threshold,
+                               int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
+                               void* d_workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

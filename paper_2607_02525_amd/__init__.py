@@ -51,7 +51,7 @@ EXPORTS = [
     ("peek_lpm_batch", ctypes.c_int, [_vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp]),
     ("peek_queue_signals_workspace", ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
     ("peek_queue_signals", ctypes.c_int,
-     [_vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+     [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
 ]
 
 for _name, _res, _args in EXPORTS:
@@ -85,11 +85,6 @@ def _np32(a):
 
 def _np64(a):
     return np.ascontiguousarray(a, dtype=np.int64)
-
-
-def _p32(a):
-    return a.ctypes.data_as(_i32p) if a is not None and a.size else (None if a is None else
-                                                                      np.zeros(1, np.int32).ctypes.data_as(_i32p))
 
 
 def _dptr(t):
@@ -204,11 +199,13 @@ def peek_queue_signals_workspace(n: int, num_nodes: int) -> int:
     return int(_lib.peek_queue_signals_workspace(int(n), int(num_nodes)))
 
 
-def peek_queue_signals(cache, tokens, offsets, last_node, threshold: int, cluster_id, cluster_size, demand,
-                       workspace, stream=None):
-    """cluster_id/cluster_size int32[n], demand int32[num_nodes], workspace uint8 tensor; torch tensors."""
+def peek_queue_signals(cache, tokens, offsets, last_node, match_len, threshold: int, cluster_id, cluster_size,
+                       demand, workspace, stream=None):
+    """cluster_id/cluster_size int32[n], demand int32[num_nodes], workspace uint8 tensor; torch tensors.
+    last_node/match_len: peek_lpm_batch outputs for the same prompts (or None)."""
     n = int(offsets.shape[0]) - 1
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
     _check(_lib.peek_queue_signals(None if cache is None else cache.handle, n, _dptr(tokens), _dptr(offsets),
-                                   _dptr(last_node), int(threshold), _dptr(cluster_id), _dptr(cluster_size),
-                                   _dptr(demand), _dptr(workspace), ws_bytes, _stream(stream)))
+                                   _dptr(last_node), _dptr(match_len), int(threshold), _dptr(cluster_id),
+                                   _dptr(cluster_size), _dptr(demand), _dptr(workspace), ws_bytes,
+                                   _stream(stream)))

@@ -38,6 +38,9 @@ struct Flat {
   std::vector<int32_t> child_tok;  // per-parent child tables, parents in canonical order
   std::vector<int32_t> child_id;
   std::vector<int32_t> pool;       // edge labels, each edge padded to a multiple of 4 tokens
+  std::vector<int32_t> pdep;       // depth of the parent, canonical order (root 0)
+  std::vector<int32_t> pdep_st;    // sparse table over 64-node block minima of pdep
+  int32_t pdep_nb = 0;
   int64_t edge_tokens = 0;
   int32_t max_fanout = 0;
   int64_t max_depth = 0;
@@ -144,6 +147,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     f->child_tok.resize(std::max<int32_t>(1, num_nodes - 1));
     f->child_id.resize(std::max<int32_t>(1, num_nodes - 1));
     f->pool.assign(pool_len, 0);
+    f->pdep.resize(num_nodes);
   } catch (const std::bad_alloc&) {
     return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation for the flattened tree failed");
   }
@@ -160,6 +164,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     r.n_child = kbeg[v + 1] - kbeg[v];
     r.parent = parent[v] == -1 ? -1 : f->canon[parent[v]];
     r.subtree_end = c + size[c];
+    f->pdep[c] = (int32_t)(depth_in[v] - len);
     if (len) std::memcpy(f->pool.data() + pos, etok + eoff[v], len * sizeof(int32_t));
     pos += (len + 3) & ~int64_t(3);
     for (int32_t q = kbeg[v]; q < kbeg[v + 1]; ++q) {
@@ -168,6 +173,23 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
       ++ct;
     }
   }
+  // Range minima of parent depth over preorder intervals give the depth of
+  // the lowest common ancestor of two nodes that are not ancestor-related:
+  // for a < b, depth(lca(a, b)) = min over v in (a, b] of depth(parent(v)).
+  const int32_t nb = (num_nodes + 63) / 64;
+  int levels = 1;
+  while ((int64_t(1) << levels) <= nb) ++levels;
+  f->pdep_nb = nb;
+  f->pdep_st.assign((size_t)levels * nb, 0);
+  for (int32_t b = 0; b < nb; ++b) {
+    int32_t m = INT32_MAX;
+    for (int32_t c = b * 64; c < std::min(num_nodes, b * 64 + 64); ++c) m = std::min(m, f->pdep[c]);
+    f->pdep_st[b] = m;
+  }
+  for (int k = 1; k < levels; ++k)
+    for (int32_t b = 0; b + (1 << k) <= nb; ++b)
+      f->pdep_st[(size_t)k * nb + b] =
+          std::min(f->pdep_st[(size_t)(k - 1) * nb + b], f->pdep_st[(size_t)(k - 1) * nb + b + (1 << (k - 1))]);
   return PEEK_OK;
 }
 
@@ -351,7 +373,9 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   const size_t b_ctok = align256(sizeof(int32_t) * f.child_tok.size());
   const size_t b_cid = align256(sizeof(int32_t) * f.child_id.size());
   const size_t b_pool = align256(sizeof(int32_t) * f.pool.size());
-  const size_t total = b_nodes + b_ctok + b_cid + b_pool;
+  const size_t b_pdep = align256(sizeof(int32_t) * f.pdep.size());
+  const size_t b_pst = align256(sizeof(int32_t) * f.pdep_st.size());
+  const size_t total = b_nodes + b_ctok + b_cid + b_pool + b_pdep + b_pst;
   void* base = nullptr;
   hipError_t e = hipMalloc(&base, total);
   if (e != hipSuccess) {
@@ -367,8 +391,12 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
                                        hipMemcpyHostToDevice, st);
   const hipError_t e4 = hipMemcpyAsync(p + b_nodes + b_ctok + b_cid, f.pool.data(), sizeof(int32_t) * f.pool.size(),
                                        hipMemcpyHostToDevice, st);
-  const hipError_t e5 = hipStreamSynchronize(st);
-  for (hipError_t ee : {e1, e2, e3, e4, e5}) {
+  char* p_pdep = p + b_nodes + b_ctok + b_cid + b_pool;
+  const hipError_t e5 = hipMemcpyAsync(p_pdep, f.pdep.data(), sizeof(int32_t) * f.pdep.size(), hipMemcpyHostToDevice, st);
+  const hipError_t e6 = hipMemcpyAsync(p_pdep + b_pdep, f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(),
+                                       hipMemcpyHostToDevice, st);
+  const hipError_t e7 = hipStreamSynchronize(st);
+  for (hipError_t ee : {e1, e2, e3, e4, e5, e6, e7}) {
     if (ee != hipSuccess) {
       (void)hipFree(base);
       return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(ee));
@@ -391,6 +419,9 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   c->tree.child_tok = (const int32_t*)(p + b_nodes);
   c->tree.child_id = (const int32_t*)(p + b_nodes + b_ctok);
   c->tree.pool = (const int32_t*)(p + b_nodes + b_ctok + b_cid);
+  c->tree.pdep = (const int32_t*)p_pdep;
+  c->tree.pdep_st = (const int32_t*)(p_pdep + b_pdep);
+  c->tree.pdep_nb = f.pdep_nb;
   c->tree.num_nodes = num_nodes;
   if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
   *out = c;
@@ -465,7 +496,8 @@ size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes) {
 }
 
 peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
-                               const int32_t* d_last_node, int32_t threshold, int32_t* d_cluster_id,
+                               const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
+                               int32_t* d_cluster_id,
                                int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
                                size_t workspace_bytes, void* stream) {
   clear_error();
@@ -498,8 +530,10 @@ peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_
     if (s != PEEK_OK) return s;
   }
   if (want_clusters && n > 0) {
-    peek_status s = run_clusters(n, d_tokens, d_offsets, threshold, d_cluster_id, d_cluster_size, nn, d_workspace,
-                                 workspace_bytes, st);
+    const bool anchored = c != nullptr && d_last_node != nullptr && d_match_len != nullptr;
+    peek_status s = run_clusters(anchored ? &c->tree : nullptr, n, d_tokens, d_offsets,
+                                 anchored ? d_last_node : nullptr, anchored ? d_match_len : nullptr, threshold,
+                                 d_cluster_id, d_cluster_size, nn, d_workspace, workspace_bytes, st);
     if (s != PEEK_OK) return s;
   }
   return PEEK_OK;

@@ -29,6 +29,9 @@ struct DeviceTree {
   const int32_t* child_tok; // [num_nodes - 1] first token of each child, grouped per parent
   const int32_t* child_id;  // [num_nodes - 1] canonical id of that child
   const int32_t* pool;      // edge labels, each edge starting on a 16-byte boundary
+  const int32_t* pdep;      // [num_nodes] depth of the parent (0 for the root), preorder
+  const int32_t* pdep_st;   // sparse table of 64-node block minima of pdep: levels x pdep_nb
+  int32_t pdep_nb;          // number of 64-node blocks
   int32_t num_nodes;
 };
 
@@ -72,8 +75,11 @@ size_t signals_workspace_bytes(int32_t n, int64_t num_nodes);
 peek_status run_demand(const DeviceTree& t, int32_t n, const int32_t* last_node, int32_t* demand,
                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-peek_status run_clusters(int32_t n, const int32_t* tokens, const int64_t* offsets, int32_t threshold,
-                         int32_t* cluster_id, int32_t* cluster_size, int64_t num_nodes, void* workspace,
-                         size_t workspace_bytes, hipStream_t stream);
+// t, last_node and match_len are optional (all or none): with them the
+// cluster pass starts from the walk's proven shared prefixes.
+peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
+                         int32_t* cluster_size, int64_t num_nodes, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
 
 }  // namespace peek

@@ -4,339 +4,293 @@
 // Demand (Eq. 2's pending count along a cached path): a request's walk
 // enters every node from the root down to its last node, so
 //   demand[c] = #{r : last_node[r] in subtree(c)} = P[subtree_end(c)] - P[c]
-// with P[v] = #{r : last_node[r] < v}. P comes from sorting last_node and a
-// suffix-min scan of first-occurrence positions; no atomics.
+// with P[v] = #{r : last_node[r] < v}, read off the sorted last nodes by a
+// merge-style sweep; no atomics.
 //
-// Clusters (Sec. 3.1 / App. A.3: deepest pending-tree node with
-// pending_count >= 2): the prompts are sorted lexicographically by rounds of
-// head-path refinement. A segment of prompts known to share d tokens is
-// compared against its longest member (the head); each member's first
-// mismatch l with the head and the token it has there decide its place
-// relative to the head, and members with the same (l, token) form the next
-// segment, which shares d + l + 1 tokens. Every boundary between adjacent
-// groups gets its LCP (d + the smaller l). Each member's prompt is read once
-// up to its divergence, so the traffic is about the queue's distinguishing
-// prefixes. From the adjacent-LCP array:
-//   share[i]  = max(lcp[i], lcp[i+1])            (best partner is a neighbour)
-//   [L, R)    = widest range around i with inner LCPs >= share[i]
-//   size      = R - L                            (the node's pending_count)
-//   id        = smallest request index in [L, R) among those whose own share
-//               equals share[i]   (same cluster node)
-// Range bounds and the id use sparse tables of range minima.
+// Clusters (Sec. 3.1 / App. A.3: the deepest pending-tree node with
+// pending_count >= 2 on a request's path, its count being the cluster size)
+// are read off an order of the prompts in which every pending-tree node's
+// requests are contiguous (a depth-first order of the pending tree), plus the
+// longest common prefix (LCP) of every adjacent pair:
+//   share[i] = max(lcp[i], lcp[i+1])     (a request's best partner is adjacent)
+//   [L, R)   = the widest range around i whose inner LCPs are >= share[i]
+//   size     = R - L                     (the node's pending_count)
+//   id       = the smallest request in [L, R) whose own share equals share[i]
+//
+// The order is built in two stages.
+//  1. Anchoring on the cache walk. The walk already proved that request r
+//     agrees with the cached path of last_node[r] up to match_len[r] tokens.
+//     Sorting by (last node in preorder, match length, next prompt token)
+//     yields a depth-first order of the cache tree with the queue grafted on,
+//     and the LCP of two adjacent requests follows from the tree alone:
+//       same node: min(m1, m2); ancestor node first: m1;
+//       otherwise: depth of the two nodes' lowest common ancestor
+//     (a range minimum of parent depths over the preorder interval). Only
+//     requests that also share the next token need more work, from m+1 on.
+//  2. Head-path refinement of every group that still has two or more
+//     members. A segment of requests known to share d tokens is compared with
+//     its longest member (the head) from depth d; a member's first mismatch l
+//     and its token there form its key, the head sorts last, and members with
+//     equal keys form the next segment at depth d+l+1. The LCP across a new
+//     boundary is d plus the smaller l. Each prompt byte is read about once.
 #include <algorithm>
 
 #include "peek_internal.h"
+#include "peek_sort.h"
 
 namespace peek {
 namespace {
 
 constexpr int kWave = 64;
 
-// ---------------------------------------------------------------- sorting
-struct SortElem {
-  uint64_t key;   // refinement key within the segment
-  uint32_t seg;   // start position of the segment the element belongs to
-  uint32_t nlen;  // ~length: longer prompts first among equal keys
-  uint32_t req;   // request index
-  uint32_t pad;
-};
-
-struct ElemLess {
-  __device__ __forceinline__ bool operator()(const SortElem& a, const SortElem& b) const {
-    if (a.seg != b.seg) return a.seg < b.seg;
-    if (a.key != b.key) return a.key < b.key;
-    if (a.nlen != b.nlen) return a.nlen < b.nlen;
-    return a.req < b.req;
+// Smallest p in [lo, hi] with pred(p), for a predicate that is false then
+// true and holds at hi; one wavefront, 64 probes per step.
+template <typename Pred>
+__device__ __forceinline__ int32_t wave_first_true(int32_t lo, int32_t hi, int lane, Pred pred) {
+  while (hi - lo >= kWave) {
+    const int64_t span = (int64_t)hi - lo;
+    const int32_t probe = lo + (int32_t)((span * lane) / kWave);
+    const uint64_t b = __ballot(pred(probe));
+    const int f = b ? __ffsll((unsigned long long)b) - 1 : kWave;
+    const int32_t nlo = f == 0 ? lo : lo + (int32_t)((span * (f - 1)) / kWave) + 1;
+    const int32_t nhi = f == kWave ? hi : lo + (int32_t)((span * f) / kWave);
+    lo = __builtin_amdgcn_readfirstlane(nlo);
+    hi = __builtin_amdgcn_readfirstlane(nhi);
   }
-};
+  const int32_t probe = lo + lane;
+  const uint64_t b = __ballot(probe <= hi && pred(probe));
+  return lo + (__ffsll((unsigned long long)b) - 1);
+}
 
+// ---------------------------------------------------------------- demand
 struct U32Less {
   __device__ __forceinline__ bool operator()(uint32_t a, uint32_t b) const { return a < b; }
 };
 
-constexpr int kTile = 2048;   // elements sorted per workgroup in LDS
-
-template <typename T, typename Less>
-__device__ __forceinline__ void cas_shared(T* s, int i, int l, bool up, Less less) {
-  const T x = s[i], y = s[l];
-  if (up ? less(y, x) : less(x, y)) {
-    s[i] = y;
-    s[l] = x;
-  }
-}
-
-// Full bitonic sort of each `ts`-element tile (ts <= kTile, power of two),
-// with the direction of each stage taken from the global index so that the
-// tiles form bitonic sequences for the global merges.
-template <typename T, typename Less>
-__global__ __launch_bounds__(kTile / 2) void k_bitonic_tile_sort(T* __restrict__ a, int ts, Less less) {
-  __shared__ T s[kTile];
-  const int tid = threadIdx.x;
-  const int half = ts >> 1;
-  const size_t base = (size_t)blockIdx.x * ts;
-  s[tid] = a[base + tid];
-  s[tid + half] = a[base + tid + half];
-  __syncthreads();
-  for (int k = 2; k <= ts; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const int i = 2 * tid - (tid & (j - 1));
-      cas_shared(s, i, i + j, ((base + i) & (size_t)k) == 0, less);
-      __syncthreads();
-    }
-  }
-  a[base + tid] = s[tid];
-  a[base + tid + half] = s[tid + half];
-}
-
-// Stages j = ts/2 .. 1 of merge step k, inside each tile.
-template <typename T, typename Less>
-__global__ __launch_bounds__(kTile / 2) void k_bitonic_tile_merge(T* __restrict__ a, int ts, size_t k, Less less) {
-  __shared__ T s[kTile];
-  const int tid = threadIdx.x;
-  const int half = ts >> 1;
-  const size_t base = (size_t)blockIdx.x * ts;
-  s[tid] = a[base + tid];
-  s[tid + half] = a[base + tid + half];
-  __syncthreads();
-  for (int j = half; j > 0; j >>= 1) {
-    const int i = 2 * tid - (tid & (j - 1));
-    cas_shared(s, i, i + j, ((base + i) & k) == 0, less);
-    __syncthreads();
-  }
-  a[base + tid] = s[tid];
-  a[base + tid + half] = s[tid + half];
-}
-
-// One global stage (k, j) with j >= tile size.
-template <typename T, typename Less>
-__global__ __launch_bounds__(256) void k_bitonic_global(T* __restrict__ a, size_t np, size_t k, size_t j, Less less) {
-  const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= np / 2) return;
-  const size_t i = 2 * t - (t & (j - 1));
-  const size_t l = i + j;
-  const T x = a[i], y = a[l];
-  const bool up = (i & k) == 0;
-  if (up ? less(y, x) : less(x, y)) {
-    a[i] = y;
-    a[l] = x;
-  }
-}
-
-template <typename T, typename Less>
-hipError_t bitonic_sort(T* a, size_t np, Less less, hipStream_t st) {
-  const int ts = (int)std::min<size_t>(np, kTile);
-  const unsigned tiles = (unsigned)(np / ts);
-  hipLaunchKernelGGL((k_bitonic_tile_sort<T, Less>), dim3(tiles), dim3(ts / 2), 0, st, a, ts, less);
-  for (size_t k = (size_t)ts * 2; k <= np; k <<= 1) {
-    for (size_t j = k >> 1; j >= (size_t)ts; j >>= 1) {
-      const unsigned blocks = (unsigned)((np / 2 + 255) / 256);
-      hipLaunchKernelGGL((k_bitonic_global<T, Less>), dim3(blocks), dim3(256), 0, st, a, np, k, j, less);
-    }
-    hipLaunchKernelGGL((k_bitonic_tile_merge<T, Less>), dim3(tiles), dim3(ts / 2), 0, st, a, ts, k, less);
-  }
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------- scans
-// Inclusive scans of int32 with max (forward) or min (reverse direction),
-// three phases: per-tile totals, a scan of the totals, per-tile apply.
-constexpr int kScanThreads = 256;
-constexpr int kScanItems = 16;
-constexpr int kScanTile = kScanThreads * kScanItems;
-
-enum ScanKind { kPrefixMax = 0, kSuffixMin = 1 };
-
-template <int KIND>
-struct ScanOp {
-  static __device__ __forceinline__ int32_t identity() { return KIND == kPrefixMax ? INT32_MIN : INT32_MAX; }
-  static __device__ __forceinline__ int32_t apply(int32_t a, int32_t b) {
-    return KIND == kPrefixMax ? max(a, b) : min(a, b);
-  }
-  // logical position q (scan order) -> array index
-  static __device__ __forceinline__ int64_t at(int64_t q, int64_t m) { return KIND == kPrefixMax ? q : m - 1 - q; }
-};
-
-template <int KIND>
-__device__ int32_t block_exclusive(int32_t v, int32_t* sh, int32_t* total) {
-  using Op = ScanOp<KIND>;
-  const int tid = threadIdx.x;
-  sh[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const int32_t x = tid >= off ? sh[tid - off] : Op::identity();
-    __syncthreads();
-    sh[tid] = Op::apply(sh[tid], x);
-    __syncthreads();
-  }
-  const int32_t excl = tid ? sh[tid - 1] : Op::identity();
-  *total = sh[kScanThreads - 1];
-  __syncthreads();
-  return excl;
-}
-
-template <int KIND>
-__global__ __launch_bounds__(kScanThreads) void k_scan_tiles(const int32_t* __restrict__ in, int64_t m,
-                                                             int32_t* __restrict__ agg) {
-  using Op = ScanOp<KIND>;
-  __shared__ int32_t sh[kScanThreads];
-  const int64_t base = (int64_t)blockIdx.x * kScanTile;
-  int32_t acc = Op::identity();
-  for (int q = threadIdx.x; q < kScanTile; q += kScanThreads) {
-    const int64_t p = base + q;
-    if (p < m) acc = Op::apply(acc, in[Op::at(p, m)]);
-  }
-  int32_t total;
-  block_exclusive<KIND>(acc, sh, &total);
-  if (threadIdx.x == 0) agg[blockIdx.x] = total;
-}
-
-// Exclusive scan of the tile totals in place (one workgroup).
-template <int KIND>
-__global__ __launch_bounds__(kScanThreads) void k_scan_totals(int32_t* __restrict__ agg, int nb) {
-  using Op = ScanOp<KIND>;
-  __shared__ int32_t sh[kScanThreads];
-  int32_t carry = Op::identity();
-  for (int base = 0; base < nb; base += kScanThreads) {
-    const int q = base + threadIdx.x;
-    const int32_t v = q < nb ? agg[q] : Op::identity();
-    int32_t total;
-    const int32_t ex = block_exclusive<KIND>(v, sh, &total);
-    if (q < nb) agg[q] = Op::apply(carry, ex);
-    carry = Op::apply(carry, total);
-  }
-}
-
-template <int KIND>
-__global__ __launch_bounds__(kScanThreads) void k_scan_apply(const int32_t* in, int32_t* out,
-                                                             int64_t m, const int32_t* __restrict__ agg) {
-  using Op = ScanOp<KIND>;
-  __shared__ int32_t tile[kScanTile];
-  __shared__ int32_t sh[kScanThreads];
-  const int64_t base = (int64_t)blockIdx.x * kScanTile;
-  for (int q = threadIdx.x; q < kScanTile; q += kScanThreads) {
-    const int64_t p = base + q;
-    tile[q] = p < m ? in[Op::at(p, m)] : Op::identity();
-  }
-  __syncthreads();
-  const int own = threadIdx.x * kScanItems;
-  int32_t acc = Op::identity();
-  for (int e = 0; e < kScanItems; ++e) acc = Op::apply(acc, tile[own + e]);
-  int32_t total;
-  int32_t run = Op::apply(agg[blockIdx.x], block_exclusive<KIND>(acc, sh, &total));
-  for (int e = 0; e < kScanItems; ++e) {
-    run = Op::apply(run, tile[own + e]);
-    tile[own + e] = run;
-  }
-  __syncthreads();
-  for (int q = threadIdx.x; q < kScanTile; q += kScanThreads) {
-    const int64_t p = base + q;
-    if (p < m) out[Op::at(p, m)] = tile[q];
-  }
-}
-
-int64_t scan_tiles(int64_t m) { return (m + kScanTile - 1) / kScanTile; }
-
-template <int KIND>
-hipError_t inclusive_scan(const int32_t* in, int32_t* out, int64_t m, int32_t* agg, hipStream_t st) {
-  if (m <= 0) return hipSuccess;
-  const unsigned nb = (unsigned)scan_tiles(m);
-  hipLaunchKernelGGL((k_scan_tiles<KIND>), dim3(nb), dim3(kScanThreads), 0, st, in, m, agg);
-  hipLaunchKernelGGL((k_scan_totals<KIND>), dim3(1), dim3(kScanThreads), 0, st, agg, (int)nb);
-  hipLaunchKernelGGL((k_scan_apply<KIND>), dim3(nb), dim3(kScanThreads), 0, st, in, out, m, agg);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------- demand
 __global__ void k_demand_keys(const int32_t* __restrict__ last, int32_t n, uint32_t* __restrict__ keys, size_t np) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < np) keys[i] = i < (size_t)n ? (uint32_t)last[i] : 0xFFFFFFFFu;
 }
 
-__global__ void k_fill(int32_t* __restrict__ a, int64_t m, int32_t v) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < m) a[i] = v;
+// P[c] = #{r : last_node[r] < c} for c in [0, nn]; each thread covers 16
+// consecutive nodes: a binary search for the first, then galloping from one
+// lower bound to the next (long runs of one node cost log steps).
+constexpr int kPrefixRun = 16;
+
+__device__ __forceinline__ int32_t lower_bound_from(const uint32_t* __restrict__ keys, int32_t n, int32_t p, int64_t c) {
+  if (p >= n || (int64_t)keys[p] >= c) return p;
+  int32_t step = 1, lo = p;   // keys[lo] < c
+  while (lo + step < n && (int64_t)keys[lo + step] < c) {
+    lo += step;
+    step <<= 1;
+  }
+  int32_t hi = min(lo + step, n);   // first candidate >= c lies in (lo, hi]
+  ++lo;
+  while (lo < hi) {
+    const int32_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)keys[mid] < c) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
 }
 
-// first occurrence of each value in the sorted keys: Q[value] = position
-__global__ void k_demand_mark(const uint32_t* __restrict__ keys, int32_t n, uint32_t nn, int32_t* __restrict__ q) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n && keys[i] < nn && (i == 0 || keys[i] != keys[i - 1])) q[keys[i]] = i;
+__global__ void k_demand_prefix(const uint32_t* __restrict__ keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
+  const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kPrefixRun;
+  if (c0 > nn) return;
+  int32_t lo = 0, hi = n;
+  while (lo < hi) {
+    const int32_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)keys[mid] < c0) lo = mid + 1;
+    else hi = mid;
+  }
+  int32_t p = lo;
+  const int64_t c1 = min<int64_t>(c0 + kPrefixRun - 1, nn);
+  P[c0] = p;
+  for (int64_t c = c0 + 1; c <= c1; ++c) {
+    p = lower_bound_from(keys, n, p, c);
+    P[c] = p;
+  }
 }
 
-__global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, const int32_t* __restrict__ p,
+__global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, const int32_t* __restrict__ P,
                               int32_t* __restrict__ demand) {
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c < nn) demand[c] = p[nodes[c].subtree_end] - p[c];
+  if (c < nn) demand[c] = P[nodes[c].subtree_end] - P[c];
 }
 
 // ---------------------------------------------------------------- clusters
-constexpr int kSideShift = 62;
-constexpr int kEllShift = 33;
-constexpr uint64_t kEllMax = (1ull << 29) - 1;
-constexpr uint64_t kTokMask = (1ull << 33) - 1;
-constexpr uint64_t kHeadKey = 1ull << kSideShift;
+// Sort element. hi = (group << 32) | l, where the group is the anchor node
+// (first stage) or the segment start (refinement), and l the match length /
+// first mismatch with the head (0xFFFFFFFF for the head itself).
+// lo = (next-token code << 31) | (kLenMax - len): code 0 means the prompt
+// ended there; longer prompts first inside a group (the next head).
+struct ClElem {
+  uint64_t hi;
+  uint64_t lo;
+  uint32_t req;
+  uint32_t len;
+};
 
-// Refinement key of a member relative to the head:
-//   left of the head  (0, l, x+1)   ascending l, then token; x = 0 when the member ended
-//   the head and its duplicates  (1, 0, 0)
-//   right of the head (2, max-l, x+1)  descending l, then token
+struct ClLess {
+  __device__ __forceinline__ bool operator()(const ClElem& a, const ClElem& b) const {
+    return a.hi < b.hi || (a.hi == b.hi && a.lo < b.lo);
+  }
+};
+
+constexpr uint64_t kLenMax = 0x7FFFFFFFull;
+constexpr uint32_t kHeadL = 0xFFFFFFFFu;
+
 __device__ __forceinline__ uint64_t tok_code(int32_t x) { return (uint64_t)((uint32_t)x ^ 0x80000000u) + 1; }
-
-__device__ __forceinline__ int32_t key_ell(uint64_t key) {
-  const uint64_t side = key >> kSideShift;
-  const uint64_t f = (key >> kEllShift) & kEllMax;
-  if (side == 0) return (int32_t)f;
-  if (side == 2) return (int32_t)(kEllMax - f);
-  return INT32_MAX / 2;   // head group: deeper than any member
+__device__ __forceinline__ uint64_t lo_of(uint64_t code, uint32_t len) { return (code << 31) | (kLenMax - len); }
+__device__ __forceinline__ uint64_t code_of(uint64_t lo) { return lo >> 31; }
+__device__ __forceinline__ uint32_t ell_of(uint64_t hi) { return (uint32_t)hi; }
+__device__ __forceinline__ bool same_group(const ClElem& a, const ClElem& b) {
+  return a.hi == b.hi && code_of(a.lo) == code_of(b.lo);
+}
+__device__ __forceinline__ bool group_less(const ClElem& a, uint64_t hi, uint64_t code) {
+  return a.hi < hi || (a.hi == hi && code_of(a.lo) < code);
 }
 
-__global__ void k_cl_init(const int64_t* __restrict__ offsets, int32_t n, SortElem* __restrict__ el, size_t np,
-                          int32_t* __restrict__ lcp, int32_t* __restrict__ depth, uint8_t* __restrict__ active) {
+// Minimum of a[lo..hi] (inclusive) using 64-wide block minima and a sparse
+// table over the blocks (levels of nb entries each).
+__device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, const int32_t* __restrict__ st,
+                                                 int32_t nb, int32_t lo, int32_t hi) {
+  int32_t m = INT32_MAX;
+  const int32_t bl = lo >> 6, bh = hi >> 6;
+  if (bl == bh) {
+    for (int32_t v = lo; v <= hi; ++v) m = min(m, a[v]);
+    return m;
+  }
+  for (int32_t v = lo; v < (bl + 1) << 6; ++v) m = min(m, a[v]);
+  for (int32_t v = bh << 6; v <= hi; ++v) m = min(m, a[v]);
+  if (bh - bl >= 2) {
+    const int32_t x = bl + 1, y = bh - 1;
+    const int k = 31 - __clz(y - x + 1);
+    m = min(m, min(st[(int64_t)k * nb + x], st[(int64_t)k * nb + y - (1 << k) + 1]));
+  }
+  return m;
+}
+
+__global__ void k_anchor_keys(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets, int32_t n,
+                              const int32_t* __restrict__ last, const int32_t* __restrict__ mlen, ClElem* __restrict__ el,
+                              size_t np, int32_t* __restrict__ lcp) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < np) {
-    SortElem e;
+    ClElem e;
     if (i < (size_t)n) {
-      e.key = 0;
-      e.seg = 0;
-      e.nlen = ~(uint32_t)(offsets[i + 1] - offsets[i]);
+      const int64_t o = offsets[i];
+      const uint32_t len = (uint32_t)(offsets[i + 1] - o);
+      const uint32_t c = last ? (uint32_t)last[i] : 0u;
+      const uint32_t m = mlen ? (uint32_t)mlen[i] : 0u;
+      const uint64_t code = m < len ? tok_code(tokens[o + m]) : 0;
+      e.hi = ((uint64_t)c << 32) | m;
+      e.lo = lo_of(code, len);
       e.req = (uint32_t)i;
+      e.len = len;
     } else {
-      e.key = ~0ull;
-      e.seg = 0xFFFFFFFFu;
-      e.nlen = 0xFFFFFFFFu;
+      e.hi = ~0ull;
+      e.lo = ~0ull;
       e.req = 0xFFFFFFFFu;
+      e.len = 0;
     }
-    e.pad = 0;
     el[i] = e;
   }
   if (i <= (size_t)n) lcp[i] = 0;
-  if (i == 0) {
-    depth[0] = 0;
-    active[0] = n >= 2;
+}
+
+// Start of every lane's group, for the 64 sorted positions base..base+63 of
+// this wavefront: the nearest group start at or before the lane inside the
+// wave, or, for lanes whose group began earlier, one shared wave search
+// over [search_lo, base]. `start` marks lanes whose position opens a group.
+__device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ el, int32_t base, int lane, bool start,
+                                                    bool need_search, int32_t search_lo) {
+  const uint64_t mask = __ballot(start);
+  const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
+  const uint64_t below = mask & upto;
+  int32_t g0 = base;
+  if (need_search) {
+    const uint64_t h = el[base].hi, c = code_of(el[base].lo);
+    g0 = wave_first_true(search_lo, base, lane, [&](int32_t p) { return !group_less(el[p], h, c); });
+  }
+  return below ? base + (63 - __clzll((unsigned long long)below)) : g0;
+}
+
+// Groups of equal (node, match length, next token) after the anchor sort.
+// flags[0] is raised if any group needs refinement, flags[1] if such a
+// group has more than 64 members.
+__global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el,
+                                                       const NodeRec* __restrict__ nodes,
+                                                       const int32_t* __restrict__ pdep,
+                                                       const int32_t* __restrict__ pdep_st, int32_t pdep_nb,
+                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ depth,
+                                                       uint8_t* __restrict__ active, int32_t* __restrict__ lcp,
+                                                       int32_t* __restrict__ flags) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
+  if (base >= n) return;
+  const int32_t i = base + lane;
+  const bool valid = i < n;
+  ClElem e{};
+  bool start = false;
+  if (valid) {
+    e = el[i];
+    start = i == 0 || !same_group(el[i - 1], e);
+  }
+  const bool lane0_start = __ballot(start) & 1ull;
+  const int32_t g = lane_group_start(el, base, lane, start, !lane0_start, 0);
+  if (!valid) return;
+  nseg[i] = g;
+  const uint32_t m = (uint32_t)e.hi;
+  const uint64_t code = code_of(e.lo);
+  if (i == g) {
+    if (i > 0) {
+      const ClElem p = el[i - 1];
+      const uint32_t c1 = (uint32_t)(p.hi >> 32), m1 = (uint32_t)p.hi;
+      const uint32_t c2 = (uint32_t)(e.hi >> 32);
+      int32_t v;
+      if (c1 == c2) v = (int32_t)min(m1, m);
+      else if (c2 < (uint32_t)nodes[c1].subtree_end) v = (int32_t)m1;
+      else v = range_min_i32(pdep, pdep_st, pdep_nb, (int32_t)c1 + 1, (int32_t)c2);
+      lcp[i] = v;
+    }
+    const bool act = code != 0 && i + 1 < n && same_group(el[i + 1], e);
+    active[i] = act;
+    depth[i] = act ? (int32_t)m + 1 : 0;
+    if (act) {
+      flags[0] = 1;
+      if (i + kWave < n && same_group(el[i + kWave], e)) flags[1] = 1;
+    }
+  } else if (code == 0) {
+    lcp[i] = (int32_t)m;   // identical prompts of length m
   }
 }
 
-// One wavefront per position: compare the member with its segment's head
-// from the segment's common depth and store its refinement key.
-__global__ __launch_bounds__(256) void k_cl_compare(const int32_t* __restrict__ tokens,
-                                                    const int64_t* __restrict__ offsets, int32_t n,
-                                                    SortElem* __restrict__ el, const int32_t* __restrict__ depth,
-                                                    const uint8_t* __restrict__ active) {
+// One wavefront per position: rewrite every element's key for the next sort;
+// members of active segments are compared with their segment's head.
+__global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
+                                                        const int64_t* __restrict__ offsets, int32_t n,
+                                                        ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
+                                                        const int32_t* __restrict__ depth,
+                                                        const uint8_t* __restrict__ active) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (i >= n) return;
-  const uint32_t s = el[i].seg;
-  if (!active[s]) return;
-  uint64_t key = kHeadKey;
-  if ((uint32_t)i != s) {
+  const int32_t s = nseg[i];
+  if (!active[s]) {
+    if (lane == 0) el[i].hi = (uint64_t)(uint32_t)s << 32;
+    return;
+  }
+  const uint32_t len_j = el[i].len;
+  uint32_t ell = kHeadL;
+  uint64_t code = 0;
+  if (i != s) {
     const int32_t d = depth[s];
     const uint32_t j = el[i].req, h = el[s].req;
-    const int64_t oj = offsets[j], oh = offsets[h];
-    const int32_t lj = (int32_t)(offsets[j + 1] - oj), lh = (int32_t)(offsets[h + 1] - oh);
-    const int32_t* __restrict__ pj = tokens + oj + d;
-    const int32_t* __restrict__ ph = tokens + oh + d;
-    const int32_t lim = min(lj, lh) - d;
-    int32_t ell = lim;
+    const uint32_t len_h = el[s].len;
+    const int32_t* __restrict__ pj = tokens + offsets[j] + d;
+    const int32_t* __restrict__ ph = tokens + offsets[h] + d;
+    const int32_t lim = (int32_t)min(len_j, len_h) - d;
+    int32_t l = lim;
     for (int32_t base = 0; base < lim; base += kWave * 4) {
       int32_t va[4], vb[4];
 #pragma unroll
@@ -355,137 +309,234 @@ __global__ __launch_bounds__(256) void k_cl_compare(const int32_t* __restrict__ 
         const int32_t k = base + u * kWave + lane;
         const uint64_t mm = __ballot(k < lim && va[u] != vb[u]);
         if (mm && !found) {
-          ell = base + u * kWave + (int32_t)__ffsll((unsigned long long)mm) - 1;
+          l = base + u * kWave + (int32_t)__ffsll((unsigned long long)mm) - 1;
           found = true;
         }
       }
       if (found) break;
     }
-    if (ell == lim) {
-      // the member ran out first (it is no longer than the head)
-      key = (lj == lh) ? kHeadKey : ((uint64_t)ell << kEllShift);
-    } else {
-      const int32_t x = pj[ell], y = ph[ell];
-      key = (x < y) ? (((uint64_t)ell << kEllShift) | tok_code(x))
-                    : ((2ull << kSideShift) | ((kEllMax - (uint64_t)ell) << kEllShift) | tok_code(x));
+    ell = (uint32_t)l;
+    code = l < lim ? tok_code(pj[l]) : 0;   // 0: the member ended (the head is the longest)
+  }
+  if (lane == 0) {
+    el[i].hi = ((uint64_t)(uint32_t)s << 32) | ell;
+    el[i].lo = lo_of(code, len_j);
+  }
+}
+
+// Sorts every active segment of at most 64 members in place, one wavefront
+// per segment (stable rank by comparison with every other member).
+__global__ __launch_bounds__(256) void k_refine_small_sort(int32_t n, ClElem* __restrict__ el,
+                                                           const int32_t* __restrict__ nseg,
+                                                           const uint8_t* __restrict__ active) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t s = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
+  if (s >= n || nseg[s] != s || !active[s]) return;
+  const int32_t i = s + lane;
+  const bool mine = i < n && nseg[i] == s;
+  const int size = __popcll(__ballot(mine));
+  ClElem e{};
+  if (lane < size) e = el[i];
+  int rank = 0;
+  const ClLess less;
+  for (int j = 0; j < size; ++j) {
+    ClElem o;
+    o.hi = __shfl(e.hi, j);
+    o.lo = __shfl(e.lo, j);
+    if (less(o, e) || (j < lane && !less(e, o))) ++rank;
+  }
+  if (lane < size) el[s + rank] = e;
+}
+
+// After the refinement sort: new groups, their LCPs, depths and activity.
+__global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* __restrict__ el,
+                                                       int32_t* __restrict__ nseg,
+                                                       const int32_t* __restrict__ depth_old,
+                                                       const uint8_t* __restrict__ active_old,
+                                                       int32_t* __restrict__ depth_new,
+                                                       uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
+                                                       int32_t* __restrict__ flags) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
+  if (base >= n) return;
+  const int32_t i = base + lane;
+  const bool valid = i < n;
+  ClElem e{};
+  int32_t s = 0;
+  bool live = false, start = false;
+  if (valid) {
+    e = el[i];
+    s = (int32_t)(e.hi >> 32);
+    live = active_old[s] != 0;
+    start = live && (i == s || !same_group(el[i - 1], e));
+  }
+  // lanes of a live group that began before this wave share one search
+  const bool lane0_needs = __shfl(live && !start, 0);
+  const int32_t s0 = __shfl(s, 0);
+  const int32_t g = lane_group_start(el, base, lane, start, lane0_needs, s0);
+  if (!valid) return;
+  if (!live) {
+    if (i == s) {
+      active_new[i] = 0;
+      depth_new[i] = depth_old[i];
     }
-  }
-  if (lane == 0) el[i].key = key;
-}
-
-// After sorting: mark group starts (gval = position, else 0) and record the
-// LCP across every new group boundary and inside groups of identical prompts.
-__global__ void k_cl_groups(int32_t n, const SortElem* __restrict__ el, const int32_t* __restrict__ depth,
-                            const uint8_t* __restrict__ active, int32_t* __restrict__ lcp,
-                            int32_t* __restrict__ gval) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const SortElem e = el[i];
-  const uint32_t s = e.seg;
-  if (!active[s]) {
-    gval[i] = ((uint32_t)i == s) ? i : 0;
     return;
   }
-  const int32_t d = depth[s];
-  const bool start = (uint32_t)i == s || el[i - 1].key != e.key;
-  gval[i] = start ? i : 0;
-  if (start) {
-    if ((uint32_t)i != s) lcp[i] = d + min(key_ell(el[i - 1].key), key_ell(e.key));
-  } else {
-    const uint64_t side = e.key >> kSideShift;
-    if (side == 1) lcp[i] = (int32_t)~e.nlen;                                   // duplicate of the head
-    else if (side == 0 && (e.key & kTokMask) == 0) lcp[i] = d + key_ell(e.key);  // identical, ended
-  }
-}
-
-// With gstart[i] = start of i's new group: record the new segments' depth
-// and whether they still need refining; raise *more if any does.
-__global__ void k_cl_finish(int32_t n, SortElem* __restrict__ el, const int32_t* __restrict__ gstart,
-                            const int32_t* __restrict__ depth_old, const uint8_t* __restrict__ active_old,
-                            int32_t* __restrict__ depth_new, uint8_t* __restrict__ active_new,
-                            int32_t* __restrict__ more) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const SortElem e = el[i];
-  const uint32_t s = e.seg;
-  if (!active_old[s]) {
-    if ((uint32_t)i == s) active_new[i] = 0;
-    return;
-  }
-  const int32_t g = gstart[i];
-  if (g == i) {
-    const uint64_t side = e.key >> kSideShift;
-    const bool token_group = side == 2 || (side == 0 && (e.key & kTokMask) != 0);
-    const bool pair = i + 1 < n && gstart[i + 1] == i;
-    const bool act = token_group && pair;
+  const int32_t d = depth_old[s];
+  nseg[i] = g;
+  const uint32_t ell = ell_of(e.hi);
+  const uint64_t code = code_of(e.lo);
+  if (i == g) {
+    if (i > s) lcp[i] = d + (int32_t)min(ell_of(el[i - 1].hi), ell);
+    const bool act = ell != kHeadL && code != 0 && i + 1 < n && same_group(el[i + 1], e);
     active_new[i] = act;
-    depth_new[i] = act ? depth_old[s] + key_ell(e.key) + 1 : 0;
-    if (act) *more = 1;
+    depth_new[i] = act ? d + (int32_t)ell + 1 : 0;
+    if (act) {
+      flags[0] = 1;
+      if (i + kWave < n && same_group(el[i + kWave], e)) flags[1] = 1;
+    }
+  } else if (code == 0 && ell != kHeadL) {
+    lcp[i] = d + (int32_t)ell;   // identical prompts that ended together
   }
-  el[i].seg = (uint32_t)g;
 }
 
-__global__ void k_cl_share(int32_t n, const SortElem* __restrict__ el, const int32_t* __restrict__ lcp,
-                           int32_t* __restrict__ st1, uint64_t* __restrict__ st2) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i <= n) st1[i] = lcp[i];
+// share, the (share, request) key of every position, its in-block prefix and
+// suffix minima, and the 64-wide block minima of lcp and of the key.
+__global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* __restrict__ el,
+                                                      const int32_t* __restrict__ lcp, uint64_t* __restrict__ key2,
+                                                      uint64_t* __restrict__ pmin2, uint64_t* __restrict__ smin2,
+                                                      int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
+                                                      int32_t nb1, int32_t nb2) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
+  const int32_t i = b * kWave + lane;
+  int32_t v1 = INT32_MAX;
+  uint64_t v2 = ~0ull;
+  if (i <= n) v1 = lcp[i];
   if (i < n) {
     const int32_t share = max(lcp[i], lcp[i + 1]);
-    st2[i] = ((uint64_t)(uint32_t)share << 32) | el[i].req;
+    v2 = ((uint64_t)(uint32_t)share << 32) | el[i].req;
+    key2[i] = v2;
+  }
+  uint64_t pre = v2, suf = v2;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint64_t a = __shfl_up(pre, off);
+    if (lane >= off && a < pre) pre = a;
+    const uint64_t c = __shfl_down(suf, off);
+    if (lane + off < kWave && c < suf) suf = c;
+  }
+  if (i < n) {
+    pmin2[i] = pre;
+    smin2[i] = suf;
+  }
+  for (int off = 32; off > 0; off >>= 1) v1 = min(v1, __shfl_xor(v1, off));
+  if (lane == 0) {
+    if (b < nb1) st1[b] = v1;
+    if (b < nb2) st2[b] = suf;
   }
 }
 
-// Sparse-table level k from level k-1 (range minima over 2^k entries).
-__global__ void k_cl_level(int32_t* __restrict__ st1, uint64_t* __restrict__ st2, int32_t n, int k) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t w1 = (int64_t)n + 1, w2 = n;
-  const int32_t h = 1 << (k - 1);
-  const int32_t* a1 = st1 + (k - 1) * w1;
-  const uint64_t* a2 = st2 + (k - 1) * w2;
-  if ((int64_t)i + 2 * h <= w1) st1[k * w1 + i] = min(a1[i], a1[i + h]);
-  if ((int64_t)i + 2 * h <= w2) st2[k * w2 + i] = min(a2[i], a2[i + h]);
+// Sparse tables over the block minima, one workgroup, level by level.
+__global__ __launch_bounds__(1024) void k_final_tables(int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
+                                                       int32_t nb1, int32_t nb2, int levels) {
+  for (int k = 1; k < levels; ++k) {
+    const int32_t h = 1 << (k - 1);
+    for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) {
+      if (b + 2 * h <= nb1)
+        st1[(int64_t)k * nb1 + b] = min(st1[(int64_t)(k - 1) * nb1 + b], st1[(int64_t)(k - 1) * nb1 + b + h]);
+      if (b + 2 * h <= nb2) {
+        const uint64_t x = st2[(int64_t)(k - 1) * nb2 + b], y = st2[(int64_t)(k - 1) * nb2 + b + h];
+        st2[(int64_t)k * nb2 + b] = x < y ? x : y;
+      }
+    }
+    __syncthreads();
+  }
 }
 
-__global__ void k_cl_query(int32_t n, int32_t levels, int32_t threshold, const SortElem* __restrict__ el,
-                           const int32_t* __restrict__ st1, const uint64_t* __restrict__ st2,
-                           int32_t* __restrict__ cid, int32_t* __restrict__ csz) {
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+
+__global__ void k_final_query(int32_t n, int32_t threshold, const int32_t* __restrict__ lcp,
+                              const uint64_t* __restrict__ key2, const uint64_t* __restrict__ pmin2,
+                              const uint64_t* __restrict__ smin2, const int32_t* __restrict__ st1,
+                              const uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2, int levels,
+                              int32_t* __restrict__ cid, int32_t* __restrict__ csz) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  const int64_t w1 = (int64_t)n + 1, w2 = n;
-  const uint64_t own = st2[i];
-  const int32_t share = (int32_t)(own >> 32);
+  const uint64_t own = key2[i];
+  const int32_t s = (int32_t)(own >> 32);
   const uint32_t req = (uint32_t)own;
-  if (share < threshold) {
+  if (s < threshold) {
     cid[req] = -1;
     csz[req] = 1;
     return;
   }
-  int32_t L = i;   // lcp[L+1..i] >= share, lcp[L] < share
-  for (int k = levels - 1; k >= 0; --k) {
-    const int32_t w = 1 << k;
-    if (L - w + 1 >= 0 && st1[k * w1 + (L - w + 1)] >= share) L -= w;
+  // L: the last j <= i with lcp[j] < s (lcp[0] = 0 < s, so it exists)
+  int32_t L = -1;
+  for (int32_t j = i; j >= (i & ~63); --j)
+    if (lcp[j] < s) {
+      L = j;
+      break;
+    }
+  if (L < 0) {
+    int32_t pos = (i >> 6) - 1;   // the last block <= pos whose minimum is < s
+    for (int k = levels - 1; k >= 0; --k) {
+      const int32_t w = 1 << k;
+      if (pos - w + 1 >= 0 && st1[(int64_t)k * nb1 + pos - w + 1] >= s) pos -= w;
+    }
+    for (int32_t j = (pos << 6) + 63; j >= (pos << 6); --j)
+      if (j <= n && lcp[j] < s) {
+        L = j;
+        break;
+      }
   }
-  int32_t R = i + 1;   // lcp[i+1..R-1] >= share, lcp[R] < share
-  for (int k = levels - 1; k >= 0; --k) {
-    const int32_t w = 1 << k;
-    if ((int64_t)R + w - 1 <= n && st1[k * w1 + R] >= share) R += w;
+  // R: the first j > i with lcp[j] < s (lcp[n] = 0 < s)
+  int32_t R = -1;
+  const int32_t bend = min(((i >> 6) << 6) + 63, n);
+  for (int32_t j = i + 1; j <= bend; ++j)
+    if (lcp[j] < s) {
+      R = j;
+      break;
+    }
+  if (R < 0) {
+    int32_t pos = (i >> 6) + 1;   // the first block >= pos whose minimum is < s
+    for (int k = levels - 1; k >= 0; --k) {
+      const int32_t w = 1 << k;
+      if (pos + w <= nb1 && st1[(int64_t)k * nb1 + pos] >= s) pos += w;
+    }
+    for (int32_t j = pos << 6; j <= n; ++j)
+      if (lcp[j] < s) {
+        R = j;
+        break;
+      }
   }
-  const int32_t span = R - L;
-  const int k = 31 - __clz(span);
-  const uint64_t m = min(st2[k * w2 + L], st2[k * w2 + (R - (1 << k))]);
+  // id: minimum of (share, request) over [L, R)
+  const int32_t hi = R - 1;
+  const int32_t bl = L >> 6, bh = hi >> 6;
+  uint64_t m;
+  if (bl == bh) {
+    m = ~0ull;
+    for (int32_t v = L; v <= hi; ++v) m = umin64(m, key2[v]);
+  } else {
+    m = umin64(smin2[L], pmin2[hi]);
+    if (bh - bl >= 2) {
+      const int32_t x = bl + 1, y = bh - 1;
+      const int k = 31 - __clz(y - x + 1);
+      m = umin64(m, umin64(st2[(int64_t)k * nb2 + x], st2[(int64_t)k * nb2 + y - (1 << k) + 1]));
+    }
+  }
   cid[req] = (int32_t)(uint32_t)m;
-  csz[req] = span;
+  csz[req] = R - L;
 }
 
 size_t np_of(int32_t n) {
-  size_t np = 2;
+  size_t np = msort::kTile;
   while (np < (size_t)n) np <<= 1;
   return np;
 }
 
-int levels_of(int32_t n) {
+int levels_for(int64_t nb) {
   int k = 1;
-  while ((int64_t(1) << k) <= (int64_t)n + 1) ++k;
+  while ((int64_t(1) << k) <= nb) ++k;
   return k;
 }
 
@@ -493,33 +544,42 @@ size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
-  size_t elems, depth_a, depth_b, active_a, active_b, lcp, gval, agg, st1, st2, flag, keys, q, total;
+  size_t el_a, el_b, nseg, depth_a, depth_b, active_a, active_b, lcp, key2, pmin2, smin2, st1, st2, flags, keys_a,
+      keys_b, prefix, total;
+  int32_t nb1, nb2;
+  int levels;
 };
 
 Layout layout(int32_t n, int64_t num_nodes) {
   Layout L{};
   const size_t np = np_of(n);
-  const int lv = levels_of(n);
+  const size_t nn = (size_t)std::max<int32_t>(n, 1);
+  L.nb1 = (int32_t)(((int64_t)n + 1 + 63) / 64);
+  L.nb2 = (int32_t)std::max<int64_t>(1, ((int64_t)n + 63) / 64);
+  L.levels = levels_for(std::max(L.nb1, L.nb2));
   size_t o = 0;
   auto take = [&](size_t bytes) {
     const size_t at = o;
     o += a256(bytes);
     return at;
   };
-  L.elems = take(sizeof(SortElem) * np);
-  L.depth_a = take(sizeof(int32_t) * (size_t)std::max(n, 1));
-  L.depth_b = take(sizeof(int32_t) * (size_t)std::max(n, 1));
-  L.active_a = take((size_t)std::max(n, 1));
-  L.active_b = take((size_t)std::max(n, 1));
+  L.el_a = take(sizeof(ClElem) * np);
+  L.el_b = take(sizeof(ClElem) * np);
+  L.nseg = take(sizeof(int32_t) * nn);
+  L.depth_a = take(sizeof(int32_t) * nn);
+  L.depth_b = take(sizeof(int32_t) * nn);
+  L.active_a = take(nn);
+  L.active_b = take(nn);
   L.lcp = take(sizeof(int32_t) * ((size_t)n + 1));
-  L.gval = take(sizeof(int32_t) * (size_t)std::max(n, 1));
-  const int64_t scan_len = std::max<int64_t>((int64_t)n, num_nodes + 1);
-  L.agg = take(sizeof(int32_t) * (size_t)scan_tiles(scan_len));
-  L.st1 = take(sizeof(int32_t) * (size_t)lv * ((size_t)n + 1));
-  L.st2 = take(sizeof(uint64_t) * (size_t)lv * (size_t)std::max(n, 1));
-  L.flag = take(sizeof(int32_t));
-  L.keys = take(sizeof(uint32_t) * np);
-  L.q = take(sizeof(int32_t) * (size_t)(num_nodes + 1));
+  L.key2 = take(sizeof(uint64_t) * nn);
+  L.pmin2 = take(sizeof(uint64_t) * nn);
+  L.smin2 = take(sizeof(uint64_t) * nn);
+  L.st1 = take(sizeof(int32_t) * (size_t)L.levels * L.nb1);
+  L.st2 = take(sizeof(uint64_t) * (size_t)L.levels * L.nb2);
+  L.flags = take(sizeof(int32_t) * 2);
+  L.keys_a = take(sizeof(uint32_t) * np);
+  L.keys_b = take(sizeof(uint32_t) * np);
+  L.prefix = take(sizeof(int32_t) * (size_t)(num_nodes + 1));
   L.total = o;
   return L;
 }
@@ -534,73 +594,88 @@ peek_status run_demand(const DeviceTree& t, int32_t n, const int32_t* last_node,
                        size_t ws_bytes, hipStream_t st) {
   const Layout L = layout(n, t.num_nodes);
   char* w = (char*)ws;
-  const int64_t nn = t.num_nodes;
-  int32_t* q = (int32_t*)(w + L.q);
-  int32_t* agg = (int32_t*)(w + L.agg);
+  const int32_t nn = t.num_nodes;
+  int32_t* P = (int32_t*)(w + L.prefix);
+  const size_t np = np_of(n);
+  uint32_t* ka = (uint32_t*)(w + L.keys_a);
+  uint32_t* kb = (uint32_t*)(w + L.keys_b);
+  const uint32_t* keys = ka;
   if (n > 0) {
-    const size_t np = np_of(n);
-    uint32_t* keys = (uint32_t*)(w + L.keys);
-    hipLaunchKernelGGL(k_demand_keys, dim3(blocks_for(np)), dim3(256), 0, st, last_node, n, keys, np);
-    PEEK_HIP_TRY(bitonic_sort(keys, np, U32Less{}, st));
-    hipLaunchKernelGGL(k_fill, dim3(blocks_for(nn + 1)), dim3(256), 0, st, q, nn + 1, n);
-    hipLaunchKernelGGL(k_demand_mark, dim3(blocks_for(n)), dim3(256), 0, st, keys, n, (uint32_t)nn, q);
-  } else {
-    hipLaunchKernelGGL(k_fill, dim3(blocks_for(nn + 1)), dim3(256), 0, st, q, nn + 1, 0);
+    hipLaunchKernelGGL(k_demand_keys, dim3(blocks_for(np)), dim3(256), 0, st, last_node, n, ka, np);
+    keys = msort::sort(ka, kb, np, U32Less{}, st);
   }
-  PEEK_HIP_TRY(inclusive_scan<kSuffixMin>(q, q, nn + 1, agg, st));
-  hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, (int32_t)nn, q, demand);
+  hipLaunchKernelGGL(k_demand_prefix, dim3(blocks_for((int64_t)nn / kPrefixRun + 1)), dim3(256), 0, st, keys, n, nn,
+                     P);
+  hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }
 
-peek_status run_clusters(int32_t n, const int32_t* tokens, const int64_t* offsets, int32_t threshold, int32_t* cid,
+peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
                          int32_t* csz, int64_t num_nodes, void* ws, size_t ws_bytes, hipStream_t st) {
   const Layout L = layout(n, num_nodes);
   char* w = (char*)ws;
   const size_t np = np_of(n);
-  SortElem* el = (SortElem*)(w + L.elems);
+  ClElem* el_a = (ClElem*)(w + L.el_a);
+  ClElem* el_b = (ClElem*)(w + L.el_b);
+  int32_t* nseg = (int32_t*)(w + L.nseg);
   int32_t* depth_a = (int32_t*)(w + L.depth_a);
   int32_t* depth_b = (int32_t*)(w + L.depth_b);
   uint8_t* active_a = (uint8_t*)(w + L.active_a);
   uint8_t* active_b = (uint8_t*)(w + L.active_b);
   int32_t* lcp = (int32_t*)(w + L.lcp);
-  int32_t* gval = (int32_t*)(w + L.gval);
-  int32_t* agg = (int32_t*)(w + L.agg);
+  uint64_t* key2 = (uint64_t*)(w + L.key2);
+  uint64_t* pmin2 = (uint64_t*)(w + L.pmin2);
+  uint64_t* smin2 = (uint64_t*)(w + L.smin2);
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
-  int32_t* flag = (int32_t*)(w + L.flag);
+  int32_t* flags = (int32_t*)(w + L.flags);
 
-  hipLaunchKernelGGL(k_cl_init, dim3(blocks_for((int64_t)np + 1)), dim3(256), 0, st, offsets, n, el, np, lcp,
-                     depth_a, active_a);
-  PEEK_HIP_TRY(bitonic_sort(el, np, ElemLess{}, st));   // longest prompt first: the first head
-  bool more = n >= 2;
-  // Every round makes each still-active segment strictly deeper, so the
-  // loop ends after at most (longest prompt + 1) rounds; the cap only turns
-  // a broken invariant into an error instead of an endless loop.
+  // anchoring needs the walk's results and the cache they refer to
+  const bool anchored = t != nullptr && last_node != nullptr && match_len != nullptr;
+  PEEK_HIP_TRY(hipMemsetAsync(flags, 0, sizeof(int32_t) * 2, st));
+  hipLaunchKernelGGL(k_anchor_keys, dim3(blocks_for((int64_t)np + 1)), dim3(256), 0, st, tokens, offsets, n,
+                     anchored ? last_node : nullptr, anchored ? match_len : nullptr, el_a, np, lcp);
+  ClElem* el = msort::sort(el_a, el_b, np, ClLess{}, st);
+  ClElem* other = el == el_a ? el_b : el_a;
+  const unsigned wave_blocks = blocks_for(n, 4 * kWave);
+  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, anchored ? t->nodes : nullptr,
+                     anchored ? t->pdep : nullptr, anchored ? t->pdep_st : nullptr, anchored ? t->pdep_nb : 0, nseg,
+                     depth_a, active_a, lcp, flags);
+  int32_t h_flags[2] = {0, 0};
+  PEEK_HIP_TRY(hipMemcpyAsync(h_flags, flags, sizeof(h_flags), hipMemcpyDeviceToHost, st));
+  PEEK_HIP_TRY(hipStreamSynchronize(st));
+  // Every round makes each still-active segment strictly deeper, so the loop
+  // ends after at most (longest prompt + 1) rounds; the cap only turns a
+  // broken invariant into an error instead of an endless loop.
   int64_t rounds = 0;
-  constexpr int64_t kMaxRounds = int64_t(1) << 29;
-  while (more) {
+  constexpr int64_t kMaxRounds = int64_t(1) << 31;
+  while (h_flags[0]) {
     if (++rounds > kMaxRounds) return fail(PEEK_ERR_DEVICE, "cluster refinement did not converge");
-    PEEK_HIP_TRY(hipMemsetAsync(flag, 0, sizeof(int32_t), st));
-    hipLaunchKernelGGL(k_cl_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, depth_a,
-                       active_a);
-    PEEK_HIP_TRY(bitonic_sort(el, np, ElemLess{}, st));
-    hipLaunchKernelGGL(k_cl_groups, dim3(blocks_for(n)), dim3(256), 0, st, n, el, depth_a, active_a, lcp, gval);
-    PEEK_HIP_TRY(inclusive_scan<kPrefixMax>(gval, gval, n, agg, st));
-    hipLaunchKernelGGL(k_cl_finish, dim3(blocks_for(n)), dim3(256), 0, st, n, el, gval, depth_a, active_a, depth_b,
-                       active_b, flag);
-    int32_t h_flag = 0;
-    PEEK_HIP_TRY(hipMemcpyAsync(&h_flag, flag, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    const bool big = h_flags[1] != 0;
+    PEEK_HIP_TRY(hipMemsetAsync(flags, 0, sizeof(int32_t) * 2, st));
+    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg,
+                       depth_a, active_a);
+    if (big) {
+      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st);
+      other = sorted == el ? other : el;
+      el = sorted;
+    } else {
+      hipLaunchKernelGGL(k_refine_small_sort, dim3(blocks_for(n, 4)), dim3(256), 0, st, n, el, nseg, active_a);
+    }
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, depth_a, active_a, depth_b,
+                       active_b, lcp, flags);
+    PEEK_HIP_TRY(hipMemcpyAsync(h_flags, flags, sizeof(h_flags), hipMemcpyDeviceToHost, st));
     PEEK_HIP_TRY(hipStreamSynchronize(st));
     std::swap(depth_a, depth_b);
     std::swap(active_a, active_b);
-    more = h_flag != 0;
   }
-  const int lv = levels_of(n);
-  hipLaunchKernelGGL(k_cl_share, dim3(blocks_for((int64_t)n + 1)), dim3(256), 0, st, n, el, lcp, st1, st2);
-  for (int k = 1; k < lv; ++k)
-    hipLaunchKernelGGL(k_cl_level, dim3(blocks_for((int64_t)n + 1)), dim3(256), 0, st, st1, st2, n, k);
-  hipLaunchKernelGGL(k_cl_query, dim3(blocks_for(n)), dim3(256), 0, st, n, lv, threshold, el, st1, st2, cid, csz);
+  hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
+                     pmin2, smin2, st1, st2, L.nb1, L.nb2);
+  hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
+  hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, lcp, key2, pmin2, smin2, st1,
+                     st2, L.nb1, L.nb2, L.levels, cid, csz);
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }

@@ -1,0 +1,171 @@
+// Stable merge sort for the queue-signal kernels (device templates).
+//
+// Tile pass: 128 threads x 2 items = 256 elements per workgroup (small tiles
+// keep a 64K-element sort spread over all 256 CUs); each thread orders its
+// items in registers, then runs are merged in LDS with merge-path
+// partitioning (every thread produces its outputs after a binary search on
+// its diagonal).
+// Global passes: each workgroup emits 256 outputs of a pair of sorted runs;
+// its start and end diagonals are found by a wave-wide 64-ary search, the
+// two input slices are staged in LDS and merged as above.
+// Ties keep input order (stable), so results are deterministic.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace peek {
+namespace msort {
+
+constexpr int kThreads = 128;
+constexpr int kItems = 2;
+constexpr int kTile = kThreads * kItems;   // 256
+
+// Number of items taken from A among the first k outputs of a stable merge
+// of A[0, la) and B[0, lb): the smallest i in [max(0,k-lb), min(k,la)] with
+// less(B[k-1-i], A[i]).
+template <typename T, typename Less>
+__device__ __forceinline__ int merge_path(const T* A, int la, const T* B, int lb, int k, Less less) {
+  int lo = k > lb ? k - lb : 0;
+  int hi = k < la ? k : la;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (!less(B[k - 1 - mid], A[mid])) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+template <typename T, typename Less>
+__device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb, int i, int j, T (&out)[kItems],
+                                          Less less) {
+#pragma unroll
+  for (int q = 0; q < kItems; ++q) {
+    const bool take_a = i < la && (j >= lb || !less(B[j], A[i]));
+    out[q] = take_a ? A[i] : B[j];
+    if (take_a) ++i;
+    else ++j;
+  }
+}
+
+template <typename T, typename Less>
+__global__ __launch_bounds__(kThreads) void k_tile_sort(const T* __restrict__ src, T* __restrict__ dst, Less less) {
+  __shared__ T s[kTile];
+  const int t = threadIdx.x;
+  const size_t base = (size_t)blockIdx.x * kTile;
+  T v[kItems];
+#pragma unroll
+  for (int q = 0; q < kItems; ++q) v[q] = src[base + t * kItems + q];
+  // odd-even transposition sort of the thread's items (stable)
+#pragma unroll
+  for (int round = 0; round < kItems; ++round) {
+#pragma unroll
+    for (int q = round & 1; q + 1 < kItems; q += 2) {
+      if (less(v[q + 1], v[q])) {
+        const T x = v[q];
+        v[q] = v[q + 1];
+        v[q + 1] = x;
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kItems; ++q) s[t * kItems + q] = v[q];
+  __syncthreads();
+  for (int w = kItems; w < kTile; w <<= 1) {
+    const int o = t * kItems;
+    const int pair = o & ~(2 * w - 1);
+    const int k = o - pair;
+    const T* A = s + pair;
+    const T* B = A + w;
+    const int i = merge_path(A, w, B, w, k, less);
+    merge_seq(A, w, B, w, i, k - i, v, less);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) s[o + q] = v[q];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < kItems; ++q) dst[base + t * kItems + q] = s[t * kItems + q];
+}
+
+// Diagonal split for output k of a stable merge of A[0,la) and B[0,lb),
+// computed by one wavefront with 64 probes per step.
+template <typename T, typename Less>
+__device__ __forceinline__ int wave_merge_path(const T* A, int64_t la, const T* B, int64_t lb, int64_t k, int lane,
+                                               Less less) {
+  int64_t lo = k > lb ? k - lb : 0;
+  int64_t hi = k < la ? k : la;
+  // predicate p(i) = less(B[k-1-i], A[i]) is false...false,true...true on [lo, hi)
+  while (hi - lo > 64) {
+    const int64_t span = hi - lo;
+    const int64_t probe = lo + (span * lane) / 64;
+    const bool p = less(B[k - 1 - probe], A[probe]);
+    const uint64_t b = __ballot(p);
+    // first lane whose probe is true; the answer lies in (probe[f-1], probe[f]]
+    const int f = b ? __ffsll((unsigned long long)b) - 1 : 64;
+    const int64_t nlo = f == 0 ? lo : lo + (span * (f - 1)) / 64 + 1;
+    const int64_t nhi = f == 64 ? hi : lo + (span * f) / 64;
+    lo = nlo;
+    hi = nhi;
+  }
+  const int64_t probe = lo + lane;
+  const bool p = probe < hi && less(B[k - 1 - probe], A[probe]);
+  const uint64_t b = __ballot(p);
+  const int f = b ? __ffsll((unsigned long long)b) - 1 : (int)(hi - lo);
+  return (int)(lo + f);
+}
+
+// Merge pass: runs of width w (power of two, >= kTile) in src, pairs merged into dst.
+template <typename T, typename Less>
+__global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ src, T* __restrict__ dst, int64_t w,
+                                                         Less less) {
+  __shared__ T s[kTile];
+  __shared__ int64_t split[2];
+  const int t = threadIdx.x;
+  const int64_t out0 = (int64_t)blockIdx.x * kTile;
+  const int64_t pair = out0 & ~(2 * w - 1);
+  const T* A = src + pair;
+  const T* B = A + w;
+  const int64_t k0 = out0 - pair;
+  if (t < 64) {
+    const int i0 = wave_merge_path(A, w, B, w, k0, t, less);
+    if (t == 0) split[0] = i0;
+  } else if (t < 128) {
+    const int i1 = wave_merge_path(A, w, B, w, k0 + kTile, t - 64, less);
+    if (t == 64) split[1] = i1;
+  }
+  __syncthreads();
+  const int64_t ia = split[0], ja = k0 - split[0];
+  const int la = (int)(split[1] - split[0]);
+  const int lb = kTile - la;
+  for (int q = t; q < kTile; q += kThreads) s[q] = q < la ? A[ia + q] : B[ja + (q - la)];
+  __syncthreads();
+  const int o = t * kItems;
+  const int i = merge_path(s, la, s + la, lb, o, less);
+  T v[kItems];
+  merge_seq(s, la, s + la, lb, i, o - i, v, less);
+#pragma unroll
+  for (int q = 0; q < kItems; ++q) dst[out0 + o + q] = v[q];
+}
+
+// Sorts np elements (np a power of two, >= kTile) from a into a or b;
+// returns the buffer that holds the result.
+template <typename T, typename Less>
+T* sort(T* a, T* b, size_t np, Less less, hipStream_t st) {
+  const unsigned tiles = (unsigned)(np / kTile);
+  hipLaunchKernelGGL((k_tile_sort<T, Less>), dim3(tiles), dim3(kThreads), 0, st, a, b, less);
+  T* cur = b;
+  T* oth = a;
+  for (size_t w = kTile; w < np; w <<= 1) {
+    hipLaunchKernelGGL((k_merge_pass<T, Less>), dim3(tiles), dim3(kThreads), 0, st, cur, oth, (int64_t)w, less);
+    T* x = cur;
+    cur = oth;
+    oth = x;
+  }
+  return cur;
+}
+
+}  // namespace msort
+}  // namespace peek

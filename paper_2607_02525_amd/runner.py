@@ -55,9 +55,10 @@ class HotPath:
         peek_lpm_batch(self.cache, self.d_tokens, self.d_offsets, self.block_size, self.d_h, self.d_last, self.d_m,
                        stream=stream)
 
-    def signals(self, stream=None):
-        peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last, self.threshold, self.d_cid,
-                           self.d_csz, self.d_demand, self.d_ws, stream=stream)
+    def signals(self, stream=None, anchored: bool = True):
+        peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last,
+                           self.d_m if anchored else None, self.threshold, self.d_cid, self.d_csz,
+                           self.d_demand, self.d_ws, stream=stream)
 
     def step(self, stream=None):
         self.lpm(stream)

@@ -118,20 +118,20 @@ def test_argument_errors_before_any_gpu_work():
     assert lib.peek_cache_stats(None, None, None, None, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
     assert lib.peek_cache_free(None) == P.PEEK_OK
     # threshold < 1, n < 0, mismatched cluster outputs
-    assert lib.peek_queue_signals(None, 4, None, None, None, 0, None, None, None, None, 0, None) \
+    assert lib.peek_queue_signals(None, 4, None, None, None, None, 0, None, None, None, None, 0, None) \
         == P.PEEK_ERR_INVALID_ARGUMENT
-    assert lib.peek_queue_signals(None, -1, None, None, None, 8, None, None, None, None, 0, None) \
+    assert lib.peek_queue_signals(None, -1, None, None, None, None, 8, None, None, None, None, 0, None) \
         == P.PEEK_ERR_INVALID_ARGUMENT
     fake = ctypes.c_void_p(0x1000)
-    assert lib.peek_queue_signals(None, 4, fake, fake, None, 8, fake, None, None, None, 0, None) \
+    assert lib.peek_queue_signals(None, 4, fake, fake, None, None, 8, fake, None, None, None, 0, None) \
         == P.PEEK_ERR_INVALID_ARGUMENT
     # workspace too small for the cluster pass (checked before any launch)
     need = P.peek_queue_signals_workspace(4, 0)
     assert need > 0
-    assert lib.peek_queue_signals(None, 4, fake, fake, None, 8, fake, fake, None, fake, need - 1, None) \
+    assert lib.peek_queue_signals(None, 4, fake, fake, None, None, 8, fake, fake, None, fake, need - 1, None) \
         == P.PEEK_ERR_WORKSPACE_TOO_SMALL
     # demand without a cache
-    assert lib.peek_queue_signals(None, 4, fake, fake, fake, 8, None, None, fake, fake, need, None) \
+    assert lib.peek_queue_signals(None, 4, fake, fake, fake, None, 8, None, None, fake, fake, need, None) \
         == P.PEEK_ERR_INVALID_ARGUMENT
 
 

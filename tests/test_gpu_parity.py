@@ -34,6 +34,11 @@ def gpu_run(w, repeat=1):
     for _ in range(repeat):
         hp.step()
         outs.append(hp.results())
+    # the cluster pass started from scratch (no walk anchoring) must agree too
+    hp.signals(anchored=False)
+    res = hp.results()
+    for k in ("cluster_id", "cluster_size"):
+        assert np.array_equal(res[k], outs[0][k]), f"{k}: anchored and unanchored cluster passes differ"
     return hp, outs
 
 
