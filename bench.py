@@ -174,6 +174,24 @@ def main():
         log("calibration copy: 3 x 1 GiB device-to-device")
         del src, dst
 
+    # achievable streaming-read bandwidth on this device: a plain 2 GiB sum
+    big = torch.ones(1 << 29, dtype=torch.int32, device="cuda")
+    big.sum()
+    torch.cuda.synchronize()
+    rd = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        big.sum()
+        b.record()
+        torch.cuda.synchronize()
+        rd.append(a.elapsed_time(b))
+    read_peak = big.numel() * 4 / (min(rd) / 1e3) / 1e9
+    del big
+    roofline["measured_read_peak_gbs"] = round(read_peak, 1)
+    roofline["frac_of_measured_read_peak"] = round(achieved / read_peak, 4)
+    log(f"streaming read of 2 GiB: {read_peak:.0f} GB/s")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host for cpu_baseline")

@@ -36,8 +36,8 @@ struct Flat {
   std::vector<int32_t> canon;      // input index -> canonical id
   std::vector<NodeRec> recs;       // canonical order
   std::vector<int32_t> child_tok;  // per-parent child tables, parents in canonical order
-  std::vector<int32_t> child_id;
-  std::vector<int32_t> pool;       // edge labels, each edge padded to a multiple of 4 tokens
+  std::vector<int32_t> child_id;   // canonical id of each child-table entry
+  std::vector<int32_t> pool;       // edge labels back to back in preorder (a unary chain is contiguous)
   std::vector<int32_t> pdep;       // depth of the parent, canonical order (root 0)
   std::vector<int32_t> pdep_st;    // sparse table over 64-node block minima of pdep
   int32_t pdep_nb = 0;
@@ -139,7 +139,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
   int64_t pool_len = 0;
   for (int32_t c = 0; c < num_nodes; ++c) {
     const int64_t len = eoff[order[c] + 1] - eoff[order[c]];
-    pool_len += (len + 3) & ~int64_t(3);
+    pool_len += len;
   }
   pool_len += kPoolTailPad;
   try {
@@ -166,7 +166,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     r.subtree_end = c + size[c];
     f->pdep[c] = (int32_t)(depth_in[v] - len);
     if (len) std::memcpy(f->pool.data() + pos, etok + eoff[v], len * sizeof(int32_t));
-    pos += (len + 3) & ~int64_t(3);
+    pos += len;
     for (int32_t q = kbeg[v]; q < kbeg[v + 1]; ++q) {
       f->child_tok[ct] = first_tok(kids[q]);
       f->child_id[ct] = f->canon[kids[q]];
@@ -369,13 +369,93 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   s = check_device(&dev);
   if (s != PEEK_OK) return s;
 
-  const size_t b_nodes = align256(sizeof(NodeRec) * (size_t)num_nodes);
-  const size_t b_ctok = align256(sizeof(int32_t) * f.child_tok.size());
-  const size_t b_cid = align256(sizeof(int32_t) * f.child_id.size());
-  const size_t b_pool = align256(sizeof(int32_t) * f.pool.size());
-  const size_t b_pdep = align256(sizeof(int32_t) * f.pdep.size());
-  const size_t b_pst = align256(sizeof(int32_t) * f.pdep_st.size());
-  const size_t total = b_nodes + b_ctok + b_cid + b_pool + b_pdep + b_pst;
+  // Maximal unary runs: a node with exactly one child is followed in
+  // preorder by that child, and their edges are adjacent in the pool, so
+  // the walk compares the whole run c .. run_last[c] in one sweep.
+  std::vector<int32_t> run_len, run_last, hash_off, depth_by_id;
+  std::vector<WalkRec> wrec, htab;
+  try {
+    run_len.resize(num_nodes);
+    run_last.resize(num_nodes);
+    hash_off.assign(num_nodes, -1);
+    depth_by_id.resize(num_nodes);
+    wrec.resize(num_nodes);
+  } catch (const std::bad_alloc&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  for (int32_t c = num_nodes - 1; c >= 0; --c) {
+    const NodeRec& r = f.recs[c];
+    const bool unary = c > 0 && r.n_child == 1;   // the root is never merged
+    const int64_t len = (int64_t)r.edge_len + (unary ? run_len[c + 1] : 0);
+    if (len > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "unary chain longer than 2^31-1 tokens");
+    run_len[c] = (int32_t)len;
+    run_last[c] = unary ? run_last[c + 1] : c;
+    depth_by_id[c] = r.depth;
+  }
+  // open-addressing tables (linear probing) for nodes with many children
+  int64_t htotal = 0;
+  for (int32_t c = 0; c < num_nodes; ++c) {
+    if (f.recs[c].n_child <= kHashMin) continue;
+    hash_off[c] = (int32_t)htotal;
+    htotal += int64_t(1) << hash_bits(f.recs[c].n_child);
+  }
+  if (htotal > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "too many children for the lookup tables");
+  // walk records in slot order: slot 0 = root, slot 1 + j = child-table entry j
+  auto walk_rec = [&](int32_t c, int32_t first_tok) {
+    const int32_t last = c == 0 ? 0 : run_last[c];
+    const NodeRec& e = f.recs[last];
+    WalkRec w{};
+    w.edge_off = f.recs[c].edge_off;
+    w.run_len = c == 0 ? 0 : run_len[c];
+    w.n_child = e.n_child;
+    w.child_ref = e.n_child > kHashMin ? hash_off[last] : e.child_beg;
+    w.id = c;
+    w.last_id = last;
+    w.first_tok = first_tok;
+    return w;
+  };
+  wrec[0] = walk_rec(0, 0);
+  for (int32_t j = 0; j + 1 < num_nodes; ++j) wrec[1 + j] = walk_rec(f.child_id[j], f.child_tok[j]);
+  try {
+    WalkRec empty{};
+    empty.id = -1;
+    htab.assign(std::max<int64_t>(htotal, 1), empty);
+  } catch (const std::bad_alloc&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  for (int32_t c = 0; c < num_nodes; ++c) {
+    const NodeRec& r = f.recs[c];
+    if (r.n_child <= kHashMin) continue;
+    const int32_t bits = hash_bits(r.n_child);
+    const uint32_t mask = (1u << bits) - 1;
+    WalkRec* table = htab.data() + hash_off[c];
+    for (int32_t i = 0; i < r.n_child; ++i) {
+      const WalkRec& ch = wrec[1 + r.child_beg + i];
+      uint32_t pos = hash_slot(ch.first_tok, bits);
+      while (table[pos].id >= 0) pos = (pos + 1) & mask;
+      table[pos] = ch;
+    }
+  }
+
+  struct Part {
+    const void* src;
+    size_t bytes;
+    size_t at;
+  };
+  Part parts[] = {
+      {f.recs.data(), sizeof(NodeRec) * (size_t)num_nodes, 0},
+      {wrec.data(), sizeof(WalkRec) * (size_t)num_nodes, 0},
+      {htab.data(), sizeof(WalkRec) * htab.size(), 0},
+      {depth_by_id.data(), sizeof(int32_t) * depth_by_id.size(), 0},
+      {f.pool.data(), sizeof(int32_t) * f.pool.size(), 0},
+      {f.pdep.data(), sizeof(int32_t) * f.pdep.size(), 0},
+      {f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(), 0},
+  };
+  size_t total = 0;
+  for (Part& q : parts) {
+    q.at = total;
+    total += align256(q.bytes);
+  }
   void* base = nullptr;
   hipError_t e = hipMalloc(&base, total);
   if (e != hipSuccess) {
@@ -384,23 +464,16 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   }
   char* p = (char*)base;
   hipStream_t st = (hipStream_t)stream;
-  const hipError_t e1 = hipMemcpyAsync(p, f.recs.data(), sizeof(NodeRec) * num_nodes, hipMemcpyHostToDevice, st);
-  const hipError_t e2 = hipMemcpyAsync(p + b_nodes, f.child_tok.data(), sizeof(int32_t) * f.child_tok.size(),
-                                       hipMemcpyHostToDevice, st);
-  const hipError_t e3 = hipMemcpyAsync(p + b_nodes + b_ctok, f.child_id.data(), sizeof(int32_t) * f.child_id.size(),
-                                       hipMemcpyHostToDevice, st);
-  const hipError_t e4 = hipMemcpyAsync(p + b_nodes + b_ctok + b_cid, f.pool.data(), sizeof(int32_t) * f.pool.size(),
-                                       hipMemcpyHostToDevice, st);
-  char* p_pdep = p + b_nodes + b_ctok + b_cid + b_pool;
-  const hipError_t e5 = hipMemcpyAsync(p_pdep, f.pdep.data(), sizeof(int32_t) * f.pdep.size(), hipMemcpyHostToDevice, st);
-  const hipError_t e6 = hipMemcpyAsync(p_pdep + b_pdep, f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(),
-                                       hipMemcpyHostToDevice, st);
-  const hipError_t e7 = hipStreamSynchronize(st);
-  for (hipError_t ee : {e1, e2, e3, e4, e5, e6, e7}) {
-    if (ee != hipSuccess) {
-      (void)hipFree(base);
-      return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(ee));
-    }
+  hipError_t first_err = hipSuccess;
+  for (const Part& q : parts) {
+    const hipError_t ee = hipMemcpyAsync(p + q.at, q.src, q.bytes, hipMemcpyHostToDevice, st);
+    if (ee != hipSuccess && first_err == hipSuccess) first_err = ee;
+  }
+  const hipError_t es = hipStreamSynchronize(st);
+  if (first_err == hipSuccess) first_err = es;
+  if (first_err != hipSuccess) {
+    (void)hipFree(base);
+    return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(first_err));
   }
   peek_cache* c = new (std::nothrow) peek_cache();
   if (!c) {
@@ -415,12 +488,14 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   c->max_depth = f.max_depth;
   c->device_bytes = (int64_t)total;
   c->d_base = base;
-  c->tree.nodes = (const NodeRec*)p;
-  c->tree.child_tok = (const int32_t*)(p + b_nodes);
-  c->tree.child_id = (const int32_t*)(p + b_nodes + b_ctok);
-  c->tree.pool = (const int32_t*)(p + b_nodes + b_ctok + b_cid);
-  c->tree.pdep = (const int32_t*)p_pdep;
-  c->tree.pdep_st = (const int32_t*)(p_pdep + b_pdep);
+  c->tree.nodes = (const NodeRec*)(p + parts[0].at);
+  c->tree.walk.recs = (const WalkRec*)(p + parts[1].at);
+  c->tree.walk.hash = (const WalkRec*)(p + parts[2].at);
+  c->tree.walk.depth = (const int32_t*)(p + parts[3].at);
+  c->tree.walk.pool = (const int32_t*)(p + parts[4].at);
+  c->tree.pool = c->tree.walk.pool;
+  c->tree.pdep = (const int32_t*)(p + parts[5].at);
+  c->tree.pdep_st = (const int32_t*)(p + parts[6].at);
   c->tree.pdep_nb = f.pdep_nb;
   c->tree.num_nodes = num_nodes;
   if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);

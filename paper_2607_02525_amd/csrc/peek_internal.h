@@ -13,7 +13,7 @@ namespace peek {
 // One cache node in canonical (DFS preorder) order; 32 bytes so a wave
 // fetches it with one scalar load.
 struct alignas(32) NodeRec {
-  int64_t edge_off;     // pool index of the edge's first token (pool is 16-byte aligned per edge)
+  int64_t edge_off;     // pool index of the edge's first token
   int32_t edge_len;     // tokens on the edge from the parent
   int32_t depth;        // tokens from the root to the end of the edge
   int32_t child_beg;    // first entry of this node's child table
@@ -23,12 +23,50 @@ struct alignas(32) NodeRec {
 };
 static_assert(sizeof(NodeRec) == 32, "NodeRec must stay 32 bytes");
 
+// What the walk reads when it enters a node (32 bytes, one scalar load or
+// two vector loads). A node with exactly one child is followed in preorder
+// by that child and their edges are adjacent in the pool, so a maximal unary
+// run c -> c+1 -> ... -> last is compared in one sweep of run_len tokens;
+// the lookup that follows happens at `last`, whose children are described
+// here. Records live at slots: slot 0 is the root, slot 1 + j the j-th entry
+// of the child table (children grouped per parent, ascending first token).
+// A node with more than kHashMin children also has an open-addressing table
+// of copies of its children's records, keyed by first token.
+struct alignas(32) WalkRec {
+  int64_t edge_off;     // pool index of this node's edge (start of the run)
+  int32_t run_len;      // tokens from this edge's start to the end of the run
+  int32_t child_ref;    // children of `last`: slot base (n_child <= kHashMin) or hash-table start
+  int32_t n_child;      // children of `last`
+  int32_t id;           // canonical id of this node; -1 marks an empty hash-table entry
+  int32_t last_id;      // canonical id of the run's last node (ids id..last_id are the run)
+  int32_t first_tok;    // first token of this node's edge (its key among siblings)
+};
+static_assert(sizeof(WalkRec) == 32, "WalkRec must stay 32 bytes");
+
+constexpr int32_t kHashMin = 64;   // nodes with more children use a hash table
+
+// Table size for n children: the power of two >= 2n (load factor <= 1/2).
+__host__ __device__ inline int32_t hash_bits(int32_t n) {
+  int32_t b = 1;
+  while ((int64_t(1) << b) < 2 * (int64_t)n) ++b;
+  return b;
+}
+__host__ __device__ inline uint32_t hash_slot(int32_t tok, int32_t bits) {
+  return ((uint32_t)tok * 2654435761u) >> (32 - bits);
+}
+
+struct WalkTree {
+  const WalkRec* recs;      // [num_nodes], slot order
+  const WalkRec* hash;      // children hash tables of high-fan-out nodes
+  const int32_t* depth;     // [num_nodes] depth at the end of each edge, by canonical id
+  const int32_t* pool;      // edge labels back to back in preorder
+};
+
 // Device image of a flattened cache tree.
 struct DeviceTree {
-  const NodeRec* nodes;     // [num_nodes]
-  const int32_t* child_tok; // [num_nodes - 1] first token of each child, grouped per parent
-  const int32_t* child_id;  // [num_nodes - 1] canonical id of that child
-  const int32_t* pool;      // edge labels, each edge starting on a 16-byte boundary
+  WalkTree walk;
+  const NodeRec* nodes;     // [num_nodes] canonical order
+  const int32_t* pool;      // edge labels back to back in preorder
   const int32_t* pdep;      // [num_nodes] depth of the parent (0 for the root), preorder
   const int32_t* pdep_st;   // sparse table of 64-node block minima of pdep: levels x pdep_nb
   int32_t pdep_nb;          // number of 64-node blocks
