@@ -40,6 +40,8 @@ struct Flat {
   std::vector<int32_t> pool;       // edge labels back to back in preorder (a unary chain is contiguous)
   std::vector<int32_t> pdep;       // depth of the parent, canonical order (root 0)
   std::vector<int32_t> pdep_st;    // sparse table over 64-node block minima of pdep
+  std::vector<int32_t> pdep_pre;   // minimum of pdep from the start of c's 64-node block to c
+  std::vector<int32_t> pdep_suf;   // minimum of pdep from c to the end of its block
   int32_t pdep_nb = 0;
   int64_t edge_tokens = 0;
   int32_t max_fanout = 0;
@@ -186,6 +188,12 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     for (int32_t c = b * 64; c < std::min(num_nodes, b * 64 + 64); ++c) m = std::min(m, f->pdep[c]);
     f->pdep_st[b] = m;
   }
+  f->pdep_pre.resize(num_nodes);
+  f->pdep_suf.resize(num_nodes);
+  for (int32_t c = 0; c < num_nodes; ++c)
+    f->pdep_pre[c] = (c & 63) ? std::min(f->pdep_pre[c - 1], f->pdep[c]) : f->pdep[c];
+  for (int32_t c = num_nodes - 1; c >= 0; --c)
+    f->pdep_suf[c] = ((c & 63) != 63 && c + 1 < num_nodes) ? std::min(f->pdep_suf[c + 1], f->pdep[c]) : f->pdep[c];
   for (int k = 1; k < levels; ++k)
     for (int32_t b = 0; b + (1 << k) <= nb; ++b)
       f->pdep_st[(size_t)k * nb + b] =
@@ -450,6 +458,8 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
       {f.pool.data(), sizeof(int32_t) * f.pool.size(), 0},
       {f.pdep.data(), sizeof(int32_t) * f.pdep.size(), 0},
       {f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(), 0},
+      {f.pdep_pre.data(), sizeof(int32_t) * f.pdep_pre.size(), 0},
+      {f.pdep_suf.data(), sizeof(int32_t) * f.pdep_suf.size(), 0},
   };
   size_t total = 0;
   for (Part& q : parts) {
@@ -496,6 +506,8 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   c->tree.pool = c->tree.walk.pool;
   c->tree.pdep = (const int32_t*)(p + parts[5].at);
   c->tree.pdep_st = (const int32_t*)(p + parts[6].at);
+  c->tree.pdep_pre = (const int32_t*)(p + parts[7].at);
+  c->tree.pdep_suf = (const int32_t*)(p + parts[8].at);
   c->tree.pdep_nb = f.pdep_nb;
   c->tree.num_nodes = num_nodes;
   if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
@@ -599,18 +611,10 @@ peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_
     peek_status s = check_same_device(c);
     if (s != PEEK_OK) return s;
   }
-  hipStream_t st = (hipStream_t)stream;
-  if (want_demand) {
-    peek_status s = run_demand(c->tree, n, d_last_node, d_demand, d_workspace, workspace_bytes, st);
-    if (s != PEEK_OK) return s;
-  }
-  if (want_clusters && n > 0) {
-    const bool anchored = c != nullptr && d_last_node != nullptr && d_match_len != nullptr;
-    peek_status s = run_clusters(anchored ? &c->tree : nullptr, n, d_tokens, d_offsets,
-                                 anchored ? d_last_node : nullptr, anchored ? d_match_len : nullptr, threshold,
-                                 d_cluster_id, d_cluster_size, nn, d_workspace, workspace_bytes, st);
-    if (s != PEEK_OK) return s;
-  }
+  peek_status s = run_signals(c ? &c->tree : nullptr, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
+                              want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
+                              want_demand ? d_demand : nullptr, d_workspace, workspace_bytes, (hipStream_t)stream);
+  if (s != PEEK_OK) return s;
   return PEEK_OK;
 }
 

@@ -69,6 +69,8 @@ struct DeviceTree {
   const int32_t* pool;      // edge labels back to back in preorder
   const int32_t* pdep;      // [num_nodes] depth of the parent (0 for the root), preorder
   const int32_t* pdep_st;   // sparse table of 64-node block minima of pdep: levels x pdep_nb
+  const int32_t* pdep_pre;  // [num_nodes] min of pdep from the start of the node's 64-block
+  const int32_t* pdep_suf;  // [num_nodes] min of pdep to the end of the node's 64-block
   int32_t pdep_nb;          // number of 64-node blocks
   int32_t num_nodes;
 };
@@ -110,14 +112,12 @@ hipError_t launch_lpm_walk(const DeviceTree& t, int32_t n, const int32_t* tokens
 
 size_t signals_workspace_bytes(int32_t n, int64_t num_nodes);
 
-peek_status run_demand(const DeviceTree& t, int32_t n, const int32_t* last_node, int32_t* demand,
-                       void* workspace, size_t workspace_bytes, hipStream_t stream);
-
-// t, last_node and match_len are optional (all or none): with them the
-// cluster pass starts from the walk's proven shared prefixes.
-peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
-                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
-                         int32_t* cluster_size, int64_t num_nodes, void* workspace, size_t workspace_bytes,
-                         hipStream_t stream);
+// Demand (when demand != NULL) and clusters (when cluster_id != NULL) in
+// one pass; t may be NULL when only clusters are wanted. With t, last_node
+// and match_len the cluster pass starts from the walk's proven prefixes.
+peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+                        const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
+                        int32_t* cluster_size, int32_t* demand, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
 
 }  // namespace peek

@@ -35,6 +35,7 @@
 //     boundary is d plus the smaller l. Each prompt byte is read about once.
 #include <algorithm>
 
+#include "peek_compare.h"
 #include "peek_internal.h"
 #include "peek_sort.h"
 
@@ -72,44 +73,34 @@ __global__ void k_demand_keys(const int32_t* __restrict__ last, int32_t n, uint3
   if (i < np) keys[i] = i < (size_t)n ? (uint32_t)last[i] : 0xFFFFFFFFu;
 }
 
-// P[c] = #{r : last_node[r] < c} for c in [0, nn]; each thread covers 16
-// consecutive nodes: a binary search for the first, then galloping from one
-// lower bound to the next (long runs of one node cost log steps).
-constexpr int kPrefixRun = 16;
+// sorted last nodes: a plain array, or the node field of the cluster pass's
+// anchor-sorted elements (sorted by last node first)
+struct PlainKeys {
+  const uint32_t* k;
+  __device__ __forceinline__ uint32_t operator()(int32_t i) const { return k[i]; }
+};
 
-__device__ __forceinline__ int32_t lower_bound_from(const uint32_t* __restrict__ keys, int32_t n, int32_t p, int64_t c) {
-  if (p >= n || (int64_t)keys[p] >= c) return p;
-  int32_t step = 1, lo = p;   // keys[lo] < c
-  while (lo + step < n && (int64_t)keys[lo + step] < c) {
-    lo += step;
-    step <<= 1;
+// P[c] for c in [0, nn], one node per lane: a wave-wide search brackets the
+// keys of the wave's 64 nodes once, then each lane binary-searches inside
+// the bracket (usually a handful of keys), so no lane waits on a chain.
+template <typename Keys>
+__global__ __launch_bounds__(256) void k_demand_prefix(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wbase =
+      (int64_t)__builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave;
+  if (wbase > nn) return;
+  const int64_t wend = wbase + kWave;   // exclusive
+  const int32_t lo = n == 0 ? 0 : wave_first_true(0, n, lane, [&](int32_t p) { return p >= n || (int64_t)keys(p) >= wbase; });
+  const int32_t hi = n == 0 ? 0 : wave_first_true(lo, n, lane, [&](int32_t p) { return p >= n || (int64_t)keys(p) >= wend; });
+  const int64_t c = wbase + lane;
+  if (c > nn) return;
+  int32_t a = lo, b = hi;
+  while (a < b) {
+    const int32_t mid = a + ((b - a) >> 1);
+    if ((int64_t)keys(mid) < c) a = mid + 1;
+    else b = mid;
   }
-  int32_t hi = min(lo + step, n);   // first candidate >= c lies in (lo, hi]
-  ++lo;
-  while (lo < hi) {
-    const int32_t mid = lo + ((hi - lo) >> 1);
-    if ((int64_t)keys[mid] < c) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
-__global__ void k_demand_prefix(const uint32_t* __restrict__ keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
-  const int64_t c0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * kPrefixRun;
-  if (c0 > nn) return;
-  int32_t lo = 0, hi = n;
-  while (lo < hi) {
-    const int32_t mid = lo + ((hi - lo) >> 1);
-    if ((int64_t)keys[mid] < c0) lo = mid + 1;
-    else hi = mid;
-  }
-  int32_t p = lo;
-  const int64_t c1 = min<int64_t>(c0 + kPrefixRun - 1, nn);
-  P[c0] = p;
-  for (int64_t c = c0 + 1; c <= c1; ++c) {
-    p = lower_bound_from(keys, n, p, c);
-    P[c] = p;
-  }
+  P[c] = a;
 }
 
 __global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, const int32_t* __restrict__ P,
@@ -140,6 +131,11 @@ struct ClLess {
 constexpr uint64_t kLenMax = 0x7FFFFFFFull;
 constexpr uint32_t kHeadL = 0xFFFFFFFFu;
 
+struct AnchorKeys {
+  const ClElem* el;
+  __device__ __forceinline__ uint32_t operator()(int32_t i) const { return (uint32_t)(el[i].hi >> 32); }
+};
+
 __device__ __forceinline__ uint64_t tok_code(int32_t x) { return (uint64_t)((uint32_t)x ^ 0x80000000u) + 1; }
 __device__ __forceinline__ uint64_t lo_of(uint64_t code, uint32_t len) { return (code << 31) | (kLenMax - len); }
 __device__ __forceinline__ uint64_t code_of(uint64_t lo) { return lo >> 31; }
@@ -149,6 +145,26 @@ __device__ __forceinline__ bool same_group(const ClElem& a, const ClElem& b) {
 }
 __device__ __forceinline__ bool group_less(const ClElem& a, uint64_t hi, uint64_t code) {
   return a.hi < hi || (a.hi == hi && code_of(a.lo) < code);
+}
+
+// Depth of the lowest common ancestor of preorder nodes c1 < c2 that are
+// not ancestor-related: the minimum parent depth over (c1, c2], from the
+// in-block suffix/prefix minima and the sparse table over 64-node blocks.
+__device__ __forceinline__ int32_t lca_depth(const DeviceTree& t, int32_t c1, int32_t c2) {
+  const int32_t lo = c1 + 1, hi = c2;
+  const int32_t bl = lo >> 6, bh = hi >> 6;
+  if (bl == bh) {
+    int32_t m = INT32_MAX;
+    for (int32_t v = lo; v <= hi; ++v) m = min(m, t.pdep[v]);
+    return m;
+  }
+  int32_t m = min(t.pdep_suf[lo], t.pdep_pre[hi]);
+  if (bh - bl >= 2) {
+    const int32_t x = bl + 1, y = bh - 1;
+    const int k = 31 - __clz(y - x + 1);
+    m = min(m, min(t.pdep_st[(int64_t)k * t.pdep_nb + x], t.pdep_st[(int64_t)k * t.pdep_nb + y - (1 << k) + 1]));
+  }
+  return m;
 }
 
 // Minimum of a[lo..hi] (inclusive) using 64-wide block minima and a sparse
@@ -173,8 +189,9 @@ __device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, 
 
 __global__ void k_anchor_keys(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets, int32_t n,
                               const int32_t* __restrict__ last, const int32_t* __restrict__ mlen, ClElem* __restrict__ el,
-                              size_t np, int32_t* __restrict__ lcp) {
+                              size_t np, int32_t* __restrict__ lcp, int32_t* __restrict__ flags, int32_t n_flags) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < (size_t)n_flags) flags[i] = 0;
   if (i < np) {
     ClElem e;
     if (i < (size_t)n) {
@@ -218,10 +235,7 @@ __device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ e
 // Groups of equal (node, match length, next token) after the anchor sort.
 // flags[0] is raised if any group needs refinement, flags[1] if such a
 // group has more than 64 members.
-__global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el,
-                                                       const NodeRec* __restrict__ nodes,
-                                                       const int32_t* __restrict__ pdep,
-                                                       const int32_t* __restrict__ pdep_st, int32_t pdep_nb,
+__global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el, DeviceTree t,
                                                        int32_t* __restrict__ nseg, int32_t* __restrict__ depth,
                                                        uint8_t* __restrict__ active, int32_t* __restrict__ lcp,
                                                        int32_t* __restrict__ flags) {
@@ -249,8 +263,8 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
       const uint32_t c2 = (uint32_t)(e.hi >> 32);
       int32_t v;
       if (c1 == c2) v = (int32_t)min(m1, m);
-      else if (c2 < (uint32_t)nodes[c1].subtree_end) v = (int32_t)m1;
-      else v = range_min_i32(pdep, pdep_st, pdep_nb, (int32_t)c1 + 1, (int32_t)c2);
+      else if (c2 < (uint32_t)t.nodes[c1].subtree_end) v = (int32_t)m1;
+      else v = lca_depth(t, (int32_t)c1, (int32_t)c2);
       lcp[i] = v;
     }
     const bool act = code != 0 && i + 1 < n && same_group(el[i + 1], e);
@@ -267,11 +281,14 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
 
 // One wavefront per position: rewrite every element's key for the next sort;
 // members of active segments are compared with their segment's head.
+// `flags_in` are the previous round's flags (nothing to do when [0] is 0).
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
                                                         const int32_t* __restrict__ depth,
-                                                        const uint8_t* __restrict__ active) {
+                                                        const uint8_t* __restrict__ active,
+                                                        const int32_t* __restrict__ flags_in) {
+  if (!flags_in[0]) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (i >= n) return;
@@ -290,31 +307,7 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
     const int32_t* __restrict__ pj = tokens + offsets[j] + d;
     const int32_t* __restrict__ ph = tokens + offsets[h] + d;
     const int32_t lim = (int32_t)min(len_j, len_h) - d;
-    int32_t l = lim;
-    for (int32_t base = 0; base < lim; base += kWave * 4) {
-      int32_t va[4], vb[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int32_t k = base + u * kWave + lane;
-        va[u] = 0;
-        vb[u] = 0;
-        if (k < lim) {
-          va[u] = pj[k];
-          vb[u] = ph[k];
-        }
-      }
-      bool found = false;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int32_t k = base + u * kWave + lane;
-        const uint64_t mm = __ballot(k < lim && va[u] != vb[u]);
-        if (mm && !found) {
-          l = base + u * kWave + (int32_t)__ffsll((unsigned long long)mm) - 1;
-          found = true;
-        }
-      }
-      if (found) break;
-    }
+    const int32_t l = cmp::first_mismatch(pj, ph, lim, lane);
     ell = (uint32_t)l;
     code = l < lim ? tok_code(pj[l]) : 0;   // 0: the member ended (the head is the longest)
   }
@@ -328,7 +321,9 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
 // per segment (stable rank by comparison with every other member).
 __global__ __launch_bounds__(256) void k_refine_small_sort(int32_t n, ClElem* __restrict__ el,
                                                            const int32_t* __restrict__ nseg,
-                                                           const uint8_t* __restrict__ active) {
+                                                           const uint8_t* __restrict__ active,
+                                                           const int32_t* __restrict__ flags_in) {
+  if (!flags_in[0] || flags_in[1]) return;   // nothing to do, or the global sort runs
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t s = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (s >= n || nseg[s] != s || !active[s]) return;
@@ -355,7 +350,9 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
                                                        const uint8_t* __restrict__ active_old,
                                                        int32_t* __restrict__ depth_new,
                                                        uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
+                                                       const int32_t* __restrict__ flags_in,
                                                        int32_t* __restrict__ flags) {
+  if (!flags_in[0]) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -400,13 +397,19 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   }
 }
 
-// share, the (share, request) key of every position, its in-block prefix and
-// suffix minima, and the 64-wide block minima of lcp and of the key.
+// In-block range-minimum tables: level k holds the minimum over the 2^k
+// positions starting at j (k = 0..5), valid while the window stays inside
+// j's 64-position block. With the block minima and a sparse table over
+// blocks they answer every range minimum below in a few loads.
+constexpr int kInBlockLevels = 6;
+
+// share, the (share, request) key of every position, the in-block tables of
+// lcp and of the key, and the 64-wide block minima of both.
 __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* __restrict__ el,
                                                       const int32_t* __restrict__ lcp, uint64_t* __restrict__ key2,
-                                                      uint64_t* __restrict__ pmin2, uint64_t* __restrict__ smin2,
-                                                      int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
-                                                      int32_t nb1, int32_t nb2) {
+                                                      int32_t* __restrict__ ib1, uint64_t* __restrict__ ib2,
+                                                      int64_t ib_stride, int32_t* __restrict__ st1,
+                                                      uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
   const int32_t i = b * kWave + lane;
@@ -418,21 +421,34 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
     v2 = ((uint64_t)(uint32_t)share << 32) | el[i].req;
     key2[i] = v2;
   }
-  uint64_t pre = v2, suf = v2;
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint64_t a = __shfl_up(pre, off);
-    if (lane >= off && a < pre) pre = a;
-    const uint64_t c = __shfl_down(suf, off);
-    if (lane + off < kWave && c < suf) suf = c;
+  int32_t m1 = v1;
+  uint64_t m2 = v2;
+  for (int k = 0; k < kInBlockLevels; ++k) {
+    if (k > 0) {
+      const int w = 1 << (k - 1);
+      const int32_t o1 = __shfl_down(m1, w);
+      const uint64_t o2 = __shfl_down(m2, w);
+      if (lane + w < kWave) {
+        m1 = min(m1, o1);
+        m2 = o2 < m2 ? o2 : m2;
+      }
+    }
+    if (i <= n) {
+      ib1[k * ib_stride + i] = m1;
+      ib2[k * ib_stride + i] = m2;
+    }
   }
-  if (i < n) {
-    pmin2[i] = pre;
-    smin2[i] = suf;
+  // whole-block minima: the level-5 window of lane 0 covers lanes 0..31
+  int32_t b1 = v1;
+  uint64_t b2 = v2;
+  for (int off = 32; off > 0; off >>= 1) {
+    b1 = min(b1, __shfl_xor(b1, off));
+    const uint64_t o = __shfl_xor(b2, off);
+    b2 = o < b2 ? o : b2;
   }
-  for (int off = 32; off > 0; off >>= 1) v1 = min(v1, __shfl_xor(v1, off));
   if (lane == 0) {
-    if (b < nb1) st1[b] = v1;
-    if (b < nb2) st2[b] = suf;
+    if (b < nb1) st1[b] = b1;
+    if (b < nb2) st2[b] = b2;
   }
 }
 
@@ -455,11 +471,46 @@ __global__ __launch_bounds__(1024) void k_final_tables(int32_t* __restrict__ st1
 
 __device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
-__global__ void k_final_query(int32_t n, int32_t threshold, const int32_t* __restrict__ lcp,
-                              const uint64_t* __restrict__ key2, const uint64_t* __restrict__ pmin2,
-                              const uint64_t* __restrict__ smin2, const int32_t* __restrict__ st1,
-                              const uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2, int levels,
-                              int32_t* __restrict__ cid, int32_t* __restrict__ csz) {
+// Minimum of a[lo..hi] inside one 64-block, from the in-block table: two
+// windows of the largest stored width (at most 32) that cover the range.
+template <typename T>
+__device__ __forceinline__ T in_block_min(const T* __restrict__ ib, int64_t stride, int32_t lo, int32_t hi) {
+  const int k = min(31 - __clz(hi - lo + 1), kInBlockLevels - 1);
+  const T x = ib[k * stride + lo], y = ib[k * stride + hi - (1 << k) + 1];
+  return x < y ? x : y;
+}
+
+// Last j in [lo, hi] (one block, at most 64 positions) with lcp[j] < s, or
+// lo - 1 if none. Lifting by 32, 16, .., 1 skips up to 63 positions; a
+// final single step covers a block that is >= s throughout.
+__device__ __forceinline__ int32_t last_below(const int32_t* __restrict__ ib1, int64_t stride, int32_t lo, int32_t hi,
+                                              int32_t s) {
+  int32_t pos = hi;   // lcp[pos+1..hi] >= s
+  for (int k = kInBlockLevels - 1; k >= 0; --k) {
+    const int32_t w = 1 << k;
+    if (pos - w + 1 >= lo && ib1[k * stride + pos - w + 1] >= s) pos -= w;
+  }
+  if (pos >= lo && ib1[pos] >= s) --pos;
+  return pos;
+}
+
+// First j in [lo, hi] (one block, at most 64 positions) with lcp[j] < s, or
+// hi + 1 if none.
+__device__ __forceinline__ int32_t first_below(const int32_t* __restrict__ ib1, int64_t stride, int32_t lo, int32_t hi,
+                                               int32_t s) {
+  int32_t pos = lo;   // lcp[lo..pos-1] >= s
+  for (int k = kInBlockLevels - 1; k >= 0; --k) {
+    const int32_t w = 1 << k;
+    if (pos + w - 1 <= hi && ib1[k * stride + pos] >= s) pos += w;
+  }
+  if (pos <= hi && ib1[pos] >= s) ++pos;
+  return pos;
+}
+
+__global__ void k_final_query(int32_t n, int32_t threshold, const uint64_t* __restrict__ key2,
+                              const int32_t* __restrict__ ib1, const uint64_t* __restrict__ ib2, int64_t ib_stride,
+                              const int32_t* __restrict__ st1, const uint64_t* __restrict__ st2, int32_t nb1,
+                              int32_t nb2, int levels, int32_t* __restrict__ cid, int32_t* __restrict__ csz) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint64_t own = key2[i];
@@ -471,53 +522,35 @@ __global__ void k_final_query(int32_t n, int32_t threshold, const int32_t* __res
     return;
   }
   // L: the last j <= i with lcp[j] < s (lcp[0] = 0 < s, so it exists)
-  int32_t L = -1;
-  for (int32_t j = i; j >= (i & ~63); --j)
-    if (lcp[j] < s) {
-      L = j;
-      break;
-    }
-  if (L < 0) {
-    int32_t pos = (i >> 6) - 1;   // the last block <= pos whose minimum is < s
+  const int32_t bi = i >> 6;
+  int32_t L = last_below(ib1, ib_stride, bi << 6, i, s);
+  if (L < (bi << 6)) {
+    int32_t pos = bi - 1;   // the last block <= pos whose minimum is < s
     for (int k = levels - 1; k >= 0; --k) {
       const int32_t w = 1 << k;
       if (pos - w + 1 >= 0 && st1[(int64_t)k * nb1 + pos - w + 1] >= s) pos -= w;
     }
-    for (int32_t j = (pos << 6) + 63; j >= (pos << 6); --j)
-      if (j <= n && lcp[j] < s) {
-        L = j;
-        break;
-      }
+    L = last_below(ib1, ib_stride, pos << 6, min((pos << 6) + 63, n), s);
   }
   // R: the first j > i with lcp[j] < s (lcp[n] = 0 < s)
-  int32_t R = -1;
-  const int32_t bend = min(((i >> 6) << 6) + 63, n);
-  for (int32_t j = i + 1; j <= bend; ++j)
-    if (lcp[j] < s) {
-      R = j;
-      break;
-    }
-  if (R < 0) {
-    int32_t pos = (i >> 6) + 1;   // the first block >= pos whose minimum is < s
+  const int32_t bend = min((bi << 6) + 63, n);
+  int32_t R = i + 1 <= bend ? first_below(ib1, ib_stride, i + 1, bend, s) : bend + 1;
+  if (R > bend) {
+    int32_t pos = bi + 1;   // the first block >= pos whose minimum is < s
     for (int k = levels - 1; k >= 0; --k) {
       const int32_t w = 1 << k;
       if (pos + w <= nb1 && st1[(int64_t)k * nb1 + pos] >= s) pos += w;
     }
-    for (int32_t j = pos << 6; j <= n; ++j)
-      if (lcp[j] < s) {
-        R = j;
-        break;
-      }
+    R = first_below(ib1, ib_stride, pos << 6, min((pos << 6) + 63, n), s);
   }
   // id: minimum of (share, request) over [L, R)
   const int32_t hi = R - 1;
   const int32_t bl = L >> 6, bh = hi >> 6;
   uint64_t m;
   if (bl == bh) {
-    m = ~0ull;
-    for (int32_t v = L; v <= hi; ++v) m = umin64(m, key2[v]);
+    m = in_block_min(ib2, ib_stride, L, hi);
   } else {
-    m = umin64(smin2[L], pmin2[hi]);
+    m = umin64(in_block_min(ib2, ib_stride, L, (bl << 6) + 63), in_block_min(ib2, ib_stride, bh << 6, hi));
     if (bh - bl >= 2) {
       const int32_t x = bl + 1, y = bh - 1;
       const int k = 31 - __clz(y - x + 1);
@@ -542,10 +575,13 @@ int levels_for(int64_t nb) {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
+constexpr int kSpeculativeRoundsL = 2;   // flag slots: one per speculative round, plus two
+
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
-  size_t el_a, el_b, nseg, depth_a, depth_b, active_a, active_b, lcp, key2, pmin2, smin2, st1, st2, flags, keys_a,
-      keys_b, prefix, total;
+  size_t el_a, el_b, nseg, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
+      keys_b, prefix, total, flags_bytes;
+  int64_t ib_stride;
   int32_t nb1, nb2;
   int levels;
 };
@@ -572,11 +608,13 @@ Layout layout(int32_t n, int64_t num_nodes) {
   L.active_b = take(nn);
   L.lcp = take(sizeof(int32_t) * ((size_t)n + 1));
   L.key2 = take(sizeof(uint64_t) * nn);
-  L.pmin2 = take(sizeof(uint64_t) * nn);
-  L.smin2 = take(sizeof(uint64_t) * nn);
+  L.ib_stride = (int64_t)L.nb1 * 64;
+  L.ib1 = take(sizeof(int32_t) * kInBlockLevels * (size_t)L.ib_stride);
+  L.ib2 = take(sizeof(uint64_t) * kInBlockLevels * (size_t)L.ib_stride);
   L.st1 = take(sizeof(int32_t) * (size_t)L.levels * L.nb1);
   L.st2 = take(sizeof(uint64_t) * (size_t)L.levels * L.nb2);
-  L.flags = take(sizeof(int32_t) * 2);
+  L.flags_bytes = sizeof(int32_t) * 2 * (kSpeculativeRoundsL + 2);
+  L.flags = take(L.flags_bytes);
   L.keys_a = take(sizeof(uint32_t) * np);
   L.keys_b = take(sizeof(uint32_t) * np);
   L.prefix = take(sizeof(int32_t) * (size_t)(num_nodes + 1));
@@ -590,33 +628,50 @@ unsigned blocks_for(int64_t m, int t = 256) { return (unsigned)((m + t - 1) / t)
 
 size_t signals_workspace_bytes(int32_t n, int64_t num_nodes) { return layout(n, num_nodes).total; }
 
-peek_status run_demand(const DeviceTree& t, int32_t n, const int32_t* last_node, int32_t* demand, void* ws,
-                       size_t ws_bytes, hipStream_t st) {
-  const Layout L = layout(n, t.num_nodes);
-  char* w = (char*)ws;
+namespace {
+
+// demand[c] = P[subtree_end(c)] - P[c] from sorted last nodes
+template <typename Keys>
+void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_t* P, int32_t* demand,
+                               hipStream_t st) {
   const int32_t nn = t.num_nodes;
-  int32_t* P = (int32_t*)(w + L.prefix);
-  const size_t np = np_of(n);
-  uint32_t* ka = (uint32_t*)(w + L.keys_a);
-  uint32_t* kb = (uint32_t*)(w + L.keys_b);
-  const uint32_t* keys = ka;
-  if (n > 0) {
-    hipLaunchKernelGGL(k_demand_keys, dim3(blocks_for(np)), dim3(256), 0, st, last_node, n, ka, np);
-    keys = msort::sort(ka, kb, np, U32Less{}, st);
-  }
-  hipLaunchKernelGGL(k_demand_prefix, dim3(blocks_for((int64_t)nn / kPrefixRun + 1)), dim3(256), 0, st, keys, n, nn,
-                     P);
+  hipLaunchKernelGGL((k_demand_prefix<Keys>), dim3(blocks_for((int64_t)nn + 1)), dim3(256), 0, st, keys, n, nn, P);
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
-  PEEK_HIP_TRY(hipGetLastError());
-  return PEEK_OK;
 }
 
-peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
-                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
-                         int32_t* csz, int64_t num_nodes, void* ws, size_t ws_bytes, hipStream_t st) {
+constexpr int kSpeculativeRounds = kSpeculativeRoundsL;   // rounds launched before the first flag read
+
+enum class SortPath { kGated, kGlobal, kSmall };
+
+}  // namespace
+
+peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+                        const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
+                        int32_t* csz, int32_t* demand, void* ws, size_t ws_bytes, hipStream_t st) {
+  const int64_t num_nodes = t ? t->num_nodes : 0;
   const Layout L = layout(n, num_nodes);
   char* w = (char*)ws;
   const size_t np = np_of(n);
+  int32_t* P = (int32_t*)(w + L.prefix);
+  const bool want_clusters = cid != nullptr && n > 0;
+  // anchoring needs the walk's results and the cache they refer to
+  const bool anchored = want_clusters && t != nullptr && last_node != nullptr && match_len != nullptr;
+
+  if (demand != nullptr && !anchored) {
+    uint32_t* ka = (uint32_t*)(w + L.keys_a);
+    uint32_t* kb = (uint32_t*)(w + L.keys_b);
+    const uint32_t* keys = ka;
+    if (n > 0) {
+      hipLaunchKernelGGL(k_demand_keys, dim3(blocks_for(np)), dim3(256), 0, st, last_node, n, ka, np);
+      keys = msort::sort(ka, kb, np, U32Less{}, st);
+    }
+    launch_demand_from_sorted(*t, PlainKeys{keys}, n, P, demand, st);
+  }
+  if (!want_clusters) {
+    PEEK_HIP_TRY(hipGetLastError());
+    return PEEK_OK;
+  }
+
   ClElem* el_a = (ClElem*)(w + L.el_a);
   ClElem* el_b = (ClElem*)(w + L.el_b);
   int32_t* nseg = (int32_t*)(w + L.nseg);
@@ -626,25 +681,45 @@ peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, 
   uint8_t* active_b = (uint8_t*)(w + L.active_b);
   int32_t* lcp = (int32_t*)(w + L.lcp);
   uint64_t* key2 = (uint64_t*)(w + L.key2);
-  uint64_t* pmin2 = (uint64_t*)(w + L.pmin2);
-  uint64_t* smin2 = (uint64_t*)(w + L.smin2);
+  int32_t* ib1 = (int32_t*)(w + L.ib1);
+  uint64_t* ib2 = (uint64_t*)(w + L.ib2);
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
-  int32_t* flags = (int32_t*)(w + L.flags);
+  int32_t* flags = (int32_t*)(w + L.flags);   // 2 ints per round: [any active, any active group > 64]
 
-  // anchoring needs the walk's results and the cache they refer to
-  const bool anchored = t != nullptr && last_node != nullptr && match_len != nullptr;
-  PEEK_HIP_TRY(hipMemsetAsync(flags, 0, sizeof(int32_t) * 2, st));
   hipLaunchKernelGGL(k_anchor_keys, dim3(blocks_for((int64_t)np + 1)), dim3(256), 0, st, tokens, offsets, n,
-                     anchored ? last_node : nullptr, anchored ? match_len : nullptr, el_a, np, lcp);
+                     anchored ? last_node : nullptr, anchored ? match_len : nullptr, el_a, np, lcp, flags,
+                     (int32_t)(L.flags_bytes / sizeof(int32_t)));
   ClElem* el = msort::sort(el_a, el_b, np, ClLess{}, st);
   ClElem* other = el == el_a ? el_b : el_a;
+  // the anchor order is sorted by last node first: demand reads it directly
+  if (demand != nullptr && anchored) launch_demand_from_sorted(*t, AnchorKeys{el}, n, P, demand, st);
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
-  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, anchored ? t->nodes : nullptr,
-                     anchored ? t->pdep : nullptr, anchored ? t->pdep_st : nullptr, anchored ? t->pdep_nb : 0, nseg,
+  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, anchored ? *t : DeviceTree{}, nseg,
                      depth_a, active_a, lcp, flags);
+
+  auto round = [&](const int32_t* fin, int32_t* fout, SortPath path) {
+    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg,
+                       depth_a, active_a, fin);
+    if (path != SortPath::kSmall) {
+      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st, path == SortPath::kGated ? fin + 1 : nullptr);
+      other = sorted == el ? other : el;
+      el = sorted;
+    }
+    if (path != SortPath::kGlobal)
+      hipLaunchKernelGGL(k_refine_small_sort, dim3(blocks_for(n, 4)), dim3(256), 0, st, n, el, nseg, active_a, fin);
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, depth_a, active_a, depth_b,
+                       active_b, lcp, fin, fout);
+    std::swap(depth_a, depth_b);
+    std::swap(active_a, active_b);
+  };
+  // A few rounds go out before the host looks at any flag (each kernel
+  // checks the previous round's flags and idles if there is nothing to do).
+  for (int r = 1; r <= kSpeculativeRounds; ++r) round(flags + 2 * (r - 1), flags + 2 * r, SortPath::kGated);
+  int32_t* fin = flags + 2 * kSpeculativeRounds;
+  int32_t* fout = flags + 2 * (kSpeculativeRounds + 1);
   int32_t h_flags[2] = {0, 0};
-  PEEK_HIP_TRY(hipMemcpyAsync(h_flags, flags, sizeof(h_flags), hipMemcpyDeviceToHost, st));
+  PEEK_HIP_TRY(hipMemcpyAsync(h_flags, fin, sizeof(h_flags), hipMemcpyDeviceToHost, st));
   PEEK_HIP_TRY(hipStreamSynchronize(st));
   // Every round makes each still-active segment strictly deeper, so the loop
   // ends after at most (longest prompt + 1) rounds; the cap only turns a
@@ -653,29 +728,17 @@ peek_status run_clusters(const DeviceTree* t, int32_t n, const int32_t* tokens, 
   constexpr int64_t kMaxRounds = int64_t(1) << 31;
   while (h_flags[0]) {
     if (++rounds > kMaxRounds) return fail(PEEK_ERR_DEVICE, "cluster refinement did not converge");
-    const bool big = h_flags[1] != 0;
-    PEEK_HIP_TRY(hipMemsetAsync(flags, 0, sizeof(int32_t) * 2, st));
-    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg,
-                       depth_a, active_a);
-    if (big) {
-      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st);
-      other = sorted == el ? other : el;
-      el = sorted;
-    } else {
-      hipLaunchKernelGGL(k_refine_small_sort, dim3(blocks_for(n, 4)), dim3(256), 0, st, n, el, nseg, active_a);
-    }
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, depth_a, active_a, depth_b,
-                       active_b, lcp, flags);
-    PEEK_HIP_TRY(hipMemcpyAsync(h_flags, flags, sizeof(h_flags), hipMemcpyDeviceToHost, st));
+    PEEK_HIP_TRY(hipMemsetAsync(fout, 0, sizeof(int32_t) * 2, st));
+    round(fin, fout, h_flags[1] ? SortPath::kGlobal : SortPath::kSmall);
+    std::swap(fin, fout);
+    PEEK_HIP_TRY(hipMemcpyAsync(h_flags, fin, sizeof(h_flags), hipMemcpyDeviceToHost, st));
     PEEK_HIP_TRY(hipStreamSynchronize(st));
-    std::swap(depth_a, depth_b);
-    std::swap(active_a, active_b);
   }
   hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
-                     pmin2, smin2, st1, st2, L.nb1, L.nb2);
+                     ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2);
   hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
-  hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, lcp, key2, pmin2, smin2, st1,
-                     st2, L.nb1, L.nb2, L.levels, cid, csz);
+  hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, key2, ib1, ib2, L.ib_stride,
+                     st1, st2, L.nb1, L.nb2, L.levels, cid, csz);
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }

@@ -50,11 +50,26 @@ __device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb
   }
 }
 
+// A gated sort (gate != nullptr and *gate == 0) is skipped: the tile pass
+// copies its input to its output and every merge pass returns at once. The
+// buffer the host expects then holds the unsorted input either way: after
+// an even number of merge passes it is the tile pass's copy, after an odd
+// number it is the untouched input.
+template <typename T>
+__device__ __forceinline__ bool gated_copy(const int32_t* gate, const T* __restrict__ src, T* __restrict__ dst,
+                                           size_t base) {
+  if (gate == nullptr || *gate != 0) return false;
+  for (int q = threadIdx.x; q < kTile; q += kThreads) dst[base + q] = src[base + q];
+  return true;
+}
+
 template <typename T, typename Less>
-__global__ __launch_bounds__(kThreads) void k_tile_sort(const T* __restrict__ src, T* __restrict__ dst, Less less) {
+__global__ __launch_bounds__(kThreads) void k_tile_sort(const T* __restrict__ src, T* __restrict__ dst, Less less,
+                                                        const int32_t* gate) {
   __shared__ T s[kTile];
   const int t = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * kTile;
+  if (gated_copy(gate, src, dst, base)) return;
   T v[kItems];
 #pragma unroll
   for (int q = 0; q < kItems; ++q) v[q] = src[base + t * kItems + q];
@@ -120,11 +135,12 @@ __device__ __forceinline__ int wave_merge_path(const T* A, int64_t la, const T* 
 // Merge pass: runs of width w (power of two, >= kTile) in src, pairs merged into dst.
 template <typename T, typename Less>
 __global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ src, T* __restrict__ dst, int64_t w,
-                                                         Less less) {
+                                                         Less less, const int32_t* gate) {
   __shared__ T s[kTile];
   __shared__ int64_t split[2];
   const int t = threadIdx.x;
   const int64_t out0 = (int64_t)blockIdx.x * kTile;
+  if (gate != nullptr && *gate == 0) return;
   const int64_t pair = out0 & ~(2 * w - 1);
   const T* A = src + pair;
   const T* B = A + w;
@@ -151,15 +167,17 @@ __global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ s
 }
 
 // Sorts np elements (np a power of two, >= kTile) from a into a or b;
-// returns the buffer that holds the result.
+// returns the buffer that holds the result. With a gate, the sort happens
+// only if *gate != 0 when the passes run (otherwise the data is copied).
 template <typename T, typename Less>
-T* sort(T* a, T* b, size_t np, Less less, hipStream_t st) {
+T* sort(T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
   const unsigned tiles = (unsigned)(np / kTile);
-  hipLaunchKernelGGL((k_tile_sort<T, Less>), dim3(tiles), dim3(kThreads), 0, st, a, b, less);
+  hipLaunchKernelGGL((k_tile_sort<T, Less>), dim3(tiles), dim3(kThreads), 0, st, a, b, less, gate);
   T* cur = b;
   T* oth = a;
   for (size_t w = kTile; w < np; w <<= 1) {
-    hipLaunchKernelGGL((k_merge_pass<T, Less>), dim3(tiles), dim3(kThreads), 0, st, cur, oth, (int64_t)w, less);
+    hipLaunchKernelGGL((k_merge_pass<T, Less>), dim3(tiles), dim3(kThreads), 0, st, cur, oth, (int64_t)w, less,
+                       gate);
     T* x = cur;
     cur = oth;
     oth = x;

@@ -160,3 +160,14 @@ def test_repeated_runs_are_identical():
     hp, outs = gpu_run(w, repeat=3)
     for res in outs:
         assert_parity(w, res, s)
+
+
+@pytest.mark.parametrize("copies", [63, 64, 65, 128, 129, 200])
+def test_cluster_ranges_that_fill_whole_blocks(copies):
+    # long runs of equal adjacent LCPs: a cluster range covering one or more
+    # complete 64-position blocks of the sorted order
+    rng = np.random.default_rng(copies)
+    base = rng.integers(0, 1000, size=300).tolist()
+    prompts = [base + [int(x)] + rng.integers(0, 1000, size=5).tolist() for x in rng.permutation(2000)[:copies]]
+    prompts += [base[:100] + [7, 7]] * 3 + [rng.integers(0, 1000, size=50).tolist() for _ in range(20)]
+    run_and_compare(_w(prompts, cached=[base[:150]], T=16))
