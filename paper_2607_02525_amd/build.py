@@ -12,6 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libpeek.so")
+CALIB_LIB = os.path.join(HERE, "libpeek_calib.so")   # measurement helper for bench.py
 BUILD_DIR = os.path.join(HERE, "_build")
 
 SOURCES = ["peek_host.hip", "peek_walk.hip", "peek_signals.hip"]
@@ -47,6 +48,12 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    tmp = CALIB_LIB + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-shared", "-o", tmp, os.path.join(CSRC, "peek_calib.hip")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(tmp, CALIB_LIB)
     return LIB
 
 

@@ -25,6 +25,7 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
+constexpr int kProbe = 16;   // hash-table slots read per probe step
 
 __device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -66,16 +67,20 @@ __device__ __forceinline__ bool find_child(const WalkRec* __restrict__ hash, con
   const uint32_t mask = (1u << bits) - 1;
   const WalkRec* table = hash + node.child_ref;
   uint32_t pos = hash_slot(t, bits);
-  while (true) {   // load factor <= 1/2: an empty slot ends every probe run
-    const WalkRec e = table[(pos + lane) & mask];
+  // windows of kProbe slots (load factor <= 1/2 keeps probe runs short);
+  // the other lanes stay idle
+  while (true) {
+    WalkRec e;
+    if (lane < kProbe) e = table[(pos + lane) & mask];
+    else e.id = -2;
     const uint64_t hit = __ballot(e.id >= 0 && e.first_tok == t);
     if (hit) {
       *out = take_lane(e, __ffsll((unsigned long long)hit) - 1);
       return true;
     }
-    const uint64_t empty = __ballot(e.id < 0);
+    const uint64_t empty = __ballot(e.id == -1);
     if (empty) return false;   // linear probing: t would sit before the first empty slot
-    pos = (pos + kWave) & mask;
+    pos = (pos + kProbe) & mask;
   }
 }
 
