@@ -85,6 +85,31 @@ def measured_read_peak(torch) -> float:
     return nbytes / (min(times[1:]) / 1e3) / 1e9
 
 
+WALK_SOURCES = ("peek_walk.hip", "peek_compare.h", "peek_internal.h")
+WALK_COUNTERS = os.path.join(ROOT, "profiles", "k_lpm_walk_scale_counters.txt")
+
+
+def walk_traffic(config: str):
+    """HBM bytes per walk launch from the committed counter summary (FETCH_SIZE
+    and WRITE_SIZE scaled by a plain-copy calibration), or None when the walk
+    sources changed since the counters were taken or another config runs."""
+    import hashlib
+    if config != "scale" or not os.path.exists(WALK_COUNTERS):
+        return None
+    kv = {}
+    for line in open(WALK_COUNTERS):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            kv[k] = v
+    h = hashlib.sha256()
+    for f in WALK_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_02525_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if kv.get("source_sha256") != h.hexdigest():
+        return None
+    return int(kv["traffic_bytes_per_dispatch"])
+
+
 def cpu_baseline(w, budget_s: float):
     import oracle as O
     O.build(force=False)
@@ -185,7 +210,7 @@ def main():
     lpm_avg_s = float(lpm_ms.mean()) / 1e3
     achieved = b_alg / lpm_avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": walk_traffic(args.config),
                 "kernel": "k_lpm_walk", "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
                 "avg_launch_ms": round(float(lpm_ms.mean()), 4), "min_launch_ms": round(float(lpm_ms.min()), 4)}
 
