@@ -131,6 +131,17 @@ struct ClLess {
 constexpr uint64_t kLenMax = 0x7FFFFFFFull;
 constexpr uint32_t kHeadL = 0xFFFFFFFFu;
 
+// Largest segment the segment sort ranks inside one workgroup; rounds with
+// a larger active segment sort globally.
+constexpr int kSegSortMax = 512;
+
+// Whether a refinement round has work: flags_in = {any active segment, some
+// active segment larger than kSegSortMax}; only a round that sorts globally
+// takes the latter.
+__device__ __forceinline__ bool round_runs(const int32_t* flags_in, int32_t global) {
+  return flags_in[0] != 0 && (global != 0 || flags_in[1] == 0);
+}
+
 struct AnchorKeys {
   const ClElem* el;
   __device__ __forceinline__ uint32_t operator()(int32_t i) const { return (uint32_t)(el[i].hi >> 32); }
@@ -234,11 +245,12 @@ __device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ e
 
 // Groups of equal (node, match length, next token) after the anchor sort.
 // flags[0] is raised if any group needs refinement, flags[1] if such a
-// group has more than 64 members.
+// group is too large for the in-LDS segment sort. gsize[g] is written at
+// every group start g.
 __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el, DeviceTree t,
-                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ depth,
-                                                       uint8_t* __restrict__ active, int32_t* __restrict__ lcp,
-                                                       int32_t* __restrict__ flags) {
+                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
+                                                       int32_t* __restrict__ depth, uint8_t* __restrict__ active,
+                                                       int32_t* __restrict__ lcp, int32_t* __restrict__ flags) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -256,6 +268,12 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
   nseg[i] = g;
   const uint32_t m = (uint32_t)e.hi;
   const uint64_t code = code_of(e.lo);
+  const bool last = i + 1 == n || !same_group(e, el[i + 1]);
+  if (last) {
+    const int32_t size = i - g + 1;
+    gsize[g] = size;
+    if (code != 0 && size >= 2 && size > kSegSortMax) flags[1] = 1;
+  }
   if (i == g) {
     if (i > 0) {
       const ClElem p = el[i - 1];
@@ -267,13 +285,10 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
       else v = lca_depth(t, (int32_t)c1, (int32_t)c2);
       lcp[i] = v;
     }
-    const bool act = code != 0 && i + 1 < n && same_group(el[i + 1], e);
+    const bool act = code != 0 && !last;
     active[i] = act;
     depth[i] = act ? (int32_t)m + 1 : 0;
-    if (act) {
-      flags[0] = 1;
-      if (i + kWave < n && same_group(el[i + kWave], e)) flags[1] = 1;
-    }
+    if (act) flags[0] = 1;
   } else if (code == 0) {
     lcp[i] = (int32_t)m;   // identical prompts of length m
   }
@@ -281,14 +296,15 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
 
 // One wavefront per position: rewrite every element's key for the next sort;
 // members of active segments are compared with their segment's head.
-// `flags_in` are the previous round's flags (nothing to do when [0] is 0).
+// `flags_in` are the previous round's flags: nothing to do when [0] is 0;
+// with [1] raised only a round that sorts globally (`global`) may run.
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
                                                         const int32_t* __restrict__ depth,
                                                         const uint8_t* __restrict__ active,
-                                                        const int32_t* __restrict__ flags_in) {
-  if (!flags_in[0]) return;
+                                                        const int32_t* __restrict__ flags_in, int32_t global) {
+  if (!round_runs(flags_in, global)) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (i >= n) return;
@@ -317,42 +333,115 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
   }
 }
 
-// Sorts every active segment of at most 64 members in place, one wavefront
-// per segment (stable rank by comparison with every other member).
-__global__ __launch_bounds__(256) void k_refine_small_sort(int32_t n, ClElem* __restrict__ el,
-                                                           const int32_t* __restrict__ nseg,
-                                                           const uint8_t* __restrict__ active,
-                                                           const int32_t* __restrict__ flags_in) {
-  if (!flags_in[0] || flags_in[1]) return;   // nothing to do, or the global sort runs
-  const int lane = threadIdx.x & (kWave - 1);
-  const int32_t s = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
-  if (s >= n || nseg[s] != s || !active[s]) return;
-  const int32_t i = s + lane;
-  const bool mine = i < n && nseg[i] == s;
-  const int size = __popcll(__ballot(mine));
-  ClElem e{};
-  if (lane < size) e = el[i];
-  int rank = 0;
-  const ClLess less;
-  for (int j = 0; j < size; ++j) {
-    ClElem o;
-    o.hi = __shfl(e.hi, j);
-    o.lo = __shfl(e.lo, j);
-    if (less(o, e) || (j < lane && !less(e, o))) ++rank;
-  }
-  if (lane < size) el[s + rank] = e;
+// Sort key of a segment member inside the segment sort: the segment start
+// is common to all members, so (l, lo) order them as ClLess does.
+struct SegKey {
+  uint32_t ell;
+  uint32_t req;
+  uint64_t lo;
+};
+__device__ __forceinline__ bool seg_less(const SegKey& a, const SegKey& b) {
+  return a.ell < b.ell || (a.ell == b.ell && a.lo < b.lo);
+}
+__device__ __forceinline__ SegKey seg_key(const ClElem& e) { return SegKey{ell_of(e.hi), e.req, e.lo}; }
+__device__ __forceinline__ ClElem seg_elem(const SegKey& k, int32_t s) {
+  ClElem e;
+  e.hi = ((uint64_t)(uint32_t)s << 32) | k.ell;
+  e.lo = k.lo;
+  e.req = k.req;
+  e.len = (uint32_t)(kLenMax - (k.lo & kLenMax));
+  return e;
 }
 
-// After the refinement sort: new groups, their LCPs, depths and activity.
+constexpr int kSegThreads = kSegSortMax;   // one thread per member of a medium segment
+constexpr int kSegRange = 256;             // segment starts owned by one workgroup
+
+// Sorts every active segment of at most kSegSortMax members in place. Each
+// workgroup owns the segment starts in kSegRange consecutive positions:
+//  - a segment of at most 64 members is ranked by one wavefront;
+//  - a larger one is ranked by the whole workgroup, one member per thread,
+//    against the segment's keys staged in LDS (every read is a broadcast).
+// A member's rank is the number of members that order before it (ties by
+// position), so the sort is stable. Rounds with a larger segment
+// (flags_in[1]) sort globally instead and this kernel does nothing.
+__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClElem* __restrict__ el,
+                                                                 const int32_t* __restrict__ nseg,
+                                                                 const int32_t* __restrict__ gsize,
+                                                                 const uint8_t* __restrict__ active,
+                                                                 const int32_t* __restrict__ flags_in) {
+  if (!round_runs(flags_in, 0)) return;
+  __shared__ SegKey sk[kSegSortMax];
+  __shared__ int32_t mid[kSegRange / 64 + 1];
+  __shared__ int32_t n_mid;
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1);
+  const int wave = t / kWave;
+  const int32_t r0 = (int32_t)blockIdx.x * kSegRange;
+  if (t == 0) n_mid = 0;
+  __syncthreads();
+  // small segments: wave w looks at the starts r0 + 32w .. r0 + 32w + 31
+  constexpr int kPerWave = kSegRange / (kSegThreads / kWave);
+  static_assert(kPerWave <= kWave, "one start per lane");
+  {
+    const int32_t p = r0 + wave * kPerWave + lane;
+    bool small = false;
+    if (lane < kPerWave && p < n && nseg[p] == p && active[p]) {
+      if (gsize[p] <= kWave) small = true;
+      else mid[atomicAdd(&n_mid, 1)] = p;   // members > 64: at most one start per 64 positions
+    }
+    uint64_t todo = __ballot(small);
+    while (todo) {
+      const int f = __ffsll((unsigned long long)todo) - 1;
+      todo &= todo - 1;
+      const int32_t s = r0 + wave * kPerWave + f;
+      const int32_t size = gsize[s];
+      ClElem e{};
+      if (lane < size) e = el[s + lane];
+      int rank = 0;
+      const ClLess less;
+      for (int j = 0; j < size; ++j) {
+        ClElem o;
+        o.hi = __shfl(e.hi, j);
+        o.lo = __shfl(e.lo, j);
+        if (less(o, e) || (j < lane && !less(e, o))) ++rank;
+      }
+      if (lane < size) el[s + rank] = e;
+    }
+  }
+  __syncthreads();
+  const int32_t nm = n_mid;
+  for (int b = 0; b < nm; ++b) {
+    const int32_t s = mid[b];
+    const int32_t size = gsize[s];
+    SegKey v{};
+    if (t < size) {
+      v = seg_key(el[s + t]);
+      sk[t] = v;
+    }
+    __syncthreads();
+    if (t < size) {
+      int32_t rank = 0;
+      for (int32_t j = 0; j < size; ++j) {
+        const SegKey o = sk[j];
+        rank += (seg_less(o, v) || (j < t && !seg_less(v, o))) ? 1 : 0;
+      }
+      el[s + rank] = seg_elem(v, s);
+    }
+    __syncthreads();
+  }
+}
+
+// After the refinement sort: new groups, their LCPs, depths, sizes and
+// activity.
 __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* __restrict__ el,
-                                                       int32_t* __restrict__ nseg,
+                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
                                                        const int32_t* __restrict__ depth_old,
                                                        const uint8_t* __restrict__ active_old,
                                                        int32_t* __restrict__ depth_new,
                                                        uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
                                                        const int32_t* __restrict__ flags_in,
-                                                       int32_t* __restrict__ flags) {
-  if (!flags_in[0]) return;
+                                                       int32_t* __restrict__ flags, int32_t global) {
+  if (!round_runs(flags_in, global)) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -383,15 +472,19 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   nseg[i] = g;
   const uint32_t ell = ell_of(e.hi);
   const uint64_t code = code_of(e.lo);
+  const bool last = i + 1 == n || !same_group(e, el[i + 1]);
+  const bool can_split = ell != kHeadL && code != 0;
+  if (last) {
+    const int32_t size = i - g + 1;
+    gsize[g] = size;
+    if (can_split && size >= 2 && size > kSegSortMax) flags[1] = 1;
+  }
   if (i == g) {
     if (i > s) lcp[i] = d + (int32_t)min(ell_of(el[i - 1].hi), ell);
-    const bool act = ell != kHeadL && code != 0 && i + 1 < n && same_group(el[i + 1], e);
+    const bool act = can_split && !last;
     active_new[i] = act;
     depth_new[i] = act ? d + (int32_t)ell + 1 : 0;
-    if (act) {
-      flags[0] = 1;
-      if (i + kWave < n && same_group(el[i + kWave], e)) flags[1] = 1;
-    }
+    if (act) flags[0] = 1;
   } else if (code == 0 && ell != kHeadL) {
     lcp[i] = d + (int32_t)ell;   // identical prompts that ended together
   }
@@ -575,11 +668,15 @@ int levels_for(int64_t nb) {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
-constexpr int kSpeculativeRoundsL = 2;   // flag slots: one per speculative round, plus two
+// Refinement rounds launched before the host reads any flag. Flag pairs:
+// slot 0 for the anchor groups, slot r for round r, two more for rounds the
+// host drives afterwards.
+constexpr int kSpeculativeRounds = 2;
+constexpr int kFlagPairs = kSpeculativeRounds + 3;
 
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
-  size_t el_a, el_b, nseg, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
+  size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
       keys_b, prefix, total, flags_bytes;
   int64_t ib_stride;
   int32_t nb1, nb2;
@@ -602,6 +699,7 @@ Layout layout(int32_t n, int64_t num_nodes) {
   L.el_a = take(sizeof(ClElem) * np);
   L.el_b = take(sizeof(ClElem) * np);
   L.nseg = take(sizeof(int32_t) * nn);
+  L.gsize = take(sizeof(int32_t) * nn);
   L.depth_a = take(sizeof(int32_t) * nn);
   L.depth_b = take(sizeof(int32_t) * nn);
   L.active_a = take(nn);
@@ -613,7 +711,7 @@ Layout layout(int32_t n, int64_t num_nodes) {
   L.ib2 = take(sizeof(uint64_t) * kInBlockLevels * (size_t)L.ib_stride);
   L.st1 = take(sizeof(int32_t) * (size_t)L.levels * L.nb1);
   L.st2 = take(sizeof(uint64_t) * (size_t)L.levels * L.nb2);
-  L.flags_bytes = sizeof(int32_t) * 2 * (kSpeculativeRoundsL + 2);
+  L.flags_bytes = sizeof(int32_t) * 2 * kFlagPairs;
   L.flags = take(L.flags_bytes);
   L.keys_a = take(sizeof(uint32_t) * np);
   L.keys_b = take(sizeof(uint32_t) * np);
@@ -639,9 +737,14 @@ void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
 }
 
-constexpr int kSpeculativeRounds = kSpeculativeRoundsL;   // rounds launched before the first flag read
-
-enum class SortPath { kGated, kGlobal, kSmall };
+// Pinned host words the flag pairs are read into (one set per host thread,
+// kept for the life of the process).
+int32_t* host_flags() {
+  thread_local int32_t* p = nullptr;
+  if (p == nullptr && hipHostMalloc((void**)&p, sizeof(int32_t) * 2 * kFlagPairs, hipHostMallocDefault) != hipSuccess)
+    p = nullptr;
+  return p;
+}
 
 }  // namespace
 
@@ -675,17 +778,19 @@ peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, c
   ClElem* el_a = (ClElem*)(w + L.el_a);
   ClElem* el_b = (ClElem*)(w + L.el_b);
   int32_t* nseg = (int32_t*)(w + L.nseg);
-  int32_t* depth_a = (int32_t*)(w + L.depth_a);
-  int32_t* depth_b = (int32_t*)(w + L.depth_b);
-  uint8_t* active_a = (uint8_t*)(w + L.active_a);
-  uint8_t* active_b = (uint8_t*)(w + L.active_b);
+  int32_t* gsize = (int32_t*)(w + L.gsize);
+  // segment depth and activity after round r live in slot r & 1
+  int32_t* depth[2] = {(int32_t*)(w + L.depth_a), (int32_t*)(w + L.depth_b)};
+  uint8_t* active[2] = {(uint8_t*)(w + L.active_a), (uint8_t*)(w + L.active_b)};
   int32_t* lcp = (int32_t*)(w + L.lcp);
   uint64_t* key2 = (uint64_t*)(w + L.key2);
   int32_t* ib1 = (int32_t*)(w + L.ib1);
   uint64_t* ib2 = (uint64_t*)(w + L.ib2);
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
-  int32_t* flags = (int32_t*)(w + L.flags);   // 2 ints per round: [any active, any active group > 64]
+  int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
+  int32_t* hf = host_flags();
+  if (hf == nullptr) return fail(PEEK_ERR_OUT_OF_MEMORY, "pinned host flag buffer could not be allocated");
 
   hipLaunchKernelGGL(k_anchor_keys, dim3(blocks_for((int64_t)np + 1)), dim3(256), 0, st, tokens, offsets, n,
                      anchored ? last_node : nullptr, anchored ? match_len : nullptr, el_a, np, lcp, flags,
@@ -696,49 +801,79 @@ peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, c
   if (demand != nullptr && anchored) launch_demand_from_sorted(*t, AnchorKeys{el}, n, P, demand, st);
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
   hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, anchored ? *t : DeviceTree{}, nseg,
-                     depth_a, active_a, lcp, flags);
+                     gsize, depth[0], active[0], lcp, flags);
 
-  auto round = [&](const int32_t* fin, int32_t* fout, SortPath path) {
-    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg,
-                       depth_a, active_a, fin);
-    if (path != SortPath::kSmall) {
-      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st, path == SortPath::kGated ? fin + 1 : nullptr);
+  // Round r compares every member of an active segment with its head, sorts
+  // each segment by the new keys (in LDS, or globally when a segment is too
+  // large for that) and splits it into the next segments.
+  // kind: kSeg sorts in segments only (the round idles if a segment is too
+  // large), kGlobal sorts globally, kEither lets the device choose (both
+  // sorts are launched, each gated on the flag that selects it).
+  enum Kind { kSeg, kGlobal, kEither };
+  auto round = [&](int64_t r, const int32_t* fin, int32_t* fout, Kind kind) {
+    const int32_t* dep = depth[(r - 1) & 1];
+    const uint8_t* act = active[(r - 1) & 1];
+    const int32_t any = kind != kSeg;
+    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg, dep,
+                       act, fin, any);
+    if (kind != kSeg) {
+      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st, kind == kEither ? fin + 1 : nullptr);
       other = sorted == el ? other : el;
       el = sorted;
     }
-    if (path != SortPath::kGlobal)
-      hipLaunchKernelGGL(k_refine_small_sort, dim3(blocks_for(n, 4)), dim3(256), 0, st, n, el, nseg, active_a, fin);
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, depth_a, active_a, depth_b,
-                       active_b, lcp, fin, fout);
-    std::swap(depth_a, depth_b);
-    std::swap(active_a, active_b);
+    if (kind != kGlobal)
+      hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, el, nseg,
+                         gsize, act, fin);
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, gsize, dep, act,
+                       depth[r & 1], active[r & 1], lcp, fin, fout, any);
   };
-  // A few rounds go out before the host looks at any flag (each kernel
-  // checks the previous round's flags and idles if there is nothing to do).
-  for (int r = 1; r <= kSpeculativeRounds; ++r) round(flags + 2 * (r - 1), flags + 2 * r, SortPath::kGated);
-  int32_t* fin = flags + 2 * kSpeculativeRounds;
-  int32_t* fout = flags + 2 * (kSpeculativeRounds + 1);
-  int32_t h_flags[2] = {0, 0};
-  PEEK_HIP_TRY(hipMemcpyAsync(h_flags, fin, sizeof(h_flags), hipMemcpyDeviceToHost, st));
+  auto final_stage = [&]() {
+    hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
+                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2);
+    hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
+    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, key2, ib1, ib2,
+                       L.ib_stride, st1, st2, L.nb1, L.nb2, L.levels, cid, csz);
+  };
+  // A few rounds and the final stage go out before the host looks at any
+  // flag; each round's kernels read the previous round's flags and do
+  // nothing once the segments are settled. The first round picks its sort
+  // on the device (anchor groups are often large); later ones idle when a
+  // segment is too large for the segment sort, and the host then takes over
+  // from that round.
+  for (int r = 1; r <= kSpeculativeRounds; ++r)
+    round(r, flags + 2 * (r - 1), flags + 2 * r, r == 1 ? kEither : kSeg);
+  final_stage();
+  PEEK_HIP_TRY(hipMemcpyAsync(hf, flags, sizeof(int32_t) * 2 * (kSpeculativeRounds + 1), hipMemcpyDeviceToHost, st));
   PEEK_HIP_TRY(hipStreamSynchronize(st));
+  int64_t r = 0;
+  // round 1 ran whatever its segment sizes; a later one only without a
+  // segment beyond the segment sort
+  while (r < kSpeculativeRounds && hf[2 * r] && (r == 0 || !hf[2 * r + 1])) ++r;
+  if (!hf[2 * r]) {
+    PEEK_HIP_TRY(hipGetLastError());
+    return PEEK_OK;   // settled after round r; the final stage saw the settled order
+  }
+  // The host drives the remaining rounds from the state after round r.
   // Every round makes each still-active segment strictly deeper, so the loop
   // ends after at most (longest prompt + 1) rounds; the cap only turns a
   // broken invariant into an error instead of an endless loop.
-  int64_t rounds = 0;
+  const int32_t* fin = flags + 2 * r;
+  int32_t* spare[2] = {flags + 2 * (kSpeculativeRounds + 1), flags + 2 * (kSpeculativeRounds + 2)};
+  int32_t cur[2] = {hf[2 * r], hf[2 * r + 1]};
   constexpr int64_t kMaxRounds = int64_t(1) << 31;
-  while (h_flags[0]) {
-    if (++rounds > kMaxRounds) return fail(PEEK_ERR_DEVICE, "cluster refinement did not converge");
+  while (cur[0]) {
+    if (r > kMaxRounds) return fail(PEEK_ERR_DEVICE, "cluster refinement did not converge");
+    ++r;
+    int32_t* fout = spare[r & 1];
     PEEK_HIP_TRY(hipMemsetAsync(fout, 0, sizeof(int32_t) * 2, st));
-    round(fin, fout, h_flags[1] ? SortPath::kGlobal : SortPath::kSmall);
-    std::swap(fin, fout);
-    PEEK_HIP_TRY(hipMemcpyAsync(h_flags, fin, sizeof(h_flags), hipMemcpyDeviceToHost, st));
+    round(r, fin, fout, cur[1] != 0 ? kGlobal : kSeg);
+    fin = fout;
+    PEEK_HIP_TRY(hipMemcpyAsync(hf, fout, sizeof(int32_t) * 2, hipMemcpyDeviceToHost, st));
     PEEK_HIP_TRY(hipStreamSynchronize(st));
+    cur[0] = hf[0];
+    cur[1] = hf[1];
   }
-  hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
-                     ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2);
-  hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
-  hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, key2, ib1, ib2, L.ib_stride,
-                     st1, st2, L.nb1, L.nb2, L.levels, cid, csz);
+  final_stage();
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }

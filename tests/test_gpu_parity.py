@@ -171,3 +171,34 @@ def test_cluster_ranges_that_fill_whole_blocks(copies):
     prompts = [base + [int(x)] + rng.integers(0, 1000, size=5).tolist() for x in rng.permutation(2000)[:copies]]
     prompts += [base[:100] + [7, 7]] * 3 + [rng.integers(0, 1000, size=50).tolist() for _ in range(20)]
     run_and_compare(_w(prompts, cached=[base[:150]], T=16))
+
+
+@pytest.mark.parametrize("copies", [64, 65, 511, 512, 513, 1024, 12000])
+def test_segment_sizes_at_the_anchor(copies):
+    # one group of `copies` requests that share the cached path and the next
+    # token: ranked by one wavefront (<= 64), by one workgroup (<= 512) or
+    # sorted globally
+    rng = np.random.default_rng(1000 + copies)
+    base = rng.integers(0, 1000, size=300).tolist()
+    xs = rng.permutation(10**6)[:copies]
+    prompts = [base + [int(x)] + rng.integers(0, 1000, size=int(rng.integers(1, 6))).tolist() for x in xs]
+    prompts += [rng.integers(0, 1000, size=40).tolist() for _ in range(30)]
+    run_and_compare(_w(prompts, cached=[base[:150]], T=16))
+
+
+@pytest.mark.parametrize("copies,fan", [(600, 2), (1500, 2), (2000, 1), (9300, 2), (20000, 3)])
+def test_large_segments_in_later_rounds(copies, fan):
+    # the anchor group splits into `fan` groups in the first round, each into
+    # four in the second and into single requests in the third; a group above
+    # 512 members after the first round makes the host drive the next round
+    # with a global sort
+    rng = np.random.default_rng(copies + fan)
+    base = rng.integers(0, 1000, size=200).tolist()
+    mid = rng.integers(0, 1000, size=100).tolist()
+    mid2 = rng.integers(0, 1000, size=50).tolist()
+    prompts = []
+    for i in range(copies):
+        tail = rng.integers(0, 1000, size=int(rng.integers(1, 6))).tolist()
+        prompts.append(base + [1000 + i % fan] + mid + [2000 + int(rng.integers(0, 4))] + mid2 + [3000 + i] + tail)
+    prompts += [base[:120] + [5]] * 3 + [rng.integers(0, 1000, size=30).tolist() for _ in range(10)]
+    run_and_compare(_w(prompts, cached=[base[:150]], T=64))
