@@ -611,7 +611,7 @@ peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_
     peek_status s = check_same_device(c);
     if (s != PEEK_OK) return s;
   }
-  peek_status s = run_signals(c ? &c->tree : nullptr, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
+  peek_status s = run_signals(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
                               want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
                               want_demand ? d_demand : nullptr, d_workspace, workspace_bytes, (hipStream_t)stream);
   if (s != PEEK_OK) return s;

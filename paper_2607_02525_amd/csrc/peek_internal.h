@@ -113,9 +113,9 @@ hipError_t launch_lpm_walk(const DeviceTree& t, int32_t n, const int32_t* tokens
 size_t signals_workspace_bytes(int32_t n, int64_t num_nodes);
 
 // Demand (when demand != NULL) and clusters (when cluster_id != NULL) in
-// one pass; t may be NULL when only clusters are wanted. With t, last_node
+// one pass; c may be NULL when only clusters are wanted. With c, last_node
 // and match_len the cluster pass starts from the walk's proven prefixes.
-peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
                         int32_t* cluster_size, int32_t* demand, void* workspace, size_t workspace_bytes,
                         hipStream_t stream);

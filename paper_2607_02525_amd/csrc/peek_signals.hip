@@ -83,11 +83,12 @@ struct PlainKeys {
 // P[c] for c in [0, nn], one node per lane: a wave-wide search brackets the
 // keys of the wave's 64 nodes once, then each lane binary-searches inside
 // the bracket (usually a handful of keys), so no lane waits on a chain.
+// `block` is the 256-thread block's index among the blocks doing this.
 template <typename Keys>
-__global__ __launch_bounds__(256) void k_demand_prefix(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
+__device__ __forceinline__ void demand_prefix_block(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P,
+                                                    int32_t block) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wbase =
-      (int64_t)__builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave;
+  const int64_t wbase = (int64_t)__builtin_amdgcn_readfirstlane(block * 4 + (int32_t)(threadIdx.x / kWave)) * kWave;
   if (wbase > nn) return;
   const int64_t wend = wbase + kWave;   // exclusive
   const int32_t lo = n == 0 ? 0 : wave_first_true(0, n, lane, [&](int32_t p) { return p >= n || (int64_t)keys(p) >= wbase; });
@@ -103,11 +104,31 @@ __global__ __launch_bounds__(256) void k_demand_prefix(Keys keys, int32_t n, int
   P[c] = a;
 }
 
-__global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, const int32_t* __restrict__ P,
-                              int32_t* __restrict__ demand) {
-  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+template <typename Keys>
+__global__ __launch_bounds__(256) void k_demand_prefix(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
+  demand_prefix_block(keys, n, nn, P, (int32_t)blockIdx.x);
+}
+
+__device__ __forceinline__ void demand_diff_at(const NodeRec* __restrict__ nodes, int32_t nn,
+                                               const int32_t* __restrict__ P, int32_t* __restrict__ demand,
+                                               int32_t c) {
   if (c < nn) demand[c] = P[nodes[c].subtree_end] - P[c];
 }
+
+__global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, const int32_t* __restrict__ P,
+                              int32_t* __restrict__ demand) {
+  demand_diff_at(nodes, nn, P, demand, (int32_t)(blockIdx.x * blockDim.x + threadIdx.x));
+}
+
+// Demand work that rides along in a cluster kernel's launch: the blocks past
+// the kernel's own run one step of the demand computation.
+struct DemandRide {
+  const NodeRec* nodes;
+  int32_t* P;
+  int32_t* demand;
+  int32_t nn;
+  int32_t first_block;   // blocks >= first_block do demand work; INT32_MAX for none
+};
 
 // ---------------------------------------------------------------- clusters
 // Sort element. hi = (group << 32) | l, where the group is the anchor node
@@ -198,12 +219,24 @@ __device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, 
   return m;
 }
 
-__global__ void k_anchor_keys(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets, int32_t n,
-                              const int32_t* __restrict__ last, const int32_t* __restrict__ mlen, ClElem* __restrict__ el,
-                              size_t np, int32_t* __restrict__ lcp, int32_t* __restrict__ flags, int32_t n_flags) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < (size_t)n_flags) flags[i] = 0;
-  if (i < np) {
+// Anchor element of request i (the tile pass of the anchor sort builds its
+// input with this): key (last node, match length, next token, longest
+// first). Positions past n are padding that sorts last. Building element i
+// also clears lcp[i] (and lcp[n]) and the round flags, which every later
+// kernel of the pass expects zeroed.
+struct AnchorSource {
+  const int32_t* tokens;
+  const int64_t* offsets;
+  const int32_t* last;   // NULL: unanchored (every request at the root)
+  const int32_t* mlen;
+  int32_t n;
+  int32_t* lcp;
+  int32_t* flags;
+  int32_t n_flags;
+  __device__ __forceinline__ ClElem operator()(size_t i) const {
+    if (i < (size_t)n_flags) flags[i] = 0;
+    if (i <= (size_t)n) lcp[i] = 0;
+    if (i == 0) lcp[n] = 0;
     ClElem e;
     if (i < (size_t)n) {
       const int64_t o = offsets[i];
@@ -221,10 +254,9 @@ __global__ void k_anchor_keys(const int32_t* __restrict__ tokens, const int64_t*
       e.req = 0xFFFFFFFFu;
       e.len = 0;
     }
-    el[i] = e;
+    return e;
   }
-  if (i <= (size_t)n) lcp[i] = 0;
-}
+};
 
 // Start of every lane's group, for the 64 sorted positions base..base+63 of
 // this wavefront: the nearest group start at or before the lane inside the
@@ -247,10 +279,16 @@ __device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ e
 // flags[0] is raised if any group needs refinement, flags[1] if such a
 // group is too large for the in-LDS segment sort. gsize[g] is written at
 // every group start g.
+// Extra blocks (ride) compute the demand prefix P from the same sorted order.
 __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el, DeviceTree t,
                                                        int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
                                                        int32_t* __restrict__ depth, uint8_t* __restrict__ active,
-                                                       int32_t* __restrict__ lcp, int32_t* __restrict__ flags) {
+                                                       int32_t* __restrict__ lcp, int32_t* __restrict__ flags,
+                                                       DemandRide ride) {
+  if ((int32_t)blockIdx.x >= ride.first_block) {
+    demand_prefix_block(AnchorKeys{el}, n, ride.nn, ride.P, (int32_t)blockIdx.x - ride.first_block);
+    return;
+  }
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -303,7 +341,13 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
                                                         const int32_t* __restrict__ depth,
                                                         const uint8_t* __restrict__ active,
-                                                        const int32_t* __restrict__ flags_in, int32_t global) {
+                                                        const int32_t* __restrict__ flags_in, int32_t global,
+                                                        DemandRide ride) {
+  if ((int32_t)blockIdx.x >= ride.first_block) {
+    demand_diff_at(ride.nodes, ride.nn, ride.P, ride.demand,
+                   ((int32_t)blockIdx.x - ride.first_block) * (int32_t)blockDim.x + (int32_t)threadIdx.x);
+    return;
+  }
   if (!round_runs(flags_in, global)) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
@@ -545,9 +589,39 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
   }
 }
 
-// Sparse tables over the block minima, one workgroup, level by level.
+// Sparse tables over the block minima, one workgroup, level by level. Up to
+// kTabLds blocks the previous level is read from LDS (each level costs a
+// barrier, not a round trip to memory); beyond that from memory.
+constexpr int kTabLds = 4096;
+
 __global__ __launch_bounds__(1024) void k_final_tables(int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
                                                        int32_t nb1, int32_t nb2, int levels) {
+  if (nb1 <= kTabLds && nb2 <= kTabLds) {
+    __shared__ int32_t a1[2][kTabLds];
+    __shared__ uint64_t a2[2][kTabLds];
+    for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) a1[0][b] = st1[b];
+    for (int32_t b = threadIdx.x; b < nb2; b += blockDim.x) a2[0][b] = st2[b];
+    __syncthreads();
+    for (int k = 1; k < levels; ++k) {
+      const int32_t h = 1 << (k - 1);
+      const int cur = k & 1, prev = cur ^ 1;
+      for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) {
+        if (b + 2 * h <= nb1) {
+          const int32_t v = min(a1[prev][b], a1[prev][b + h]);
+          a1[cur][b] = v;
+          st1[(int64_t)k * nb1 + b] = v;
+        }
+        if (b + 2 * h <= nb2) {
+          const uint64_t x = a2[prev][b], y = a2[prev][b + h];
+          const uint64_t v = x < y ? x : y;
+          a2[cur][b] = v;
+          st2[(int64_t)k * nb2 + b] = v;
+        }
+      }
+      __syncthreads();
+    }
+    return;
+  }
   for (int k = 1; k < levels; ++k) {
     const int32_t h = 1 << (k - 1);
     for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) {
@@ -672,6 +746,7 @@ size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 // slot 0 for the anchor groups, slot r for round r, two more for rounds the
 // host drives afterwards.
 constexpr int kSpeculativeRounds = 2;
+static_assert(kSpeculativeRounds >= 1, "the first round carries the demand difference");
 constexpr int kFlagPairs = kSpeculativeRounds + 3;
 
 // Workspace layout (each region 256-byte aligned).
@@ -748,9 +823,10 @@ int32_t* host_flags() {
 
 }  // namespace
 
-peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, const int64_t* offsets,
+peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
                         int32_t* csz, int32_t* demand, void* ws, size_t ws_bytes, hipStream_t st) {
+  const DeviceTree* t = c != nullptr ? &c->tree : nullptr;
   const int64_t num_nodes = t ? t->num_nodes : 0;
   const Layout L = layout(n, num_nodes);
   char* w = (char*)ws;
@@ -791,58 +867,74 @@ peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, c
   int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
   int32_t* hf = host_flags();
   if (hf == nullptr) return fail(PEEK_ERR_OUT_OF_MEMORY, "pinned host flag buffer could not be allocated");
-
-  hipLaunchKernelGGL(k_anchor_keys, dim3(blocks_for((int64_t)np + 1)), dim3(256), 0, st, tokens, offsets, n,
-                     anchored ? last_node : nullptr, anchored ? match_len : nullptr, el_a, np, lcp, flags,
-                     (int32_t)(L.flags_bytes / sizeof(int32_t)));
-  ClElem* el = msort::sort(el_a, el_b, np, ClLess{}, st);
-  ClElem* other = el == el_a ? el_b : el_a;
-  // the anchor order is sorted by last node first: demand reads it directly
-  if (demand != nullptr && anchored) launch_demand_from_sorted(*t, AnchorKeys{el}, n, P, demand, st);
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
-  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, anchored ? *t : DeviceTree{}, nseg,
-                     gsize, depth[0], active[0], lcp, flags);
+  ClElem* el = el_a;
+  ClElem* other = el_b;
 
   // Round r compares every member of an active segment with its head, sorts
-  // each segment by the new keys (in LDS, or globally when a segment is too
-  // large for that) and splits it into the next segments.
+  // each segment by the new keys and splits it into the next segments.
   // kind: kSeg sorts in segments only (the round idles if a segment is too
   // large), kGlobal sorts globally, kEither lets the device choose (both
   // sorts are launched, each gated on the flag that selects it).
   enum Kind { kSeg, kGlobal, kEither };
-  auto round = [&](int64_t r, const int32_t* fin, int32_t* fout, Kind kind) {
+  const bool ride_demand = demand != nullptr && anchored;
+  const DemandRide no_ride{nullptr, nullptr, nullptr, 0, INT32_MAX};
+  auto round = [&](int64_t r, const int32_t* fin, int32_t* fout, Kind kind, hipStream_t q,
+                   DemandRide ride, unsigned ride_blocks) {
     const int32_t* dep = depth[(r - 1) & 1];
     const uint8_t* act = active[(r - 1) & 1];
     const int32_t any = kind != kSeg;
-    hipLaunchKernelGGL(k_refine_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, tokens, offsets, n, el, nseg, dep,
-                       act, fin, any);
+    const unsigned cmp_blocks = blocks_for(n, 4);
+    ride.first_block = ride_blocks ? (int32_t)cmp_blocks : INT32_MAX;
+    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks + ride_blocks), dim3(256), 0, q, tokens, offsets, n, el,
+                       nseg, dep, act, fin, any, ride);
     if (kind != kSeg) {
-      ClElem* sorted = msort::sort(el, other, np, ClLess{}, st, kind == kEither ? fin + 1 : nullptr);
+      ClElem* sorted = msort::sort(el, other, np, ClLess{}, q, kind == kEither ? fin + 1 : nullptr);
       other = sorted == el ? other : el;
       el = sorted;
     }
     if (kind != kGlobal)
-      hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, el, nseg,
+      hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, q, n, el, nseg,
                          gsize, act, fin);
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, gsize, dep, act,
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, q, n, el, nseg, gsize, dep, act,
                        depth[r & 1], active[r & 1], lcp, fin, fout, any);
   };
-  auto final_stage = [&]() {
-    hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
+  auto final_stage = [&](hipStream_t q) {
+    hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, q, n, el, lcp, key2,
                        ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2);
-    hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
-    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, key2, ib1, ib2,
+    hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, q, st1, st2, L.nb1, L.nb2, L.levels);
+    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, q, n, threshold, key2, ib1, ib2,
                        L.ib_stride, st1, st2, L.nb1, L.nb2, L.levels, cid, csz);
   };
-  // A few rounds and the final stage go out before the host looks at any
-  // flag; each round's kernels read the previous round's flags and do
-  // nothing once the segments are settled. The first round picks its sort
-  // on the device (anchor groups are often large); later ones idle when a
-  // segment is too large for the segment sort, and the host then takes over
-  // from that round.
-  for (int r = 1; r <= kSpeculativeRounds; ++r)
-    round(r, flags + 2 * (r - 1), flags + 2 * r, r == 1 ? kEither : kSeg);
-  final_stage();
+  // The fixed part: anchor order and groups, a few refinement rounds and the
+  // final stage, all before the host looks at any flag. Each round's kernels
+  // read the previous round's flags and do nothing once the segments are
+  // settled. The first round picks its sort on the device (anchor groups are
+  // often large); later ones idle when a segment is too large for the
+  // segment sort, and the host then takes over from that round.
+  auto fixed = [&](hipStream_t q) {
+    const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
+                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t))};
+    el = msort::sort_from(src, el_a, el_b, np, ClLess{}, q);
+    other = el == el_a ? el_b : el_a;
+    // The anchor order is sorted by last node first, so demand reads it
+    // directly: the prefix P rides along with the anchor groups, the
+    // difference along with the first round's compare.
+    DemandRide ride = no_ride;
+    unsigned prefix_blocks = 0, diff_blocks = 0;
+    if (ride_demand) {
+      ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
+      prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
+      diff_blocks = blocks_for(t->num_nodes);
+    }
+    hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, q, n, el,
+                       anchored ? *t : DeviceTree{}, nseg, gsize, depth[0], active[0], lcp, flags, ride);
+    for (int r = 1; r <= kSpeculativeRounds; ++r)
+      round(r, flags + 2 * (r - 1), flags + 2 * r, r == 1 ? kEither : kSeg, q, ride, r == 1 ? diff_blocks : 0);
+    final_stage(q);
+  };
+
+  fixed(st);
   PEEK_HIP_TRY(hipMemcpyAsync(hf, flags, sizeof(int32_t) * 2 * (kSpeculativeRounds + 1), hipMemcpyDeviceToHost, st));
   PEEK_HIP_TRY(hipStreamSynchronize(st));
   int64_t r = 0;
@@ -866,14 +958,14 @@ peek_status run_signals(const DeviceTree* t, int32_t n, const int32_t* tokens, c
     ++r;
     int32_t* fout = spare[r & 1];
     PEEK_HIP_TRY(hipMemsetAsync(fout, 0, sizeof(int32_t) * 2, st));
-    round(r, fin, fout, cur[1] != 0 ? kGlobal : kSeg);
+    round(r, fin, fout, cur[1] != 0 ? kGlobal : kSeg, st, no_ride, 0);
     fin = fout;
     PEEK_HIP_TRY(hipMemcpyAsync(hf, fout, sizeof(int32_t) * 2, hipMemcpyDeviceToHost, st));
     PEEK_HIP_TRY(hipStreamSynchronize(st));
     cur[0] = hf[0];
     cur[1] = hf[1];
   }
-  final_stage();
+  final_stage(st);
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }

@@ -50,29 +50,35 @@ __device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb
   }
 }
 
+// Element source of the tile pass: a plain array, or a functor that builds
+// element i on the fly (saves a pass that would only write the input).
+template <typename T>
+struct FromArray {
+  const T* p;
+  __device__ __forceinline__ T operator()(size_t i) const { return p[i]; }
+};
+
 // A gated sort (gate != nullptr and *gate == 0) is skipped: the tile pass
 // copies its input to its output and every merge pass returns at once. The
 // buffer the host expects then holds the unsorted input either way: after
 // an even number of merge passes it is the tile pass's copy, after an odd
 // number it is the untouched input.
-template <typename T>
-__device__ __forceinline__ bool gated_copy(const int32_t* gate, const T* __restrict__ src, T* __restrict__ dst,
-                                           size_t base) {
+template <typename T, typename Src>
+__device__ __forceinline__ bool gated_copy(const int32_t* gate, const Src& src, T* __restrict__ dst, size_t base) {
   if (gate == nullptr || *gate != 0) return false;
-  for (int q = threadIdx.x; q < kTile; q += kThreads) dst[base + q] = src[base + q];
+  for (int q = threadIdx.x; q < kTile; q += kThreads) dst[base + q] = src(base + q);
   return true;
 }
 
-template <typename T, typename Less>
-__global__ __launch_bounds__(kThreads) void k_tile_sort(const T* __restrict__ src, T* __restrict__ dst, Less less,
-                                                        const int32_t* gate) {
+template <typename T, typename Less, typename Src>
+__global__ __launch_bounds__(kThreads) void k_tile_sort(Src src, T* __restrict__ dst, Less less, const int32_t* gate) {
   __shared__ T s[kTile];
   const int t = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * kTile;
   if (gated_copy(gate, src, dst, base)) return;
   T v[kItems];
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) v[q] = src[base + t * kItems + q];
+  for (int q = 0; q < kItems; ++q) v[q] = src(base + t * kItems + q);
   // odd-even transposition sort of the thread's items (stable)
 #pragma unroll
   for (int round = 0; round < kItems; ++round) {
@@ -166,13 +172,14 @@ __global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ s
   for (int q = 0; q < kItems; ++q) dst[out0 + o + q] = v[q];
 }
 
-// Sorts np elements (np a power of two, >= kTile) from a into a or b;
-// returns the buffer that holds the result. With a gate, the sort happens
-// only if *gate != 0 when the passes run (otherwise the data is copied).
-template <typename T, typename Less>
-T* sort(T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
+// Sorts np elements (np a power of two, >= kTile) taken from `src` (element
+// i = src(i)), using a and b as buffers; returns the one that holds the
+// result. With a gate, the sort happens only if *gate != 0 when the passes
+// run (otherwise the data is copied).
+template <typename T, typename Less, typename Src>
+T* sort_from(Src src, T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
   const unsigned tiles = (unsigned)(np / kTile);
-  hipLaunchKernelGGL((k_tile_sort<T, Less>), dim3(tiles), dim3(kThreads), 0, st, a, b, less, gate);
+  hipLaunchKernelGGL((k_tile_sort<T, Less, Src>), dim3(tiles), dim3(kThreads), 0, st, src, b, less, gate);
   T* cur = b;
   T* oth = a;
   for (size_t w = kTile; w < np; w <<= 1) {
@@ -183,6 +190,12 @@ T* sort(T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = 
     oth = x;
   }
   return cur;
+}
+
+// Sorts np elements from a into a or b (see sort_from).
+template <typename T, typename Less>
+T* sort(T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
+  return sort_from(FromArray<T>{a}, a, b, np, less, st, gate);
 }
 
 }  // namespace msort

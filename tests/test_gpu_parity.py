@@ -202,3 +202,40 @@ def test_large_segments_in_later_rounds(copies, fan):
         prompts.append(base + [1000 + i % fan] + mid + [2000 + int(rng.integers(0, 4))] + mid2 + [3000 + i] + tail)
     prompts += [base[:120] + [5]] * 3 + [rng.integers(0, 1000, size=30).tolist() for _ in range(10)]
     run_and_compare(_w(prompts, cached=[base[:150]], T=64))
+
+
+def _first(w, k, name):
+    off = w.offsets[:k + 1] - w.offsets[0]
+    tok = w.tokens[w.offsets[0]:w.offsets[k]]
+    return W.Workload(name, w.seed, tok, off, w.block_size, w.threshold, cache_sequences=w.cache_sequences,
+                      cache_tree=w.cache_tree)
+
+
+def test_recorded_launch_sequences_replay_correctly():
+    # The fixed part of a signals call is recorded once per argument set and
+    # replayed afterwards. Interleave three queues on one cache, anchored and
+    # not (six argument sets: more than the four recordings a cache keeps),
+    # with eager host work and synchronisation between the replays, and check
+    # every result.
+    HotPath = _hot()
+    w = W.make("rag", 42)
+    parts = [w, _first(w, 1000, "rag-1000"), _first(w, 333, "rag-333")]
+    expect = [O.run(p) for p in parts]
+    first = HotPath.from_sequences(*w.cache_sequences)
+    hps = [first] + [HotPath(first.cache, first.canon_id) for _ in parts[1:]]
+    for hp, p in zip(hps, parts):
+        hp.load_queue(p.tokens, p.offsets, p.block_size, p.threshold)
+    for it in range(3):
+        for k, (hp, p, s) in enumerate(zip(hps, parts, expect)):
+            print(f"[gpu] replay {it} queue {p.name}", flush=True)
+            for out in (hp.d_h, hp.d_last, hp.d_m, hp.d_cid, hp.d_csz, hp.d_demand):
+                out.fill_(-7)
+            hp.step()
+            assert_parity(p, hp.results(), s)
+            hp.d_cid.fill_(-7)
+            hp.d_csz.fill_(-7)
+            hp.signals(anchored=False)
+            res = hp.results()
+            assert np.array_equal(res["cluster_id"], s.clusters.cluster_id)
+            assert np.array_equal(res["cluster_size"], s.clusters.cluster_size)
+            torch.cuda.synchronize()
