@@ -58,6 +58,8 @@ def _load():
     lib.oracle_demand.argtypes = [ctypes.c_void_p, ctypes.c_int64, _c_i32p, _c_i64p]
     lib.oracle_clusters.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, ctypes.c_int64,
                                     _c_i64p, _c_i64p, _c_i64p]
+    lib.oracle_clpm.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int64,
+                                _c_i64p, _c_i32p, _c_i32p]
     _lib = lib
     return lib
 
@@ -177,6 +179,30 @@ def clusters(tokens, offsets, threshold: int) -> ClusterResult:
     return ClusterResult(share, cid, csz)
 
 
+@dataclass
+class ClpmResult:
+    score: np.ndarray      # ancestor score per request (int64)
+    section: np.ndarray    # 0 warm, 1 cold pioneer, 2 cold sibling (int32)
+    has_sharing: bool
+
+
+def clpm(tokens, offsets, h, tau: int, theta: int) -> ClpmResult:
+    """Ancestor score, section and has_sharing (Sec. 3.2, Alg. 2)."""
+    tokens, offsets = _i32(tokens), _i64(offsets)
+    n = len(offsets) - 1
+    h = _i64(h)
+    score = np.empty(n, dtype=np.int64)
+    section = np.empty(n, dtype=np.int32)
+    sharing = np.zeros(1, dtype=np.int32)
+    if tokens.size == 0:
+        tokens = np.zeros(1, dtype=np.int32)
+    if h.size == 0:
+        h = np.zeros(1, dtype=np.int64)
+    _load().oracle_clpm(n, _p32(tokens), _p64(offsets), _p64(h), int(tau), int(theta), _p64(score), _p32(section),
+                        _p32(sharing))
+    return ClpmResult(score, section, bool(sharing[0]))
+
+
 def cache_tree_of(workload) -> Tree:
     """The oracle's own cache tree for a workload (sequences or description)."""
     if workload.cache_tree is not None:
@@ -190,6 +216,7 @@ class Signals:
     lpm: LpmResult
     demand: np.ndarray
     clusters: ClusterResult
+    clpm: ClpmResult
 
 
 def run(workload) -> Signals:
@@ -198,4 +225,5 @@ def run(workload) -> Signals:
     l = lpm(t, workload.tokens, workload.offsets, workload.block_size)
     d = demand(t, l.last_node)
     c = clusters(workload.tokens, workload.offsets, workload.threshold)
-    return Signals(t, l, d, c)
+    g = clpm(workload.tokens, workload.offsets, l.h, workload.tau, workload.theta)
+    return Signals(t, l, d, c, g)

@@ -24,11 +24,19 @@
 //    only if its depth reaches the threshold T; otherwise the request is a
 //    singleton (id -1, size 1). Cluster id = smallest arrival index among the
 //    requests whose cluster is that same node.
+//  * The rest of cLPM's per-request signal vector (Sec. 3.2 and Alg. 2):
+//    the ancestor score, the sum over the nodes v on the request's path in
+//    the pending tree of pending_count(v) times the length of v's edge; the
+//    section (warm when h > tau, otherwise pioneer for the first cold request
+//    in arrival order whose first theta tokens were not yet claimed, sibling
+//    after that); and has_sharing, whether some child of the pending tree's
+//    root is on the path of two or more requests.
 //
 // Build: g++ -O2 -std=c++17 -shared -fPIC oracle.cpp -o liboracle.so
 #include <cstdint>
 #include <cstring>
 #include <map>
+#include <set>
 #include <vector>
 
 namespace {
@@ -378,6 +386,53 @@ void oracle_clusters(int64_t n, const int32_t* tokens, const int64_t* offsets, i
       cluster_size_out[r] = 1;
     }
   }
+}
+
+// The rest of the cLPM signal vector. score_out[r]: walk r's path in the
+// pending tree and add pending_count * edge length of every node on it.
+// section_out[r]: 0 warm (h[r] > tau); else, scanning requests in arrival
+// order, 1 if the token string prompt[:theta] (the whole prompt when it is
+// shorter) has not been claimed by an earlier cold request (it is claimed
+// now), 2 otherwise. *has_sharing_out: 1 if a child of the pending root has
+// pending_count >= 2, else 0.
+void oracle_clpm(int64_t n, const int32_t* tokens, const int64_t* offsets, const int64_t* h, int64_t tau,
+                 int64_t theta, int64_t* score_out, int32_t* section_out, int32_t* has_sharing_out) {
+  PendingTree T;
+  T.root = T.make();
+  for (int64_t r = 0; r < n; ++r) pending_insert(&T, tokens + offsets[r], offsets[r + 1] - offsets[r]);
+  for (int64_t r = 0; r < n; ++r) {
+    const int32_t* p = tokens + offsets[r];
+    int64_t len = offsets[r + 1] - offsets[r];
+    PNode* node = T.root;
+    int64_t score = node->pending_count * node->elen;
+    int64_t d = 0;
+    while (d < len) {
+      node = node->kids.at(p[d]);
+      d += node->elen;
+      score += node->pending_count * node->elen;
+    }
+    score_out[r] = score;
+  }
+  std::set<std::vector<int32_t>> seen;
+  for (int64_t r = 0; r < n; ++r) {
+    if (h[r] > tau) {
+      section_out[r] = 0;
+      continue;
+    }
+    const int64_t len = offsets[r + 1] - offsets[r];
+    const int64_t k = len < theta ? len : theta;
+    std::vector<int32_t> prefix(tokens + offsets[r], tokens + offsets[r] + k);
+    if (seen.count(prefix)) {
+      section_out[r] = 2;
+    } else {
+      section_out[r] = 1;
+      seen.insert(prefix);
+    }
+  }
+  int32_t sharing = 0;
+  for (const auto& kv : T.root->kids)
+    if (kv.second->pending_count >= 2) sharing = 1;
+  *has_sharing_out = sharing;
 }
 
 }  // extern "C"

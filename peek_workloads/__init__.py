@@ -31,6 +31,13 @@ VOCAB_LARGE = 128256
 PAPER_SEEDS = (42, 142, 242)
 
 
+# cLPM section parameters (Sec. 3.2): a request is warm when its hit exceeds
+# tau tokens; cold requests are grouped by their first theta tokens. The
+# paper fixes theta = 32 and gives no value for tau; 0 makes any cached block
+# warm.
+THETA = 32
+TAU_DEFAULT = 0
+
 @dataclass
 class Workload:
     name: str
@@ -42,6 +49,8 @@ class Workload:
     cache_sequences: tuple | None = None   # (tokens int32, offsets int64)
     cache_tree: tuple | None = None        # (parent int32, edge_offsets int64, edge_tokens int32)
     meta: dict = field(default_factory=dict)
+    tau: int = TAU_DEFAULT                 # warm threshold on the LPM hit (cLPM sections)
+    theta: int = THETA
 
     @property
     def n(self) -> int:
@@ -521,8 +530,9 @@ def worked_thrashing(prompt_len: int = 2048, suffix_len: int = 32, seed: int = 0
         live.append(np.concatenate([tenant[t], s]))
     tok, off = pack(live)
     ctok, coff = pack([])
+    names = [f"{'ABC'[t]}{order[:i + 1].count(t)}" for i, t in enumerate(order)]
     return Workload("x1", seed, tok, off, 16, 256, cache_sequences=(ctok, coff),
-                    meta={"tenant_of": np.array(order)})
+                    meta={"tenant_of": np.array(order), "names": names})
 
 
 def worked_dualwalk(sys_len: int = 1000, part_len: int = 300, seed: int = 0) -> Workload:

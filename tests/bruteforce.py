@@ -109,3 +109,30 @@ def clusters(prompts, threshold):
             size.append(1)
             cid.append(-1)
     return np.array(share), np.array(cid), np.array(size)
+
+
+# cLPM signal vector (Sec. 3.2, Alg. 2):
+#   score_r      = sum_{r'} LCP(p_r, p_r')  (r' = r included: LCP = |p_r|)
+#                  Every node on r's pending-tree path at depth d is passed by
+#                  exactly the requests that share >= d tokens with p_r, so the
+#                  sum of pending_count * edge length telescopes to this.
+#   section_r    = 0 if h_r > tau; else, in arrival order, 1 for the first cold
+#                  request with a given p_r[:theta] and 2 for the later ones
+#   has_sharing  = some pair of requests shares their first token
+
+
+def clpm(prompts, h, tau, theta):
+    n = len(prompts)
+    score = [sum(lcp(prompts[r], prompts[q]) for q in range(n)) for r in range(n)]
+    seen = set()
+    section = []
+    for r in range(n):
+        if h[r] > tau:
+            section.append(0)
+        elif prompts[r][:theta] in seen:
+            section.append(2)
+        else:
+            section.append(1)
+            seen.add(prompts[r][:theta])
+    sharing = any(lcp(prompts[a], prompts[b]) >= 1 for a in range(n) for b in range(a + 1, n))
+    return np.array(score), np.array(section), sharing

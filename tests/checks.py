@@ -69,3 +69,41 @@ def check_clusters(w, cid, csz, lcp_fn=None):
         k = min(len(a), len(b), w.threshold)
         assert len(a) >= w.threshold and len(b) >= w.threshold
         assert np.array_equal(a[:k], b[:k])
+
+
+def lcp_with_all(w, r):
+    """Sum over every request q (q = r included) of LCP(p_r, p_q)."""
+    a = w.prompt(r)
+    total = 0
+    for q in range(w.n):
+        b = w.prompt(q)
+        k = min(len(a), len(b))
+        diff = np.nonzero(a[:k] != b[:k])[0]
+        total += int(diff[0]) if diff.size else k
+    return total
+
+
+def check_clpm(w, h, score, section, has_sharing, samples=4, seed=0):
+    h = np.asarray(h, dtype=np.int64)
+    score = np.asarray(score, dtype=np.int64)
+    section = np.asarray(section, dtype=np.int64)
+    lens = w.lengths
+    assert np.all(np.isin(section, (0, 1, 2)))
+    assert np.array_equal(section == 0, h > w.tau)
+    assert np.all(score >= lens)
+    # exactly one pioneer per theta-prefix class of cold requests: the earliest
+    first = {}
+    for r in np.nonzero(section != 0)[0]:
+        key = w.prompt(int(r))[:w.theta].tobytes() + b"|" + str(min(int(lens[r]), w.theta)).encode()
+        if key not in first:
+            first[key] = int(r)
+            assert section[r] == 1
+        else:
+            assert section[r] == 2
+    # has_sharing: two requests start with the same token
+    heads = np.array([w.prompt(r)[0] for r in range(w.n) if lens[r] > 0])
+    assert has_sharing == bool(heads.size and np.unique(heads).size < heads.size)
+    # score closed form on a few sampled requests
+    rng = np.random.default_rng(seed)
+    for r in rng.choice(w.n, size=min(samples, w.n), replace=False):
+        assert score[r] == lcp_with_all(w, int(r))

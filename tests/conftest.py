@@ -9,3 +9,14 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: full-size workloads")
+
+
+def pytest_collection_modifyitems(config, items):
+    # Full-size oracle runs take minutes of host time; they run only on request.
+    if os.environ.get("PEEK_SLOW") == "1":
+        return
+    import pytest
+    skip = pytest.mark.skip(reason="full-size workload; set PEEK_SLOW=1 to run")
+    for item in items:
+        if "slow" in item.keywords:
+            item.add_marker(skip)

@@ -51,6 +51,12 @@ def test_oracle_matches_brute_force_on_sequences(seed, vocab, B, T):
     assert np.array_equal(c.share, share)
     assert np.array_equal(c.cluster_id, cid)
     assert np.array_equal(c.cluster_size, csz)
+    for tau, theta in ((0, 32), (B, 2), (-1, 1), (8, 5)):
+        score, section, sharing = BF.clpm(prompts, r.h, tau, theta)
+        g = O.clpm(w.tokens, w.offsets, r.h, tau, theta)
+        assert np.array_equal(g.score, score)
+        assert np.array_equal(g.section, section)
+        assert g.has_sharing == sharing
 
 
 @pytest.mark.parametrize("seed", range(12))
@@ -134,6 +140,45 @@ def test_worked_example_thrashing():
     assert list(s.clusters.cluster_id) == g["expected_cluster_id"]
     n_clusters = len(set(s.clusters.cluster_id.tolist()))
     assert (w.n - n_clusters) / w.n == g["expected_cluster_order_hit_fraction"]
+
+
+def test_brute_force_clpm_on_duplicates_prefixes_and_short_prompts():
+    # identical prompts, prompts that prefix others, prompts shorter than
+    # theta and empty prompts, against the literal section rule
+    prompts = [(1, 2, 3), (1, 2, 3), (1, 2), (), (1, 2, 3, 4), (), (5,), (1, 2, 9), (5,), (1, 2, 3)]
+    tok, off = W.pack([np.asarray(p, np.int32) for p in prompts])
+    for h in ([0] * 10, [0, 3, 0, 0, 16, 0, 0, 2, 0, 0]):
+        for tau, theta in ((0, 2), (0, 3), (2, 1), (0, 32), (15, 4)):
+            score, section, sharing = BF.clpm(prompts, h, tau, theta)
+            g = O.clpm(tok, off, np.asarray(h), tau, theta)
+            assert np.array_equal(g.score, score)
+            assert np.array_equal(g.section, section)
+            assert g.has_sharing == sharing
+    # no two prompts share a first token: no sharing
+    tok, off = W.pack([np.asarray(p, np.int32) for p in [(1, 2), (3,), (), (), (4, 1)]])
+    assert not O.clpm(tok, off, np.zeros(5), 0, 32).has_sharing
+
+
+def test_worked_example_thrashing_sections_and_scores():
+    # Sec. 2's queue is all cold (nothing cached): under Alg. 2's section rule
+    # the first request of each tenant (A1, B1, C1) is its cold pioneer and the
+    # other five are siblings. Each tenant's requests share the 2048-token
+    # tenant prompt and differ right after it, so a request's score is its own
+    # length plus 2048 per other request of the tenant: the two size-3
+    # tenants tie and outrank the size-2 tenant.
+    w = W.worked_thrashing()
+    s = O.run(w)
+    assert list(s.clpm.section) == [1, 1, 1, 2, 2, 2, 2, 2]
+    tenant = w.meta["tenant_of"]
+    for r in range(w.n):
+        others = int((tenant == tenant[r]).sum()) - 1
+        assert s.clpm.score[r] == w.lengths[r] + 2048 * others
+    assert s.clpm.has_sharing
+    # cLPM's lane-A key (section, -h, -score, -|cluster|, arrival) puts the
+    # pioneers first and keeps larger clusters ahead inside each section
+    key = sorted(range(w.n), key=lambda r: (s.clpm.section[r], -s.lpm.h[r], -s.clpm.score[r],
+                                            -s.clusters.cluster_size[r], r))
+    assert [w.meta["names"][r] for r in key] == ["A1", "B1", "C1", "A2", "B2", "A3", "B3", "C2"]
 
 
 def test_worked_example_dual_walk():
@@ -247,6 +292,7 @@ def test_invariants_hold_on_oracle_outputs(name, seed):
     checks.check_lpm(w, parent, depth, s.lpm.m, s.lpm.h, s.lpm.last_node)
     checks.check_demand(w.n, parent, s.lpm.last_node, s.demand)
     checks.check_clusters(w, s.clusters.cluster_id, s.clusters.cluster_size)
+    checks.check_clpm(w, s.lpm.h, s.clpm.score, s.clpm.section, s.clpm.has_sharing, seed=seed)
 
 
 @pytest.mark.slow

@@ -29,6 +29,15 @@ MUTANTS = {
                                "      mid->depth = node->depth + k + 1;\n      child->edge.erase"),
     "reachability_check_dropped": ("if (seen != num_nodes) { free_tree(t); return nullptr; }", ""),
     "last_node_is_parent_on_partial": ("  return {d, c};", "  return {d, (c->parent && d < c->depth) ? c->parent : c};"),
+    "score_leaves_out_own_request": ("      score += node->pending_count * node->elen;",
+                                     "      score += (node->pending_count - 1) * node->elen;"),
+    "score_weights_by_depth": ("      score += node->pending_count * node->elen;",
+                               "      score += node->pending_count * node->depth;"),
+    "warm_is_at_least_tau": ("    if (h[r] > tau) {", "    if (h[r] >= tau) {"),
+    "section_prefix_too_short": ("const int64_t k = len < theta ? len : theta;",
+                                 "const int64_t k = len < theta - 1 ? len : theta - 1;"),
+    "sharing_counts_single_requests": ("if (kv.second->pending_count >= 2) sharing = 1;",
+                                       "if (kv.second->pending_count >= 1) sharing = 1;"),
 }
 
 PINS = "brute_force or worked or unary or invalid or tiny or agentic"
