@@ -203,6 +203,19 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (lpm {lpm_ms.mean():.3f} ms, signals {sig_ms.mean():.3f} ms)")
 
+    # the rest of cLPM's signal vector (score, section, has_sharing) on the
+    # same queue: one peek_clpm_signals call replaces peek_queue_signals
+    clpm_ms = []
+    for i in range(max(3, args.steps // 2) + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        hp.clpm(w.tau, w.theta)
+        b.record(stream)
+        torch.cuda.synchronize()
+        if i > 0:
+            clpm_ms.append(a.elapsed_time(b))
+    log(f"cLPM signals (clusters + demand + score + section + has_sharing): {np.mean(clpm_ms):.3f} ms")
+
     res = hp.results()
     exp = peek_cache_export(hp.cache)
     b_alg, parts = walk_algorithmic_bytes(w.lengths.astype(np.int64), res["match_len"].astype(np.int64),
@@ -254,6 +267,7 @@ def main():
         "lpm_queries_per_s": round(w.n / lpm_avg_s, 1),
         "lpm_ms": round(float(lpm_ms.mean()), 4),
         "signals_ms": round(float(sig_ms.mean()), 4),
+        "clpm_signals_ms": round(float(np.mean(clpm_ms)), 4),
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,

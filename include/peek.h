@@ -163,12 +163,14 @@ peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_
  * them again; with either pointer NULL (or no cache) it starts from scratch.
  * The results are the same either way.
  *
- * Scratch comes only from d_workspace (device, 256-byte aligned, at least
+ * Scratch comes from d_workspace (device, 256-byte aligned, at least
  * peek_queue_signals_workspace(n, num_nodes) bytes, num_nodes = 0 without a
- * cache); the library allocates nothing here. The cluster pass refines a
- * sort in rounds and synchronizes `stream` once per round to read a device
- * flag, so this call returns after the stream has finished its work.
- * threshold >= 1.
+ * cache); apart from a few pinned host words allocated once per calling
+ * thread the library allocates nothing here. The cluster pass refines a sort
+ * in rounds: it runs a few rounds and the final stage, then synchronizes
+ * `stream` to read device flags, and synchronizes once more per further
+ * round when the queue needs more; this call returns after the stream has
+ * finished its work. threshold >= 1.
  * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
  * ---------------------------------------------------------------------- */
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes);
@@ -178,6 +180,33 @@ peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t
                                const int32_t* d_match_len, int32_t threshold,
                                int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
                                void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * peek_clpm_signals: everything peek_queue_signals computes plus the rest
+ * of cLPM's per-request signal vector (Sec. 3.2 signals (2)-(3); Alg. 2,
+ * which reads them as section, score and cluster info):
+ *   d_score[r]   = sum over the nodes v on r's path in the pending tree of
+ *                  pending_count(v) * |edge(v)|  (int64; equals the sum over
+ *                  every request q, q = r included, of LCP(p_r, p_q))
+ *   d_section[r] = 0 (warm) if d_h[r] > tau; otherwise, scanning requests in
+ *                  arrival order, 1 (cold pioneer) for the first cold request
+ *                  whose prompt[:theta] (whole prompt when shorter) is new
+ *                  among cold requests, 2 (cold sibling) for later ones (int32)
+ *   *d_has_sharing = 1 if two requests share their first token, else 0
+ *                  (the pending tree's check over its root's children)
+ * d_h is the LPM hit per request (peek_lpm_batch's d_h, or any int32 hit
+ * vector); it is needed when d_section is given. d_score, d_section and
+ * d_has_sharing are each optional (NULL: not written); d_cluster_id and
+ * d_cluster_size are required. theta >= 0 (the paper uses 32); tau is any
+ * int32 (the paper leaves it unset). Same workspace, synchronization and
+ * errors as peek_queue_signals.
+ * ---------------------------------------------------------------------- */
+peek_status peek_clpm_signals(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
+                              const int64_t* d_offsets, const int32_t* d_h, const int32_t* d_last_node,
+                              const int32_t* d_match_len, int32_t threshold, int32_t tau, int32_t theta,
+                              int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
+                              int64_t* d_score, int32_t* d_section, int32_t* d_has_sharing,
+                              void* d_workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -52,6 +52,9 @@ EXPORTS = [
     ("peek_queue_signals_workspace", ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
     ("peek_queue_signals", ctypes.c_int,
      [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("peek_clpm_signals", ctypes.c_int,
+     [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
+      _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
 ]
 
 for _name, _res, _args in EXPORTS:
@@ -209,3 +212,15 @@ def peek_queue_signals(cache, tokens, offsets, last_node, match_len, threshold: 
                                    _dptr(last_node), _dptr(match_len), int(threshold), _dptr(cluster_id),
                                    _dptr(cluster_size), _dptr(demand), _dptr(workspace), ws_bytes,
                                    _stream(stream)))
+
+
+def peek_clpm_signals(cache, tokens, offsets, h, last_node, match_len, threshold: int, tau: int, theta: int,
+                      cluster_id, cluster_size, demand, score, section, has_sharing, workspace, stream=None):
+    """peek_queue_signals plus the ancestor score (int64[n]), the section (int32[n]) and has_sharing (int32[1]);
+    torch tensors, any of score/section/has_sharing may be None."""
+    n = int(offsets.shape[0]) - 1
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(_lib.peek_clpm_signals(None if cache is None else cache.handle, n, _dptr(tokens), _dptr(offsets), _dptr(h),
+                                  _dptr(last_node), _dptr(match_len), int(threshold), int(tau), int(theta),
+                                  _dptr(cluster_id), _dptr(cluster_size), _dptr(demand), _dptr(score),
+                                  _dptr(section), _dptr(has_sharing), _dptr(workspace), ws_bytes, _stream(stream)))

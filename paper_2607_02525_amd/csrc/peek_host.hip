@@ -582,18 +582,22 @@ size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes) {
   return signals_workspace_bytes(n, num_nodes);
 }
 
-peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
-                               const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
-                               int32_t* d_cluster_id,
-                               int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
-                               size_t workspace_bytes, void* stream) {
-  clear_error();
+static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                                 const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
+                                 int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
+                                 const ClpmRequest* clpm, void* d_workspace, size_t workspace_bytes, void* stream) {
   if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
   if (threshold < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "threshold must be >= 1 (got %d)", threshold);
   const bool want_demand = d_demand != nullptr;
   const bool want_clusters = d_cluster_id != nullptr || d_cluster_size != nullptr;
   if (want_clusters && (!d_cluster_id || !d_cluster_size))
     return fail(PEEK_ERR_INVALID_ARGUMENT, "d_cluster_id and d_cluster_size must both be given");
+  if (clpm != nullptr && !want_clusters)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "the cLPM signals need d_cluster_id and d_cluster_size");
+  if (clpm != nullptr && n > 0 && clpm->section != nullptr && clpm->h == nullptr)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "the section needs d_h");
+  if (clpm != nullptr && clpm->theta < 0)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "theta must be >= 0 (got %d)", clpm->theta);
   if (want_demand && !c) return fail(PEEK_ERR_INVALID_ARGUMENT, "demand needs the cache");
   if (want_demand && n > 0 && !d_last_node) return fail(PEEK_ERR_INVALID_ARGUMENT, "demand needs d_last_node");
   if (want_clusters && n > 0 && (!d_tokens || !d_offsets))
@@ -611,11 +615,29 @@ peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_
     peek_status s = check_same_device(c);
     if (s != PEEK_OK) return s;
   }
-  peek_status s = run_signals(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
-                              want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
-                              want_demand ? d_demand : nullptr, d_workspace, workspace_bytes, (hipStream_t)stream);
-  if (s != PEEK_OK) return s;
-  return PEEK_OK;
+  return run_signals(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
+                     want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
+                     want_demand ? d_demand : nullptr, clpm, d_workspace, workspace_bytes, (hipStream_t)stream);
+}
+
+peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                               const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
+                               int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
+                               size_t workspace_bytes, void* stream) {
+  clear_error();
+  return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
+                       d_demand, nullptr, d_workspace, workspace_bytes, stream);
+}
+
+peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                              const int32_t* d_h, const int32_t* d_last_node, const int32_t* d_match_len,
+                              int32_t threshold, int32_t tau, int32_t theta, int32_t* d_cluster_id,
+                              int32_t* d_cluster_size, int32_t* d_demand, int64_t* d_score, int32_t* d_section,
+                              int32_t* d_has_sharing, void* d_workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  const ClpmRequest req{d_h, tau, theta, d_score, d_section, d_has_sharing};
+  return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
+                       d_demand, &req, d_workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

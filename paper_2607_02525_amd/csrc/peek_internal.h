@@ -112,12 +112,22 @@ hipError_t launch_lpm_walk(const DeviceTree& t, int32_t n, const int32_t* tokens
 
 size_t signals_workspace_bytes(int32_t n, int64_t num_nodes);
 
+// The rest of cLPM's per-request signals, asked of run_signals.
+struct ClpmRequest {
+  const int32_t* h;       // [n] LPM hit per request (device)
+  int32_t tau;            // warm when h > tau
+  int32_t theta;          // cold requests are grouped by their first theta tokens
+  int64_t* score;         // [n] ancestor score, or NULL
+  int32_t* section;       // [n] 0 warm, 1 cold pioneer, 2 cold sibling, or NULL
+  int32_t* has_sharing;   // device scalar, or NULL
+};
+
 // Demand (when demand != NULL) and clusters (when cluster_id != NULL) in
 // one pass; c may be NULL when only clusters are wanted. With c, last_node
 // and match_len the cluster pass starts from the walk's proven prefixes.
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
-                        int32_t* cluster_size, int32_t* demand, void* workspace, size_t workspace_bytes,
-                        hipStream_t stream);
+                        int32_t* cluster_size, int32_t* demand, const ClpmRequest* clpm, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
 
 }  // namespace peek

@@ -222,8 +222,8 @@ __device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, 
 // Anchor element of request i (the tile pass of the anchor sort builds its
 // input with this): key (last node, match length, next token, longest
 // first). Positions past n are padding that sorts last. Building element i
-// also clears lcp[i] (and lcp[n]) and the round flags, which every later
-// kernel of the pass expects zeroed.
+// also clears lcp[i] (and lcp[n]), the round flags and the has_sharing
+// output, which later kernels of the pass expect zeroed.
 struct AnchorSource {
   const int32_t* tokens;
   const int64_t* offsets;
@@ -233,10 +233,14 @@ struct AnchorSource {
   int32_t* lcp;
   int32_t* flags;
   int32_t n_flags;
+  int32_t* sharing;   // NULL, or the has_sharing output (cleared here, raised by the final stage)
   __device__ __forceinline__ ClElem operator()(size_t i) const {
     if (i < (size_t)n_flags) flags[i] = 0;
     if (i <= (size_t)n) lcp[i] = 0;
-    if (i == 0) lcp[n] = 0;
+    if (i == 0) {
+      lcp[n] = 0;
+      if (sharing) *sharing = 0;
+    }
     ClElem e;
     if (i < (size_t)n) {
       const int64_t o = offsets[i];
@@ -534,6 +538,34 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   }
 }
 
+// The rest of cLPM's per-request signals (Sec. 3.2, Alg. 2), computed from
+// the same order and LCPs as the clusters. In the order every pending-tree
+// node is a contiguous range of requests; the node of depth D covers
+// [L, R) with lcp >= D inside and lcp < D at L and at R.
+//  - ancestor score: a node adds pending_count * edge length = (R - L) *
+//    (D - parent depth) to each request under it, and a request's own leaf
+//    (when no other prompt reaches its end) adds len - share. The node
+//    weights go into a difference array (int64 atomics), whose prefix sum
+//    gives each position its total.
+//  - section: requests with equal prompt[:theta] form a contiguous run whose
+//    first position is the last j with lcp[j] < min(theta, len) (the run of
+//    identical prompts for prompts shorter than theta); the smallest cold
+//    request of the run (atomic minimum) is its pioneer.
+//  - has_sharing: some adjacent pair shares a token (lcp > 0).
+struct ClpmArgs {
+  const int32_t* h;       // LPM hit per request (input)
+  int32_t tau;            // warm when h > tau
+  int32_t theta;          // prefix length that groups cold requests
+  int64_t* diff;          // [n + 1] node weights by position
+  int32_t* pmin;          // [n] smallest cold request per run start
+  int32_t* run;           // [n] run start per position
+  int64_t* part;          // block sums of diff
+  int64_t* score;         // [n] by request, or NULL
+  int32_t* section;       // [n] by request, or NULL
+  int32_t* sharing;       // device scalar (workspace when the caller did not ask)
+  bool on;                // anything requested
+};
+
 // In-block range-minimum tables: level k holds the minimum over the 2^k
 // positions starting at j (k = 0..5), valid while the window stays inside
 // j's 64-position block. With the block minima and a sparse table over
@@ -546,13 +578,19 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
                                                       const int32_t* __restrict__ lcp, uint64_t* __restrict__ key2,
                                                       int32_t* __restrict__ ib1, uint64_t* __restrict__ ib2,
                                                       int64_t ib_stride, int32_t* __restrict__ st1,
-                                                      uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2) {
+                                                      uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2,
+                                                      ClpmArgs cl) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
   const int32_t i = b * kWave + lane;
   int32_t v1 = INT32_MAX;
   uint64_t v2 = ~0ull;
   if (i <= n) v1 = lcp[i];
+  if (cl.on) {
+    if (i <= n) cl.diff[i] = 0;
+    if (i < n) cl.pmin[i] = INT32_MAX;
+    if (i >= 1 && i < n && v1 > 0) *cl.sharing = 1;
+  }
   if (i < n) {
     const int32_t share = max(lcp[i], lcp[i + 1]);
     v2 = ((uint64_t)(uint32_t)share << 32) | el[i].req;
@@ -674,10 +712,55 @@ __device__ __forceinline__ int32_t first_below(const int32_t* __restrict__ ib1, 
   return pos;
 }
 
+// Range queries over lcp[0..n] from the in-block tables and the sparse
+// table over 64-position blocks.
+struct LcpIndex {
+  const int32_t* ib1;
+  int64_t stride;
+  const int32_t* st1;
+  int32_t nb1;
+  int levels;
+  int32_t n;
+
+  // Last j <= i with lcp[j] < s, for s >= 1 (lcp[0] = 0, so one exists).
+  __device__ __forceinline__ int32_t last_below_from(int32_t i, int32_t s) const {
+    const int32_t bi = i >> 6;
+    int32_t L = last_below(ib1, stride, bi << 6, i, s);
+    if (L < (bi << 6)) {
+      int32_t pos = bi - 1;   // the last block <= pos whose minimum is < s
+      for (int k = levels - 1; k >= 0; --k) {
+        const int32_t w = 1 << k;
+        if (pos - w + 1 >= 0 && st1[(int64_t)k * nb1 + pos - w + 1] >= s) pos -= w;
+      }
+      L = last_below(ib1, stride, pos << 6, min((pos << 6) + 63, n), s);
+    }
+    return L;
+  }
+
+  // First j >= i (i <= n) with lcp[j] < s, for s >= 1 (lcp[n] = 0).
+  __device__ __forceinline__ int32_t first_below_from(int32_t i, int32_t s) const {
+    const int32_t bi = i >> 6;
+    const int32_t bend = min((bi << 6) + 63, n);
+    int32_t R = first_below(ib1, stride, i, bend, s);
+    if (R > bend) {
+      int32_t pos = bi + 1;   // the first block >= pos whose minimum is < s
+      for (int k = levels - 1; k >= 0; --k) {
+        const int32_t w = 1 << k;
+        if (pos + w <= nb1 && st1[(int64_t)k * nb1 + pos] >= s) pos += w;
+      }
+      R = first_below(ib1, stride, pos << 6, min((pos << 6) + 63, n), s);
+    }
+    return R;
+  }
+};
+
+// One thread per sorted position i: cluster id and size of its request;
+// with cLPM signals requested also the weight of the pending-tree node
+// whose leftmost inner position is i, and the section run of position i.
 __global__ void k_final_query(int32_t n, int32_t threshold, const uint64_t* __restrict__ key2,
-                              const int32_t* __restrict__ ib1, const uint64_t* __restrict__ ib2, int64_t ib_stride,
-                              const int32_t* __restrict__ st1, const uint64_t* __restrict__ st2, int32_t nb1,
-                              int32_t nb2, int levels, int32_t* __restrict__ cid, int32_t* __restrict__ csz) {
+                              const int32_t* __restrict__ lcp, const ClElem* __restrict__ el, LcpIndex ix,
+                              const uint64_t* __restrict__ ib2, const uint64_t* __restrict__ st2, int32_t nb2,
+                              int32_t* __restrict__ cid, int32_t* __restrict__ csz, ClpmArgs cl) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint64_t own = key2[i];
@@ -686,46 +769,97 @@ __global__ void k_final_query(int32_t n, int32_t threshold, const uint64_t* __re
   if (s < threshold) {
     cid[req] = -1;
     csz[req] = 1;
-    return;
-  }
-  // L: the last j <= i with lcp[j] < s (lcp[0] = 0 < s, so it exists)
-  const int32_t bi = i >> 6;
-  int32_t L = last_below(ib1, ib_stride, bi << 6, i, s);
-  if (L < (bi << 6)) {
-    int32_t pos = bi - 1;   // the last block <= pos whose minimum is < s
-    for (int k = levels - 1; k >= 0; --k) {
-      const int32_t w = 1 << k;
-      if (pos - w + 1 >= 0 && st1[(int64_t)k * nb1 + pos - w + 1] >= s) pos -= w;
-    }
-    L = last_below(ib1, ib_stride, pos << 6, min((pos << 6) + 63, n), s);
-  }
-  // R: the first j > i with lcp[j] < s (lcp[n] = 0 < s)
-  const int32_t bend = min((bi << 6) + 63, n);
-  int32_t R = i + 1 <= bend ? first_below(ib1, ib_stride, i + 1, bend, s) : bend + 1;
-  if (R > bend) {
-    int32_t pos = bi + 1;   // the first block >= pos whose minimum is < s
-    for (int k = levels - 1; k >= 0; --k) {
-      const int32_t w = 1 << k;
-      if (pos + w <= nb1 && st1[(int64_t)k * nb1 + pos] >= s) pos += w;
-    }
-    R = first_below(ib1, ib_stride, pos << 6, min((pos << 6) + 63, n), s);
-  }
-  // id: minimum of (share, request) over [L, R)
-  const int32_t hi = R - 1;
-  const int32_t bl = L >> 6, bh = hi >> 6;
-  uint64_t m;
-  if (bl == bh) {
-    m = in_block_min(ib2, ib_stride, L, hi);
   } else {
-    m = umin64(in_block_min(ib2, ib_stride, L, (bl << 6) + 63), in_block_min(ib2, ib_stride, bh << 6, hi));
-    if (bh - bl >= 2) {
-      const int32_t x = bl + 1, y = bh - 1;
-      const int k = 31 - __clz(y - x + 1);
-      m = umin64(m, umin64(st2[(int64_t)k * nb2 + x], st2[(int64_t)k * nb2 + y - (1 << k) + 1]));
+    // [L, R): the widest range around i whose inner lcps are >= s
+    const int32_t L = ix.last_below_from(i, s);
+    const int32_t R = ix.first_below_from(i + 1, s);
+    // id: minimum of (share, request) over [L, R)
+    const int32_t hi = R - 1;
+    const int32_t bl = L >> 6, bh = hi >> 6;
+    uint64_t m;
+    if (bl == bh) {
+      m = in_block_min(ib2, ix.stride, L, hi);
+    } else {
+      m = umin64(in_block_min(ib2, ix.stride, L, (bl << 6) + 63), in_block_min(ib2, ix.stride, bh << 6, hi));
+      if (bh - bl >= 2) {
+        const int32_t x = bl + 1, y = bh - 1;
+        const int k = 31 - __clz(y - x + 1);
+        m = umin64(m, umin64(st2[(int64_t)k * nb2 + x], st2[(int64_t)k * nb2 + y - (1 << k) + 1]));
+      }
+    }
+    cid[req] = (int32_t)(uint32_t)m;
+    csz[req] = R - L;
+  }
+  if (!cl.on) return;
+  // the node of depth D = lcp[i] > 0 is counted once, at its leftmost inner
+  // position: the previous position with lcp <= D must have lcp < D
+  const int32_t D = i >= 1 ? lcp[i] : 0;
+  if (D > 0) {
+    const int32_t L = ix.last_below_from(i - 1, D + 1);
+    const int32_t lL = lcp[L];
+    if (lL < D) {
+      const int32_t R = ix.first_below_from(i + 1, D);
+      const int64_t wgt = (int64_t)(R - L) * (D - max(lL, lcp[R]));
+      atomicAdd((unsigned long long*)&cl.diff[L], (unsigned long long)wgt);
+      atomicAdd((unsigned long long*)&cl.diff[R], (unsigned long long)(-wgt));
     }
   }
-  cid[req] = (int32_t)(uint32_t)m;
-  csz[req] = R - L;
+  const int32_t len = (int32_t)el[i].len;
+  const int32_t cut = min(cl.theta, len);
+  const int32_t start = cut <= 0 ? 0 : ix.last_below_from(i, cut);
+  cl.run[i] = start;
+  if (cl.h[req] <= cl.tau) atomicMin(&cl.pmin[start], (int32_t)req);
+}
+
+constexpr int kScanThreads = 1024;
+
+// Inclusive block scan of diff (kScanThreads positions per block) into
+// `local` with the block totals in cl.part; also the section of every
+// position (its run's pioneer is known once the query kernel is done).
+__global__ __launch_bounds__(kScanThreads) void k_clpm_scan(int32_t n, const uint64_t* __restrict__ key2,
+                                                            int64_t* __restrict__ local, ClpmArgs cl) {
+  __shared__ int64_t wsum[kScanThreads / kWave];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int32_t i = (int32_t)blockIdx.x * kScanThreads + t;
+  int64_t v = i < n ? cl.diff[i] : 0;
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t o = __shfl(v, lane >= d ? lane - d : lane);
+    if (lane >= d) v += o;
+  }
+  if (lane == kWave - 1) wsum[wave] = v;
+  __syncthreads();
+  int64_t before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  v += before;
+  if (i < n) local[i] = v;
+  if (t == kScanThreads - 1) cl.part[blockIdx.x] = v;
+  if (i < n && cl.section != nullptr) {
+    const uint32_t req = (uint32_t)key2[i];
+    cl.section[req] = cl.h[req] > cl.tau ? 0 : (cl.pmin[cl.run[i]] == (int32_t)req ? 1 : 2);
+  }
+}
+
+// score = own leaf (len - share when positive) + every node above it:
+// the prefix sum of diff up to the position.
+__global__ __launch_bounds__(kScanThreads) void k_clpm_score(int32_t n, const uint64_t* __restrict__ key2,
+                                                             const ClElem* __restrict__ el,
+                                                             const int64_t* __restrict__ local, ClpmArgs cl) {
+  __shared__ int64_t red[kScanThreads / kWave];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  int64_t v = 0;
+  for (int32_t b = t; b < (int32_t)blockIdx.x; b += kScanThreads) v += cl.part[b];
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  int64_t offset = 0;
+  for (int w = 0; w < kScanThreads / kWave; ++w) offset += red[w];
+  const int32_t i = (int32_t)blockIdx.x * kScanThreads + t;
+  if (i >= n || cl.score == nullptr) return;
+  const uint64_t k2 = key2[i];
+  const uint32_t req = (uint32_t)k2;
+  const int64_t share = (int64_t)(k2 >> 32);
+  const int64_t len = el[i].len;
+  cl.score[req] = (len > share ? len - share : 0) + offset + local[i];
 }
 
 size_t np_of(int32_t n) {
@@ -752,7 +886,7 @@ constexpr int kFlagPairs = kSpeculativeRounds + 3;
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
   size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
-      keys_b, prefix, total, flags_bytes;
+      keys_b, prefix, diff, pmin, run, local, part, sharing, total, flags_bytes;
   int64_t ib_stride;
   int32_t nb1, nb2;
   int levels;
@@ -791,6 +925,12 @@ Layout layout(int32_t n, int64_t num_nodes) {
   L.keys_a = take(sizeof(uint32_t) * np);
   L.keys_b = take(sizeof(uint32_t) * np);
   L.prefix = take(sizeof(int32_t) * (size_t)(num_nodes + 1));
+  L.diff = take(sizeof(int64_t) * ((size_t)n + 1));
+  L.pmin = take(sizeof(int32_t) * nn);
+  L.run = take(sizeof(int32_t) * nn);
+  L.local = take(sizeof(int64_t) * nn);
+  L.part = take(sizeof(int64_t) * (((size_t)n + kScanThreads - 1) / kScanThreads + 1));
+  L.sharing = take(sizeof(int32_t));
   L.total = o;
   return L;
 }
@@ -825,7 +965,8 @@ int32_t* host_flags() {
 
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
-                        int32_t* csz, int32_t* demand, void* ws, size_t ws_bytes, hipStream_t st) {
+                        int32_t* csz, int32_t* demand, const ClpmRequest* clpm, void* ws, size_t ws_bytes,
+                        hipStream_t st) {
   const DeviceTree* t = c != nullptr ? &c->tree : nullptr;
   const int64_t num_nodes = t ? t->num_nodes : 0;
   const Layout L = layout(n, num_nodes);
@@ -847,6 +988,9 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
     launch_demand_from_sorted(*t, PlainKeys{keys}, n, P, demand, st);
   }
   if (!want_clusters) {
+    // an empty queue shares nothing
+    if (clpm != nullptr && clpm->has_sharing != nullptr)
+      PEEK_HIP_TRY(hipMemsetAsync(clpm->has_sharing, 0, sizeof(int32_t), st));
     PEEK_HIP_TRY(hipGetLastError());
     return PEEK_OK;
   }
@@ -870,6 +1014,22 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
   ClElem* el = el_a;
   ClElem* other = el_b;
+  ClpmArgs cl{};
+  if (clpm != nullptr) {
+    cl.h = clpm->h;
+    cl.tau = clpm->tau;
+    cl.theta = clpm->theta;
+    cl.diff = (int64_t*)(w + L.diff);
+    cl.pmin = (int32_t*)(w + L.pmin);
+    cl.run = (int32_t*)(w + L.run);
+    cl.part = (int64_t*)(w + L.part);
+    cl.score = clpm->score;
+    cl.section = clpm->section;
+    cl.sharing = clpm->has_sharing != nullptr ? clpm->has_sharing : (int32_t*)(w + L.sharing);
+    cl.on = true;
+  }
+  int64_t* local = (int64_t*)(w + L.local);
+  const LcpIndex ix{ib1, L.ib_stride, st1, L.nb1, L.levels, n};
 
   // Round r compares every member of an active segment with its head, sorts
   // each segment by the new keys and splits it into the next segments.
@@ -901,10 +1061,16 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   };
   auto final_stage = [&](hipStream_t q) {
     hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, q, n, el, lcp, key2,
-                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2);
+                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl);
     hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, q, st1, st2, L.nb1, L.nb2, L.levels);
-    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, q, n, threshold, key2, ib1, ib2,
-                       L.ib_stride, st1, st2, L.nb1, L.nb2, L.levels, cid, csz);
+    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, q, n, threshold, key2, lcp, el, ix, ib2, st2,
+                       L.nb2, cid, csz, cl);
+    if (cl.on) {
+      const unsigned sb = blocks_for(n, kScanThreads);
+      hipLaunchKernelGGL(k_clpm_scan, dim3(sb), dim3(kScanThreads), 0, q, n, key2, local, cl);
+      if (cl.score != nullptr)
+        hipLaunchKernelGGL(k_clpm_score, dim3(sb), dim3(kScanThreads), 0, q, n, key2, el, local, cl);
+    }
   };
   // The fixed part: anchor order and groups, a few refinement rounds and the
   // final stage, all before the host looks at any flag. Each round's kernels
@@ -914,7 +1080,7 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   // segment sort, and the host then takes over from that round.
   auto fixed = [&](hipStream_t q) {
     const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
-                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t))};
+                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr};
     el = msort::sort_from(src, el_a, el_b, np, ClLess{}, q);
     other = el == el_a ? el_b : el_a;
     // The anchor order is sorted by last node first, so demand reads it

@@ -11,7 +11,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (Cache, peek_cache_build, peek_cache_stats, peek_lpm_batch, peek_queue_signals,
+from . import (Cache, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_lpm_batch, peek_queue_signals,
                peek_queue_signals_workspace, peek_tree_from_sequences)
 
 
@@ -48,6 +48,9 @@ class HotPath:
         self.d_cid = torch.empty(n, dtype=torch.int32, device=dev)
         self.d_csz = torch.empty(n, dtype=torch.int32, device=dev)
         self.d_demand = torch.empty(self.num_nodes, dtype=torch.int32, device=dev)
+        self.d_score = torch.empty(n, dtype=torch.int64, device=dev)
+        self.d_section = torch.empty(n, dtype=torch.int32, device=dev)
+        self.d_sharing = torch.empty(1, dtype=torch.int32, device=dev)
         ws = peek_queue_signals_workspace(self.n, self.num_nodes)
         self.d_ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
 
@@ -56,9 +59,17 @@ class HotPath:
                        stream=stream)
 
     def signals(self, stream=None, anchored: bool = True):
+        self._clpm_valid = False
         peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last,
                            self.d_m if anchored else None, self.threshold, self.d_cid, self.d_csz,
                            self.d_demand, self.d_ws, stream=stream)
+
+    def clpm(self, tau: int, theta: int, stream=None, anchored: bool = True):
+        """Clusters and demand plus cLPM's ancestor score, section and has_sharing."""
+        peek_clpm_signals(self.cache, self.d_tokens, self.d_offsets, self.d_h, self.d_last,
+                          self.d_m if anchored else None, self.threshold, tau, theta, self.d_cid, self.d_csz,
+                          self.d_demand, self.d_score, self.d_section, self.d_sharing, self.d_ws, stream=stream)
+        self._clpm_valid = True
 
     def step(self, stream=None):
         self.lpm(stream)
@@ -67,7 +78,7 @@ class HotPath:
     def results(self) -> dict:
         torch.cuda.synchronize(self.device)
         n = self.n
-        return {
+        out = {
             "h": self.d_h[:n].cpu().numpy(),
             "last_node": self.d_last[:n].cpu().numpy(),
             "match_len": self.d_m[:n].cpu().numpy(),
@@ -75,3 +86,8 @@ class HotPath:
             "cluster_size": self.d_csz[:n].cpu().numpy(),
             "demand": self.d_demand.cpu().numpy(),
         }
+        if getattr(self, "_clpm_valid", False):   # written by the last clpm() call
+            out["score"] = self.d_score[:n].cpu().numpy()
+            out["section"] = self.d_section[:n].cpu().numpy()
+            out["has_sharing"] = bool(self.d_sharing.cpu().numpy()[0])
+        return out

@@ -133,6 +133,18 @@ def test_argument_errors_before_any_gpu_work():
     # demand without a cache
     assert lib.peek_queue_signals(None, 4, fake, fake, fake, None, 8, None, None, fake, fake, need, None) \
         == P.PEEK_ERR_INVALID_ARGUMENT
+    # cLPM signals: need the cluster outputs, d_h for the section, theta >= 0
+    assert lib.peek_clpm_signals(None, 4, fake, fake, fake, None, None, 8, 0, 32, None, None, None, fake, fake,
+                                 fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "d_cluster_id" in P.peek_last_error()
+    assert lib.peek_clpm_signals(None, 4, fake, fake, None, None, None, 8, 0, 32, fake, fake, None, None, fake,
+                                 None, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "d_h" in P.peek_last_error()
+    assert lib.peek_clpm_signals(None, 4, fake, fake, fake, None, None, 8, 0, -1, fake, fake, None, fake, fake,
+                                 fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "theta" in P.peek_last_error()
+    assert lib.peek_clpm_signals(None, 4, fake, fake, fake, None, None, 8, 0, 32, fake, fake, None, fake, fake,
+                                 fake, fake, need - 1, None) == P.PEEK_ERR_WORKSPACE_TOO_SMALL
 
 
 def test_workspace_grows_with_the_queue_and_the_cache():

@@ -39,6 +39,13 @@ def gpu_run(w, repeat=1):
     res = hp.results()
     for k in ("cluster_id", "cluster_size"):
         assert np.array_equal(res[k], outs[0][k]), f"{k}: anchored and unanchored cluster passes differ"
+    # and so must the cLPM entry point, which computes the same plus the
+    # score, section and has_sharing
+    hp.clpm(w.tau, w.theta)
+    cl = hp.results()
+    for k in ("cluster_id", "cluster_size", "demand"):
+        assert np.array_equal(cl[k], outs[0][k]), f"{k}: cLPM entry point differs"
+    outs[0]["score"], outs[0]["section"], outs[0]["has_sharing"] = cl["score"], cl["section"], cl["has_sharing"]
     return hp, outs
 
 
@@ -49,6 +56,10 @@ def assert_parity(w, res, s):
     assert np.array_equal(res["demand"], s.demand), "demand"
     assert np.array_equal(res["cluster_id"], s.clusters.cluster_id), "cluster_id"
     assert np.array_equal(res["cluster_size"], s.clusters.cluster_size), "cluster_size"
+    if "score" in res:
+        assert np.array_equal(res["score"], s.clpm.score), "score"
+        assert np.array_equal(res["section"], s.clpm.section), "section"
+        assert res["has_sharing"] == s.clpm.has_sharing, "has_sharing"
 
 
 def run_and_compare(w, repeat=1):
@@ -82,7 +93,11 @@ def test_scale_bit_exact_full_size():
 @pytest.mark.parametrize("seed", range(16))
 @pytest.mark.parametrize("vocab,B,T", [(2, 1, 1), (3, 2, 2), (4, 4, 8), (32000, 16, 4)])
 def test_random_sequence_cases(seed, vocab, B, T):
+    # tau and theta vary with the case: warm cut-offs at 0 and at B, prefix
+    # classes from one token to longer than most prompts
     w = W.random_case(seed * 13 + vocab, n=40, n_cached=24, vocab=vocab, max_len=80, block_size=B, threshold=T)
+    w.tau = (0, B, -1, 3 * B)[seed % 4]
+    w.theta = (1, 2, 32, 0, 100)[seed % 5]
     run_and_compare(w)
 
 
@@ -211,12 +226,11 @@ def _first(w, k, name):
                       cache_tree=w.cache_tree)
 
 
-def test_recorded_launch_sequences_replay_correctly():
-    # The fixed part of a signals call is recorded once per argument set and
-    # replayed afterwards. Interleave three queues on one cache, anchored and
-    # not (six argument sets: more than the four recordings a cache keeps),
-    # with eager host work and synchronisation between the replays, and check
-    # every result.
+def test_interleaved_queues_on_one_cache():
+    # Three queues of different sizes share one cache, each with its own
+    # buffers and workspace; interleave their steps (anchored and not) with
+    # host work and synchronisation in between, poisoning the outputs before
+    # each call, and check every result.
     HotPath = _hot()
     w = W.make("rag", 42)
     parts = [w, _first(w, 1000, "rag-1000"), _first(w, 333, "rag-333")]
@@ -227,7 +241,7 @@ def test_recorded_launch_sequences_replay_correctly():
         hp.load_queue(p.tokens, p.offsets, p.block_size, p.threshold)
     for it in range(3):
         for k, (hp, p, s) in enumerate(zip(hps, parts, expect)):
-            print(f"[gpu] replay {it} queue {p.name}", flush=True)
+            print(f"[gpu] pass {it} queue {p.name}", flush=True)
             for out in (hp.d_h, hp.d_last, hp.d_m, hp.d_cid, hp.d_csz, hp.d_demand):
                 out.fill_(-7)
             hp.step()
