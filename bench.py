@@ -215,6 +215,17 @@ def main():
         if i > 0:
             clpm_ms.append(a.elapsed_time(b))
     log(f"cLPM signals (clusters + demand + score + section + has_sharing): {np.mean(clpm_ms):.3f} ms")
+    # eviction ranking of the cached nodes from that demand (scores + victim order)
+    evict_ms = []
+    for i in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        hp.evict()
+        b.record(stream)
+        torch.cuda.synchronize()
+        if i > 0:
+            evict_ms.append(a.elapsed_time(b))
+    log(f"eviction ranking of {hp.num_nodes} cached nodes: {np.mean(evict_ms):.3f} ms")
 
     res = hp.results()
     exp = peek_cache_export(hp.cache)
@@ -268,6 +279,7 @@ def main():
         "lpm_ms": round(float(lpm_ms.mean()), 4),
         "signals_ms": round(float(sig_ms.mean()), 4),
         "clpm_signals_ms": round(float(np.mean(clpm_ms)), 4),
+        "evict_rank_ms": round(float(np.mean(evict_ms)), 4),
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,

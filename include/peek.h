@@ -208,6 +208,27 @@ peek_status peek_clpm_signals(const peek_cache* cache, int32_t n, const int32_t*
                               int64_t* d_score, int32_t* d_section, int32_t* d_has_sharing,
                               void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * peek_evict_rank: eviction ranking of the cached nodes (Eq. 2).
+ *   d_score[c] = max over c and its ancestors a of demand[a] * depth(a)
+ *                (int64[num_nodes], canonical ids; depth = tokens from the
+ *                root to the end of a's edge; a cache node's pending count is
+ *                its demand). The lowest score evicts first.
+ *   d_order    = the num_nodes - 1 non-root nodes in the order a leaf-only
+ *                eviction loop frees them: always the available leaf with the
+ *                smallest (score, id), a node becoming available once its
+ *                last child is freed (int32[num_nodes - 1]).
+ * d_demand is peek_queue_signals' demand (int32[num_nodes], device). Either
+ * output may be NULL, not both. Scratch comes only from d_workspace (device,
+ * 256-byte aligned, at least peek_evict_rank_workspace(num_nodes) bytes).
+ * Asynchronous on `stream`.
+ * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
+ * ---------------------------------------------------------------------- */
+size_t peek_evict_rank_workspace(int64_t num_nodes);
+
+peek_status peek_evict_rank(const peek_cache* cache, const int32_t* d_demand, int64_t* d_score,
+                            int32_t* d_order, void* d_workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -58,6 +58,7 @@ def _load():
     lib.oracle_demand.argtypes = [ctypes.c_void_p, ctypes.c_int64, _c_i32p, _c_i64p]
     lib.oracle_clusters.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, ctypes.c_int64,
                                     _c_i64p, _c_i64p, _c_i64p]
+    lib.oracle_evict.argtypes = [ctypes.c_void_p, _c_i64p, _c_i64p, _c_i32p]
     lib.oracle_clpm.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int64,
                                 _c_i64p, _c_i32p, _c_i32p]
     _lib = lib
@@ -158,6 +159,22 @@ def demand(tree: Tree, last_node) -> np.ndarray:
     out = np.empty(tree.num_nodes, dtype=np.int64)
     _load().oracle_demand(tree._h, len(last_node), _p32(last_node), _p64(out))
     return out
+
+
+@dataclass
+class EvictResult:
+    score: np.ndarray      # per canonical node (int64)
+    order: np.ndarray      # non-root nodes in victim order (int32)
+
+
+def evict(tree: Tree, demand) -> EvictResult:
+    """Eviction scores (Eq. 2) and the leaf-only victim order."""
+    demand = _i64(demand)
+    nn = tree.num_nodes
+    score = np.empty(nn, dtype=np.int64)
+    order = np.empty(max(nn - 1, 1), dtype=np.int32)
+    _load().oracle_evict(tree._h, _p64(demand), _p64(score), _p32(order))
+    return EvictResult(score, order[:nn - 1])
 
 
 @dataclass

@@ -24,6 +24,12 @@
 //    only if its depth reaches the threshold T; otherwise the request is a
 //    singleton (id -1, size 1). Cluster id = smallest arrival index among the
 //    requests whose cluster is that same node.
+//  * Eviction ranking (Eq. 2): a cached node's eviction score is the largest
+//    pending_count * depth over the nodes of its ancestor chain, itself
+//    included, where a cache node's pending count is its demand; the lowest
+//    score goes first. A radix cache frees leaves only, so the victim order
+//    repeatedly takes the leaf with the smallest (score, node id) and exposes
+//    its parent once the parent's last child is gone (the root stays).
 //  * The rest of cLPM's per-request signal vector (Sec. 3.2 and Alg. 2):
 //    the ancestor score, the sum over the nodes v on the request's path in
 //    the pending tree of pending_count(v) times the length of v's edge; the
@@ -385,6 +391,38 @@ void oracle_clusters(int64_t n, const int32_t* tokens, const int64_t* offsets, i
       cluster_id_out[r] = -1;
       cluster_size_out[r] = 1;
     }
+  }
+}
+
+// Eviction scores and victim order over canonical node ids. demand[c] is the
+// pending demand of every node. score_out[c] = max over c and its ancestors a
+// of demand[a] * depth(a). order_out[0 .. num_nodes-2] = the non-root nodes
+// in the order a leaf-only eviction loop frees them: always the available
+// leaf with the smallest (score, id); a node becomes available when its last
+// child has been freed.
+void oracle_evict(const oracle_tree* t, const int64_t* demand, int64_t* score_out, int32_t* order_out) {
+  const size_t nn = t->by_canon.size();
+  for (size_t c = 0; c < nn; ++c) {
+    int64_t best = 0;
+    for (const Node* a = t->by_canon[c]; a != nullptr; a = a->parent) {
+      const int64_t v = demand[a->canon] * a->depth;
+      if (v > best) best = v;
+    }
+    score_out[c] = best;
+  }
+  std::vector<int64_t> kids_left(nn, 0);
+  for (size_t c = 0; c < nn; ++c) kids_left[c] = (int64_t)t->by_canon[c]->kids.size();
+  std::set<std::pair<int64_t, int32_t>> leaves;
+  for (size_t c = 1; c < nn; ++c)
+    if (kids_left[c] == 0) leaves.insert({score_out[c], (int32_t)c});
+  size_t k = 0;
+  while (!leaves.empty()) {
+    const auto it = leaves.begin();
+    const int32_t c = it->second;
+    leaves.erase(it);
+    order_out[k++] = c;
+    const Node* p = t->by_canon[c]->parent;
+    if (p != nullptr && p->canon != 0 && --kids_left[p->canon] == 0) leaves.insert({score_out[p->canon], p->canon});
   }
 }
 

@@ -52,6 +52,8 @@ EXPORTS = [
     ("peek_queue_signals_workspace", ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
     ("peek_queue_signals", ctypes.c_int,
      [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("peek_evict_rank_workspace", ctypes.c_size_t, [ctypes.c_int64]),
+    ("peek_evict_rank", ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     ("peek_clpm_signals", ctypes.c_int,
      [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
       _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -224,3 +226,15 @@ def peek_clpm_signals(cache, tokens, offsets, h, last_node, match_len, threshold
                                   _dptr(last_node), _dptr(match_len), int(threshold), int(tau), int(theta),
                                   _dptr(cluster_id), _dptr(cluster_size), _dptr(demand), _dptr(score),
                                   _dptr(section), _dptr(has_sharing), _dptr(workspace), ws_bytes, _stream(stream)))
+
+
+def peek_evict_rank_workspace(num_nodes: int) -> int:
+    return int(_lib.peek_evict_rank_workspace(int(num_nodes)))
+
+
+def peek_evict_rank(cache, demand, score, order, workspace, stream=None):
+    """Eviction score int64[num_nodes] and victim order int32[num_nodes-1] from demand int32[num_nodes];
+    torch tensors, score or order may be None."""
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(_lib.peek_evict_rank(cache.handle, _dptr(demand), _dptr(score), _dptr(order), _dptr(workspace), ws_bytes,
+                                _stream(stream)))

@@ -46,6 +46,7 @@ struct Flat {
   int64_t edge_tokens = 0;
   int32_t max_fanout = 0;
   int64_t max_depth = 0;
+  int32_t max_level = 0;   // most edges on a root-to-node path
 };
 
 constexpr int64_t kPoolTailPad = 64;   // tokens of zero padding after the last edge
@@ -107,6 +108,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
   std::vector<int32_t> order;
   order.reserve(num_nodes);
   std::vector<int64_t> depth_in(num_nodes, -1);
+  std::vector<int32_t> level_in(num_nodes, 0);   // nodes between the root and the node
   {
     std::vector<int32_t> stack{root};
     depth_in[root] = 0;
@@ -117,6 +119,7 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
       for (int32_t q = kbeg[v + 1] - 1; q >= kbeg[v]; --q) {
         const int32_t c = kids[q];
         depth_in[c] = depth_in[v] + (eoff[c + 1] - eoff[c]);
+        level_in[c] = level_in[v] + 1;
         stack.push_back(c);
       }
     }
@@ -129,7 +132,11 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
   for (int32_t c = 0; c < num_nodes; ++c) f->canon[order[c]] = c;
   f->max_fanout = max_fanout;
   f->max_depth = 0;
-  for (int32_t i = 0; i < num_nodes; ++i) f->max_depth = std::max(f->max_depth, depth_in[i]);
+  f->max_level = 0;
+  for (int32_t i = 0; i < num_nodes; ++i) {
+    f->max_depth = std::max(f->max_depth, depth_in[i]);
+    f->max_level = std::max(f->max_level, level_in[i]);
+  }
   if (f->max_depth > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "tree deeper than 2^31-1 tokens");
   f->edge_tokens = eoff[num_nodes] - eoff[0];
   if (!out_full) return PEEK_OK;
@@ -496,6 +503,7 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   c->pool_tokens = (int64_t)f.pool.size();
   c->max_fanout = f.max_fanout;
   c->max_depth = f.max_depth;
+  c->max_level = f.max_level;
   c->device_bytes = (int64_t)total;
   c->d_base = base;
   c->tree.nodes = (const NodeRec*)(p + parts[0].at);
@@ -580,6 +588,25 @@ peek_status peek_lpm_batch(const peek_cache* c, int32_t n, const int32_t* d_toke
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes) {
   if (n < 0 || num_nodes < 0) return 0;
   return signals_workspace_bytes(n, num_nodes);
+}
+
+size_t peek_evict_rank_workspace(int64_t num_nodes) { return evict_workspace_bytes(num_nodes); }
+
+peek_status peek_evict_rank(const peek_cache* c, const int32_t* d_demand, int64_t* d_score, int32_t* d_order,
+                            void* d_workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+  if (!d_demand) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_demand is NULL");
+  if (!d_score && !d_order) return fail(PEEK_ERR_INVALID_ARGUMENT, "nothing to compute: d_score and d_order are NULL");
+  const size_t need = evict_workspace_bytes(c->num_nodes);
+  if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
+  if (workspace_bytes < need)
+    return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+  peek_status s = check_same_device(c);
+  if (s != PEEK_OK) return s;
+  return run_evict(c, d_demand, d_score, d_order, d_workspace, workspace_bytes, (hipStream_t)stream);
 }
 
 static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,

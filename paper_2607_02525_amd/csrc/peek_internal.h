@@ -87,6 +87,7 @@ struct peek_cache {
   int64_t pool_tokens;
   int32_t max_fanout;
   int64_t max_depth;
+  int32_t max_level;        // most edges on a root-to-node path
   int64_t device_bytes;
   void* d_base;             // one allocation holding every array below
   peek::DeviceTree tree;
@@ -125,6 +126,11 @@ struct ClpmRequest {
 // Demand (when demand != NULL) and clusters (when cluster_id != NULL) in
 // one pass; c may be NULL when only clusters are wanted. With c, last_node
 // and match_len the cluster pass starts from the walk's proven prefixes.
+// Eviction scores (and, when order != NULL, the victim order) of a cache.
+size_t evict_workspace_bytes(int64_t num_nodes);
+peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score, int32_t* order, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
                         int32_t* cluster_size, int32_t* demand, const ClpmRequest* clpm, void* workspace,

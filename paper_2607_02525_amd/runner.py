@@ -11,8 +11,9 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (Cache, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_lpm_batch, peek_queue_signals,
-               peek_queue_signals_workspace, peek_tree_from_sequences)
+from . import (Cache, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
+               peek_evict_rank_workspace, peek_lpm_batch, peek_queue_signals, peek_queue_signals_workspace,
+               peek_tree_from_sequences)
 
 
 class HotPath:
@@ -60,16 +61,30 @@ class HotPath:
 
     def signals(self, stream=None, anchored: bool = True):
         self._clpm_valid = False
+        self._evict_valid = False
         peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last,
                            self.d_m if anchored else None, self.threshold, self.d_cid, self.d_csz,
                            self.d_demand, self.d_ws, stream=stream)
 
     def clpm(self, tau: int, theta: int, stream=None, anchored: bool = True):
         """Clusters and demand plus cLPM's ancestor score, section and has_sharing."""
+        self._evict_valid = False
         peek_clpm_signals(self.cache, self.d_tokens, self.d_offsets, self.d_h, self.d_last,
                           self.d_m if anchored else None, self.threshold, tau, theta, self.d_cid, self.d_csz,
                           self.d_demand, self.d_score, self.d_section, self.d_sharing, self.d_ws, stream=stream)
         self._clpm_valid = True
+
+    def evict(self, stream=None, order: bool = True):
+        """Eviction scores (and the victim order) from the demand of the last signals call."""
+        if not hasattr(self, "d_evict_ws"):
+            dev = self.device
+            self.d_evict_score = torch.empty(self.num_nodes, dtype=torch.int64, device=dev)
+            self.d_evict_order = torch.empty(max(self.num_nodes - 1, 1), dtype=torch.int32, device=dev)
+            self.d_evict_ws = torch.empty(max(peek_evict_rank_workspace(self.num_nodes), 256), dtype=torch.uint8,
+                                          device=dev)
+        peek_evict_rank(self.cache, self.d_demand, self.d_evict_score, self.d_evict_order if order else None,
+                        self.d_evict_ws, stream=stream)
+        self._evict_valid = True
 
     def step(self, stream=None):
         self.lpm(stream)
@@ -86,6 +101,9 @@ class HotPath:
             "cluster_size": self.d_csz[:n].cpu().numpy(),
             "demand": self.d_demand.cpu().numpy(),
         }
+        if getattr(self, "_evict_valid", False):   # written by the last evict() call
+            out["evict_score"] = self.d_evict_score.cpu().numpy()
+            out["evict_order"] = self.d_evict_order[:max(self.num_nodes - 1, 0)].cpu().numpy()
         if getattr(self, "_clpm_valid", False):   # written by the last clpm() call
             out["score"] = self.d_score[:n].cpu().numpy()
             out["section"] = self.d_section[:n].cpu().numpy()

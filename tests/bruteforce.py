@@ -136,3 +136,26 @@ def clpm(prompts, h, tau, theta):
             seen.add(prompts[r][:theta])
     sharing = any(lcp(prompts[a], prompts[b]) >= 1 for a in range(n) for b in range(a + 1, n))
     return np.array(score), np.array(section), sharing
+
+
+# Eviction ranking (Eq. 2) over cache nodes given as strings:
+#   score_c = max over the ancestors a of c, c included, of demand_a * |P(a)|
+#   victim order: repeatedly free the leaf with the smallest (score, id); a
+#   node whose children are all freed becomes a leaf; the root stays
+
+
+def evict(nodes, demand):
+    nodeset = {s: i for i, s in enumerate(nodes)}
+    anc = []
+    for s in nodes:
+        anc.append([nodeset[s[:k]] for k in range(len(s) + 1) if s[:k] in nodeset])
+    score = [max(demand[a] * len(nodes[a]) for a in anc[c]) for c in range(len(nodes))]
+    parent = [None] + [anc[c][-2] for c in range(1, len(nodes))]
+    alive = set(range(1, len(nodes)))
+    order = []
+    while alive:
+        leaves = [c for c in alive if not any(parent[d] == c for d in alive)]
+        c = min(leaves, key=lambda x: (score[x], x))
+        order.append(c)
+        alive.remove(c)
+    return np.array(score), np.array(order)

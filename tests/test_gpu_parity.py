@@ -67,6 +67,12 @@ def run_and_compare(w, repeat=1):
     hp, outs = gpu_run(w, repeat)
     for res in outs:
         assert_parity(w, res, s)
+    # eviction ranking from the demand just computed
+    hp.evict()
+    ev = hp.results()
+    e = O.evict(s.tree, s.demand)
+    assert np.array_equal(ev["evict_score"], e.score), "evict_score"
+    assert np.array_equal(ev["evict_order"], e.order), "evict_order"
     return hp, outs[0], s
 
 

@@ -46,6 +46,10 @@ def test_oracle_matches_brute_force_on_sequences(seed, vocab, B, T):
     assert np.array_equal(r.h, h)
     assert np.array_equal(r.last_node, last)
     assert np.array_equal(O.demand(t, r.last_node), demand)
+    escore, eorder = BF.evict(nodes, demand)
+    e = O.evict(t, demand)
+    assert np.array_equal(e.score, escore)
+    assert np.array_equal(e.order, eorder)
     share, cid, csz = BF.clusters(prompts, w.threshold)
     c = O.clusters(w.tokens, w.offsets, w.threshold)
     assert np.array_equal(c.share, share)
@@ -75,6 +79,9 @@ def test_oracle_matches_brute_force_on_described_trees(seed, vocab, fan):
     assert np.array_equal(r.m, m) and np.array_equal(r.h, h)
     assert np.array_equal(r.last_node, last)
     assert np.array_equal(O.demand(t, r.last_node), demand)
+    escore, eorder = BF.evict(nodes, demand)
+    e = O.evict(t, demand)
+    assert np.array_equal(e.score, escore) and np.array_equal(e.order, eorder)
 
 
 def test_block_size_one_is_plain_lcp_against_a_set():
@@ -207,6 +214,10 @@ def test_worked_example_eviction():
     assert s.demand[node_of[int(A[0])]] == g["expected_demand_A"]
     assert s.demand[node_of[int(B[0])]] == g["expected_demand_B"]
     assert s.demand[0] == g["expected_demand_root"]
+    # Eq. 2 ranks B (no pending demand) below A, so B is the first victim
+    e = O.evict(s.tree, s.demand)
+    assert e.score[node_of[int(B[0])]] == 0 < e.score[node_of[int(A[0])]]
+    assert e.order[0] == node_of[int(B[0])]
 
 
 # ------------------------------------------ closed forms of the workloads

@@ -29,6 +29,10 @@ MUTANTS = {
                                "      mid->depth = node->depth + k + 1;\n      child->edge.erase"),
     "reachability_check_dropped": ("if (seen != num_nodes) { free_tree(t); return nullptr; }", ""),
     "last_node_is_parent_on_partial": ("  return {d, c};", "  return {d, (c->parent && d < c->depth) ? c->parent : c};"),
+    "evict_score_skips_self": ("for (const Node* a = t->by_canon[c]; a != nullptr; a = a->parent) {",
+                               "for (const Node* a = t->by_canon[c]->parent; a != nullptr; a = a->parent) {"),
+    "evict_largest_first": ("    const auto it = leaves.begin();", "    const auto it = std::prev(leaves.end());"),
+    "evict_frees_inner_nodes_early": ("--kids_left[p->canon] == 0", "--kids_left[p->canon] <= 1"),
     "score_leaves_out_own_request": ("      score += node->pending_count * node->elen;",
                                      "      score += (node->pending_count - 1) * node->elen;"),
     "score_weights_by_depth": ("      score += node->pending_count * node->elen;",
