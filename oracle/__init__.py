@@ -59,6 +59,9 @@ def _load():
     lib.oracle_clusters.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, ctypes.c_int64,
                                     _c_i64p, _c_i64p, _c_i64p]
     lib.oracle_evict.argtypes = [ctypes.c_void_p, _c_i64p, _c_i64p, _c_i32p]
+    lib.oracle_mix64.restype = ctypes.c_uint64
+    lib.oracle_mix64.argtypes = [ctypes.c_uint64]
+    lib.oracle_block_lpm.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p]
     lib.oracle_clpm.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int64,
                                 _c_i64p, _c_i32p, _c_i32p]
     _lib = lib
@@ -159,6 +162,21 @@ def demand(tree: Tree, last_node) -> np.ndarray:
     out = np.empty(tree.num_nodes, dtype=np.int64)
     _load().oracle_demand(tree._h, len(last_node), _p32(last_node), _p64(out))
     return out
+
+
+def mix64(z: int) -> int:
+    return int(_load().oracle_mix64(ctypes.c_uint64(z & (2**64 - 1))))
+
+
+def block_lpm(tree: Tree, tokens, offsets, block_size: int) -> np.ndarray:
+    """Hashed-block hit per request (int64)."""
+    tokens, offsets = _i32(tokens), _i64(offsets)
+    n = len(offsets) - 1
+    h = np.empty(n, dtype=np.int64)
+    if tokens.size == 0:
+        tokens = np.zeros(1, dtype=np.int32)
+    _load().oracle_block_lpm(tree._h, int(block_size), n, _p32(tokens), _p64(offsets), _p64(h))
+    return h
 
 
 @dataclass

@@ -30,6 +30,15 @@
 //    score goes first. A radix cache frees leaves only, so the victim order
 //    repeatedly takes the leaf with the smallest (score, node id) and exposes
 //    its parent once the parent's last child is gone (the root stays).
+//  * Hashed-block LPM, the engine variant with a flat block-hash cache (Sec.
+//    3.1 on vLLM: one longest-cache-hit probe per request): every full block
+//    of B tokens of a cached path is stored as a chained hash of the path up
+//    to it, and a request's hit is B times the number of its leading full
+//    blocks whose chained hash is stored. The hash (this codebase's own
+//    definition): mix64 is the SplitMix64 output mix; a block's digest is
+//    mix64 of the XOR of mix64((j << 32) | token_j) over its positions j; the
+//    chain starts at 0x243F6A8885A308D3 and each block applies
+//    k = mix64(k XOR digest).
 //  * The rest of cLPM's per-request signal vector (Sec. 3.2 and Alg. 2):
 //    the ancestor score, the sum over the nodes v on the request's path in
 //    the pending tree of pending_count(v) times the length of v's edge; the
@@ -391,6 +400,63 @@ void oracle_clusters(int64_t n, const int32_t* tokens, const int64_t* offsets, i
       cluster_id_out[r] = -1;
       cluster_size_out[r] = 1;
     }
+  }
+}
+
+// SplitMix64's output mix (Vigna; Stafford's Mix13 constants).
+uint64_t oracle_mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+  return z ^ (z >> 31);
+}
+
+// Chained hashes of the full blocks of one token string, in order.
+static std::vector<uint64_t> block_chain(const int32_t* s, int64_t len, int64_t B) {
+  std::vector<uint64_t> out;
+  uint64_t k = 0x243F6A8885A308D3ULL;
+  for (int64_t b = 0; (b + 1) * B <= len; ++b) {
+    uint64_t x = 0;
+    for (int64_t j = 0; j < B; ++j) x ^= oracle_mix64(((uint64_t)j << 32) | (uint32_t)s[b * B + j]);
+    k = oracle_mix64(k ^ oracle_mix64(x));
+    out.push_back(k);
+  }
+  return out;
+}
+
+// Hashed-block hit of every request: the cache stores the chained hash of
+// every full block of every root-to-node path; h_out[r] = B * (number of
+// leading full blocks of p_r whose chained hash is stored).
+void oracle_block_lpm(const oracle_tree* t, int64_t block_size, int64_t n, const int32_t* tokens,
+                      const int64_t* offsets, int64_t* h_out) {
+  // depth first over the cache, carrying the chain state at each node's
+  // start: the hash after the last full block, the XOR of the current
+  // block's token terms so far and the position inside that block
+  struct State {
+    const Node* node;
+    uint64_t k, x;
+    int64_t pos;
+  };
+  std::set<uint64_t> stored;
+  std::vector<State> stack{{t->root, 0x243F6A8885A308D3ULL, 0, 0}};
+  while (!stack.empty()) {
+    State st = stack.back();
+    stack.pop_back();
+    for (int32_t tok : st.node->edge) {
+      st.x ^= oracle_mix64(((uint64_t)st.pos << 32) | (uint32_t)tok);
+      if (++st.pos == block_size) {
+        st.k = oracle_mix64(st.k ^ oracle_mix64(st.x));
+        stored.insert(st.k);
+        st.x = 0;
+        st.pos = 0;
+      }
+    }
+    for (const auto& kv : st.node->kids) stack.push_back({kv.second, st.k, st.x, st.pos});
+  }
+  for (int64_t r = 0; r < n; ++r) {
+    const std::vector<uint64_t> chain = block_chain(tokens + offsets[r], offsets[r + 1] - offsets[r], block_size);
+    int64_t found = 0;
+    while (found < (int64_t)chain.size() && stored.count(chain[found])) ++found;
+    h_out[r] = block_size * found;
   }
 }
 

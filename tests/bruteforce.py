@@ -159,3 +159,22 @@ def evict(nodes, demand):
         order.append(c)
         alive.remove(c)
     return np.array(score), np.array(order)
+
+
+# Hashed-block LPM without any hashing: block j of a prompt (its first j*B
+# tokens) is cached when those tokens are a prefix of some cached path;
+# h = B * (number of leading cached blocks).
+
+
+def block_lpm(nodes, prompts, B):
+    cached = set()
+    for s in nodes:
+        for j in range(1, len(s) // B + 1):
+            cached.add(s[:j * B])
+    h = []
+    for p in prompts:
+        j = 0
+        while (j + 1) * B <= len(p) and p[:(j + 1) * B] in cached:
+            j += 1
+        h.append(B * j)
+    return np.array(h)

@@ -50,6 +50,8 @@ def test_oracle_matches_brute_force_on_sequences(seed, vocab, B, T):
     e = O.evict(t, demand)
     assert np.array_equal(e.score, escore)
     assert np.array_equal(e.order, eorder)
+    for bb in {1, B, 3}:
+        assert np.array_equal(O.block_lpm(t, w.tokens, w.offsets, bb), BF.block_lpm(nodes, prompts, bb))
     share, cid, csz = BF.clusters(prompts, w.threshold)
     c = O.clusters(w.tokens, w.offsets, w.threshold)
     assert np.array_equal(c.share, share)
@@ -82,6 +84,24 @@ def test_oracle_matches_brute_force_on_described_trees(seed, vocab, fan):
     escore, eorder = BF.evict(nodes, demand)
     e = O.evict(t, demand)
     assert np.array_equal(e.score, escore) and np.array_equal(e.order, eorder)
+
+
+def test_mix64_is_splitmix64():
+    # the first two outputs of SplitMix64 seeded with 0 (its state advances by
+    # the golden-ratio constant and each output is the mix of the state)
+    gamma = 0x9E3779B97F4A7C15
+    assert O.mix64(gamma) == 0xE220A8397B1DCDAF
+    assert O.mix64((2 * gamma) % 2**64) == 0x6E789E6AA1B965F4
+
+
+@pytest.mark.parametrize("name,seed", [(n, s) for n in ("tiny", "rag", "agentic", "nosharing") for s in (42, 142)])
+def test_hashed_block_hit_equals_the_radix_hit(name, seed):
+    # a cache whose sequences are whole blocks stores every full-block prefix
+    # of every cached path, so the hashed-block hit is B * floor(m / B)
+    w = W.make(name, seed)
+    t = O.cache_tree_of(w)
+    h = O.block_lpm(t, w.tokens, w.offsets, w.block_size)
+    assert np.array_equal(h, O.lpm(t, w.tokens, w.offsets, w.block_size).h)
 
 
 def test_block_size_one_is_plain_lcp_against_a_set():

@@ -33,6 +33,11 @@ MUTANTS = {
                                "for (const Node* a = t->by_canon[c]->parent; a != nullptr; a = a->parent) {"),
     "evict_largest_first": ("    const auto it = leaves.begin();", "    const auto it = std::prev(leaves.end());"),
     "evict_frees_inner_nodes_early": ("--kids_left[p->canon] == 0", "--kids_left[p->canon] <= 1"),
+    "block_hit_counts_partial_block": ("for (int64_t b = 0; (b + 1) * B <= len; ++b) {",
+                                       "for (int64_t b = 0; b * B < len; ++b) {"),
+    "block_hash_not_chained": ("    k = oracle_mix64(k ^ oracle_mix64(x));\n    out.push_back(k);",
+                               "    k = oracle_mix64(0x243F6A8885A308D3ULL ^ oracle_mix64(x));\n    out.push_back(k);"),
+    "block_hashes_never_stored": ("        stored.insert(st.k);\n", ""),
     "score_leaves_out_own_request": ("      score += node->pending_count * node->elen;",
                                      "      score += (node->pending_count - 1) * node->elen;"),
     "score_weights_by_depth": ("      score += node->pending_count * node->elen;",
@@ -44,7 +49,7 @@ MUTANTS = {
                                        "if (kv.second->pending_count >= 1) sharing = 1;"),
 }
 
-PINS = "brute_force or worked or unary or invalid or tiny or agentic"
+PINS = "brute_force or worked or unary or invalid or tiny or agentic or hashed or mix64"
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
