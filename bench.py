@@ -31,6 +31,15 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def block_algorithmic_bytes(lengths, block_h, B):
+    """Bytes the hashed-block probe walk must move: the tokens of every full
+    block it hashes (the hits and the first miss), one 8-byte table slot per
+    probed block, the request's two offsets and its hit."""
+    full = lengths // B
+    probed = np.minimum(full, block_h // B + 1)
+    return int((probed * B * 4).sum() + (probed * 8).sum() + len(lengths) * (16 + 4))
+
+
 def walk_algorithmic_bytes(lengths, m, last, demand, exp):
     """Bytes the LPM walk must move: the prompt up to and including the first
     mismatch, the distinct cache edge tokens it compares, one 32-byte node
@@ -227,7 +236,26 @@ def main():
             evict_ms.append(a.elapsed_time(b))
     log(f"eviction ranking of {hp.num_nodes} cached nodes: {np.mean(evict_ms):.3f} ms")
 
+    # the hashed-block cache variant on the same tree and queue: table built
+    # once on the host, then one probe walk per request
+    t0 = time.perf_counter()
+    table = hp.block_table(w.block_size)
+    table_s = time.perf_counter() - t0
+    block_ms = []
+    for i in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        hp.block_lpm()
+        b.record(stream)
+        torch.cuda.synchronize()
+        if i > 0:
+            block_ms.append(a.elapsed_time(b))
+    log(f"hashed-block LPM ({table.stats()['num_blocks']} stored blocks, table built in {table_s:.1f}s): "
+        f"{np.mean(block_ms):.3f} ms")
+
     res = hp.results()
+    block_bytes = block_algorithmic_bytes(w.lengths.astype(np.int64), res["block_h"].astype(np.int64),
+                                          w.block_size)
     exp = peek_cache_export(hp.cache)
     b_alg, parts = walk_algorithmic_bytes(w.lengths.astype(np.int64), res["match_len"].astype(np.int64),
                                           res["last_node"].astype(np.int64), res["demand"].astype(np.int64), exp)
@@ -280,6 +308,9 @@ def main():
         "signals_ms": round(float(sig_ms.mean()), 4),
         "clpm_signals_ms": round(float(np.mean(clpm_ms)), 4),
         "evict_rank_ms": round(float(np.mean(evict_ms)), 4),
+        "block_lpm_ms": round(float(np.mean(block_ms)), 4),
+        "block_lpm_gbs": round(block_bytes / (float(np.mean(block_ms)) / 1e3) / 1e9, 1),
+        "block_table_build_s": round(table_s, 2),
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -229,6 +229,52 @@ size_t peek_evict_rank_workspace(int64_t num_nodes);
 peek_status peek_evict_rank(const peek_cache* cache, const int32_t* d_demand, int64_t* d_score,
                             int32_t* d_order, void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Hashed-block prefix cache: the engine variant whose cache is a flat table
+ * of block hashes rather than a radix tree (Sec. 3.1 on vLLM, where one
+ * longest-cache-hit probe per request gives H[r]).
+ *
+ * Every full block of block_size tokens on a cached root-to-node path is
+ * stored as the chained hash of the path up to and including that block:
+ *   mix64(z)    = SplitMix64 output mix (z ^= z>>30; z *= 0xbf58476d1ce4e5b9;
+ *                 z ^= z>>27; z *= 0x94d049bb133111eb; z ^= z>>31)
+ *   term(j, t)  = mix64(((uint64)j << 32) | (uint32)t), j = position in block
+ *   digest      = mix64(XOR of term(j, t_j) over the block)
+ *   k_0 = 0x243F6A8885A308D3,   k_i = mix64(k_{i-1} ^ digest_i)
+ * This hash is the library's own definition; equal hashes are taken as equal
+ * blocks, so with no collision the hit equals B * floor(m / B) of
+ * peek_lpm_batch on the same tree.
+ * ---------------------------------------------------------------------- */
+typedef struct peek_block_table peek_block_table;
+
+/* Builds the table of every path's chained full-block hashes from a tree
+ * description (same rules and errors as peek_cache_build; node numbering is
+ * irrelevant here) and uploads it to the current device. block_size is a
+ * power of two in [4, 256]. Open addressing with linear probing, at most
+ * half full. Host arrays are read before return; the call waits for the
+ * upload. *out owns the device memory; release with peek_block_table_free.
+ * Errors: INVALID_ARGUMENT, INVALID_TREE, OUT_OF_MEMORY, DEVICE,
+ * UNSUPPORTED_DEVICE; *out is set to NULL. */
+peek_status peek_block_table_build(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
+                                   const int32_t* edge_tokens, int32_t block_size, void* stream,
+                                   peek_block_table** out);
+
+/* Any output pointer may be NULL: distinct stored hashes, slots, block size. */
+peek_status peek_block_table_stats(const peek_block_table* table, int64_t* num_blocks, int64_t* num_slots,
+                                   int32_t* block_size);
+
+/* Frees the table (NULL is a no-op); no enqueued work may still use it. */
+peek_status peek_block_table_free(peek_block_table* table);
+
+/* Hit of every request against the table: d_h[r] = block_size * (number of
+ * leading full blocks of prompt r whose chained hash is stored), int32[n].
+ * One probe walk per request stops at the first missing block. n = 0 is a
+ * no-op. Asynchronous on `stream`; no workspace.
+ * Errors: INVALID_ARGUMENT (n < 0, null pointers, table built on another
+ * device), DEVICE. */
+peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const int32_t* d_tokens,
+                                 const int64_t* d_offsets, int32_t* d_h, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -57,6 +57,11 @@ EXPORTS = [
     ("peek_clpm_signals", ctypes.c_int,
      [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
       _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("peek_block_table_build", ctypes.c_int,
+     [ctypes.c_int32, _i32p, _i64p, _i32p, ctypes.c_int32, _vp, ctypes.POINTER(_vp)]),
+    ("peek_block_table_stats", ctypes.c_int, [_vp, _i64p, _i64p, _i32p]),
+    ("peek_block_table_free", ctypes.c_int, [_vp]),
+    ("peek_block_lpm_batch", ctypes.c_int, [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp]),
 ]
 
 for _name, _res, _args in EXPORTS:
@@ -238,3 +243,54 @@ def peek_evict_rank(cache, demand, score, order, workspace, stream=None):
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
     _check(_lib.peek_evict_rank(cache.handle, _dptr(demand), _dptr(score), _dptr(order), _dptr(workspace), ws_bytes,
                                 _stream(stream)))
+
+
+class BlockTable:
+    """Owns a peek_block_table handle (device table of chained block hashes)."""
+
+    def __init__(self, handle: int):
+        self.handle = ctypes.c_void_p(handle)
+
+    def free(self):
+        if self.handle:
+            _check(_lib.peek_block_table_free(self.handle))
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            if self.handle:
+                _lib.peek_block_table_free(self.handle)
+        except Exception:
+            pass
+
+    def stats(self) -> dict:
+        return peek_block_table_stats(self)
+
+
+def peek_block_table_build(parent, edge_offsets, edge_tokens, block_size: int, stream=None) -> BlockTable:
+    """Host tree description -> BlockTable on the current device."""
+    parent, edge_offsets, edge_tokens = _np32(parent), _np64(edge_offsets), _np32(edge_tokens)
+    keep = edge_tokens if edge_tokens.size else np.zeros(1, np.int32)
+    out = ctypes.c_void_p()
+    _check(_lib.peek_block_table_build(len(parent), parent.ctypes.data_as(_i32p), edge_offsets.ctypes.data_as(_i64p),
+                                       keep.ctypes.data_as(_i32p), int(block_size), _stream(stream),
+                                       ctypes.byref(out)))
+    return BlockTable(out.value)
+
+
+def peek_block_table_stats(table: BlockTable) -> dict:
+    nb, ns = ctypes.c_int64(), ctypes.c_int64()
+    bs = ctypes.c_int32()
+    _check(_lib.peek_block_table_stats(table.handle, ctypes.byref(nb), ctypes.byref(ns), ctypes.byref(bs)))
+    return {"num_blocks": nb.value, "num_slots": ns.value, "block_size": bs.value}
+
+
+def peek_block_table_free(table: BlockTable):
+    table.free()
+
+
+def peek_block_lpm_batch(table, tokens, offsets, h, stream=None):
+    """Hashed-block hit int32[n] of every prompt; tokens int32[*], offsets int64[n+1]: torch tensors on the device."""
+    n = int(offsets.shape[0]) - 1
+    _check(_lib.peek_block_lpm_batch(None if table is None else table.handle, n, _dptr(tokens), _dptr(offsets),
+                                     _dptr(h), _stream(stream)))

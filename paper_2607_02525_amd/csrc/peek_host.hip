@@ -208,18 +208,6 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
   return PEEK_OK;
 }
 
-peek_status check_device(int* dev_out) {
-  int dev = 0;
-  PEEK_HIP_TRY(hipGetDevice(&dev));
-  hipDeviceProp_t prop;
-  PEEK_HIP_TRY(hipGetDeviceProperties(&prop, dev));
-  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-    return fail(PEEK_ERR_UNSUPPORTED_DEVICE, "device %d is %s; this library is built for gfx950 only", dev,
-                prop.gcnArchName);
-  *dev_out = dev;
-  return PEEK_OK;
-}
-
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Lexicographic order of two token strings (signed tokens; a proper prefix first).
@@ -243,6 +231,19 @@ int64_t seq_lcp(const SeqRef& a, const SeqRef& b) {
 }
 
 }  // namespace
+
+peek_status check_device(int* dev_out) {
+  int dev = 0;
+  PEEK_HIP_TRY(hipGetDevice(&dev));
+  hipDeviceProp_t prop;
+  PEEK_HIP_TRY(hipGetDeviceProperties(&prop, dev));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(PEEK_ERR_UNSUPPORTED_DEVICE, "device %d is %s; this library is built for gfx950 only", dev,
+                prop.gcnArchName);
+  *dev_out = dev;
+  return PEEK_OK;
+}
+
 }  // namespace peek
 
 using namespace peek;

@@ -99,6 +99,9 @@ namespace peek {
 peek_status fail(peek_status s, const char* fmt, ...);
 void clear_error();
 
+// Current device id if it is a gfx950, else UNSUPPORTED_DEVICE.
+peek_status check_device(int* dev_out);
+
 #define PEEK_HIP_TRY(call)                                                              \
   do {                                                                                  \
     hipError_t e_ = (call);                                                             \

@@ -11,15 +11,17 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (Cache, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
+from . import (Cache, peek_block_lpm_batch, peek_block_table_build, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
                peek_evict_rank_workspace, peek_lpm_batch, peek_queue_signals, peek_queue_signals_workspace,
                peek_tree_from_sequences)
 
 
 class HotPath:
-    def __init__(self, cache: Cache, canon_id: np.ndarray, device=None):
+    def __init__(self, cache: Cache, canon_id: np.ndarray, device=None, description=None):
         self.cache = cache
         self.canon_id = canon_id
+        self.description = description     # host (parent, edge_offsets, edge_tokens), for the block table
+        self._tables = {}
         self.device = torch.device("cuda") if device is None else torch.device(device)
         self.num_nodes = peek_cache_stats(cache)["num_nodes"]
         self.n = 0
@@ -27,7 +29,7 @@ class HotPath:
     @classmethod
     def from_description(cls, parent, edge_offsets, edge_tokens, device=None):
         cache, canon = peek_cache_build(parent, edge_offsets, edge_tokens)
-        return cls(cache, canon, device)
+        return cls(cache, canon, device, description=(parent, edge_offsets, edge_tokens))
 
     @classmethod
     def from_sequences(cls, tokens, offsets, device=None):
@@ -37,6 +39,7 @@ class HotPath:
         tokens = np.ascontiguousarray(tokens, dtype=np.int32)
         offsets = np.ascontiguousarray(offsets, dtype=np.int64)
         self.n = int(offsets.shape[0] - 1)
+        self._block_valid = False
         self.block_size = int(block_size)
         self.threshold = int(threshold)
         dev = self.device
@@ -86,6 +89,22 @@ class HotPath:
                         self.d_evict_ws, stream=stream)
         self._evict_valid = True
 
+    def block_table(self, block_size: int):
+        """The hashed-block table of the same cache tree (built once per block size)."""
+        if block_size not in self._tables:
+            if self.description is None:
+                raise ValueError("the block table needs the host tree description")
+            self._tables[block_size] = peek_block_table_build(*self.description, block_size)
+        return self._tables[block_size]
+
+    def block_lpm(self, stream=None):
+        """Hashed-block hit of every request at the queue's block size."""
+        table = self.block_table(self.block_size)
+        if not hasattr(self, "d_block_h") or self.d_block_h.numel() < max(self.n, 1):
+            self.d_block_h = torch.empty(max(self.n, 1), dtype=torch.int32, device=self.device)
+        peek_block_lpm_batch(table, self.d_tokens, self.d_offsets, self.d_block_h, stream=stream)
+        self._block_valid = True
+
     def step(self, stream=None):
         self.lpm(stream)
         self.signals(stream)
@@ -104,6 +123,8 @@ class HotPath:
         if getattr(self, "_evict_valid", False):   # written by the last evict() call
             out["evict_score"] = self.d_evict_score.cpu().numpy()
             out["evict_order"] = self.d_evict_order[:max(self.num_nodes - 1, 0)].cpu().numpy()
+        if getattr(self, "_block_valid", False):   # written by the last block_lpm() call
+            out["block_h"] = self.d_block_h[:n].cpu().numpy()
         if getattr(self, "_clpm_valid", False):   # written by the last clpm() call
             out["score"] = self.d_score[:n].cpu().numpy()
             out["section"] = self.d_section[:n].cpu().numpy()

@@ -147,6 +147,29 @@ def test_argument_errors_before_any_gpu_work():
                                  fake, fake, need - 1, None) == P.PEEK_ERR_WORKSPACE_TOO_SMALL
 
 
+def test_block_table_argument_errors_before_any_gpu_work():
+    lib = P._lib
+    parent = np.array([-1, 0, 0], dtype=np.int32)
+    eoff = np.array([0, 0, 3, 5], dtype=np.int64)
+    etok = np.array([1, 2, 3, 4, 5], dtype=np.int32)
+    out = ctypes.c_void_p(0x1234)
+    args = (3, parent.ctypes.data_as(P._i32p), eoff.ctypes.data_as(P._i64p), etok.ctypes.data_as(P._i32p))
+    for bad in (0, 1, 2, 3, 12, 512, -16):
+        out = ctypes.c_void_p(0x1234)
+        assert lib.peek_block_table_build(*args, bad, None, ctypes.byref(out)) == P.PEEK_ERR_INVALID_ARGUMENT
+        assert "block_size" in P.peek_last_error()
+        assert out.value is None
+    assert lib.peek_block_table_build(*args, 16, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    # siblings with the same first token: not a radix tree
+    etok2 = np.array([1, 2, 3, 1, 5], dtype=np.int32)
+    assert lib.peek_block_table_build(3, parent.ctypes.data_as(P._i32p), eoff.ctypes.data_as(P._i64p),
+                                      etok2.ctypes.data_as(P._i32p), 16, None, ctypes.byref(out)) \
+        == P.PEEK_ERR_INVALID_TREE
+    assert lib.peek_block_lpm_batch(None, 1, None, None, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_block_table_stats(None, None, None, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_block_table_free(None) == P.PEEK_OK
+
+
 def test_workspace_grows_with_the_queue_and_the_cache():
     a = P.peek_queue_signals_workspace(1000, 10)
     assert P.peek_queue_signals_workspace(2000, 10) > a

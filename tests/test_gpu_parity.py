@@ -62,7 +62,45 @@ def assert_parity(w, res, s):
         assert res["has_sharing"] == s.clpm.has_sharing, "has_sharing"
 
 
-def run_and_compare(w, repeat=1):
+BLOCK_SIZES = (4, 8, 16, 32, 64, 128, 256)   # the hashed-block table's supported sizes
+
+
+def subset(w, idx):
+    """Requests idx of a workload, packed again (same cache)."""
+    idx = np.asarray(idx, dtype=np.int64)
+    lens = w.offsets[idx + 1] - w.offsets[idx]
+    off = np.zeros(len(idx) + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    tok = np.concatenate([w.tokens[w.offsets[i]:w.offsets[i + 1]] for i in idx]) if len(idx) else w.tokens[:0]
+    return tok.astype(np.int32), off
+
+
+def check_block_lpm(hp, w, s, block_size=None, sample=None):
+    """Hashed-block hit at one block size against the oracle (on every
+    request, or on `sample` of them) and, with no hash collision, against
+    the radix path's block-floored hit."""
+    B = w.block_size if block_size is None else block_size
+    saved = hp.block_size
+    hp.block_size = B
+    try:
+        hp.block_lpm()
+        got = hp.results()["block_h"]
+    finally:
+        hp.block_size = saved
+    if sample is None:
+        exp = O.block_lpm(s.tree, w.tokens, w.offsets, B)
+        assert np.array_equal(got, exp), f"block_h (B={B})"
+    else:
+        idx = np.random.default_rng(B).choice(w.n, size=min(sample, w.n), replace=False)
+        tok, off = subset(w, idx)
+        exp = O.block_lpm(s.tree, tok, off, B)
+        assert np.array_equal(got[idx], exp), f"block_h sample (B={B})"
+    m = s.lpm.m if B == w.block_size else O.lpm(s.tree, w.tokens, w.offsets, B).m
+    assert np.array_equal(got, B * (m // B)), f"block_h vs radix hit (B={B})"
+    return got
+
+
+def run_and_compare(w, repeat=1, block_sample=None):
     s = O.run(w)
     hp, outs = gpu_run(w, repeat)
     for res in outs:
@@ -73,6 +111,9 @@ def run_and_compare(w, repeat=1):
     e = O.evict(s.tree, s.demand)
     assert np.array_equal(ev["evict_score"], e.score), "evict_score"
     assert np.array_equal(ev["evict_order"], e.order), "evict_order"
+    # the hashed-block variant of the same cache, where the block size allows it
+    if w.block_size in BLOCK_SIZES:
+        check_block_lpm(hp, w, s, sample=block_sample)
     return hp, outs[0], s
 
 
@@ -88,7 +129,7 @@ def test_configs_bit_exact(name, seed):
 
 def test_scale_bit_exact_full_size():
     w = W.make("scale", 42)
-    hp, res, s = run_and_compare(w, repeat=2)
+    hp, res, s = run_and_compare(w, repeat=2, block_sample=3000)
     parent, depth, _, _ = s.tree.export()
     checks.check_lpm(w, parent, depth, res["match_len"], res["h"], res["last_node"])
     checks.check_demand(w.n, parent, res["last_node"], res["demand"])
@@ -259,3 +300,59 @@ def test_interleaved_queues_on_one_cache():
             assert np.array_equal(res["cluster_id"], s.clusters.cluster_id)
             assert np.array_equal(res["cluster_size"], s.clusters.cluster_size)
             torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("B", BLOCK_SIZES)
+def test_block_lpm_every_block_size(B):
+    """Hashed-block hits at every supported block size: long shared prefixes
+    (walks over several 256-token steps), block boundaries, empty, short and
+    ragged prompts, and a cache whose paths end inside a block."""
+    HotPath = _hot()
+    cases = [W.random_case(seed, n=300, n_cached=40, vocab=3, max_len=1400, block_size=B, threshold=3)
+             for seed in (1, 2)]
+    base = list(range(1000, 1800))
+    edge = [base[:k] + [1] for k in (B - 1, B, B + 1, 2 * B, 255, 256, 257, 511, 512, 513, 700)]
+    cases.append(_w(edge + [[], [5], base, base[:B]], cached=[base[:k] for k in (3 * B // 2, 600, 800)], B=B))
+    for w in cases:
+        s = O.run(w)
+        hp = HotPath.from_sequences(*w.cache_sequences)
+        hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+        print(f"[gpu] block_lpm B={B} {w.name} seed={w.seed} n={w.n}", flush=True)
+        check_block_lpm(hp, w, s)
+
+
+def test_block_lpm_deep_chain_and_described_tree():
+    HotPath = _hot()
+    rng = np.random.default_rng(9)
+    long = rng.integers(0, 128256, size=70000, dtype=np.int32).tolist()
+    w = _w([long[:69000], long[:70000], long[:66000] + [5], long[:100], []],
+           cached=[long[:c] for c in (4800, 24000, 64000, 70000)], B=16)
+    s = O.run(w)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    print("[gpu] block_lpm deep chain", flush=True)
+    got = check_block_lpm(hp, w, s)
+    assert got[1] == 70000
+    w = W.random_tree_case(3, n_nodes=400, n=500, vocab=6, max_edge=40, block_size=8, threshold=2)
+    s = O.run(w)
+    hp = HotPath.from_description(*w.cache_tree)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    print("[gpu] block_lpm described tree", flush=True)
+    for B in (4, 8, 32):
+        check_block_lpm(hp, w, s, block_size=B)
+
+
+def test_block_table_stats_and_empty_cache():
+    HotPath = _hot()
+    base = list(range(50))
+    hp = HotPath.from_sequences(*W.pack([np.asarray(base, np.int32), np.asarray(base[:20] + [7] * 30, np.int32)]))
+    st = hp.block_table(16).stats()
+    # shared blocks 0 of both paths coincide: 3 + 3 full blocks, one in common
+    assert st == {"num_blocks": 5, "num_slots": 64, "block_size": 16}
+    w = _w([[], [1, 2, 3, 4, 5, 6, 7, 8]], cached=[], B=4)
+    s = O.run(w)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    assert hp.block_table(4).stats()["num_blocks"] == 0
+    got = check_block_lpm(hp, w, s)
+    assert np.array_equal(got, [0, 0])
