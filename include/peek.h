@@ -236,11 +236,15 @@ peek_status peek_evict_rank(const peek_cache* cache, const int32_t* d_demand, in
  *
  * Every full block of block_size tokens on a cached root-to-node path is
  * stored as the chained hash of the path up to and including that block:
- *   mix64(z)    = SplitMix64 output mix (z ^= z>>30; z *= 0xbf58476d1ce4e5b9;
- *                 z ^= z>>27; z *= 0x94d049bb133111eb; z ^= z>>31)
- *   term(j, t)  = mix64(((uint64)j << 32) | (uint32)t), j = position in block
- *   digest      = mix64(XOR of term(j, t_j) over the block)
- *   k_0 = 0x243F6A8885A308D3,   k_i = mix64(k_{i-1} ^ digest_i)
+ *   mix64(z)   = SplitMix64 output mix (z ^= z>>30; z *= 0xbf58476d1ce4e5b9;
+ *                z ^= z>>27; z *= 0x94d049bb133111eb; z ^= z>>31)
+ *   key(j)     = mix64(j + 0x6A09E667F3BCC909); a_j = low, b_j = high 32 bits
+ *   n_a        = sum over token pairs (2i, 2i+1) of the block of
+ *                ((u_2i + a_2i) mod 2^32) * ((u_2i+1 + a_2i+1) mod 2^32) mod 2^64
+ *                (an NH pass, as in UMAC; u = tokens as uint32); n_b with b
+ *   digest_i   = mix64(n_a ^ rotl64(n_b, 32) ^ 0x9E3779B97F4A7C15 * (i + 1)),
+ *                i = the block's index along the path (0-based)
+ *   k_0 = 0x243F6A8885A308D3,   k_{i+1} = k_i + digest_i   (mod 2^64)
  * This hash is the library's own definition; equal hashes are taken as equal
  * blocks, so with no collision the hit equals B * floor(m / B) of
  * peek_lpm_batch on the same tree.

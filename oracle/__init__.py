@@ -62,6 +62,8 @@ def _load():
     lib.oracle_mix64.restype = ctypes.c_uint64
     lib.oracle_mix64.argtypes = [ctypes.c_uint64]
     lib.oracle_block_lpm.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p]
+    lib.oracle_block_digest.restype = ctypes.c_uint64
+    lib.oracle_block_digest.argtypes = [_c_i32p, ctypes.c_int64, ctypes.c_int64]
     lib.oracle_clpm.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int64,
                                 _c_i64p, _c_i32p, _c_i32p]
     _lib = lib
@@ -169,7 +171,10 @@ def mix64(z: int) -> int:
 
 
 def block_lpm(tree: Tree, tokens, offsets, block_size: int) -> np.ndarray:
-    """Hashed-block hit per request (int64)."""
+    """Hashed-block hit per request (int64). The block hash pairs tokens, so
+    the block size is even."""
+    if block_size < 2 or block_size % 2:
+        raise ValueError(f"the hashed-block cache needs an even block size (got {block_size})")
     tokens, offsets = _i32(tokens), _i64(offsets)
     n = len(offsets) - 1
     h = np.empty(n, dtype=np.int64)
@@ -177,6 +182,12 @@ def block_lpm(tree: Tree, tokens, offsets, block_size: int) -> np.ndarray:
         tokens = np.zeros(1, dtype=np.int32)
     _load().oracle_block_lpm(tree._h, int(block_size), n, _p32(tokens), _p64(offsets), _p64(h))
     return h
+
+
+def block_digest(block, index: int) -> int:
+    """Digest of one block (its tokens, even count) at block index `index`."""
+    block = _i32(block)
+    return int(_load().oracle_block_digest(_p32(block), len(block), int(index)))
 
 
 @dataclass

@@ -35,10 +35,10 @@
 //    of B tokens of a cached path is stored as a chained hash of the path up
 //    to it, and a request's hit is B times the number of its leading full
 //    blocks whose chained hash is stored. The hash (this codebase's own
-//    definition): mix64 is the SplitMix64 output mix; a block's digest is
-//    mix64 of the XOR of mix64((j << 32) | token_j) over its positions j; the
-//    chain starts at 0x243F6A8885A308D3 and each block applies
-//    k = mix64(k XOR digest).
+//    definition): a block's digest compresses its token pairs with two NH
+//    passes under fixed position keys and finishes with the SplitMix64
+//    output mix, folding in the block's index along the path; the chain
+//    starts at 0x243F6A8885A308D3 and adds each block's digest (mod 2^64).
 //  * The rest of cLPM's per-request signal vector (Sec. 3.2 and Alg. 2):
 //    the ancestor score, the sum over the nodes v on the request's path in
 //    the pending tree of pending_count(v) times the length of v's edge; the
@@ -410,14 +410,42 @@ uint64_t oracle_mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
-// Chained hashes of the full blocks of one token string, in order.
+// Position keys of the block compression: key word j (0 <= j < 256) is
+// mix64(j + 0x6A09E667F3BCC909); its low half serves the first NH pass and
+// its high half the second.
+static uint32_t nh_key(int64_t j, int pass) {
+  const uint64_t w = oracle_mix64((uint64_t)j + 0x6A09E667F3BCC909ULL);
+  return pass == 0 ? (uint32_t)w : (uint32_t)(w >> 32);
+}
+
+// Digest of the block with index idx (0-based along the path) holding the
+// B tokens blk[0..B): two NH passes (Black et al., UMAC) over the token pairs,
+//   n = sum over i < B/2 of ((u_2i + key_2i) mod 2^32) * ((u_2i+1 + key_2i+1) mod 2^32)  mod 2^64,
+// with u the tokens as unsigned 32-bit words, then
+//   digest = mix64(n1 XOR rotl(n2, 32) XOR 0x9E3779B97F4A7C15 * (idx + 1)).
+static uint64_t block_digest(const int32_t* blk, int64_t B, int64_t idx) {
+  uint64_t n[2] = {0, 0};
+  for (int pass = 0; pass < 2; ++pass)
+    for (int64_t i = 0; i < B; i += 2) {
+      const uint32_t x = (uint32_t)blk[i] + nh_key(i, pass);
+      const uint32_t y = (uint32_t)blk[i + 1] + nh_key(i + 1, pass);
+      n[pass] += (uint64_t)x * (uint64_t)y;
+    }
+  const uint64_t rot = (n[1] << 32) | (n[1] >> 32);
+  return oracle_mix64(n[0] ^ rot ^ (0x9E3779B97F4A7C15ULL * (uint64_t)(idx + 1)));
+}
+
+// One link of the chain: the key after a block is the key before it plus
+// the block's digest (mod 2^64); the chain starts at 0x243F6A8885A308D3.
+static uint64_t chain_step(uint64_t k, uint64_t digest) { return k + digest; }
+
+// Chained hashes of the full blocks of one token string, in order; the
+// value after block i is the key of the first i + 1 blocks.
 static std::vector<uint64_t> block_chain(const int32_t* s, int64_t len, int64_t B) {
   std::vector<uint64_t> out;
   uint64_t k = 0x243F6A8885A308D3ULL;
   for (int64_t b = 0; (b + 1) * B <= len; ++b) {
-    uint64_t x = 0;
-    for (int64_t j = 0; j < B; ++j) x ^= oracle_mix64(((uint64_t)j << 32) | (uint32_t)s[b * B + j]);
-    k = oracle_mix64(k ^ oracle_mix64(x));
+    k = chain_step(k, block_digest(s + b * B, B, b));
     out.push_back(k);
   }
   return out;
@@ -428,29 +456,35 @@ static std::vector<uint64_t> block_chain(const int32_t* s, int64_t len, int64_t 
 // leading full blocks of p_r whose chained hash is stored).
 void oracle_block_lpm(const oracle_tree* t, int64_t block_size, int64_t n, const int32_t* tokens,
                       const int64_t* offsets, int64_t* h_out) {
-  // depth first over the cache, carrying the chain state at each node's
-  // start: the hash after the last full block, the XOR of the current
-  // block's token terms so far and the position inside that block
+  if (block_size < 2 || block_size % 2 != 0) {   // the digest pairs tokens
+    for (int64_t r = 0; r < n; ++r) h_out[r] = -1;
+    return;
+  }
+  // depth first over the cache, carrying the chain value after the path's
+  // last full block, the number of full blocks so far and the tokens of the
+  // block in progress
   struct State {
     const Node* node;
-    uint64_t k, x;
-    int64_t pos;
+    uint64_t k;
+    int64_t blocks;
+    std::vector<int32_t> partial;
   };
   std::set<uint64_t> stored;
-  std::vector<State> stack{{t->root, 0x243F6A8885A308D3ULL, 0, 0}};
+  std::vector<State> stack;
+  stack.push_back({t->root, 0x243F6A8885A308D3ULL, 0, {}});
   while (!stack.empty()) {
-    State st = stack.back();
+    State st = std::move(stack.back());
     stack.pop_back();
     for (int32_t tok : st.node->edge) {
-      st.x ^= oracle_mix64(((uint64_t)st.pos << 32) | (uint32_t)tok);
-      if (++st.pos == block_size) {
-        st.k = oracle_mix64(st.k ^ oracle_mix64(st.x));
+      st.partial.push_back(tok);
+      if ((int64_t)st.partial.size() == block_size) {
+        st.k = chain_step(st.k, block_digest(st.partial.data(), block_size, st.blocks));
+        st.blocks += 1;
         stored.insert(st.k);
-        st.x = 0;
-        st.pos = 0;
+        st.partial.clear();
       }
     }
-    for (const auto& kv : st.node->kids) stack.push_back({kv.second, st.k, st.x, st.pos});
+    for (const auto& kv : st.node->kids) stack.push_back({kv.second, st.k, st.blocks, st.partial});
   }
   for (int64_t r = 0; r < n; ++r) {
     const std::vector<uint64_t> chain = block_chain(tokens + offsets[r], offsets[r + 1] - offsets[r], block_size);
@@ -458,6 +492,11 @@ void oracle_block_lpm(const oracle_tree* t, int64_t block_size, int64_t n, const
     while (found < (int64_t)chain.size() && stored.count(chain[found])) ++found;
     h_out[r] = block_size * found;
   }
+}
+
+// Digest of one block (exported for tests of the hash itself).
+uint64_t oracle_block_digest(const int32_t* blk, int64_t block_size, int64_t idx) {
+  return block_digest(blk, block_size, idx);
 }
 
 // Eviction scores and victim order over canonical node ids. demand[c] is the

@@ -4,26 +4,34 @@
 // Every full block of B tokens of a cached path is stored as a chained hash
 // of the path up to and including it, so a request's hit is B times the
 // number of its leading full blocks whose chained hash is in the table.
-// The hash (defined by this library):
-//   term(j, t)  = mix64((j << 32) | t)           j = position inside the block
-//   digest(b)   = mix64(XOR of term over the block's positions)
-//   k_0 = 0x243F6A8885A308D3,  k_i = mix64(k_{i-1} XOR digest(b_i))
-// with mix64 the SplitMix64 output mix. The digest is a XOR of position-
-// tagged terms, so a wavefront computes a block's digest in parallel; only
-// the chain over blocks is sequential.
+// The hash (defined by this library, B even):
+//   key(j)   = mix64(j + 0x6A09E667F3BCC909), a_j its low and b_j its high half
+//   n_a      = sum over pairs i of ((u_2i + a_2i) mod 2^32) * ((u_2i+1 + a_2i+1) mod 2^32)
+//              mod 2^64 (an NH pass, UMAC), n_b the same with b; u = tokens as uint32
+//   digest_i = mix64(n_a ^ rotl(n_b, 32) ^ 0x9E3779B97F4A7C15 * (i + 1)), i = block index
+//   k_0 = 0x243F6A8885A308D3,  k_{i+1} = k_i + digest_i  (mod 2^64)
+// with mix64 the SplitMix64 output mix. Both the compression (a sum of
+// products) and the chain (a sum of digests that carry their block index)
+// are additive, so a wavefront reduces a block and scans a step's blocks in
+// log2 rounds instead of running a sequential chain.
 //
-// Table: open addressing with linear probing over uint64 slots holding the
-// chained hashes themselves, slot = k >> (64 - bits), load factor <= 1/2;
+// Table: open addressing over 64-byte buckets of 8 uint64 slots holding the
+// chained hashes themselves. A hash k lives in its home bucket
+// k >> (64 - bucket_bits) or, if that was full when k was inserted, in the
+// first later bucket (cyclically) with a free slot; at most half the slots
+// are used, so a search ends at the first bucket that holds k or an empty
+// slot, nearly always the home bucket: one 64-byte read per probed block.
 // 0 marks an empty slot, so a stored hash equal to 0 is kept as a flag
 // beside the table instead. Built on the host from a tree description and
 // uploaded once.
 //
 // Kernel: one 64-lane wavefront per request. Each step covers 256 tokens:
-// lane l hashes tokens [4l, 4l + 4) of the step with one 16-byte load, a
-// XOR butterfly over the B/4 lanes of each block forms the block digests,
-// every lane replays the chain over the step's 256/B blocks (keeping its own
-// block's hash), and the lane of each block probes the table. The first
-// missing block ends the walk. B is a power of two in [4, 256].
+// lane l compresses tokens [4l, 4l + 4) of the step (one 16-byte load, two
+// token pairs per NH pass), a sum butterfly over the B/4 lanes of each block
+// completes the block's NH values, every lane finishes its block's digest,
+// an inclusive scan over the step's 256/B blocks adds the chain, and the
+// first lane of each block probes the table. The first missing block ends
+// the walk. B is a power of two in [4, 256].
 #include <algorithm>
 #include <new>
 #include <vector>
@@ -33,7 +41,7 @@
 struct peek_block_table {
   int device;
   int32_t block_size;
-  int32_t bits;            // the table has 2^bits slots
+  int32_t bucket_bits;     // the table has 2^bucket_bits buckets of 8 slots
   int32_t zero_stored;     // the hash value 0 is stored (it cannot sit in a slot)
   int64_t num_blocks;      // distinct stored block hashes
   uint64_t* d_slots;
@@ -45,6 +53,7 @@ namespace {
 constexpr uint64_t kChainStart = 0x243F6A8885A308D3ull;
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
+constexpr int kBucketSlots = 8;   // slots per bucket: one 64-byte line
 
 __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
@@ -52,71 +61,194 @@ __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
-__host__ __device__ __forceinline__ uint64_t term(uint32_t j, int32_t t) {
-  return mix64(((uint64_t)j << 32) | (uint32_t)t);
+constexpr uint64_t kKeySeed = 0x6A09E667F3BCC909ull;
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+
+// Position key of token j of a block: low half for the first NH pass, high
+// half for the second.
+__host__ __device__ __forceinline__ uint64_t pos_key(uint32_t j) { return mix64((uint64_t)j + kKeySeed); }
+
+__host__ __device__ __forceinline__ uint64_t nh_pair(uint32_t x, uint32_t y) { return (uint64_t)x * (uint64_t)y; }
+
+// Digest of a block from its two NH sums and its index i along the path.
+__host__ __device__ __forceinline__ uint64_t finish_digest(uint64_t na, uint64_t nb, uint64_t gamma_i1) {
+  return mix64(na ^ ((nb << 32) | (nb >> 32)) ^ gamma_i1);
 }
 
 typedef int32_t v4i __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint64_t v2u64 __attribute__((ext_vector_type(2)));
 
+// One bucket of the table: 8 slots, 64 bytes, 64-byte aligned.
+struct Bucket {
+  v2u64 q[4];
+};
+
+__device__ __forceinline__ Bucket load_bucket(const uint64_t* __restrict__ slots, uint64_t b) {
+  const v2u64* src = reinterpret_cast<const v2u64*>(slots + b * kBucketSlots);
+  return Bucket{{src[0], src[1], src[2], src[3]}};
+}
+
+// 1 = key found, 0 = an empty slot ends the search, -1 = bucket full without the key.
+__device__ __forceinline__ int bucket_lookup(const Bucket& e, uint64_t key) {
+  bool found = false, empty = false;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    found |= (e.q[i].x == key) | (e.q[i].y == key);
+    empty |= (e.q[i].x == 0) | (e.q[i].y == 0);
+  }
+  return found ? 1 : (empty ? 0 : -1);
+}
+
+// Whether the nonzero key is stored, given its home bucket already loaded.
+__device__ __forceinline__ bool finish_probe(const uint64_t* __restrict__ slots, uint64_t bmask, uint64_t key,
+                                             uint64_t b, Bucket e) {
+  while (true) {
+    const int st = bucket_lookup(e, key);
+    if (st >= 0) return st == 1;
+    b = (b + 1) & bmask;   // the table is at most half full: some bucket has an empty slot
+    e = load_bucket(slots, b);
+  }
+}
+
+// Wave-wide token load of one step, clamped to the request's last full
+// 4-token group so that it is always issued (and always in bounds); lanes
+// past the last full block ignore what they get.
+__device__ __forceinline__ v4i load_step(const int32_t* __restrict__ p, int64_t step, int lane, int64_t last4) {
+  const int64_t idx = min(step * 256 + (int64_t)lane * 4, last4);
+  return __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p + idx));
+}
+
+// A probe in flight: the step's block count, this lane's key and the part of
+// the key's home bucket this lane loaded.
+template <int SPL>
+struct Probe {
+  int32_t cnt;
+  uint64_t key;
+  uint64_t v[SPL];
+};
+
+// The walk is software-pipelined two steps deep: while step s is hashed, the
+// tokens of steps s + 1 and s + 2 are being loaded and the buckets probed for
+// steps s - 1 and s - 2 are in flight; step s - 2's verdict is read after
+// step s is hashed. A miss found that way ends the walk, so at most two steps
+// past the first missing block are hashed for nothing. The loads are issued
+// unconditionally (clamped addresses) so that every wait is a static count.
+// The B/4 lanes of a block share its bucket load: up to 4 of them read 16,
+// 32 or 64 bytes each of the 64-byte bucket.
+template <int LS>
 __global__ __launch_bounds__(kWave* kWavesPerBlock) void k_block_lpm(const int32_t* __restrict__ tokens,
                                                                       const int64_t* __restrict__ offsets, int32_t n,
-                                                                      int32_t B, const uint64_t* __restrict__ slots,
-                                                                      int32_t bits, int32_t zero_stored,
+                                                                      const uint64_t* __restrict__ slots,
+                                                                      int32_t bucket_bits, int32_t zero_stored,
                                                                       int32_t* __restrict__ h_out) {
+  constexpr int LPB = 1 << LS;                 // lanes per block
+  constexpr int BPS = 64 >> LS;                // blocks per step
+  constexpr int B = 4 << LS;                   // block size
+  constexpr int PL = LPB < 4 ? LPB : 4;        // lanes that load a block's bucket
+  constexpr int SPL = kBucketSlots / PL;       // slots each of them loads
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t r = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * kWavesPerBlock + (int32_t)(threadIdx.x / kWave));
   if (r >= n) return;
   const int64_t off = offsets[r];
-  const int64_t nfull = (offsets[r + 1] - off) / B;
+  const int64_t nfull = (offsets[r + 1] - off) >> (LS + 2);
+  if (nfull == 0) {
+    if (lane == 0) h_out[r] = 0;
+    return;
+  }
   const int32_t* __restrict__ p = tokens + off;
-  const int32_t lanes_per_block = B / 4;
-  const int32_t blocks_per_step = 256 / B;
-  const uint64_t mask = (bits >= 64) ? ~0ull : ((1ull << bits) - 1);
+  const int64_t last4 = nfull * B - 4;
+  const int myblock = lane >> LS;              // this lane's block within a step
+  const int sub = lane & (LPB - 1);            // its place in that block
+  const bool leader = sub == 0;
+  const bool loader = sub < PL;
+  const uint64_t gmask = (LPB == 64 ? ~0ull : ((1ull << LPB) - 1)) << (myblock * LPB);   // its block's lanes
+  // position keys of this lane's 4 tokens
+  const uint32_t j0 = (uint32_t)((lane * 4) & (B - 1));
+  const uint64_t w0 = pos_key(j0), w1 = pos_key(j0 + 1), w2 = pos_key(j0 + 2), w3 = pos_key(j0 + 3);
+  const uint64_t bmask = (1ull << bucket_bits) - 1;
+  const int hshift = 64 - bucket_bits;
+  // gamma * (block index + 1) for this lane's block, advanced one step's blocks per step
+  uint64_t gidx = kGamma * (uint64_t)(myblock + 1);
+  constexpr uint64_t gstep = kGamma * (uint64_t)BPS;
   uint64_t k = kChainStart;
   int64_t found = 0;
-  for (int64_t b0 = 0; b0 < nfull; b0 += blocks_per_step) {
-    const int32_t cnt = (int32_t)min((int64_t)blocks_per_step, nfull - b0);
-    // this lane's 4 tokens, if they belong to one of the cnt full blocks
-    const int32_t myblock = lane / lanes_per_block;
-    uint64_t x = 0;
-    if (myblock < cnt) {
-      const int64_t idx = b0 * B + (int64_t)lane * 4;
-      const v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p + idx));
-      const uint32_t j0 = (uint32_t)((lane * 4) & (B - 1));
-      x = term(j0, v.x) ^ term(j0 + 1, v.y) ^ term(j0 + 2, v.z) ^ term(j0 + 3, v.w);
-    }
-    for (int m = 1; m < lanes_per_block; m <<= 1) x ^= __shfl_xor(x, m);
-    const uint64_t digest = mix64(x);
-    // the chain over this step's blocks; lane j keeps block j's hash
+  v4i v0 = load_step(p, 0, lane, last4);
+  v4i v1 = load_step(p, 1, lane, last4);
+  Probe<SPL> pa{}, pb{};   // steps s - 2 and s - 1
+  for (int64_t s = 0;; ++s) {
+    const int32_t cnt = (int32_t)min((int64_t)BPS, nfull - s * BPS);   // <= 0 past the last full block
     uint64_t mine = 0;
-    for (int32_t j = 0; j < cnt; ++j) {
-      k = mix64(k ^ __shfl(digest, j * lanes_per_block));
-      if (lane == j) mine = k;
+    if (cnt > 0) {
+      uint64_t na = 0, nb = 0;
+      if (myblock < cnt) {
+        const uint32_t u0 = (uint32_t)v0.x, u1 = (uint32_t)v0.y, u2 = (uint32_t)v0.z, u3 = (uint32_t)v0.w;
+        na = nh_pair(u0 + (uint32_t)w0, u1 + (uint32_t)w1) + nh_pair(u2 + (uint32_t)w2, u3 + (uint32_t)w3);
+        nb = nh_pair(u0 + (uint32_t)(w0 >> 32), u1 + (uint32_t)(w1 >> 32)) +
+             nh_pair(u2 + (uint32_t)(w2 >> 32), u3 + (uint32_t)(w3 >> 32));
+      }
+#pragma unroll
+      for (int m = 1; m < LPB; m <<= 1) {
+        na += __shfl_xor(na, m);
+        nb += __shfl_xor(nb, m);
+      }
+      uint64_t d = finish_digest(na, nb, gidx);
+      // inclusive scan of the digests over the step's blocks
+#pragma unroll
+      for (int o = 1; o < BPS; o <<= 1) {
+        const int src = lane - (o << LS);
+        const uint64_t t = __shfl(d, src >= 0 ? src : lane);
+        if (myblock >= o) d += t;
+      }
+      mine = k + d;
+      const int last = (cnt - 1) << LS;
+      k = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(mine >> 32), last) << 32) |
+          (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine, last);
+      gidx += gstep;
     }
-    bool hit = false;
-    if (lane < cnt) {
-      if (mine == 0) {
-        hit = zero_stored != 0;
-      } else {
-        // the table is at most half full, so an empty slot ends every probe
-        uint64_t s = mine >> (64 - bits);
-        while (true) {
-          const uint64_t v = slots[s];
-          if (v == mine) {
-            hit = true;
-            break;
-          }
-          if (v == 0) break;
-          s = (s + 1) & mask;
+    v0 = v1;
+    v1 = load_step(p, s + 2, lane, last4);
+    // the verdict of step s - 2's probe
+    if (pa.cnt > 0) {
+      bool f = false, e = false;
+      if (loader) {
+#pragma unroll
+        for (int i = 0; i < SPL; ++i) {
+          f |= pa.v[i] == pa.key;
+          e |= pa.v[i] == 0;
         }
       }
+      const uint64_t F = __ballot(f), E = __ballot(e);
+      const bool probing = leader && myblock < pa.cnt;
+      bool hit = (F & gmask) != 0;
+      if (pa.key == 0) hit = zero_stored != 0;
+      // home bucket full without the key: search on from the next bucket
+      else if (probing && !hit && (E & gmask) == 0) {
+        const uint64_t hb = ((pa.key >> hshift) + 1) & bmask;
+        hit = finish_probe(slots, bmask, pa.key, hb, load_bucket(slots, hb));
+      }
+      const uint64_t miss = __ballot(probing && !hit);
+      if (miss) {
+        found += (__ffsll((unsigned long long)miss) - 1) >> LS;
+        break;
+      }
+      found += pa.cnt;
     }
-    const uint64_t miss = __ballot(lane < cnt && !hit);
-    if (miss) {
-      found += __ffsll((unsigned long long)miss) - 1;
-      break;
+    // this step's probe: the loaders of each block read its home bucket
+    pa = pb;
+    pb.cnt = cnt > 0 ? cnt : 0;
+    pb.key = mine;
+    {
+      const bool use = loader && myblock < cnt && mine != 0;
+      const uint64_t at = use ? (mine >> hshift) * kBucketSlots + (uint64_t)sub * SPL : 0;
+      const v2u64* src = reinterpret_cast<const v2u64*>(slots + at);
+#pragma unroll
+      for (int i = 0; i < SPL / 2; ++i) {
+        const v2u64 q = src[i];
+        pb.v[2 * i] = q.x;
+        pb.v[2 * i + 1] = q.y;
+      }
     }
-    found += cnt;
+    if (pa.cnt == 0 && pb.cnt == 0) break;
   }
   if (lane == 0) h_out[r] = (int32_t)(found * B);
 }
@@ -156,40 +288,63 @@ peek_status peek_block_table_build(int32_t num_nodes, const int32_t* parent, con
     for (int32_t i = 0; i < num_nodes; ++i)
       if (parent[i] >= 0) kids[fill[parent[i]]++] = i;
   }
+  // position keys of one block
+  std::vector<uint32_t> ka(block_size), kb(block_size);
+  for (int32_t j = 0; j < block_size; ++j) {
+    const uint64_t w = pos_key((uint32_t)j);
+    ka[j] = (uint32_t)w;
+    kb[j] = (uint32_t)(w >> 32);
+  }
+  // depth first, carrying the chain value, the full blocks so far and the
+  // block in progress (its NH sums, position and an unpaired even token)
   struct State {
     int32_t node;
-    uint64_t k, x;
     int32_t pos;
+    uint32_t pend;
+    uint64_t k, na, nb, blocks;
   };
   std::vector<uint64_t> keys;
-  std::vector<State> stack{{root, kChainStart, 0, 0}};
+  std::vector<State> stack{{root, 0, 0, kChainStart, 0, 0, 0}};
   while (!stack.empty()) {
     State st = stack.back();
     stack.pop_back();
     for (int64_t q = edge_offsets[st.node]; q < edge_offsets[st.node + 1]; ++q) {
-      st.x ^= term((uint32_t)st.pos, edge_tokens[q]);
+      const uint32_t u = (uint32_t)edge_tokens[q];
+      if ((st.pos & 1) == 0) {
+        st.pend = u;
+      } else {
+        st.na += nh_pair(st.pend + ka[st.pos - 1], u + ka[st.pos]);
+        st.nb += nh_pair(st.pend + kb[st.pos - 1], u + kb[st.pos]);
+      }
       if (++st.pos == block_size) {
-        st.k = mix64(st.k ^ mix64(st.x));
+        st.k += finish_digest(st.na, st.nb, kGamma * (st.blocks + 1));
         keys.push_back(st.k);
-        st.x = 0;
+        st.blocks += 1;
+        st.na = st.nb = 0;
         st.pos = 0;
       }
     }
-    for (int32_t q = kbeg[st.node]; q < kbeg[st.node + 1]; ++q) stack.push_back({kids[q], st.k, st.x, st.pos});
+    for (int32_t q = kbeg[st.node]; q < kbeg[st.node + 1]; ++q) {
+      State c = st;
+      c.node = kids[q];
+      stack.push_back(c);
+    }
   }
   std::sort(keys.begin(), keys.end());
   keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
   const int64_t num_blocks = (int64_t)keys.size();
   const bool zero_stored = !keys.empty() && keys.front() == 0;
   if (zero_stored) keys.erase(keys.begin());
-  int32_t bits = 6;
-  while ((int64_t(1) << bits) < 2 * (int64_t)keys.size()) ++bits;
-  const uint64_t slots_n = uint64_t(1) << bits;
+  int32_t bucket_bits = 3;
+  while ((int64_t(kBucketSlots) << bucket_bits) < 2 * (int64_t)keys.size()) ++bucket_bits;
+  const uint64_t buckets = uint64_t(1) << bucket_bits;
+  const uint64_t slots_n = buckets * kBucketSlots;
   std::vector<uint64_t> table(slots_n, 0);
+  std::vector<uint8_t> used(buckets, 0);
   for (uint64_t key : keys) {
-    uint64_t s = key >> (64 - bits);
-    while (table[s] != 0) s = (s + 1) & (slots_n - 1);
-    table[s] = key;
+    uint64_t b = key >> (64 - bucket_bits);
+    while (used[b] == kBucketSlots) b = (b + 1) & (buckets - 1);
+    table[b * kBucketSlots + used[b]++] = key;
   }
   uint64_t* d = nullptr;
   hipError_t e = hipMalloc((void**)&d, sizeof(uint64_t) * slots_n);
@@ -211,7 +366,7 @@ peek_status peek_block_table_build(int32_t num_nodes, const int32_t* parent, con
   }
   t->device = device;
   t->block_size = block_size;
-  t->bits = bits;
+  t->bucket_bits = bucket_bits;
   t->zero_stored = zero_stored ? 1 : 0;
   t->num_blocks = num_blocks;
   t->d_slots = d;
@@ -224,7 +379,7 @@ peek_status peek_block_table_stats(const peek_block_table* t, int64_t* num_block
   clear_error();
   if (!t) return fail(PEEK_ERR_INVALID_ARGUMENT, "table is NULL");
   if (num_blocks) *num_blocks = t->num_blocks;
-  if (num_slots) *num_slots = int64_t(1) << t->bits;
+  if (num_slots) *num_slots = int64_t(kBucketSlots) << t->bucket_bits;
   if (block_size) *block_size = t->block_size;
   return PEEK_OK;
 }
@@ -250,8 +405,25 @@ peek_status peek_block_lpm_batch(const peek_block_table* t, int32_t n, const int
   if (dev != t->device)
     return fail(PEEK_ERR_INVALID_ARGUMENT, "table lives on device %d, current device is %d", t->device, dev);
   const int64_t blocks = ((int64_t)n + kWavesPerBlock - 1) / kWavesPerBlock;
-  hipLaunchKernelGGL(k_block_lpm, dim3((unsigned)blocks), dim3(kWave * kWavesPerBlock), 0, (hipStream_t)stream, d_tokens,
-                     d_offsets, n, t->block_size, t->d_slots, t->bits, t->zero_stored, d_h);
+  const dim3 grid((unsigned)blocks), block(kWave * kWavesPerBlock);
+  hipStream_t st = (hipStream_t)stream;
+  switch (t->block_size) {
+#define PEEK_BLOCK_CASE(LS)                                                                                        \
+  case 4 << LS:                                                                                                    \
+    hipLaunchKernelGGL(k_block_lpm<LS>, grid, block, 0, st, d_tokens, d_offsets, n, t->d_slots, t->bucket_bits,  \
+                       t->zero_stored, d_h);                                                                       \
+    break;
+    PEEK_BLOCK_CASE(0)
+    PEEK_BLOCK_CASE(1)
+    PEEK_BLOCK_CASE(2)
+    PEEK_BLOCK_CASE(3)
+    PEEK_BLOCK_CASE(4)
+    PEEK_BLOCK_CASE(5)
+    PEEK_BLOCK_CASE(6)
+#undef PEEK_BLOCK_CASE
+    default:
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "table has an unsupported block size %d", t->block_size);
+  }
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }

@@ -50,7 +50,7 @@ def test_oracle_matches_brute_force_on_sequences(seed, vocab, B, T):
     e = O.evict(t, demand)
     assert np.array_equal(e.score, escore)
     assert np.array_equal(e.order, eorder)
-    for bb in {1, B, 3}:
+    for bb in {2, 4, 6, max(B, 2)}:
         assert np.array_equal(O.block_lpm(t, w.tokens, w.offsets, bb), BF.block_lpm(nodes, prompts, bb))
     share, cid, csz = BF.clusters(prompts, w.threshold)
     c = O.clusters(w.tokens, w.offsets, w.threshold)
@@ -102,6 +102,47 @@ def test_hashed_block_hit_equals_the_radix_hit(name, seed):
     t = O.cache_tree_of(w)
     h = O.block_lpm(t, w.tokens, w.offsets, w.block_size)
     assert np.array_equal(h, O.lpm(t, w.tokens, w.offsets, w.block_size).h)
+
+
+def _block_hit(cached, prompt, B):
+    t = O.Tree.from_sequences(*W.pack([np.asarray(c, np.int32) for c in cached]))
+    tok, off = W.pack([np.asarray(prompt, np.int32)])
+    return int(O.block_lpm(t, tok, off, B)[0])
+
+
+def test_hashed_swapped_blocks_do_not_match():
+    # the chain adds block digests, so a block's digest must carry its index:
+    # with Y and X+Y cached, the prompt Y+X hits Y only
+    X, Y = [1, 2, 3, 4], [5, 6, 7, 8]
+    assert _block_hit([Y, X + Y], Y + X, 4) == 4
+    assert _block_hit([Y, X + Y], X + Y, 4) == 8
+
+
+def test_hashed_swapped_tokens_in_a_pair_do_not_match():
+    # NH multiplies the two tokens of a pair: without position keys the
+    # product would not see their order
+    assert _block_hit([[3, 9, 1, 1]], [9, 3, 1, 1], 4) == 0
+    assert _block_hit([[3, 9, 1, 1, 2, 2, 5, 6]], [3, 9, 1, 1, 2, 2, 6, 5], 4) == 4
+
+
+def test_hashed_zero_product_does_not_hide_a_token():
+    # a pair whose first word plus its position key is 0 mod 2^32 has a zero
+    # NH product in that pass whatever its partner; the second pass (its own
+    # keys) still sees the partner. Position keys are mix64(j + 0x6A09E667F3BCC909).
+    w0 = O.mix64(0x6A09E667F3BCC909)
+    for key in (w0 & 0xFFFFFFFF, w0 >> 32, 0):
+        t0 = (-key) & 0xFFFFFFFF
+        t0 = t0 - 2**32 if t0 >= 2**31 else t0
+        assert _block_hit([[t0, 7, 9, 9]], [t0, 8, 9, 9], 4) == 0
+        assert _block_hit([[t0, 7, 9, 9]], [t0, 7, 9, 9, 1], 4) == 4
+
+
+def test_hashed_block_size_must_be_even():
+    t = O.Tree.from_sequences(*W.pack([np.arange(8, dtype=np.int32)]))
+    tok, off = W.pack([np.arange(8, dtype=np.int32)])
+    for bad in (1, 3, 0):
+        with pytest.raises(ValueError):
+            O.block_lpm(t, tok, off, bad)
 
 
 def test_block_size_one_is_plain_lcp_against_a_set():

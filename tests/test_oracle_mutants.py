@@ -35,8 +35,11 @@ MUTANTS = {
     "evict_frees_inner_nodes_early": ("--kids_left[p->canon] == 0", "--kids_left[p->canon] <= 1"),
     "block_hit_counts_partial_block": ("for (int64_t b = 0; (b + 1) * B <= len; ++b) {",
                                        "for (int64_t b = 0; b * B < len; ++b) {"),
-    "block_hash_not_chained": ("    k = oracle_mix64(k ^ oracle_mix64(x));\n    out.push_back(k);",
-                               "    k = oracle_mix64(0x243F6A8885A308D3ULL ^ oracle_mix64(x));\n    out.push_back(k);"),
+    "block_hash_not_chained": ("{ return k + digest; }", "{ return 0x243F6A8885A308D3ULL + digest + 0 * k; }"),
+    "block_digest_ignores_its_index": (" ^ (0x9E3779B97F4A7C15ULL * (uint64_t)(idx + 1)));", ");"),
+    "nh_without_position_keys": ("const uint32_t x = (uint32_t)blk[i] + nh_key(i, pass);",
+                                 "const uint32_t x = (uint32_t)blk[i];"),
+    "nh_single_pass": ("for (int pass = 0; pass < 2; ++pass)", "for (int pass = 0; pass < 1; ++pass)"),
     "block_hashes_never_stored": ("        stored.insert(st.k);\n", ""),
     "score_leaves_out_own_request": ("      score += node->pending_count * node->elen;",
                                      "      score += (node->pending_count - 1) * node->elen;"),
