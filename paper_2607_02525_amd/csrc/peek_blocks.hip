@@ -25,13 +25,14 @@
 // beside the table instead. Built on the host from a tree description and
 // uploaded once.
 //
-// Kernel: one 64-lane wavefront per request. Each step covers 256 tokens:
-// lane l compresses tokens [4l, 4l + 4) of the step (one 16-byte load, two
-// token pairs per NH pass), a sum butterfly over the B/4 lanes of each block
-// completes the block's NH values, every lane finishes its block's digest,
-// an inclusive scan over the step's 256/B blocks adds the chain, and the
-// first lane of each block probes the table. The first missing block ends
-// the walk. B is a power of two in [4, 256].
+// Kernel: one 64-lane wavefront per request. Each step covers 64 T tokens:
+// lane l compresses the T consecutive tokens [T l, T l + T) of the step
+// (T = 8 for B = 8, else 4, so a block spans B / T lanes), a sum
+// butterfly over a block's lanes completes its NH values, every lane
+// finishes its block's digest, an inclusive scan over the step's blocks adds
+// the chain, and the step's last block is probed (all of its blocks only
+// when that one is missing). The first missing block ends the walk. B is a
+// power of two in [4, 256].
 #include <algorithm>
 #include <new>
 #include <vector>
@@ -110,14 +111,6 @@ __device__ __forceinline__ bool finish_probe(const uint64_t* __restrict__ slots,
   }
 }
 
-// Wave-wide token load of one step, clamped to the request's last full
-// 4-token group so that it is always issued (and always in bounds); lanes
-// past the last full block ignore what they get.
-__device__ __forceinline__ v4i load_step(const int32_t* __restrict__ p, int64_t step, int lane, int64_t last4) {
-  const int64_t idx = min(step * 256 + (int64_t)lane * 4, last4);
-  return __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p + idx));
-}
-
 // A probe in flight: the step's block count, this lane's key and the part of
 // the key's home bucket this lane loaded.
 template <int SPL>
@@ -127,30 +120,103 @@ struct Probe {
   uint64_t v[SPL];
 };
 
-// The walk is software-pipelined two steps deep: while step s is hashed, the
-// tokens of steps s + 1 and s + 2 are being loaded and the buckets probed for
-// steps s - 1 and s - 2 are in flight; step s - 2's verdict is read after
-// step s is hashed. A miss found that way ends the walk, so at most two steps
-// past the first missing block are hashed for nothing. The loads are issued
-// unconditionally (clamped addresses) so that every wait is a static count.
-// The B/4 lanes of a block share its bucket load: up to 4 of them read 16,
-// 32 or 64 bytes each of the 64-byte bucket.
-template <int LS>
+// The T tokens of one lane in one step: T/4 16-byte loads, each clamped to
+// the request's last full 4-token group so that every load is issued (a
+// static wait count) and in bounds; lanes past the last full block ignore
+// what they get.
+template <int T>
+struct Tokens {
+  v4i g[T / 4];
+};
+
+template <int T>
+__device__ __forceinline__ Tokens<T> load_tokens(const int32_t* __restrict__ p, int64_t first, int64_t last4) {
+  Tokens<T> t;
+#pragma unroll
+  for (int i = 0; i < T / 4; ++i)
+    t.g[i] = __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p + min(first + 4 * i, last4)));
+  return t;
+}
+
+// The loaders of a block read their part of the key's home bucket (use =
+// false reads slot 0 instead, so the load is still issued).
+template <int SPL>
+__device__ __forceinline__ void load_parts(uint64_t (&v)[SPL], const uint64_t* __restrict__ slots, uint64_t key,
+                                           bool use, int sub, int hshift) {
+  const uint64_t at = use ? (key >> hshift) * kBucketSlots + (uint64_t)sub * SPL : 0;
+  const v2u64* src = reinterpret_cast<const v2u64*>(slots + at);
+#pragma unroll
+  for (int i = 0; i < SPL / 2; ++i) {
+    const v2u64 q = src[i];
+    v[2 * i] = q.x;
+    v[2 * i + 1] = q.y;
+  }
+}
+
+// Whether this lane's block's key is stored, for the blocks selected by
+// `sel` (the same in all lanes of a block), given the home-bucket parts
+// their loaders hold. Valid in every lane of a selected block.
+template <int SPL>
+__device__ __forceinline__ bool block_stored(const uint64_t (&v)[SPL], uint64_t key, bool sel, bool loader,
+                                             uint64_t gmask, const uint64_t* __restrict__ slots, uint64_t bmask,
+                                             int hshift, int32_t zero_stored) {
+  bool f = false, e = false;
+  if (sel && loader) {
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      f |= v[i] == key;
+      e |= v[i] == 0;
+    }
+  }
+  const uint64_t F = __ballot(f), E = __ballot(e);
+  bool hit = (F & gmask) != 0;
+  if (key == 0) {
+    hit = zero_stored != 0;
+  } else if (sel && !hit && (E & gmask) == 0) {
+    // home bucket full without the key: search on from the next bucket
+    const uint64_t hb = ((key >> hshift) + 1) & bmask;
+    hit = finish_probe(slots, bmask, key, hb, load_bucket(slots, hb));
+  }
+  return hit;
+}
+
+// The walk. Lane l holds T consecutive tokens of each step (64 T tokens per
+// step); a block spans LPB = B / T lanes. With one lane per block the
+// position keys are compile-time constants. T = 8 for B = 8 and 4 otherwise
+// (measured: fatter steps hash more tokens past the first miss and load
+// less contiguously).
+//
+// The table holds every full-block prefix of every cached path, so the
+// stored keys along a request's chain form a prefix of it: if a step's last
+// block is stored, so is every block before it. Each step therefore probes
+// only its last block; only the step whose last block is missing probes all
+// of its blocks to find the first miss. This returns the number of leading
+// stored blocks exactly unless two different block prefixes share a 64-bit
+// key (the premise of any hashed cache).
+//
+// Step s is hashed while the tokens of step s + 1 are loading and the
+// last-block probe of step s - 1 is in flight; step s - 1's verdict is read
+// after step s is hashed, so at most one step past the first missing block
+// is hashed for nothing. The LPB lanes of a block share its 64-byte bucket
+// load: up to 4 of them read 16, 32 or 64 bytes each.
+template <int LT, int LS>
 __global__ __launch_bounds__(kWave* kWavesPerBlock) void k_block_lpm(const int32_t* __restrict__ tokens,
                                                                       const int64_t* __restrict__ offsets, int32_t n,
                                                                       const uint64_t* __restrict__ slots,
                                                                       int32_t bucket_bits, int32_t zero_stored,
                                                                       int32_t* __restrict__ h_out) {
+  constexpr int T = 1 << LT;                   // tokens per lane per step
   constexpr int LPB = 1 << LS;                 // lanes per block
   constexpr int BPS = 64 >> LS;                // blocks per step
-  constexpr int B = 4 << LS;                   // block size
+  constexpr int B = T << LS;                   // block size
+  constexpr int STEP = 64 * T;                 // tokens per step
   constexpr int PL = LPB < 4 ? LPB : 4;        // lanes that load a block's bucket
   constexpr int SPL = kBucketSlots / PL;       // slots each of them loads
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t r = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * kWavesPerBlock + (int32_t)(threadIdx.x / kWave));
   if (r >= n) return;
   const int64_t off = offsets[r];
-  const int64_t nfull = (offsets[r + 1] - off) >> (LS + 2);
+  const int64_t nfull = (offsets[r + 1] - off) / B;
   if (nfull == 0) {
     if (lane == 0) h_out[r] = 0;
     return;
@@ -162,9 +228,14 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void k_block_lpm(const int32
   const bool leader = sub == 0;
   const bool loader = sub < PL;
   const uint64_t gmask = (LPB == 64 ? ~0ull : ((1ull << LPB) - 1)) << (myblock * LPB);   // its block's lanes
-  // position keys of this lane's 4 tokens
-  const uint32_t j0 = (uint32_t)((lane * 4) & (B - 1));
-  const uint64_t w0 = pos_key(j0), w1 = pos_key(j0 + 1), w2 = pos_key(j0 + 2), w3 = pos_key(j0 + 3);
+  // position keys of this lane's T tokens (constants when a lane holds a whole block)
+  uint32_t ka[T], kb[T];
+#pragma unroll
+  for (int q = 0; q < T; ++q) {
+    const uint64_t w = pos_key((uint32_t)((sub << LT) + q));
+    ka[q] = (uint32_t)w;
+    kb[q] = (uint32_t)(w >> 32);
+  }
   const uint64_t bmask = (1ull << bucket_bits) - 1;
   const int hshift = 64 - bucket_bits;
   // gamma * (block index + 1) for this lane's block, advanced one step's blocks per step
@@ -172,19 +243,22 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void k_block_lpm(const int32
   constexpr uint64_t gstep = kGamma * (uint64_t)BPS;
   uint64_t k = kChainStart;
   int64_t found = 0;
-  v4i v0 = load_step(p, 0, lane, last4);
-  v4i v1 = load_step(p, 1, lane, last4);
-  Probe<SPL> pa{}, pb{};   // steps s - 2 and s - 1
+  Tokens<T> cur = load_tokens<T>(p, (int64_t)lane * T, last4);
+  Probe<SPL> pr{};   // step s - 1: its blocks, this lane's key, the last block's bucket parts
   for (int64_t s = 0;; ++s) {
     const int32_t cnt = (int32_t)min((int64_t)BPS, nfull - s * BPS);   // <= 0 past the last full block
+    const Tokens<T> nxt = load_tokens<T>(p, (s + 1) * STEP + (int64_t)lane * T, last4);
     uint64_t mine = 0;
     if (cnt > 0) {
       uint64_t na = 0, nb = 0;
       if (myblock < cnt) {
-        const uint32_t u0 = (uint32_t)v0.x, u1 = (uint32_t)v0.y, u2 = (uint32_t)v0.z, u3 = (uint32_t)v0.w;
-        na = nh_pair(u0 + (uint32_t)w0, u1 + (uint32_t)w1) + nh_pair(u2 + (uint32_t)w2, u3 + (uint32_t)w3);
-        nb = nh_pair(u0 + (uint32_t)(w0 >> 32), u1 + (uint32_t)(w1 >> 32)) +
-             nh_pair(u2 + (uint32_t)(w2 >> 32), u3 + (uint32_t)(w3 >> 32));
+#pragma unroll
+        for (int i = 0; i < T / 4; ++i) {
+          const uint32_t u0 = (uint32_t)cur.g[i].x, u1 = (uint32_t)cur.g[i].y;
+          const uint32_t u2 = (uint32_t)cur.g[i].z, u3 = (uint32_t)cur.g[i].w;
+          na += nh_pair(u0 + ka[4 * i], u1 + ka[4 * i + 1]) + nh_pair(u2 + ka[4 * i + 2], u3 + ka[4 * i + 3]);
+          nb += nh_pair(u0 + kb[4 * i], u1 + kb[4 * i + 1]) + nh_pair(u2 + kb[4 * i + 2], u3 + kb[4 * i + 3]);
+        }
       }
 #pragma unroll
       for (int m = 1; m < LPB; m <<= 1) {
@@ -205,50 +279,30 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void k_block_lpm(const int32
           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine, last);
       gidx += gstep;
     }
-    v0 = v1;
-    v1 = load_step(p, s + 2, lane, last4);
-    // the verdict of step s - 2's probe
-    if (pa.cnt > 0) {
-      bool f = false, e = false;
-      if (loader) {
-#pragma unroll
-        for (int i = 0; i < SPL; ++i) {
-          f |= pa.v[i] == pa.key;
-          e |= pa.v[i] == 0;
-        }
-      }
-      const uint64_t F = __ballot(f), E = __ballot(e);
-      const bool probing = leader && myblock < pa.cnt;
-      bool hit = (F & gmask) != 0;
-      if (pa.key == 0) hit = zero_stored != 0;
-      // home bucket full without the key: search on from the next bucket
-      else if (probing && !hit && (E & gmask) == 0) {
-        const uint64_t hb = ((pa.key >> hshift) + 1) & bmask;
-        hit = finish_probe(slots, bmask, pa.key, hb, load_bucket(slots, hb));
-      }
-      const uint64_t miss = __ballot(probing && !hit);
-      if (miss) {
-        found += (__ffsll((unsigned long long)miss) - 1) >> LS;
+    cur = nxt;
+    // the verdict of step s - 1
+    if (pr.cnt > 0) {
+      const int lastb = pr.cnt - 1;
+      const bool in_last = myblock == lastb;
+      const bool last_hit = block_stored<SPL>(pr.v, pr.key, in_last, loader, gmask, slots, bmask, hshift, zero_stored);
+      if (__ballot(in_last && leader && last_hit) != 0) {
+        found += pr.cnt;
+      } else {
+        // the step holds the first miss: probe all of its blocks
+        const bool sel = myblock < pr.cnt;
+        load_parts<SPL>(pr.v, slots, pr.key, loader && sel && pr.key != 0, sub, hshift);
+        const bool hit = block_stored<SPL>(pr.v, pr.key, sel, loader, gmask, slots, bmask, hshift, zero_stored);
+        const uint64_t miss = __ballot(leader && sel && !hit);
+        // the last block misses again, so some block does
+        found += miss ? (__ffsll((unsigned long long)miss) - 1) >> LS : pr.cnt;
         break;
       }
-      found += pa.cnt;
     }
-    // this step's probe: the loaders of each block read its home bucket
-    pa = pb;
-    pb.cnt = cnt > 0 ? cnt : 0;
-    pb.key = mine;
-    {
-      const bool use = loader && myblock < cnt && mine != 0;
-      const uint64_t at = use ? (mine >> hshift) * kBucketSlots + (uint64_t)sub * SPL : 0;
-      const v2u64* src = reinterpret_cast<const v2u64*>(slots + at);
-#pragma unroll
-      for (int i = 0; i < SPL / 2; ++i) {
-        const v2u64 q = src[i];
-        pb.v[2 * i] = q.x;
-        pb.v[2 * i + 1] = q.y;
-      }
-    }
-    if (pa.cnt == 0 && pb.cnt == 0) break;
+    if (cnt <= 0) break;
+    // this step's probe: the loaders of its last block read their bucket parts
+    pr.cnt = cnt;
+    pr.key = mine;
+    load_parts<SPL>(pr.v, slots, mine, loader && myblock == cnt - 1 && mine != 0, sub, hshift);
   }
   if (lane == 0) h_out[r] = (int32_t)(found * B);
 }
@@ -408,18 +462,18 @@ peek_status peek_block_lpm_batch(const peek_block_table* t, int32_t n, const int
   const dim3 grid((unsigned)blocks), block(kWave * kWavesPerBlock);
   hipStream_t st = (hipStream_t)stream;
   switch (t->block_size) {
-#define PEEK_BLOCK_CASE(LS)                                                                                        \
-  case 4 << LS:                                                                                                    \
-    hipLaunchKernelGGL(k_block_lpm<LS>, grid, block, 0, st, d_tokens, d_offsets, n, t->d_slots, t->bucket_bits,  \
-                       t->zero_stored, d_h);                                                                       \
+#define PEEK_BLOCK_CASE(LT, LS)                                                                                \
+  case (1 << LT) << LS:                                                                                        \
+    hipLaunchKernelGGL((k_block_lpm<LT, LS>), grid, block, 0, st, d_tokens, d_offsets, n, t->d_slots,          \
+                       t->bucket_bits, t->zero_stored, d_h);                                                   \
     break;
-    PEEK_BLOCK_CASE(0)
-    PEEK_BLOCK_CASE(1)
-    PEEK_BLOCK_CASE(2)
-    PEEK_BLOCK_CASE(3)
-    PEEK_BLOCK_CASE(4)
-    PEEK_BLOCK_CASE(5)
-    PEEK_BLOCK_CASE(6)
+    PEEK_BLOCK_CASE(2, 0)
+    PEEK_BLOCK_CASE(3, 0)
+    PEEK_BLOCK_CASE(2, 2)
+    PEEK_BLOCK_CASE(2, 3)
+    PEEK_BLOCK_CASE(2, 4)
+    PEEK_BLOCK_CASE(2, 5)
+    PEEK_BLOCK_CASE(2, 6)
 #undef PEEK_BLOCK_CASE
     default:
       return fail(PEEK_ERR_INVALID_ARGUMENT, "table has an unsupported block size %d", t->block_size);
