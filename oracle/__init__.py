@@ -64,6 +64,7 @@ def _load():
     lib.oracle_block_lpm.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p]
     lib.oracle_block_digest.restype = ctypes.c_uint64
     lib.oracle_block_digest.argtypes = [_c_i32p, ctypes.c_int64, ctypes.c_int64]
+    lib.oracle_offline_order.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, ctypes.c_int64, _c_i64p]
     lib.oracle_clpm.argtypes = [ctypes.c_int64, _c_i32p, _c_i64p, _c_i64p, ctypes.c_int64, ctypes.c_int64,
                                 _c_i64p, _c_i32p, _c_i32p]
     _lib = lib
@@ -247,6 +248,17 @@ def clpm(tokens, offsets, h, tau: int, theta: int) -> ClpmResult:
     _load().oracle_clpm(n, _p32(tokens), _p64(offsets), _p64(h), int(tau), int(theta), _p64(score), _p32(section),
                         _p32(sharing))
     return ClpmResult(score, section, bool(sharing[0]))
+
+
+def offline_order(tokens, offsets, depth_limit: int = 128) -> np.ndarray:
+    """PEEK-offline Phase 1 permutation pi (int64[n]): pi[k] = the request emitted k-th."""
+    tokens, offsets = _i32(tokens), _i64(offsets)
+    n = len(offsets) - 1
+    out = np.empty(max(n, 1), dtype=np.int64)
+    if tokens.size == 0:
+        tokens = np.zeros(1, dtype=np.int32)
+    _load().oracle_offline_order(n, _p32(tokens), _p64(offsets), int(depth_limit), _p64(out))
+    return out[:n]
 
 
 def cache_tree_of(workload) -> Tree:

@@ -47,7 +47,14 @@
 //    after that); and has_sharing, whether some child of the pending tree's
 //    root is on the path of two or more requests.
 //
+//  * PEEK-offline Phase 1 (appendix on PEEK-offline, Phase 1): a token trie
+//    over the first D tokens of every prompt, traversed depth first; a node
+//    emits the requests whose truncated prompt ends there (arrival order),
+//    then visits its children by descending subtree request count, equal
+//    counts by their earliest request. The result is the permutation pi.
+//
 // Build: g++ -O2 -std=c++17 -shared -fPIC oracle.cpp -o liboracle.so
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <map>
@@ -576,6 +583,59 @@ void oracle_clpm(int64_t n, const int32_t* tokens, const int64_t* offsets, const
   for (const auto& kv : T.root->kids)
     if (kv.second->pending_count >= 2) sharing = 1;
   *has_sharing_out = sharing;
+}
+
+// PEEK-offline Phase 1 (App. "Mechanisms", Phase 1): a token trie over the
+// first D tokens of every prompt; a node records the requests whose
+// truncated prompt ends there and the number of requests in its subtree. A
+// depth-first traversal emits each node's terminating requests (in arrival
+// order), then visits its children by descending subtree count, equal
+// counts by the earliest request in the child's subtree. perm_out[k] = the
+// request emitted k-th.
+struct TrieNode {
+  std::map<int32_t, TrieNode*> kids;
+  std::vector<int64_t> ends;   // requests whose truncated prompt ends here, in arrival order
+  int64_t count = 0;           // requests in the subtree
+  int64_t first = -1;          // earliest request in the subtree
+};
+
+static void trie_free(TrieNode* v) {
+  for (auto& kv : v->kids) trie_free(kv.second);
+  delete v;
+}
+
+static void trie_emit(const TrieNode* v, int64_t* out, int64_t* k) {
+  for (int64_t r : v->ends) out[(*k)++] = r;
+  std::vector<const TrieNode*> kids;
+  for (const auto& kv : v->kids) kids.push_back(kv.second);
+  std::sort(kids.begin(), kids.end(), [](const TrieNode* a, const TrieNode* b) {
+    if (a->count != b->count) return a->count > b->count;
+    return a->first < b->first;
+  });
+  for (const TrieNode* c : kids) trie_emit(c, out, k);
+}
+
+void oracle_offline_order(int64_t n, const int32_t* tokens, const int64_t* offsets, int64_t depth_limit,
+                          int64_t* perm_out) {
+  TrieNode* root = new TrieNode();
+  for (int64_t r = 0; r < n; ++r) {
+    const int64_t len = offsets[r + 1] - offsets[r];
+    const int64_t t = len < depth_limit ? len : depth_limit;
+    TrieNode* v = root;
+    v->count += 1;
+    if (v->first < 0) v->first = r;
+    for (int64_t j = 0; j < t; ++j) {
+      TrieNode*& c = v->kids[tokens[offsets[r] + j]];
+      if (c == nullptr) c = new TrieNode();
+      v = c;
+      v->count += 1;
+      if (v->first < 0) v->first = r;
+    }
+    v->ends.push_back(r);
+  }
+  int64_t k = 0;
+  trie_emit(root, perm_out, &k);
+  trie_free(root);
 }
 
 }  // extern "C"

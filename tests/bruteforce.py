@@ -178,3 +178,38 @@ def block_lpm(nodes, prompts, B):
             j += 1
         h.append(B * j)
     return np.array(h)
+
+
+# PEEK-offline Phase 1 without a trie: with s_r = p_r[:D], count(u) = the
+# number of requests whose s starts with u and first(u) = the earliest of
+# them, request a precedes request b when, at l = LCP(s_a, s_b):
+#   both end at l: a < b (arrival);
+#   only one ends at l: that one (a node's own requests precede its children);
+#   else by (count desc, first asc) of the two length-(l+1) prefixes.
+
+
+def offline_order(prompts, D):
+    from functools import cmp_to_key
+    s = [p[:D] for p in prompts]
+    n = len(s)
+
+    def count_first(u):
+        members = [r for r in range(n) if s[r][:len(u)] == u]
+        return len(members), min(members)
+
+    def cmp(a, b):
+        if a == b:
+            return 0
+        l = lcp(s[a], s[b])
+        ea, eb = l == len(s[a]), l == len(s[b])
+        if ea and eb:
+            return -1 if a < b else 1
+        if ea:
+            return -1
+        if eb:
+            return 1
+        ca, fa = count_first(s[a][:l + 1])
+        cb, fb = count_first(s[b][:l + 1])
+        return -1 if (-ca, fa) < (-cb, fb) else 1
+
+    return np.array(sorted(range(n), key=cmp_to_key(cmp)), dtype=np.int64)

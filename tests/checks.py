@@ -107,3 +107,35 @@ def check_clpm(w, h, score, section, has_sharing, samples=4, seed=0):
     rng = np.random.default_rng(seed)
     for r in rng.choice(w.n, size=min(samples, w.n), replace=False):
         assert score[r] == lcp_with_all(w, int(r))
+
+
+def check_offline_order(tokens, offsets, D, perm):
+    """Properties of a Phase 1 permutation that hold at any size: it is a
+    permutation; the requests under every trie node (equal truncated
+    prefix) are contiguous; a node's own requests come before its children,
+    in arrival order; its children come by descending count, equal counts by
+    earliest request."""
+    n = len(offsets) - 1
+    perm = np.asarray(perm, dtype=np.int64)
+    assert sorted(perm.tolist()) == list(range(n)), "not a permutation"
+    s = [tuple(tokens[offsets[r]:offsets[r + 1]][:D].tolist()) for r in range(n)]
+    pos = np.empty(n, dtype=np.int64)
+    pos[perm] = np.arange(n)
+    groups = {}
+    for r in range(n):
+        for l in range(len(s[r]) + 1):
+            groups.setdefault(s[r][:l], []).append(r)
+    for u, members in groups.items():
+        ps = sorted(pos[members])
+        assert ps[-1] - ps[0] + 1 == len(ps), f"prefix of length {len(u)} not contiguous"
+        lo = ps[0]
+        ends = [r for r in members if len(s[r]) == len(u)]
+        assert sorted(pos[ends].tolist()) == list(range(lo, lo + len(ends))), "own requests not first"
+        assert list(pos[sorted(ends)]) == sorted(pos[ends].tolist()), "own requests not in arrival order"
+        kids = {}
+        for r in members:
+            if len(s[r]) > len(u):
+                kids.setdefault(s[r][len(u)], []).append(r)
+        order = sorted(kids.values(), key=lambda m: min(pos[m]))
+        keys = [(-len(m), min(m)) for m in order]
+        assert keys == sorted(keys), "children out of (count desc, first arrival) order"

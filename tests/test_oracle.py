@@ -145,6 +145,49 @@ def test_hashed_block_size_must_be_even():
             O.block_lpm(t, tok, off, bad)
 
 
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("vocab", [2, 3, 6])
+def test_offline_order_matches_brute_force(seed, vocab):
+    w = W.random_case(seed * 5 + vocab, n=24, n_cached=2, vocab=vocab, max_len=14)
+    prompts = BF.seqs_of(w.tokens, w.offsets)
+    for D in (0, 1, 2, 4, 7, 128):
+        perm = O.offline_order(w.tokens, w.offsets, D)
+        assert np.array_equal(perm, BF.offline_order(prompts, D)), D
+        checks.check_offline_order(w.tokens, w.offsets, D, perm)
+
+
+def test_offline_order_worked_example_thrashing():
+    g = _golden("x1_offline_order.json")
+    w = W.worked_thrashing()
+    names = w.meta["names"]
+    assert names == g["arrival"]
+    perm = O.offline_order(w.tokens, w.offsets, g["depth_limit"])
+    assert [names[r] for r in perm] == g["expected_order"]
+
+
+def test_offline_order_special_cases():
+    # D = 0: every request ends at the root, so the order is arrival
+    w = W.random_case(3, n=40, n_cached=2, vocab=3, max_len=20)
+    assert np.array_equal(O.offline_order(w.tokens, w.offsets, 0), np.arange(w.n))
+    # distinct first tokens: singleton children of the root, by arrival
+    prompts = [np.array([10 + r, 1, 2, 3], np.int32) for r in range(9)]
+    tok, off = W.pack(prompts)
+    assert np.array_equal(O.offline_order(tok, off, 128), np.arange(9))
+    # identical truncated prompts end at one node, by arrival
+    base = np.arange(300, dtype=np.int32)
+    prompts = [np.concatenate([base, np.array([r], np.int32)]) for r in range(7)]
+    tok, off = W.pack(prompts)
+    assert np.array_equal(O.offline_order(tok, off, 128), np.arange(7))
+    # a larger group goes first even when it arrives later; a prompt that
+    # ends at a node precedes the node's children
+    P = [[5, 1], [7, 1, 1], [7, 1, 2], [7], [5, 2]]
+    tok, off = W.pack([np.array(p, np.int32) for p in P])
+    assert O.offline_order(tok, off, 128).tolist() == [3, 1, 2, 0, 4]
+    # empty queue and empty prompts
+    tok, off = W.pack([np.array([], np.int32), np.array([4], np.int32), np.array([], np.int32)])
+    assert O.offline_order(tok, off, 128).tolist() == [0, 2, 1]
+
+
 def test_block_size_one_is_plain_lcp_against_a_set():
     # B = 1: h is the textbook longest common prefix against a set of strings.
     w = W.random_case(99, n=30, n_cached=15, vocab=2, max_len=30, block_size=1, threshold=1)

@@ -41,6 +41,12 @@ MUTANTS = {
                                  "const uint32_t x = (uint32_t)blk[i];"),
     "nh_single_pass": ("for (int pass = 0; pass < 2; ++pass)", "for (int pass = 0; pass < 1; ++pass)"),
     "block_hashes_never_stored": ("        stored.insert(st.k);\n", ""),
+    "offline_count_ascending": ("if (a->count != b->count) return a->count > b->count;",
+                                "if (a->count != b->count) return a->count < b->count;"),
+    "offline_ties_by_latest": ("    return a->first < b->first;\n  });", "    return a->first > b->first;\n  });"),
+    "offline_ends_reversed": ("for (int64_t r : v->ends) out[(*k)++] = r;",
+                              "for (auto it = v->ends.rbegin(); it != v->ends.rend(); ++it) out[(*k)++] = *it;"),
+    "offline_ignores_depth_limit": ("const int64_t t = len < depth_limit ? len : depth_limit;", "const int64_t t = len;"),
     "score_leaves_out_own_request": ("      score += node->pending_count * node->elen;",
                                      "      score += (node->pending_count - 1) * node->elen;"),
     "score_weights_by_depth": ("      score += node->pending_count * node->elen;",
@@ -52,7 +58,7 @@ MUTANTS = {
                                        "if (kv.second->pending_count >= 1) sharing = 1;"),
 }
 
-PINS = "brute_force or worked or unary or invalid or tiny or agentic or hashed or mix64"
+PINS = "brute_force or worked or unary or invalid or tiny or agentic or hashed or mix64 or offline"
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
