@@ -169,6 +169,7 @@ def main():
     import torch
 
     import peek_workloads as W
+    import paper_2607_02525_amd as P
     from paper_2607_02525_amd import peek_cache_export
     from paper_2607_02525_amd.runner import HotPath
 
@@ -253,6 +254,29 @@ def main():
     log(f"hashed-block LPM ({table.stats()['num_blocks']} stored blocks, table built in {table_s:.1f}s): "
         f"{np.mean(block_ms):.3f} ms")
 
+    # PEEK-offline Phase 1 (D = 128) over the whole queue, and over its first
+    # 5000 requests (the queue size the paper times its reorder at)
+    def time_offline(fn, reps=4):
+        ms = []
+        for i in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            if i > 0:
+                ms.append(a.elapsed_time(b))
+        return float(np.mean(ms))
+
+    offline_ms = time_offline(lambda: hp.offline(128))
+    n5 = min(5000, w.n)
+    sub_off = torch.from_numpy(np.ascontiguousarray(w.offsets[:n5 + 1] - w.offsets[0])).cuda()
+    sub_tok = hp.d_tokens[int(w.offsets[0]):int(w.offsets[n5])]
+    sub_perm = torch.empty(max(n5, 1), dtype=torch.int32, device="cuda")
+    sub_ws = torch.empty(max(P.peek_offline_order_workspace(n5), 256), dtype=torch.uint8, device="cuda")
+    offline5k_ms = time_offline(lambda: P.peek_offline_order(sub_tok, sub_off, 128, sub_perm, sub_ws))
+    log(f"offline Phase 1 order (D = 128): {offline_ms:.3f} ms for {w.n} requests, {offline5k_ms:.3f} ms for {n5}")
+
     res = hp.results()
     block_bytes = block_algorithmic_bytes(w.lengths.astype(np.int64), res["block_h"].astype(np.int64),
                                           w.block_size)
@@ -311,6 +335,8 @@ def main():
         "block_lpm_ms": round(float(np.mean(block_ms)), 4),
         "block_lpm_gbs": round(block_bytes / (float(np.mean(block_ms)) / 1e3) / 1e9, 1),
         "block_table_build_s": round(table_s, 2),
+        "offline_order_ms": round(offline_ms, 4),
+        "offline_order_5000_ms": round(offline5k_ms, 4),
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,

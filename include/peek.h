@@ -279,6 +279,29 @@ peek_status peek_block_table_free(peek_block_table* table);
 peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const int32_t* d_tokens,
                                  const int64_t* d_offsets, int32_t* d_h, void* stream);
 
+/* ------------------------------------------------------------------------
+ * peek_offline_order: PEEK-offline Phase 1 (appendix on PEEK-offline,
+ * "Phase 1: Prefix trie DFS reordering").
+ *
+ * Over the token trie of the prompts' first depth_limit tokens (the paper
+ * uses D = 128), a depth-first traversal emits at every node the requests
+ * whose truncated prompt ends there, in arrival order, then visits the
+ * node's children by descending subtree request count; children with equal
+ * counts go by their earliest request (the paper leaves this tie open).
+ *   d_perm[k] = the request emitted k-th (int32[n], device).
+ * Requests that share a truncated prefix are therefore contiguous in d_perm.
+ * No cache is involved (the paper's regime is a cold cache). depth_limit >= 0
+ * (0: arrival order). Scratch comes only from d_workspace (device, 256-byte
+ * aligned, at least peek_offline_order_workspace(n) bytes). Synchronizes
+ * `stream` once or a few times, as peek_queue_signals does.
+ * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY (pinned host
+ * words), DEVICE.
+ * ---------------------------------------------------------------------- */
+size_t peek_offline_order_workspace(int32_t n);
+
+peek_status peek_offline_order(int32_t n, const int32_t* d_tokens, const int64_t* d_offsets, int32_t depth_limit,
+                               int32_t* d_perm, void* d_workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -62,6 +62,9 @@ EXPORTS = [
     ("peek_block_table_stats", ctypes.c_int, [_vp, _i64p, _i64p, _i32p]),
     ("peek_block_table_free", ctypes.c_int, [_vp]),
     ("peek_block_lpm_batch", ctypes.c_int, [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp]),
+    ("peek_offline_order_workspace", ctypes.c_size_t, [ctypes.c_int32]),
+    ("peek_offline_order", ctypes.c_int,
+     [ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp, _vp, ctypes.c_size_t, _vp]),
 ]
 
 for _name, _res, _args in EXPORTS:
@@ -294,3 +297,16 @@ def peek_block_lpm_batch(table, tokens, offsets, h, stream=None):
     n = int(offsets.shape[0]) - 1
     _check(_lib.peek_block_lpm_batch(None if table is None else table.handle, n, _dptr(tokens), _dptr(offsets),
                                      _dptr(h), _stream(stream)))
+
+
+def peek_offline_order_workspace(n: int) -> int:
+    return int(_lib.peek_offline_order_workspace(int(n)))
+
+
+def peek_offline_order(tokens, offsets, depth_limit: int, perm, workspace, stream=None):
+    """PEEK-offline Phase 1 permutation int32[n] of the prompts' first depth_limit tokens; torch tensors on the
+    device."""
+    n = int(offsets.shape[0]) - 1
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(_lib.peek_offline_order(n, _dptr(tokens), _dptr(offsets), int(depth_limit), _dptr(perm),
+                                   _dptr(workspace), ws_bytes, _stream(stream)))

@@ -645,7 +645,8 @@ static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* 
   }
   return run_signals(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
                      want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
-                     want_demand ? d_demand : nullptr, clpm, d_workspace, workspace_bytes, (hipStream_t)stream);
+                     want_demand ? d_demand : nullptr, clpm, nullptr, d_workspace, workspace_bytes,
+                     (hipStream_t)stream);
 }
 
 peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
@@ -666,6 +667,27 @@ peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_t
   const ClpmRequest req{d_h, tau, theta, d_score, d_section, d_has_sharing};
   return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
                        d_demand, &req, d_workspace, workspace_bytes, stream);
+}
+
+size_t peek_offline_order_workspace(int32_t n) { return n < 0 ? 0 : offline_workspace_bytes(n); }
+
+peek_status peek_offline_order(int32_t n, const int32_t* d_tokens, const int64_t* d_offsets, int32_t depth_limit,
+                               int32_t* d_perm, void* d_workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+  if (depth_limit < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "depth_limit must be >= 0 (got %d)", depth_limit);
+  if (n == 0) return PEEK_OK;
+  if (!d_tokens || !d_offsets || !d_perm)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_perm must not be NULL");
+  const size_t need = offline_workspace_bytes(n);
+  if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
+  if (workspace_bytes < need)
+    return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+  const OfflineRequest off{depth_limit, d_perm};
+  return run_signals(nullptr, n, d_tokens, d_offsets, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, &off,
+                     d_workspace, workspace_bytes, (hipStream_t)stream);
 }
 
 }  // extern "C"

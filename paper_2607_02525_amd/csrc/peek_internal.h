@@ -134,9 +134,17 @@ size_t evict_workspace_bytes(int64_t num_nodes);
 peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score, int32_t* order, void* workspace,
                       size_t workspace_bytes, hipStream_t stream);
 
+// PEEK-offline Phase 1, asked of run_signals instead of the cluster outputs:
+// the permutation of the queue over the prompts' first depth_limit tokens.
+struct OfflineRequest {
+  int32_t depth_limit;    // D
+  int32_t* perm;          // [n] perm[k] = request emitted k-th (device)
+};
+size_t offline_workspace_bytes(int32_t n);
+
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
-                        int32_t* cluster_size, int32_t* demand, const ClpmRequest* clpm, void* workspace,
-                        size_t workspace_bytes, hipStream_t stream);
+                        int32_t* cluster_size, int32_t* demand, const ClpmRequest* clpm,
+                        const OfflineRequest* offline, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 }  // namespace peek

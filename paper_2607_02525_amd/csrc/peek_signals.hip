@@ -234,6 +234,7 @@ struct AnchorSource {
   int32_t* flags;
   int32_t n_flags;
   int32_t* sharing;   // NULL, or the has_sharing output (cleared here, raised by the final stage)
+  uint32_t len_cap;   // prompts are taken as their first len_cap tokens
   __device__ __forceinline__ ClElem operator()(size_t i) const {
     if (i < (size_t)n_flags) flags[i] = 0;
     if (i <= (size_t)n) lcp[i] = 0;
@@ -244,7 +245,7 @@ struct AnchorSource {
     ClElem e;
     if (i < (size_t)n) {
       const int64_t o = offsets[i];
-      const uint32_t len = (uint32_t)(offsets[i + 1] - o);
+      const uint32_t len = min((uint32_t)(offsets[i + 1] - o), len_cap);
       const uint32_t c = last ? (uint32_t)last[i] : 0u;
       const uint32_t m = mlen ? (uint32_t)mlen[i] : 0u;
       const uint64_t code = m < len ? tok_code(tokens[o + m]) : 0;
@@ -572,14 +573,15 @@ struct ClpmArgs {
 // blocks they answer every range minimum below in a few loads.
 constexpr int kInBlockLevels = 6;
 
-// share, the (share, request) key of every position, the in-block tables of
-// lcp and of the key, and the 64-wide block minima of both.
+// share, the (share, request) key of every position (the request alone when
+// key_is_request), the in-block tables of lcp and of the key, and the
+// 64-wide block minima of both.
 __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* __restrict__ el,
                                                       const int32_t* __restrict__ lcp, uint64_t* __restrict__ key2,
                                                       int32_t* __restrict__ ib1, uint64_t* __restrict__ ib2,
                                                       int64_t ib_stride, int32_t* __restrict__ st1,
                                                       uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2,
-                                                      ClpmArgs cl) {
+                                                      ClpmArgs cl, bool key_is_request) {
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
   const int32_t i = b * kWave + lane;
@@ -593,7 +595,7 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
   }
   if (i < n) {
     const int32_t share = max(lcp[i], lcp[i + 1]);
-    v2 = ((uint64_t)(uint32_t)share << 32) | el[i].req;
+    v2 = key_is_request ? (uint64_t)el[i].req : ((uint64_t)(uint32_t)share << 32) | el[i].req;
     key2[i] = v2;
   }
   int32_t m1 = v1;
@@ -754,6 +756,22 @@ struct LcpIndex {
   }
 };
 
+// Minimum of the position keys over [lo, hi]: in-block tables at both ends,
+// the sparse table over whole blocks in between.
+__device__ __forceinline__ uint64_t key_range_min(const uint64_t* __restrict__ ib2, int64_t stride,
+                                                  const uint64_t* __restrict__ st2, int32_t nb2, int32_t lo,
+                                                  int32_t hi) {
+  const int32_t bl = lo >> 6, bh = hi >> 6;
+  if (bl == bh) return in_block_min(ib2, stride, lo, hi);
+  uint64_t m = umin64(in_block_min(ib2, stride, lo, (bl << 6) + 63), in_block_min(ib2, stride, bh << 6, hi));
+  if (bh - bl >= 2) {
+    const int32_t x = bl + 1, y = bh - 1;
+    const int k = 31 - __clz(y - x + 1);
+    m = umin64(m, umin64(st2[(int64_t)k * nb2 + x], st2[(int64_t)k * nb2 + y - (1 << k) + 1]));
+  }
+  return m;
+}
+
 // One thread per sorted position i: cluster id and size of its request;
 // with cLPM signals requested also the weight of the pending-tree node
 // whose leftmost inner position is i, and the section run of position i.
@@ -774,19 +792,7 @@ __global__ void k_final_query(int32_t n, int32_t threshold, const uint64_t* __re
     const int32_t L = ix.last_below_from(i, s);
     const int32_t R = ix.first_below_from(i + 1, s);
     // id: minimum of (share, request) over [L, R)
-    const int32_t hi = R - 1;
-    const int32_t bl = L >> 6, bh = hi >> 6;
-    uint64_t m;
-    if (bl == bh) {
-      m = in_block_min(ib2, ix.stride, L, hi);
-    } else {
-      m = umin64(in_block_min(ib2, ix.stride, L, (bl << 6) + 63), in_block_min(ib2, ix.stride, bh << 6, hi));
-      if (bh - bl >= 2) {
-        const int32_t x = bl + 1, y = bh - 1;
-        const int k = 31 - __clz(y - x + 1);
-        m = umin64(m, umin64(st2[(int64_t)k * nb2 + x], st2[(int64_t)k * nb2 + y - (1 << k) + 1]));
-      }
-    }
+    const uint64_t m = key_range_min(ib2, ix.stride, st2, nb2, L, R - 1);
     cid[req] = (int32_t)(uint32_t)m;
     csz[req] = R - L;
   }
@@ -862,6 +868,195 @@ __global__ __launch_bounds__(kScanThreads) void k_clpm_score(int32_t n, const ui
   cl.score[req] = (len > share ? len - share : 0) + offset + local[i];
 }
 
+// PEEK-offline Phase 1 (appendix on PEEK-offline): the permutation that a
+// depth-first walk of the token trie over the prompts' first D tokens emits,
+// a node's own requests first (arrival order), then its children by
+// descending subtree count, equal counts by earliest request.
+//
+// The cluster pass, run on prompts cut to D tokens and without a cache,
+// leaves an order in which every trie node is a contiguous range with
+// exact adjacent LCPs. A trie node where the order branches is an LCP
+// interval [L, R) of depth d (inner LCPs >= d, lcp[L] and lcp[R] < d); its
+// separators are the inner boundaries with lcp = d and it is named by the
+// first of them. The pieces between separators are its children (a deeper
+// interval or a single request) and the requests that end at the node.
+// One sort orders every piece by (node, own requests first by arrival, then
+// children by descending size and earliest request); a segmented scan of
+// piece sizes gives each piece its offset inside its node; pointer jumping
+// up the interval tree adds the offsets of the ancestors, and every request
+// lands at its node's start plus its own offset.
+struct OffElem {
+  int32_t node;    // the node the piece belongs to (its first separator); INT32_MAX for padding
+  int32_t k1;      // 0 for a request that ends at the node, else n + 1 - the child's size
+  int32_t k2;      // the request, or the child's earliest request
+  int32_t owner;   // the child's node id (> 0), or -(position + 1) for a request
+};
+struct OffLess {
+  __device__ __forceinline__ bool operator()(const OffElem& a, const OffElem& b) const {
+    return a.node < b.node || (a.node == b.node && (a.k1 < b.k1 || (a.k1 == b.k1 && a.k2 < b.k2)));
+  }
+};
+
+struct OffArgs {
+  int32_t n;
+  const int32_t* lcp;         // [n + 1], capped at D, lcp[0] = lcp[n] = 0
+  const ClElem* el;           // the order
+  LcpIndex ix;
+  const uint64_t* ib2;        // range minimum of the requests (keys are the requests)
+  const uint64_t* st2;
+  int32_t nb2;
+  int32_t* nparent;           // [n] per boundary: the parent node of the node it names, -1 otherwise
+  int64_t* start;             // [n] per boundary: offset of its node inside the parent (0 at the top)
+  int32_t* rnode;             // [n] per position: the node of its request's piece
+  int64_t* roff;              // [n] per position: offset of that piece inside the node
+};
+
+// The node (first separator) of the interval of depth lcp[i] around inner boundary i.
+__device__ __forceinline__ int32_t off_node_of(const OffArgs& a, int32_t i) {
+  const int32_t d = a.lcp[i];
+  const int32_t L = d == 0 ? 0 : a.ix.last_below_from(i - 1, d);
+  return a.ix.first_below_from(L + 1, d + 1);
+}
+
+// Piece j of the sort: j < n is the request at position j; n < j < 2n is
+// the node named by boundary j - n (padding unless j - n is a first
+// separator and not the top interval). Also records each node's parent and
+// each request's node.
+struct OffSource {
+  OffArgs a;
+  __device__ __forceinline__ OffElem operator()(size_t j) const {
+    const OffElem pad{INT32_MAX, INT32_MAX, INT32_MAX, 0};
+    const int32_t n = a.n;
+    if (j < (size_t)n) {
+      const int32_t i = (int32_t)j;
+      const int32_t bl = i >= 1 ? a.lcp[i] : -1, br = i + 1 <= n - 1 ? a.lcp[i + 1] : -1;
+      const int32_t b = bl >= br ? i : i + 1;   // the deeper of its boundaries
+      const int32_t node = off_node_of(a, b);
+      a.rnode[i] = node;
+      const bool ends = (int32_t)a.el[i].len == a.lcp[b];
+      return OffElem{node, ends ? 0 : n, (int32_t)a.el[i].req, -(i + 1)};
+    }
+    if (j == (size_t)n) {   // boundary 0 names no node
+      a.nparent[0] = -1;
+      a.start[0] = 0;
+      return pad;
+    }
+    if (j >= (size_t)2 * n) return pad;
+    const int32_t i = (int32_t)(j - n);
+    const int32_t d = a.lcp[i];
+    const int32_t L = d == 0 ? 0 : a.ix.last_below_from(i - 1, d);
+    a.start[i] = 0;
+    if (a.ix.first_below_from(L + 1, d + 1) != i) {
+      a.nparent[i] = -1;
+      return pad;
+    }
+    const int32_t R = d == 0 ? n : a.ix.first_below_from(i + 1, d);
+    const int32_t lL = L >= 1 ? a.lcp[L] : -1, lR = R <= n - 1 ? a.lcp[R] : -1;
+    if (lL < 0 && lR < 0) {   // the top interval
+      a.nparent[i] = -1;
+      return pad;
+    }
+    const int32_t parent = off_node_of(a, lL >= lR ? L : R);
+    a.nparent[i] = parent;
+    const int32_t first = (int32_t)(uint32_t)key_range_min(a.ib2, a.ix.stride, a.st2, a.nb2, L, R - 1);
+    return OffElem{parent, n + 1 - (R - L), first, i};
+  }
+};
+
+__device__ __forceinline__ int64_t off_size(const OffElem& e, int32_t n) {
+  return e.node == INT32_MAX ? 0 : (e.k1 == 0 ? 1 : (int64_t)n + 1 - e.k1);
+}
+
+// Inclusive block scan of piece sizes (kScanThreads pieces per block) into
+// `local`, block totals into `part`.
+__global__ __launch_bounds__(kScanThreads) void k_off_scan(int32_t m, int32_t n, const OffElem* __restrict__ el,
+                                                           int64_t* __restrict__ local, int64_t* __restrict__ part) {
+  __shared__ int64_t wsum[kScanThreads / kWave];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int32_t j = (int32_t)blockIdx.x * kScanThreads + t;
+  int64_t v = j < m ? off_size(el[j], n) : 0;
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t o = __shfl(v, lane >= d ? lane - d : lane);
+    if (lane >= d) v += o;
+  }
+  if (lane == kWave - 1) wsum[wave] = v;
+  __syncthreads();
+  int64_t before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  v += before;
+  if (j < m) local[j] = v;
+  if (t == kScanThreads - 1) part[blockIdx.x] = v;
+}
+
+// Exclusive prefix of piece sizes; the first piece of each node records the
+// prefix at its node's start in `base` (indexed by node).
+__global__ __launch_bounds__(kScanThreads) void k_off_prefix(int32_t m, int32_t n, const OffElem* __restrict__ el,
+                                                             int64_t* __restrict__ local,
+                                                             const int64_t* __restrict__ part,
+                                                             int64_t* __restrict__ base) {
+  __shared__ int64_t red[kScanThreads / kWave];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  int64_t v = 0;
+  for (int32_t b = t; b < (int32_t)blockIdx.x; b += kScanThreads) v += part[b];
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  int64_t offset = 0;
+  for (int w = 0; w < kScanThreads / kWave; ++w) offset += red[w];
+  const int32_t j = (int32_t)blockIdx.x * kScanThreads + t;
+  if (j >= m) return;
+  const OffElem e = el[j];
+  if (e.node == INT32_MAX) return;
+  const int64_t ex = offset + local[j] - off_size(e, n);
+  local[j] = ex;
+  if (j == 0 || el[j - 1].node != e.node) base[e.node] = ex;
+}
+
+// Offset of every piece inside its node, to its owner.
+__global__ void k_off_scatter(int32_t m, const OffElem* __restrict__ el, const int64_t* __restrict__ ex,
+                              const int64_t* __restrict__ base, int64_t* __restrict__ start,
+                              int64_t* __restrict__ roff) {
+  const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= m) return;
+  const OffElem e = el[j];
+  if (e.node == INT32_MAX) return;
+  const int64_t off = ex[j] - base[e.node];
+  if (e.owner > 0)
+    start[e.owner] = off;
+  else
+    roff[-e.owner - 1] = off;
+}
+
+// One pointer-jumping round over the interval tree: each node adds the
+// offset accumulated at its current link and jumps past it.
+__global__ void k_off_jump(int32_t n, const int64_t* __restrict__ A, const int32_t* __restrict__ P,
+                           int64_t* __restrict__ A2, int32_t* __restrict__ P2) {
+  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= n) return;
+  const int32_t p = P[c];
+  if (p >= 0) {
+    A2[c] = A[c] + A[p];
+    P2[c] = P[p];
+  } else {
+    A2[c] = A[c];
+    P2[c] = -1;
+  }
+}
+
+// perm[start of the request's node + its offset] = request.
+__global__ void k_off_place(int32_t n, const ClElem* __restrict__ el, const int32_t* __restrict__ rnode,
+                            const int64_t* __restrict__ roff, const int64_t* __restrict__ start,
+                            int32_t* __restrict__ perm) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (n == 1) {
+    perm[0] = (int32_t)el[0].req;
+    return;
+  }
+  const int64_t pos = start[rnode[i]] + roff[i];
+  if (pos >= 0 && pos < n) perm[pos] = (int32_t)el[i].req;   // always in range; the check guards the caller's buffer
+}
+
 size_t np_of(int32_t n) {
   size_t np = msort::kTile;
   while (np < (size_t)n) np <<= 1;
@@ -887,12 +1082,14 @@ constexpr int kFlagPairs = kSpeculativeRounds + 3;
 struct Layout {
   size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
       keys_b, prefix, diff, pmin, run, local, part, sharing, total, flags_bytes;
+  // PEEK-offline Phase 1 only
+  size_t oel_a, oel_b, olocal, opart, obase, start_a, start_b, npar_a, npar_b, rnode, roff, onp;
   int64_t ib_stride;
   int32_t nb1, nb2;
   int levels;
 };
 
-Layout layout(int32_t n, int64_t num_nodes) {
+Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   Layout L{};
   const size_t np = np_of(n);
   const size_t nn = (size_t)std::max<int32_t>(n, 1);
@@ -931,6 +1128,23 @@ Layout layout(int32_t n, int64_t num_nodes) {
   L.local = take(sizeof(int64_t) * nn);
   L.part = take(sizeof(int64_t) * (((size_t)n + kScanThreads - 1) / kScanThreads + 1));
   L.sharing = take(sizeof(int32_t));
+  if (offline) {
+    const size_t m2 = 2 * nn;
+    size_t onp = msort::kTile;
+    while (onp < m2) onp <<= 1;
+    L.onp = onp;
+    L.oel_a = take(sizeof(OffElem) * onp);
+    L.oel_b = take(sizeof(OffElem) * onp);
+    L.olocal = take(sizeof(int64_t) * m2);
+    L.opart = take(sizeof(int64_t) * ((m2 + kScanThreads - 1) / kScanThreads + 1));
+    L.obase = take(sizeof(int64_t) * nn);
+    L.start_a = take(sizeof(int64_t) * nn);
+    L.start_b = take(sizeof(int64_t) * nn);
+    L.npar_a = take(sizeof(int32_t) * nn);
+    L.npar_b = take(sizeof(int32_t) * nn);
+    L.rnode = take(sizeof(int32_t) * nn);
+    L.roff = take(sizeof(int64_t) * nn);
+  }
   L.total = o;
   return L;
 }
@@ -940,6 +1154,7 @@ unsigned blocks_for(int64_t m, int t = 256) { return (unsigned)((m + t - 1) / t)
 }  // namespace
 
 size_t signals_workspace_bytes(int32_t n, int64_t num_nodes) { return layout(n, num_nodes).total; }
+size_t offline_workspace_bytes(int32_t n) { return n <= 0 ? 0 : layout(n, 0, true).total; }
 
 namespace {
 
@@ -965,17 +1180,19 @@ int32_t* host_flags() {
 
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
-                        int32_t* csz, int32_t* demand, const ClpmRequest* clpm, void* ws, size_t ws_bytes,
-                        hipStream_t st) {
+                        int32_t* csz, int32_t* demand, const ClpmRequest* clpm, const OfflineRequest* off,
+                        void* ws, size_t ws_bytes, hipStream_t st) {
   const DeviceTree* t = c != nullptr ? &c->tree : nullptr;
   const int64_t num_nodes = t ? t->num_nodes : 0;
-  const Layout L = layout(n, num_nodes);
+  const Layout L = layout(n, num_nodes, off != nullptr);
   char* w = (char*)ws;
   const size_t np = np_of(n);
   int32_t* P = (int32_t*)(w + L.prefix);
-  const bool want_clusters = cid != nullptr && n > 0;
+  // the offline order needs the same sorted order as the clusters
+  const bool want_clusters = (cid != nullptr || off != nullptr) && n > 0;
   // anchoring needs the walk's results and the cache they refer to
-  const bool anchored = want_clusters && t != nullptr && last_node != nullptr && match_len != nullptr;
+  const bool anchored =
+      want_clusters && off == nullptr && t != nullptr && last_node != nullptr && match_len != nullptr;
 
   if (demand != nullptr && !anchored) {
     uint32_t* ka = (uint32_t*)(w + L.keys_a);
@@ -1059,10 +1276,44 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
     hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, q, n, el, nseg, gsize, dep, act,
                        depth[r & 1], active[r & 1], lcp, fin, fout, any);
   };
+  // PEEK-offline Phase 1 from the settled order (see OffSource).
+  auto offline_stage = [&](hipStream_t q) {
+    int64_t* start[2] = {(int64_t*)(w + L.start_a), (int64_t*)(w + L.start_b)};
+    int32_t* npar[2] = {(int32_t*)(w + L.npar_a), (int32_t*)(w + L.npar_b)};
+    int32_t* rnode = (int32_t*)(w + L.rnode);
+    int64_t* roff = (int64_t*)(w + L.roff);
+    int cur = 0;
+    if (n >= 2) {
+      const OffArgs oa{n, lcp, el, ix, ib2, st2, L.nb2, npar[0], start[0], rnode, roff};
+      const OffElem* sorted = msort::sort_from(OffSource{oa}, (OffElem*)(w + L.oel_a), (OffElem*)(w + L.oel_b),
+                                               L.onp, OffLess{}, q);
+      const int32_t m2 = 2 * n;
+      int64_t* olocal = (int64_t*)(w + L.olocal);
+      int64_t* opart = (int64_t*)(w + L.opart);
+      int64_t* obase = (int64_t*)(w + L.obase);
+      const unsigned sb = blocks_for(m2, kScanThreads);
+      hipLaunchKernelGGL(k_off_scan, dim3(sb), dim3(kScanThreads), 0, q, m2, n, sorted, olocal, opart);
+      hipLaunchKernelGGL(k_off_prefix, dim3(sb), dim3(kScanThreads), 0, q, m2, n, sorted, olocal, opart, obase);
+      hipLaunchKernelGGL(k_off_scatter, dim3(blocks_for(m2)), dim3(256), 0, q, m2, sorted, olocal, obase, start[0],
+                         roff);
+      // a node's chain to the top has at most min(D, n) + 1 links
+      const int64_t links = (int64_t)std::min(off->depth_limit, n) + 2;
+      for (int64_t span = 1; span < links; span <<= 1) {
+        hipLaunchKernelGGL(k_off_jump, dim3(blocks_for(n)), dim3(256), 0, q, n, start[cur], npar[cur],
+                           start[cur ^ 1], npar[cur ^ 1]);
+        cur ^= 1;
+      }
+    }
+    hipLaunchKernelGGL(k_off_place, dim3(blocks_for(n)), dim3(256), 0, q, n, el, rnode, roff, start[cur], off->perm);
+  };
   auto final_stage = [&](hipStream_t q) {
     hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, q, n, el, lcp, key2,
-                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl);
+                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr);
     hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, q, st1, st2, L.nb1, L.nb2, L.levels);
+    if (off != nullptr) {
+      offline_stage(q);
+      return;
+    }
     hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, q, n, threshold, key2, lcp, el, ix, ib2, st2,
                        L.nb2, cid, csz, cl);
     if (cl.on) {
@@ -1080,7 +1331,8 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   // segment sort, and the host then takes over from that round.
   auto fixed = [&](hipStream_t q) {
     const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
-                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr};
+                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr,
+                           off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
     el = msort::sort_from(src, el_a, el_b, np, ClLess{}, q);
     other = el == el_a ? el_b : el_a;
     // The anchor order is sorted by last node first, so demand reads it

@@ -11,7 +11,8 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (Cache, peek_block_lpm_batch, peek_block_table_build, peek_cache_build, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
+from . import (Cache, peek_block_lpm_batch, peek_block_table_build, peek_cache_build, peek_offline_order,
+               peek_offline_order_workspace, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
                peek_evict_rank_workspace, peek_lpm_batch, peek_queue_signals, peek_queue_signals_workspace,
                peek_tree_from_sequences)
 
@@ -40,6 +41,7 @@ class HotPath:
         offsets = np.ascontiguousarray(offsets, dtype=np.int64)
         self.n = int(offsets.shape[0] - 1)
         self._block_valid = False
+        self._offline_valid = False
         self.block_size = int(block_size)
         self.threshold = int(threshold)
         dev = self.device
@@ -105,6 +107,17 @@ class HotPath:
         peek_block_lpm_batch(table, self.d_tokens, self.d_offsets, self.d_block_h, stream=stream)
         self._block_valid = True
 
+    def offline(self, depth_limit: int = 128, stream=None):
+        """PEEK-offline Phase 1 permutation of the loaded queue (its own workspace, allocated once)."""
+        if getattr(self, "_off_n", None) != self.n:
+            n = max(self.n, 1)
+            self.d_perm = torch.empty(n, dtype=torch.int32, device=self.device)
+            self.d_off_ws = torch.empty(max(peek_offline_order_workspace(self.n), 256), dtype=torch.uint8,
+                                        device=self.device)
+            self._off_n = self.n
+        peek_offline_order(self.d_tokens, self.d_offsets, depth_limit, self.d_perm, self.d_off_ws, stream=stream)
+        self._offline_valid = True
+
     def step(self, stream=None):
         self.lpm(stream)
         self.signals(stream)
@@ -123,6 +136,8 @@ class HotPath:
         if getattr(self, "_evict_valid", False):   # written by the last evict() call
             out["evict_score"] = self.d_evict_score.cpu().numpy()
             out["evict_order"] = self.d_evict_order[:max(self.num_nodes - 1, 0)].cpu().numpy()
+        if getattr(self, "_offline_valid", False):   # written by the last offline() call
+            out["perm"] = self.d_perm[:n].cpu().numpy()
         if getattr(self, "_block_valid", False):   # written by the last block_lpm() call
             out["block_h"] = self.d_block_h[:n].cpu().numpy()
         if getattr(self, "_clpm_valid", False):   # written by the last clpm() call

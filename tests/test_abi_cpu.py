@@ -170,6 +170,23 @@ def test_block_table_argument_errors_before_any_gpu_work():
     assert lib.peek_block_table_free(None) == P.PEEK_OK
 
 
+def test_offline_order_argument_errors_before_any_gpu_work():
+    lib = P._lib
+    fake = ctypes.c_void_p(0x1000)
+    need = P.peek_offline_order_workspace(8)
+    assert need > 0 and P.peek_offline_order_workspace(0) == 0 and P.peek_offline_order_workspace(-1) == 0
+    assert P.peek_offline_order_workspace(64) > need
+    assert lib.peek_offline_order(-1, fake, fake, 128, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_offline_order(8, fake, fake, -1, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "depth_limit" in P.peek_last_error()
+    assert lib.peek_offline_order(0, None, None, 128, None, None, 0, None) == P.PEEK_OK
+    assert lib.peek_offline_order(8, fake, fake, 128, None, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_offline_order(8, fake, fake, 128, fake, None, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_offline_order(8, fake, fake, 128, fake, fake, need - 1, None) == P.PEEK_ERR_WORKSPACE_TOO_SMALL
+    assert lib.peek_offline_order(8, fake, fake, 128, fake, ctypes.c_void_p(0x1010), need, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+
+
 def test_workspace_grows_with_the_queue_and_the_cache():
     a = P.peek_queue_signals_workspace(1000, 10)
     assert P.peek_queue_signals_workspace(2000, 10) > a

@@ -114,7 +114,19 @@ def run_and_compare(w, repeat=1, block_sample=None):
     # the hashed-block variant of the same cache, where the block size allows it
     if w.block_size in BLOCK_SIZES:
         check_block_lpm(hp, w, s, sample=block_sample)
+    # PEEK-offline Phase 1 over the same queue (D = 128)
+    check_offline(hp, w, 128)
     return hp, outs[0], s
+
+
+def check_offline(hp, w, D, properties=False):
+    hp.offline(D)
+    got = hp.results()["perm"]
+    exp = O.offline_order(w.tokens, w.offsets, D)
+    assert np.array_equal(got, exp), f"offline order (D={D})"
+    if properties:
+        checks.check_offline_order(w.tokens, w.offsets, D, got)
+    return got
 
 
 @pytest.mark.parametrize("name", ["tiny", "rag", "agentic", "nosharing"])
@@ -356,3 +368,44 @@ def test_block_table_stats_and_empty_cache():
     assert hp.block_table(4).stats()["num_blocks"] == 0
     got = check_block_lpm(hp, w, s)
     assert np.array_equal(got, [0, 0])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_offline_order_depths_and_edge_cases(seed):
+    HotPath = _hot()
+    w = W.random_case(seed, n=700, n_cached=10, vocab=3 + seed % 3, max_len=200, block_size=4, threshold=2)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    print(f"[gpu] offline seed={seed} n={w.n}", flush=True)
+    for D in (0, 1, 2, 5, 32, 128, 1000):
+        check_offline(hp, w, D, properties=seed < 2 and D <= 32)
+    # tiny queues, empty prompts, duplicates, extreme tokens
+    lo, hi = int(np.iinfo(np.int32).min), int(np.iinfo(np.int32).max)
+    cases = [[[5]], [[], []], [[1, 2], [1, 2], [1, 2]], [[], [3], [3, 4], [3]], [[lo, hi], [hi, lo], [lo, hi, 0], [lo]],
+             [[7] * 300, [7] * 300 + [1], [7] * 129, [7] * 128, [7] * 127, [8]]]
+    for P in cases:
+        w = _w(P, cached=[])
+        hp = HotPath.from_sequences(*w.cache_sequences)
+        hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+        for D in (0, 1, 128):
+            check_offline(hp, w, D, properties=True)
+
+
+def test_offline_order_large_groups():
+    """Big prefix groups at several depths, so the order's refinement and the
+    interval tree see deep chains and wide nodes."""
+    HotPath = _hot()
+    rng = np.random.default_rng(31)
+    heads = [rng.integers(0, 50000, size=200, dtype=np.int32) for _ in range(5)]
+    prompts = []
+    for r in range(20000):
+        h = heads[int(rng.integers(0, 5)) if r % 7 else 0]
+        cut = int(rng.integers(0, 200))
+        tail = rng.integers(0, 3, size=int(rng.integers(0, 60)), dtype=np.int32)
+        prompts.append(np.concatenate([h[:cut], tail]))
+    w = _w(prompts, cached=[])
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    print("[gpu] offline large groups", flush=True)
+    for D in (16, 128, 256):
+        check_offline(hp, w, D)
