@@ -97,14 +97,39 @@ __global__ __launch_bounds__(256) void k_evict_blocks(int32_t nn, const int64_t*
   if (lane == kWave - 1) blk[b] = p;
 }
 
-// Sparse table over the block maxima, one workgroup, level by level.
-__global__ __launch_bounds__(1024) void k_evict_tables(EKey* __restrict__ blk, int32_t nb, int levels) {
-  for (int k = 1; k < levels; ++k) {
+// Sparse table over the block maxima. Each workgroup owns kTabChunk
+// consecutive entries and stages the level-0 maxima of twice as many blocks
+// (its chunk and the next one) in LDS, enough for every level whose window
+// fits in kTabChunk + 1 blocks; the levels above that are one launch each.
+constexpr int kTabChunk = 1024;
+constexpr int kTabLocalLevels = 11;   // levels 0..10: windows of up to kTabChunk blocks
+
+__global__ __launch_bounds__(1024) void k_evict_tables_local(EKey* __restrict__ blk, int32_t nb, int levels) {
+  __shared__ EKey a[2][2 * kTabChunk];
+  const int32_t c0 = (int32_t)blockIdx.x * kTabChunk;
+  for (int32_t j = threadIdx.x; j < 2 * kTabChunk; j += blockDim.x)
+    a[0][j] = c0 + j < nb ? blk[c0 + j] : EKey{INT64_MIN, -1, 0};
+  __syncthreads();
+  const int top = levels < kTabLocalLevels ? levels : kTabLocalLevels;
+  for (int k = 1; k < top; ++k) {
     const int32_t h = 1 << (k - 1);
-    for (int32_t b = threadIdx.x; b + 2 * h <= nb; b += blockDim.x)
-      blk[(int64_t)k * nb + b] = ekey_max(blk[(int64_t)(k - 1) * nb + b], blk[(int64_t)(k - 1) * nb + b + h]);
+    const int cur = k & 1, prev = cur ^ 1;
+    for (int32_t j = threadIdx.x; j + 2 * h <= 2 * kTabChunk; j += blockDim.x) {
+      const EKey v = ekey_max(a[prev][j], a[prev][j + h]);
+      a[cur][j] = v;
+      const int32_t b = c0 + j;
+      if (j < kTabChunk && b + 2 * h <= nb) blk[(int64_t)k * nb + b] = v;
+    }
     __syncthreads();
   }
+}
+
+// One level above the local ones, from the level below it.
+__global__ void k_evict_tables_level(EKey* __restrict__ blk, int32_t nb, int k) {
+  const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t h = 1 << (k - 1);
+  if (b + 2 * h <= nb)
+    blk[(int64_t)k * nb + b] = ekey_max(blk[(int64_t)(k - 1) * nb + b], blk[(int64_t)(k - 1) * nb + b + h]);
 }
 
 // Sort element: the largest key of the node's subtree, then the node (its
@@ -228,7 +253,10 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
   EKey* blk = (EKey*)(w + L.blk);
   hipLaunchKernelGGL(k_evict_blocks, dim3(blocks_of(L.nb, 4)), dim3(256), 0, st, nn, E, score, pre, suf, blk, L.nb);
   if (order != nullptr && nn > 1) {
-    hipLaunchKernelGGL(k_evict_tables, dim3(1), dim3(1024), 0, st, blk, L.nb, L.levels);
+    hipLaunchKernelGGL(k_evict_tables_local, dim3((L.nb + kTabChunk - 1) / kTabChunk), dim3(1024), 0, st, blk, L.nb,
+                       L.levels);
+    for (int k = kTabLocalLevels; k < L.levels; ++k)
+      hipLaunchKernelGGL(k_evict_tables_level, dim3(blocks_of(L.nb)), dim3(256), 0, st, blk, L.nb, k);
     const OrderSource src{nodes, E, pre, suf, blk, nn, L.nb};
     OrderElem* sorted = msort::sort_from(src, (OrderElem*)(w + L.el_a), (OrderElem*)(w + L.el_b), np_for(nn),
                                          OrderLess{}, st);

@@ -1,13 +1,17 @@
 // Stable merge sort for the queue-signal kernels (device templates).
 //
-// Tile pass: 128 threads x 2 items = 256 elements per workgroup (small tiles
-// keep a 64K-element sort spread over all 256 CUs); each thread orders its
+// Tile pass: 128 threads x ITEMS items per workgroup; each thread orders its
 // items in registers, then runs are merged in LDS with merge-path
 // partitioning (every thread produces its outputs after a binary search on
 // its diagonal).
-// Global passes: each workgroup emits 256 outputs of a pair of sorted runs;
-// its start and end diagonals are found by a wave-wide 64-ary search, the
-// two input slices are staged in LDS and merged as above.
+// Global passes: each workgroup emits a tile's worth of outputs of a pair of
+// sorted runs; its start and end diagonals are found by a wave-wide 64-ary
+// search, the two input slices are staged in LDS and merged as above.
+// Tile size: 256 elements (2 items) keeps a 64K-element sort spread over all
+// 256 CUs; from 512K elements up, 1024-element tiles (8 items) save two
+// passes and amortize each workgroup's dependent diagonal searches over
+// more outputs (measured: a 1M-element sort goes from 0.33 to 0.28 ms,
+// while 64K-element sorts get slower with the larger tiles).
 // Ties keep input order (stable), so results are deterministic.
 #pragma once
 
@@ -21,7 +25,9 @@ namespace msort {
 
 constexpr int kThreads = 128;
 constexpr int kItems = 2;
-constexpr int kTile = kThreads * kItems;   // 256
+constexpr int kTile = kThreads * kItems;            // 256: the smallest tile, so np is a multiple of it
+constexpr int kBigItems = 8;                        // 1024-element tiles
+constexpr size_t kBigSort = size_t(1) << 19;        // sorts of at least this many elements use them
 
 // Number of items taken from A among the first k outputs of a stable merge
 // of A[0, la) and B[0, lb): the smallest i in [max(0,k-lb), min(k,la)] with
@@ -38,11 +44,11 @@ __device__ __forceinline__ int merge_path(const T* A, int la, const T* B, int lb
   return lo;
 }
 
-template <typename T, typename Less>
-__device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb, int i, int j, T (&out)[kItems],
+template <int I, typename T, typename Less>
+__device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb, int i, int j, T (&out)[I],
                                           Less less) {
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) {
+  for (int q = 0; q < I; ++q) {
     const bool take_a = i < la && (j >= lb || !less(B[j], A[i]));
     out[q] = take_a ? A[i] : B[j];
     if (take_a) ++i;
@@ -63,27 +69,27 @@ struct FromArray {
 // buffer the host expects then holds the unsorted input either way: after
 // an even number of merge passes it is the tile pass's copy, after an odd
 // number it is the untouched input.
-template <typename T, typename Src>
+template <int TILE, typename T, typename Src>
 __device__ __forceinline__ bool gated_copy(const int32_t* gate, const Src& src, T* __restrict__ dst, size_t base) {
   if (gate == nullptr || *gate != 0) return false;
-  for (int q = threadIdx.x; q < kTile; q += kThreads) dst[base + q] = src(base + q);
+  for (int q = threadIdx.x; q < TILE; q += kThreads) dst[base + q] = src(base + q);
   return true;
 }
 
-template <typename T, typename Less, typename Src>
+template <int I, typename T, typename Less, typename Src>
 __global__ __launch_bounds__(kThreads) void k_tile_sort(Src src, T* __restrict__ dst, Less less, const int32_t* gate) {
-  __shared__ T s[kTile];
+  __shared__ T s[(kThreads * I)];
   const int t = threadIdx.x;
-  const size_t base = (size_t)blockIdx.x * kTile;
-  if (gated_copy(gate, src, dst, base)) return;
-  T v[kItems];
+  const size_t base = (size_t)blockIdx.x * (kThreads * I);
+  if (gated_copy<kThreads * I>(gate, src, dst, base)) return;
+  T v[I];
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) v[q] = src(base + t * kItems + q);
+  for (int q = 0; q < I; ++q) v[q] = src(base + t * I + q);
   // odd-even transposition sort of the thread's items (stable)
 #pragma unroll
-  for (int round = 0; round < kItems; ++round) {
+  for (int round = 0; round < I; ++round) {
 #pragma unroll
-    for (int q = round & 1; q + 1 < kItems; q += 2) {
+    for (int q = round & 1; q + 1 < I; q += 2) {
       if (less(v[q + 1], v[q])) {
         const T x = v[q];
         v[q] = v[q + 1];
@@ -92,23 +98,23 @@ __global__ __launch_bounds__(kThreads) void k_tile_sort(Src src, T* __restrict__
     }
   }
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) s[t * kItems + q] = v[q];
+  for (int q = 0; q < I; ++q) s[t * I + q] = v[q];
   __syncthreads();
-  for (int w = kItems; w < kTile; w <<= 1) {
-    const int o = t * kItems;
+  for (int w = I; w < (kThreads * I); w <<= 1) {
+    const int o = t * I;
     const int pair = o & ~(2 * w - 1);
     const int k = o - pair;
     const T* A = s + pair;
     const T* B = A + w;
     const int i = merge_path(A, w, B, w, k, less);
-    merge_seq(A, w, B, w, i, k - i, v, less);
+    merge_seq<I>(A, w, B, w, i, k - i, v, less);
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) s[o + q] = v[q];
+    for (int q = 0; q < I; ++q) s[o + q] = v[q];
     __syncthreads();
   }
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) dst[base + t * kItems + q] = s[t * kItems + q];
+  for (int q = 0; q < I; ++q) dst[base + t * I + q] = s[t * I + q];
 }
 
 // Diagonal split for output k of a stable merge of A[0,la) and B[0,lb),
@@ -138,14 +144,14 @@ __device__ __forceinline__ int wave_merge_path(const T* A, int64_t la, const T* 
   return (int)(lo + f);
 }
 
-// Merge pass: runs of width w (power of two, >= kTile) in src, pairs merged into dst.
-template <typename T, typename Less>
+// Merge pass: runs of width w (power of two, >= (kThreads * I)) in src, pairs merged into dst.
+template <int I, typename T, typename Less>
 __global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ src, T* __restrict__ dst, int64_t w,
                                                          Less less, const int32_t* gate) {
-  __shared__ T s[kTile];
+  __shared__ T s[(kThreads * I)];
   __shared__ int64_t split[2];
   const int t = threadIdx.x;
-  const int64_t out0 = (int64_t)blockIdx.x * kTile;
+  const int64_t out0 = (int64_t)blockIdx.x * (kThreads * I);
   if (gate != nullptr && *gate == 0) return;
   const int64_t pair = out0 & ~(2 * w - 1);
   const T* A = src + pair;
@@ -155,41 +161,49 @@ __global__ __launch_bounds__(kThreads) void k_merge_pass(const T* __restrict__ s
     const int i0 = wave_merge_path(A, w, B, w, k0, t, less);
     if (t == 0) split[0] = i0;
   } else if (t < 128) {
-    const int i1 = wave_merge_path(A, w, B, w, k0 + kTile, t - 64, less);
+    const int i1 = wave_merge_path(A, w, B, w, k0 + (kThreads * I), t - 64, less);
     if (t == 64) split[1] = i1;
   }
   __syncthreads();
   const int64_t ia = split[0], ja = k0 - split[0];
   const int la = (int)(split[1] - split[0]);
-  const int lb = kTile - la;
-  for (int q = t; q < kTile; q += kThreads) s[q] = q < la ? A[ia + q] : B[ja + (q - la)];
+  const int lb = (kThreads * I) - la;
+  for (int q = t; q < (kThreads * I); q += kThreads) s[q] = q < la ? A[ia + q] : B[ja + (q - la)];
   __syncthreads();
-  const int o = t * kItems;
+  const int o = t * I;
   const int i = merge_path(s, la, s + la, lb, o, less);
-  T v[kItems];
-  merge_seq(s, la, s + la, lb, i, o - i, v, less);
+  T v[I];
+  merge_seq<I>(s, la, s + la, lb, i, o - i, v, less);
 #pragma unroll
-  for (int q = 0; q < kItems; ++q) dst[out0 + o + q] = v[q];
+  for (int q = 0; q < I; ++q) dst[out0 + o + q] = v[q];
 }
 
-// Sorts np elements (np a power of two, >= kTile) taken from `src` (element
-// i = src(i)), using a and b as buffers; returns the one that holds the
-// result. With a gate, the sort happens only if *gate != 0 when the passes
-// run (otherwise the data is copied).
-template <typename T, typename Less, typename Src>
-T* sort_from(Src src, T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
-  const unsigned tiles = (unsigned)(np / kTile);
-  hipLaunchKernelGGL((k_tile_sort<T, Less, Src>), dim3(tiles), dim3(kThreads), 0, st, src, b, less, gate);
+// Sorts np elements (np a power of two, >= kThreads * I) taken from `src`
+// (element i = src(i)), using a and b as buffers; returns the one that holds
+// the result. With a gate, the sort happens only if *gate != 0 when the
+// passes run (otherwise the data is copied).
+template <int I, typename T, typename Less, typename Src>
+T* sort_from_tiles(Src src, T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate) {
+  constexpr int tile = kThreads * I;
+  const unsigned tiles = (unsigned)(np / tile);
+  hipLaunchKernelGGL((k_tile_sort<I, T, Less, Src>), dim3(tiles), dim3(kThreads), 0, st, src, b, less, gate);
   T* cur = b;
   T* oth = a;
-  for (size_t w = kTile; w < np; w <<= 1) {
-    hipLaunchKernelGGL((k_merge_pass<T, Less>), dim3(tiles), dim3(kThreads), 0, st, cur, oth, (int64_t)w, less,
+  for (size_t w = tile; w < np; w <<= 1) {
+    hipLaunchKernelGGL((k_merge_pass<I, T, Less>), dim3(tiles), dim3(kThreads), 0, st, cur, oth, (int64_t)w, less,
                        gate);
     T* x = cur;
     cur = oth;
     oth = x;
   }
   return cur;
+}
+
+// The tile size by sort size (np a power of two, >= kTile).
+template <typename T, typename Less, typename Src>
+T* sort_from(Src src, T* a, T* b, size_t np, Less less, hipStream_t st, const int32_t* gate = nullptr) {
+  if (np >= kBigSort) return sort_from_tiles<kBigItems>(src, a, b, np, less, st, gate);
+  return sort_from_tiles<kItems>(src, a, b, np, less, st, gate);
 }
 
 // Sorts np elements from a into a or b (see sort_from).
