@@ -291,7 +291,7 @@ peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const
  *   d_perm[k] = the request emitted k-th (int32[n], device).
  * Requests that share a truncated prefix are therefore contiguous in d_perm.
  * No cache is involved (the paper's regime is a cold cache). depth_limit >= 0
- * (0: arrival order). Scratch comes only from d_workspace (device, 256-byte
+ * (0: arrival order); n < 2^30. Scratch comes only from d_workspace (device, 256-byte
  * aligned, at least peek_offline_order_workspace(n) bytes). Synchronizes
  * `stream` once or a few times, as peek_queue_signals does.
  * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY (pinned host

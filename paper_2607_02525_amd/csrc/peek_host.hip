@@ -676,6 +676,8 @@ peek_status peek_offline_order(int32_t n, const int32_t* d_tokens, const int64_t
   clear_error();
   if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
   if (depth_limit < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "depth_limit must be >= 0 (got %d)", depth_limit);
+  if (n > (INT32_MAX - 1) / 2)
+    return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be below 2^30 for the offline order (got %d)", n);
   if (n == 0) return PEEK_OK;
   if (!d_tokens || !d_offsets || !d_perm)
     return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_perm must not be NULL");
