@@ -178,8 +178,9 @@ def test_offline_order_argument_errors_before_any_gpu_work():
     assert P.peek_offline_order_workspace(64) > need
     assert lib.peek_offline_order(-1, fake, fake, 128, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
     assert lib.peek_offline_order(8, fake, fake, -1, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
-    assert lib.peek_offline_order(1 << 30, fake, fake, 128, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
     assert "depth_limit" in P.peek_last_error()
+    assert lib.peek_offline_order(1 << 30, fake, fake, 128, fake, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
+    assert "2^30" in P.peek_last_error()
     assert lib.peek_offline_order(0, None, None, 128, None, None, 0, None) == P.PEEK_OK
     assert lib.peek_offline_order(8, fake, fake, 128, None, fake, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
     assert lib.peek_offline_order(8, fake, fake, 128, fake, None, need, None) == P.PEEK_ERR_INVALID_ARGUMENT
