@@ -134,7 +134,7 @@ def cpu_baseline(w, budget_s: float):
         total += time.perf_counter() - t
         reps += 1
     return {"value": w.n * reps / total, "unit": "LPM queries/s", "cores": 1, "kind": "oracle",
-            "sample": f"whole scale queue ({w.n} requests): LPM + demand + clusters, single thread, "
+            "sample": f"whole {w.name} queue ({w.n} requests): LPM + demand + clusters, single thread, "
                       f"{reps} passes in {total:.1f} s; cache-tree ingest {ingest:.1f} s not counted",
             "cpu": _cpu_model()}
 
