@@ -409,3 +409,41 @@ def test_offline_order_large_groups():
     print("[gpu] offline large groups", flush=True)
     for D in (16, 128, 256):
         check_offline(hp, w, D)
+
+
+def test_two_host_threads_on_two_streams():
+    """Two host threads drive two queues on two streams at once (distinct
+    workspaces and outputs, one shared cache): results match the oracle."""
+    import threading
+    HotPath = _hot()
+    w1 = W.make("rag", 42)
+    w2 = W.random_case(5, n=3000, n_cached=10, vocab=3, max_len=300, block_size=16, threshold=4)
+    s1, s2 = O.run(w1), O.run(w2)
+    hp1 = HotPath.from_sequences(*w1.cache_sequences)
+    hp2 = HotPath.from_sequences(*w2.cache_sequences)
+    hp1.load_queue(w1.tokens, w1.offsets, w1.block_size, w1.threshold)
+    hp2.load_queue(w2.tokens, w2.offsets, w2.block_size, w2.threshold)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(hp, st):
+        try:
+            with torch.cuda.stream(st):
+                for _ in range(5):
+                    hp.lpm(st)
+                    hp.clpm(0, 32, st)
+                st.synchronize()
+        except Exception as e:   # reported below, in the main thread
+            errors.append(e)
+
+    print("[gpu] two threads, two streams", flush=True)
+    ts = [threading.Thread(target=run, args=(hp1, streams[0])), threading.Thread(target=run, args=(hp2, streams[1]))]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not errors, errors
+    for hp, w, s in ((hp1, w1, s1), (hp2, w2, s2)):
+        res = hp.results()
+        assert_parity(w, res, s)
