@@ -447,3 +447,32 @@ def test_two_host_threads_on_two_streams():
     for hp, w, s in ((hp1, w1, s1), (hp2, w2, s2)):
         res = hp.results()
         assert_parity(w, res, s)
+
+
+def test_partial_outputs():
+    """Entry points with optional outputs left out: demand alone (no cluster
+    pass), clusters alone (no cache), eviction scores without the order."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    w = W.random_case(21, n=900, n_cached=40, vocab=3, max_len=120, block_size=4, threshold=3)
+    s = O.run(w)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    hp.lpm()
+    print("[gpu] partial outputs", flush=True)
+    # demand only: no cluster outputs
+    dem = torch.full((hp.num_nodes,), -7, dtype=torch.int32, device="cuda")
+    P.peek_queue_signals(hp.cache, hp.d_tokens, hp.d_offsets, hp.d_last, None, w.threshold, None, None, dem, hp.d_ws)
+    assert np.array_equal(dem.cpu().numpy(), s.demand)
+    # clusters only, without a cache
+    cid = torch.full((w.n,), -7, dtype=torch.int32, device="cuda")
+    csz = torch.full((w.n,), -7, dtype=torch.int32, device="cuda")
+    P.peek_queue_signals(None, hp.d_tokens, hp.d_offsets, None, None, w.threshold, cid, csz, None, hp.d_ws)
+    assert np.array_equal(cid.cpu().numpy(), s.clusters.cluster_id)
+    assert np.array_equal(csz.cpu().numpy(), s.clusters.cluster_size)
+    # eviction scores only
+    hp.signals()
+    hp.evict(order=False)
+    torch.cuda.synchronize()
+    e = O.evict(s.tree, s.demand)
+    assert np.array_equal(hp.d_evict_score.cpu().numpy(), e.score)
