@@ -139,6 +139,31 @@ def cpu_baseline(w, budget_s: float):
             "cpu": _cpu_model()}
 
 
+def cpu_all_cores_lpm(w, budget_s: float, threads: int):
+    """The oracle's LPM walk over the whole queue split into request chunks,
+    one per host thread (the walk only reads the tree; the C call releases
+    the interpreter lock). Context beside the single-thread cpu_baseline."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import oracle as O
+    tree = O.cache_tree_of(w)
+    bounds = np.linspace(0, w.n, threads + 1).astype(np.int64)
+    chunks = []
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        off = w.offsets[a:b + 1]
+        chunks.append((w.tokens[off[0]:off[-1]], off - off[0]))
+    reps, total = 0, 0.0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        while total < budget_s or reps == 0:
+            t = time.perf_counter()
+            list(ex.map(lambda c: O.lpm(tree, c[0], c[1], w.block_size), chunks))
+            total += time.perf_counter() - t
+            reps += 1
+    return {"value": w.n * reps / total, "unit": "LPM queries/s", "threads": threads, "kind": "oracle",
+            "sample": f"whole {w.name} queue ({w.n} requests): LPM walk only, {threads} request chunks on "
+                      f"{threads} threads, {reps} passes in {total:.1f} s"}
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -305,10 +330,13 @@ def main():
     roofline["frac_of_measured_read_peak"] = round(achieved / read_peak, 4)
     log(f"streaming read of 4 GiB: {read_peak:.0f} GB/s")
 
-    cpu = None
+    cpu = cpu_all = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host for cpu_baseline")
         cpu = cpu_baseline(w, args.cpu_budget)
+        threads = max(1, min(16, os.cpu_count() or 1))
+        cpu_all = cpu_all_cores_lpm(w, args.cpu_budget / 2, threads)
+        log(f"oracle LPM walk on {threads} threads: {cpu_all['value']:.0f} queries/s")
 
     out = {
         "metric": METRIC,
@@ -340,6 +368,7 @@ def main():
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
     }
     print(json.dumps(out), flush=True)
 
