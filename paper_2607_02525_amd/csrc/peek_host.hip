@@ -560,6 +560,54 @@ peek_status peek_cache_free(peek_cache* c) {
   return PEEK_OK;
 }
 
+// Device-side checks of the caller's device-resident inputs (a debugging aid,
+// off unless the environment variable PEEK_VALIDATE is set to a value other
+// than 0): offsets non-decreasing from >= 0 with every prompt shorter than
+// 2^31 tokens, last nodes inside the cache, match lengths inside their
+// prompts. peek_lpm_batch, peek_queue_signals, peek_clpm_signals and
+// peek_offline_order run them. They cost a launch, a small allocation and a host round trip per
+// call, so they are not for graph capture or the hot loop.
+__global__ void k_validate_queue(int32_t n, const int64_t* __restrict__ offsets, const int32_t* __restrict__ last,
+                                 const int32_t* __restrict__ mlen, int32_t num_nodes, int32_t* __restrict__ bad) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int32_t f = 0;
+  if (offsets != nullptr) {
+    const int64_t a = offsets[i], b = offsets[i + 1];
+    if (a < 0 || b < a || b - a > INT32_MAX) f |= 1;
+    if (mlen != nullptr && (mlen[i] < 0 || (int64_t)mlen[i] > b - a)) f |= 4;
+  }
+  if (last != nullptr && (last[i] < 0 || last[i] >= num_nodes)) f |= 2;
+  if (f) atomicOr(bad, f);
+}
+
+static bool validation_enabled() {
+  const char* v = std::getenv("PEEK_VALIDATE");
+  return v != nullptr && v[0] != 0 && !(v[0] == '0' && v[1] == 0);
+}
+
+static peek_status validate_queue(int32_t n, const int64_t* d_offsets, const int32_t* d_last, const int32_t* d_mlen,
+                                  int32_t num_nodes, hipStream_t st) {
+  if (!validation_enabled() || n <= 0) return PEEK_OK;
+  int32_t* d_bad = nullptr;
+  PEEK_HIP_TRY(hipMalloc((void**)&d_bad, sizeof(int32_t)));
+  int32_t bad = 0;
+  hipError_t e = hipMemsetAsync(d_bad, 0, sizeof(int32_t), st);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_validate_queue, dim3((unsigned)(((int64_t)n + 255) / 256)), dim3(256), 0, st, n, d_offsets,
+                       d_last, d_mlen, num_nodes, d_bad);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_bad, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  (void)hipFree(d_bad);
+  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "input validation failed to run: %s", hipGetErrorString(e));
+  if (bad & 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_offsets must be non-decreasing from 0 or more, prompts < 2^31");
+  if (bad & 2) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_last_node holds ids outside the cache");
+  if (bad & 4) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_match_len holds lengths outside their prompts");
+  return PEEK_OK;
+}
+
 static peek_status check_same_device(const peek_cache* c) {
   int dev = 0;
   PEEK_HIP_TRY(hipGetDevice(&dev));
@@ -579,6 +627,8 @@ peek_status peek_lpm_batch(const peek_cache* c, int32_t n, const int32_t* d_toke
   if (!d_tokens || !d_offsets || !d_h)
     return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h must not be NULL");
   peek_status s = check_same_device(c);
+  if (s != PEEK_OK) return s;
+  s = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
   if (s != PEEK_OK) return s;
   hipError_t e = launch_lpm_walk(c->tree, n, d_tokens, d_offsets, block_size, d_h, d_last_node, d_match_len,
                                  (hipStream_t)stream);
@@ -643,6 +693,13 @@ static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* 
     peek_status s = check_same_device(c);
     if (s != PEEK_OK) return s;
   }
+  if (want_demand || want_clusters) {
+    const bool anchored = want_clusters && c != nullptr && d_last_node != nullptr && d_match_len != nullptr;
+    const int32_t* last = (c != nullptr && (want_demand || anchored)) ? d_last_node : nullptr;
+    peek_status s = validate_queue(n, want_clusters ? d_offsets : nullptr, last,
+                                   anchored ? d_match_len : nullptr, c ? c->num_nodes : 0, (hipStream_t)stream);
+    if (s != PEEK_OK) return s;
+  }
   return run_signals(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold,
                      want_clusters ? d_cluster_id : nullptr, want_clusters ? d_cluster_size : nullptr,
                      want_demand ? d_demand : nullptr, clpm, nullptr, d_workspace, workspace_bytes,
@@ -687,6 +744,8 @@ peek_status peek_offline_order(int32_t n, const int32_t* d_tokens, const int64_t
     return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
   if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
     return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+  peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
+  if (vs != PEEK_OK) return vs;
   const OfflineRequest off{depth_limit, d_perm};
   return run_signals(nullptr, n, d_tokens, d_offsets, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, &off,
                      d_workspace, workspace_bytes, (hipStream_t)stream);

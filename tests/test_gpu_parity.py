@@ -476,3 +476,38 @@ def test_partial_outputs():
     torch.cuda.synchronize()
     e = O.evict(s.tree, s.demand)
     assert np.array_equal(hp.d_evict_score.cpu().numpy(), e.score)
+
+
+def test_input_validation_on_request(monkeypatch):
+    """With PEEK_VALIDATE set, bad device inputs are refused before any walk
+    or pass runs; good ones go through unchanged."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    w = W.random_case(4, n=300, n_cached=20, vocab=3, max_len=60, block_size=4, threshold=3)
+    s = O.run(w)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    monkeypatch.setenv("PEEK_VALIDATE", "1")
+    print("[gpu] validation", flush=True)
+    hp.step()
+    assert_parity(w, hp.results(), s)
+    bad_off = hp.d_offsets.clone()
+    bad_off[5] = bad_off[7] + 1   # decreasing at 5 -> 6
+    with pytest.raises(P.PeekError, match="d_offsets"):
+        P.peek_lpm_batch(hp.cache, hp.d_tokens, bad_off, w.block_size, hp.d_h)
+    bad_last = hp.d_last.clone()
+    bad_last[3] = hp.num_nodes
+    with pytest.raises(P.PeekError, match="d_last_node"):
+        P.peek_queue_signals(hp.cache, hp.d_tokens, hp.d_offsets, bad_last, hp.d_m, w.threshold, hp.d_cid, hp.d_csz,
+                             hp.d_demand, hp.d_ws)
+    bad_m = hp.d_m.clone()
+    bad_m[0] = int(w.lengths[0]) + 1
+    with pytest.raises(P.PeekError, match="d_match_len"):
+        P.peek_queue_signals(hp.cache, hp.d_tokens, hp.d_offsets, hp.d_last, bad_m, w.threshold, hp.d_cid, hp.d_csz,
+                             hp.d_demand, hp.d_ws)
+    with pytest.raises(P.PeekError, match="d_offsets"):
+        P.peek_offline_order(hp.d_tokens, bad_off, 128, torch.empty(w.n, dtype=torch.int32, device="cuda"),
+                             torch.empty(P.peek_offline_order_workspace(w.n), dtype=torch.uint8, device="cuda"))
+    monkeypatch.delenv("PEEK_VALIDATE")
+    hp.step()
+    assert_parity(w, hp.results(), s)
