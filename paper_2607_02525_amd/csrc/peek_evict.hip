@@ -18,11 +18,10 @@
 //     subtree, K(c) = max over [c, subtree_end(c)) of (E, id) in preorder, and
 //     nodes that share K leave bottom-up: the order is the nodes sorted by
 //     (K, id descending). K comes from in-block prefix/suffix maxima and a
-//     sparse table over 64-node blocks; the sort is the library's merge sort.
+//     sparse table over 64-node blocks; the sort is a radix sort (below).
 #include <algorithm>
 
 #include "peek_internal.h"
-#include "peek_sort.h"
 
 namespace peek {
 namespace {
@@ -39,15 +38,6 @@ __device__ __forceinline__ bool ekey_less(const EKey& a, const EKey& b) {
   return a.e < b.e || (a.e == b.e && a.id < b.id);
 }
 __device__ __forceinline__ EKey ekey_max(const EKey& a, const EKey& b) { return ekey_less(a, b) ? b : a; }
-
-__global__ void k_evict_init(const NodeRec* __restrict__ nodes, const int32_t* __restrict__ demand, int32_t nn,
-                             int64_t* __restrict__ E, int32_t* __restrict__ J) {
-  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= nn) return;
-  const NodeRec r = nodes[c];
-  E[c] = (int64_t)demand[c] * r.depth;
-  J[c] = r.parent;
-}
 
 // One jump: fold in the chain segment that ends at the current link.
 __global__ void k_evict_jump(int32_t nn, const int64_t* __restrict__ E, const int32_t* __restrict__ J,
@@ -132,61 +122,314 @@ __global__ void k_evict_tables_level(EKey* __restrict__ blk, int32_t nb, int k) 
     blk[(int64_t)k * nb + b] = ekey_max(blk[(int64_t)(k - 1) * nb + b], blk[(int64_t)(k - 1) * nb + b + h]);
 }
 
-// Sort element: the largest key of the node's subtree, then the node (its
-// id descending inside one K, i.e. bottom-up along the chain).
-struct OrderElem {
-  int64_t ke;
-  int32_t kid;
+// K(c) = max of (E, id) over [c, subtree_end(c)): in-block maxima at the
+// ends, the sparse table over whole 64-node blocks in between.
+__device__ __forceinline__ EKey subtree_max(const NodeRec* __restrict__ nodes, const int64_t* __restrict__ E,
+                                            const EKey* __restrict__ pre, const EKey* __restrict__ suf,
+                                            const EKey* __restrict__ blk, int32_t nb, int32_t c) {
+  const int32_t hi = nodes[c].subtree_end - 1;
+  const int32_t bl = c >> 6, bh = hi >> 6;
+  EKey k;
+  if (bl == bh) {
+    k = EKey{E[c], c, 0};
+    for (int32_t d = c + 1; d <= hi; ++d) k = ekey_max(k, EKey{E[d], d, 0});
+  } else {
+    k = ekey_max(suf[c], pre[hi]);
+    if (bh - bl >= 2) {
+      const int32_t x = bl + 1, y = bh - 1;
+      const int lv = 31 - __clz(y - x + 1);
+      k = ekey_max(k, ekey_max(blk[(int64_t)lv * nb + x], blk[(int64_t)lv * nb + y - (1 << lv) + 1]));
+    }
+  }
+  return k;
+}
+
+// The victim order is a stable least-significant-digit radix sort of the
+// nodes by K: element i of its input is node nn - 1 - i, so nodes that share
+// K keep descending ids. The key is K.id (4 byte digits, least significant
+// first) then K.e (8 digits; E >= 0 since the root, at depth 0, is on every
+// chain). Digits the host can rule out (K.id < nn, K.e < 2^31 * max depth)
+// get no pass. The key pass also ORs and ANDs all keys: a digit on which
+// they agree is the same for every node, and its pass returns at once. The
+// buffer that holds the data before pass p follows from the parity of the
+// earlier passes that moved it.
+struct VElem {
+  uint64_t ke;   // K.e
+  uint32_t kid;  // K.id
   int32_t node;
 };
-struct OrderLess {
-  __device__ __forceinline__ bool operator()(const OrderElem& a, const OrderElem& b) const {
-    return a.ke < b.ke || (a.ke == b.ke && (a.kid < b.kid || (a.kid == b.kid && a.node > b.node)));
-  }
+constexpr int kDigits = 12;
+constexpr int kRadix = 256;
+__device__ __forceinline__ uint32_t digit_of(const VElem& v, int p) {
+  return p < 4 ? (v.kid >> (8 * p)) & 255u : (uint32_t)(v.ke >> (8 * (p - 4))) & 255u;
+}
+
+// Radix scratch. A pass counts its digit per tile of 2048 nodes, scans each
+// digit's column of tile counts, then scatters.
+struct RadixState {
+  uint64_t* orand;    // [4]: OR and AND of K.e over all nodes, then of K.id
+  uint32_t* counts;   // [kRadix][tiles] this pass's digit counts per tile
+  uint32_t* offs;     // [kRadix][tiles] nodes with the digit in earlier tiles
+  uint32_t* tot;      // [kRadix] nodes with the digit
+  int32_t tiles;
 };
 
-// Builds element c of the order sort: K(c) over [c, subtree_end(c)).
-struct OrderSource {
-  const NodeRec* nodes;
-  const int64_t* E;
-  const EKey* pre;
-  const EKey* suf;
-  const EKey* blk;
-  int32_t nn;
-  int32_t nb;
-  __device__ __forceinline__ OrderElem operator()(size_t i) const {
-    if (i >= (size_t)nn) return OrderElem{INT64_MAX, INT32_MAX, INT32_MIN};
-    const int32_t c = (int32_t)i;
-    const int32_t hi = nodes[c].subtree_end - 1;
-    const int32_t bl = c >> 6, bh = hi >> 6;
-    EKey k;
-    if (bl == bh) {
-      k = EKey{E[c], c, 0};
-      for (int32_t d = c + 1; d <= hi; ++d) k = ekey_max(k, EKey{E[d], d, 0});
-    } else {
-      k = ekey_max(suf[c], pre[hi]);
-      if (bh - bl >= 2) {
-        const int32_t x = bl + 1, y = bh - 1;
-        const int lv = 31 - __clz(y - x + 1);
-        k = ekey_max(k, ekey_max(blk[(int64_t)lv * nb + x], blk[(int64_t)lv * nb + y - (1 << lv) + 1]));
-      }
+constexpr int kRThreads = 256;
+static_assert(kRThreads == kRadix, "thread t of a pass owns digit t");
+constexpr int kRItems = 8;
+constexpr int kRTile = kRThreads * kRItems;
+constexpr int kRWaves = kRThreads / kWave;
+constexpr int64_t kKeyBlocks = 1024;   // grid of the key pass (grid-stride)
+
+__global__ void k_evict_init(const NodeRec* __restrict__ nodes, const int32_t* __restrict__ demand, int32_t nn,
+                             int64_t* __restrict__ E, int32_t* __restrict__ J, uint64_t* __restrict__ orand) {
+  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (orand != nullptr && c < 4) orand[c] = (c & 1) ? ~uint64_t(0) : 0;
+  if (c >= nn) return;
+  const NodeRec r = nodes[c];
+  E[c] = (int64_t)demand[c] * r.depth;
+  J[c] = r.parent;
+}
+
+// Whether digit p differs between nodes.
+__device__ __forceinline__ bool digit_moves(const uint64_t* orand, int p) {
+  const uint64_t x = p < 4 ? (orand[2] ^ orand[3]) >> (8 * p) : (orand[0] ^ orand[1]) >> (8 * (p - 4));
+  return (x & 255u) != 0;
+}
+
+// Whether pass p moves data, and whether it reads the second buffer.
+__device__ __forceinline__ bool pass_source(const uint64_t* orand, int p, bool& from_b) {
+  int ran = 0;
+  for (int q = 0; q < p; ++q) ran += digit_moves(orand, q) ? 1 : 0;
+  from_b = (ran & 1) != 0;
+  return digit_moves(orand, p);
+}
+
+__device__ __forceinline__ EKey shfl_key(const EKey& k, int src) {
+  return EKey{__shfl(k.e, src), __shfl(k.id, src), 0};
+}
+
+// Sort input, plus the OR and AND of all keys. A wave takes one 64-node
+// block: K of a node whose subtree ends inside the block comes from a sparse
+// table over the block held in registers (level k of lane l = max over
+// [l, l + 2^k)), the rest from the in-block prefix/suffix maxima and the
+// sparse table over blocks.
+__global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ nodes, const int64_t* __restrict__ E,
+                                                    const EKey* __restrict__ pre, const EKey* __restrict__ suf,
+                                                    const EKey* __restrict__ blk, int32_t nn, int32_t nb,
+                                                    VElem* __restrict__ out, uint64_t* __restrict__ orand) {
+  __shared__ unsigned long long red[4];
+  if (threadIdx.x < 4) red[threadIdx.x] = (threadIdx.x & 1) ? ~0ull : 0ull;
+  __syncthreads();
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t waves = (int32_t)(gridDim.x * blockDim.x / kWave);
+  uint64_t or_e = 0, and_e = ~uint64_t(0), or_i = 0, and_i = ~uint64_t(0);
+  for (int32_t b = (int32_t)((blockIdx.x * blockDim.x + threadIdx.x) / kWave); b < nb; b += waves) {
+    const int32_t c = b * kWave + lane;
+    const bool valid = c < nn;
+    int32_t hi = c;
+    EKey t[6];
+    t[0] = valid ? EKey{E[c], c, 0} : EKey{INT64_MIN, -1, 0};
+    if (valid) hi = nodes[c].subtree_end - 1;
+#pragma unroll
+    for (int k = 1; k < 6; ++k) {
+      const int d = 1 << (k - 1);
+      const EKey o = shfl_key(t[k - 1], lane + d < kWave ? lane + d : lane);
+      t[k] = lane + d < kWave ? ekey_max(t[k - 1], o) : t[k - 1];
     }
-    return OrderElem{k.e, k.id, c};
+    const bool inside = (hi >> 6) == b;
+    // in-block query [c, hi]: two overlapping windows of 2^lv, lv = floor(log2(len))
+    // (len = 64 takes two windows of 32)
+    const int32_t len = inside ? hi - c + 1 : 1;
+    const int lv = min(31 - __clz(len), 5);
+    const int src2 = (inside ? hi - (1 << lv) + 1 : c) - b * kWave;
+    EKey q = t[0];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      const EKey o = shfl_key(t[k], src2);
+      if (k == lv) q = ekey_max(t[k], o);
+    }
+    if (valid) {
+      EKey k = q;
+      if (!inside) {
+        const int32_t bh = hi >> 6;
+        k = ekey_max(suf[c], pre[hi]);
+        if (bh - b >= 2) {
+          const int32_t x = b + 1, y = bh - 1;
+          const int l2 = 31 - __clz(y - x + 1);
+          k = ekey_max(k, ekey_max(blk[(int64_t)l2 * nb + x], blk[(int64_t)l2 * nb + y - (1 << l2) + 1]));
+        }
+      }
+      out[nn - 1 - c] = VElem{(uint64_t)k.e, (uint32_t)k.id, c};
+      or_e |= (uint64_t)k.e;
+      and_e &= (uint64_t)k.e;
+      or_i |= (uint32_t)k.id;
+      and_i &= (uint32_t)k.id;
+    }
   }
-};
+  atomicOr(&red[0], (unsigned long long)or_e);
+  atomicAnd(&red[1], (unsigned long long)and_e);
+  atomicOr(&red[2], (unsigned long long)or_i);
+  atomicAnd(&red[3], (unsigned long long)and_i);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    atomicOr((unsigned long long*)&orand[0], red[0]);
+    atomicAnd((unsigned long long*)&orand[1], red[1]);
+    atomicOr((unsigned long long*)&orand[2], red[2]);
+    atomicAnd((unsigned long long*)&orand[3], red[3]);
+  }
+}
 
-__global__ void k_evict_out(int32_t nn, const OrderElem* __restrict__ el, int32_t* __restrict__ order) {
+// Lanes of the wave whose digit equals this lane's (among the lanes in m).
+__device__ __forceinline__ uint64_t same_digit(uint32_t dg, uint64_t m) {
+#pragma unroll
+  for (int bit = 0; bit < 8; ++bit) {
+    const uint64_t on = __ballot((dg >> bit) & 1u);
+    m &= ((dg >> bit) & 1u) ? on : ~on;
+  }
+  return m;
+}
+
+// Per wave: the rank of each item among the wave's earlier items with the
+// same digit, and the wave's count per digit (whist_w[d]). Items are
+// blocked per wave (item q of lane l is element base + q*64 + l), so the
+// ranks follow element order.
+__device__ __forceinline__ void wave_rank(const uint32_t (&dg)[kRItems], const bool (&valid)[kRItems],
+                                          uint32_t (&rk)[kRItems], uint32_t* whist_w, int lane) {
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+#pragma unroll
+  for (int q = 0; q < kRItems; ++q) {
+    const uint64_t m = same_digit(dg[q], __ballot(valid[q]));
+    const int lead = valid[q] ? __ffsll((unsigned long long)m) - 1 : lane;
+    uint32_t old = 0;
+    if (valid[q] && lead == lane) {
+      old = whist_w[dg[q]];
+      whist_w[dg[q]] = old + (uint32_t)__popcll(m);
+    }
+    old = __shfl(old, lead);
+    rk[q] = valid[q] ? old + (uint32_t)__popcll(m & below) : 0;
+  }
+}
+
+// Pass p, first kernel: the tile's count of every digit value.
+__global__ __launch_bounds__(kRThreads) void k_radix_count(const VElem* __restrict__ a, const VElem* __restrict__ b,
+                                                           int32_t nn, int p, RadixState rs) {
+  __shared__ uint32_t whist[kRWaves][kRadix];
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  bool from_b;
+  if (!pass_source(rs.orand, p, from_b)) return;
+  const VElem* __restrict__ src = from_b ? b : a;
+  for (int j = t; j < kRWaves * kRadix; j += kRThreads) (&whist[0][0])[j] = 0;
+  __syncthreads();
+  const int32_t tile = blockIdx.x;
+  const int64_t base = (int64_t)tile * kRTile + (int64_t)w * (kWave * kRItems);
+  uint32_t dg[kRItems], rk[kRItems];
+  bool valid[kRItems];
+#pragma unroll
+  for (int q = 0; q < kRItems; ++q) {
+    const int64_t idx = base + q * kWave + lane;
+    valid[q] = idx < nn;
+    dg[q] = valid[q] ? digit_of(src[idx], p) : 0;
+  }
+  wave_rank(dg, valid, rk, whist[w], lane);
+  __syncthreads();
+  uint32_t total = 0;
+#pragma unroll
+  for (int j = 0; j < kRWaves; ++j) total += whist[j][t];
+  rs.counts[(int64_t)t * rs.tiles + tile] = total;
+}
+
+// Pass p, second kernel: workgroup d scans digit d's column of tile counts.
+__global__ __launch_bounds__(kRThreads) void k_radix_scan(int p, RadixState rs) {
+  __shared__ uint32_t sc[kRThreads];
+  bool from_b;
+  if (!pass_source(rs.orand, p, from_b)) return;
+  const int t = threadIdx.x;
+  const int64_t row = (int64_t)blockIdx.x * rs.tiles;
+  uint32_t run = 0;
+  for (int32_t j0 = 0; j0 < rs.tiles; j0 += kRThreads) {
+    const int32_t j = j0 + t;
+    const uint32_t mine = j < rs.tiles ? rs.counts[row + j] : 0;
+    sc[t] = mine;
+    __syncthreads();
+    for (int d = 1; d < kRThreads; d <<= 1) {
+      const uint32_t o = t >= d ? sc[t - d] : 0;
+      __syncthreads();
+      sc[t] += o;
+      __syncthreads();
+    }
+    if (j < rs.tiles) rs.offs[row + j] = run + sc[t] - mine;
+    run += sc[kRThreads - 1];
+    __syncthreads();
+  }
+  if (t == 0) rs.tot[blockIdx.x] = run;
+}
+
+// Pass p, third kernel: every node of the tile to its place.
+__global__ __launch_bounds__(kRThreads) void k_radix_scatter(VElem* __restrict__ a, VElem* __restrict__ b,
+                                                             int32_t nn, int p, RadixState rs) {
+  __shared__ uint32_t whist[kRWaves][kRadix];
+  __shared__ uint32_t gbase[kRadix];
+  __shared__ uint32_t scan[kRadix];
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  bool from_b;
+  if (!pass_source(rs.orand, p, from_b)) return;
+  const VElem* __restrict__ src = from_b ? b : a;
+  VElem* __restrict__ dst = from_b ? a : b;
+  for (int j = t; j < kRWaves * kRadix; j += kRThreads) (&whist[0][0])[j] = 0;
+  const int32_t tile = blockIdx.x;
+  const int64_t base = (int64_t)tile * kRTile + (int64_t)w * (kWave * kRItems);
+  VElem v[kRItems];
+  uint32_t dg[kRItems], rk[kRItems];
+  bool valid[kRItems];
+#pragma unroll
+  for (int q = 0; q < kRItems; ++q) {
+    const int64_t idx = base + q * kWave + lane;
+    valid[q] = idx < nn;
+    if (valid[q]) v[q] = src[idx];
+    dg[q] = valid[q] ? digit_of(v[q], p) : 0;
+  }
+  const uint32_t off = rs.offs[(int64_t)t * rs.tiles + tile];
+  // bucket starts: exclusive scan of the digit totals
+  const uint32_t mine = rs.tot[t];
+  scan[t] = mine;
+  __syncthreads();
+  for (int d = 1; d < kRadix; d <<= 1) {
+    const uint32_t o = t >= d ? scan[t - d] : 0;
+    __syncthreads();
+    scan[t] += o;
+    __syncthreads();
+  }
+  gbase[t] = scan[t] - mine + off;
+  wave_rank(dg, valid, rk, whist[w], lane);
+  __syncthreads();
+  // thread t owns digit t: the waves' exclusive offsets
+  uint32_t run = 0;
+#pragma unroll
+  for (int j = 0; j < kRWaves; ++j) {
+    const uint32_t c = whist[j][t];
+    whist[j][t] = run;
+    run += c;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kRItems; ++q) {
+    const uint32_t pos = gbase[dg[q]] + whist[w][dg[q]] + rk[q];
+    if (valid[q] && pos < (uint32_t)nn) dst[pos] = v[q];
+  }
+}
+
+// The passes that moved data decide the buffer that holds the sorted nodes.
+__global__ void k_evict_out(int32_t nn, const VElem* __restrict__ a, const VElem* __restrict__ b,
+                            const uint64_t* __restrict__ orand, int32_t* __restrict__ order) {
+  int moved = 0;
+  for (int p = 0; p < kDigits; ++p) moved += digit_moves(orand, p) ? 1 : 0;
+  const VElem* el = (moved & 1) ? b : a;
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nn - 1) order[i] = el[i].node;   // the root sorts last and stays
 }
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
-
-size_t np_for(int64_t nn) {
-  size_t np = msort::kTile;
-  while (np < (size_t)nn) np <<= 1;
-  return np;
-}
 
 int levels_for(int64_t nb) {
   int k = 1;
@@ -195,15 +438,16 @@ int levels_for(int64_t nb) {
 }
 
 struct ELayout {
-  size_t e_a, e_b, j_a, j_b, pre, suf, blk, el_a, el_b, total;
+  size_t e_a, e_b, j_a, j_b, pre, suf, blk, v_a, v_b, orand, counts, offs, tot, total;
   int32_t nb;
+  int32_t tiles;
   int levels;
 };
 
 ELayout elayout(int64_t nn) {
   ELayout L{};
   const size_t n = (size_t)std::max<int64_t>(nn, 1);
-  const size_t np = np_for(nn);
+  L.tiles = (int32_t)((n + kRTile - 1) / kRTile);
   L.nb = (int32_t)((n + kWave - 1) / kWave);
   L.levels = levels_for(L.nb);
   size_t o = 0;
@@ -219,8 +463,12 @@ ELayout elayout(int64_t nn) {
   L.pre = take(sizeof(EKey) * n);
   L.suf = take(sizeof(EKey) * n);
   L.blk = take(sizeof(EKey) * (size_t)L.levels * L.nb);
-  L.el_a = take(sizeof(OrderElem) * np);
-  L.el_b = take(sizeof(OrderElem) * np);
+  L.v_a = take(sizeof(VElem) * n);
+  L.v_b = take(sizeof(VElem) * n);
+  L.orand = take(sizeof(uint64_t) * 4);
+  L.counts = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
+  L.offs = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
+  L.tot = take(sizeof(uint32_t) * kRadix);
   L.total = o;
   return L;
 }
@@ -241,7 +489,21 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
   int32_t* J = (int32_t*)(w + L.j_a);
   int32_t* J2 = (int32_t*)(w + L.j_b);
   const NodeRec* nodes = c->tree.nodes;
-  hipLaunchKernelGGL(k_evict_init, dim3(blocks_of(nn)), dim3(256), 0, st, nodes, demand, nn, E, J);
+  const bool ordered = order != nullptr && nn > 1;
+  RadixState rs{nullptr, nullptr, nullptr, nullptr, 0};
+  // digits that can differ: bytes of K.id < nn, bytes of K.e < 2^31 * max depth
+  uint32_t live = 0;
+  for (int p = 0; p < 4; ++p)
+    if (((uint64_t)(nn - 1) >> (8 * p)) != 0) live |= 1u << p;
+  const uint64_t e_bound = (uint64_t)INT32_MAX * (uint64_t)std::max<int64_t>(c->max_depth, 1);
+  for (int p = 0; p < 8; ++p)
+    if ((e_bound >> (8 * p)) != 0) live |= 1u << (4 + p);
+  if (ordered) {
+    rs = RadixState{(uint64_t*)(w + L.orand), (uint32_t*)(w + L.counts), (uint32_t*)(w + L.offs),
+                    (uint32_t*)(w + L.tot), L.tiles};
+  }
+  hipLaunchKernelGGL(k_evict_init, dim3(blocks_of(std::max<int64_t>(nn, 4))), dim3(256), 0, st, nodes, demand, nn, E,
+                     J, rs.orand);
   // ceil(log2(levels + 1)) rounds cover the longest chain (levels + 1 nodes)
   for (int64_t span = 1; span < (int64_t)c->max_level + 1; span <<= 1) {
     hipLaunchKernelGGL(k_evict_jump, dim3(blocks_of(nn)), dim3(256), 0, st, nn, E, J, E2, J2);
@@ -252,15 +514,23 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
   EKey* suf = (EKey*)(w + L.suf);
   EKey* blk = (EKey*)(w + L.blk);
   hipLaunchKernelGGL(k_evict_blocks, dim3(blocks_of(L.nb, 4)), dim3(256), 0, st, nn, E, score, pre, suf, blk, L.nb);
-  if (order != nullptr && nn > 1) {
+  if (ordered) {
     hipLaunchKernelGGL(k_evict_tables_local, dim3((L.nb + kTabChunk - 1) / kTabChunk), dim3(1024), 0, st, blk, L.nb,
                        L.levels);
     for (int k = kTabLocalLevels; k < L.levels; ++k)
       hipLaunchKernelGGL(k_evict_tables_level, dim3(blocks_of(L.nb)), dim3(256), 0, st, blk, L.nb, k);
-    const OrderSource src{nodes, E, pre, suf, blk, nn, L.nb};
-    OrderElem* sorted = msort::sort_from(src, (OrderElem*)(w + L.el_a), (OrderElem*)(w + L.el_b), np_for(nn),
-                                         OrderLess{}, st);
-    hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, sorted, order);
+    VElem* va = (VElem*)(w + L.v_a);
+    VElem* vb = (VElem*)(w + L.v_b);
+    hipLaunchKernelGGL(k_order_keys, dim3((unsigned)std::min<int64_t>(blocks_of(nn), kKeyBlocks)), dim3(256), 0, st,
+                       nodes, E, pre, suf, blk, nn, L.nb, va, rs.orand);
+    for (int p = 0; p < kDigits; ++p)
+      if ((live >> p) & 1u)
+      {
+        hipLaunchKernelGGL(k_radix_count, dim3((unsigned)L.tiles), dim3(kRThreads), 0, st, va, vb, nn, p, rs);
+        hipLaunchKernelGGL(k_radix_scan, dim3(kRadix), dim3(kRThreads), 0, st, p, rs);
+        hipLaunchKernelGGL(k_radix_scatter, dim3((unsigned)L.tiles), dim3(kRThreads), 0, st, va, vb, nn, p, rs);
+      }
+    hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, va, vb, rs.orand, order);
   }
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;

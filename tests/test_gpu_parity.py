@@ -511,3 +511,37 @@ def test_input_validation_on_request(monkeypatch):
     monkeypatch.delenv("PEEK_VALIDATE")
     hp.step()
     assert_parity(w, hp.results(), s)
+
+
+@pytest.mark.parametrize("kind", ["zero", "huge", "signed", "ties"])
+def test_evict_rank_any_demand(kind):
+    """Eviction ranking from demand vectors no queue produces: all zero (only
+    the id digits of the sort key vary), up to 2^31 - 1 (scores beyond 2^40),
+    negative entries, and a handful of distinct values (many equal keys), on
+    a 70000-node tree (many sort tiles)."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    w = W.random_tree_case(5, n_nodes=70000, n=8, vocab=40, max_edge=3, block_size=4, threshold=2)
+    tree = O.cache_tree_of(w)
+    hp = HotPath.from_description(*w.cache_tree)
+    nn = hp.num_nodes
+    rng = np.random.default_rng(7)
+    if kind == "zero":
+        d = np.zeros(nn, np.int32)
+    elif kind == "huge":
+        d = rng.integers(0, 2**31 - 1, size=nn, dtype=np.int64).astype(np.int32)
+    elif kind == "signed":
+        d = rng.integers(-2**31, 2**31 - 1, size=nn, dtype=np.int64).astype(np.int32)
+    else:
+        d = rng.choice(np.array([0, 1, 3, 1000], np.int32), size=nn)
+    print(f"[gpu] evict demand={kind} nodes={nn}", flush=True)
+    e = O.evict(tree, d)
+    dd = torch.from_numpy(d).cuda()
+    score = torch.empty(nn, dtype=torch.int64, device="cuda")
+    order = torch.empty(nn - 1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(P.peek_evict_rank_workspace(nn), dtype=torch.uint8, device="cuda")
+    for _ in range(2):   # the workspace keeps the previous call's state
+        P.peek_evict_rank(hp.cache, dd, score, order, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(score.cpu().numpy(), e.score)
+        assert np.array_equal(order.cpu().numpy(), e.order)
