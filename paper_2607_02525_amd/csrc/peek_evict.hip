@@ -166,8 +166,9 @@ __device__ __forceinline__ uint32_t digit_of(const VElem& v, int p) {
 
 // Radix scratch. A pass counts its digit per tile of 2048 nodes, scans each
 // digit's column of tile counts, then scatters.
+constexpr int kOrCopies = 64;   // workgroup w of the key pass adds to copy w % 64
 struct RadixState {
-  uint64_t* orand;    // [4]: OR and AND of K.e over all nodes, then of K.id
+  uint64_t* orand;    // [kOrCopies][4]: OR and AND of K.e over the nodes, then of K.id
   uint32_t* counts;   // [kRadix][tiles] this pass's digit counts per tile
   uint32_t* offs;     // [kRadix][tiles] nodes with the digit in earlier tiles
   uint32_t* tot;      // [kRadix] nodes with the digit
@@ -179,19 +180,41 @@ static_assert(kRThreads == kRadix, "thread t of a pass owns digit t");
 constexpr int kRItems = 8;
 constexpr int kRTile = kRThreads * kRItems;
 constexpr int kRWaves = kRThreads / kWave;
-constexpr int64_t kKeyBlocks = 1024;   // grid of the key pass (grid-stride)
+constexpr int64_t kKeyBlocks = 1 << 16;   // grid cap of the key pass (grid-stride beyond it)
 
 __global__ void k_evict_init(const NodeRec* __restrict__ nodes, const int32_t* __restrict__ demand, int32_t nn,
                              int64_t* __restrict__ E, int32_t* __restrict__ J, uint64_t* __restrict__ orand) {
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (orand != nullptr && c < 4) orand[c] = (c & 1) ? ~uint64_t(0) : 0;
+  if (orand != nullptr && c < 4 * kOrCopies) orand[c] = (c & 1) ? ~uint64_t(0) : 0;
   if (c >= nn) return;
   const NodeRec r = nodes[c];
   E[c] = (int64_t)demand[c] * r.depth;
   J[c] = r.parent;
 }
 
-// Whether digit p differs between nodes.
+// The OR/AND copies folded into sh[4] (the first wave loads them, every
+// thread of the workgroup calls this).
+__device__ __forceinline__ void fold_orand(const uint64_t* __restrict__ orand, uint64_t* sh) {
+  const int t = threadIdx.x;
+  if (t < kWave) {
+    static_assert(kOrCopies == kWave, "one copy per lane");
+    uint64_t v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = orand[t * 4 + k];
+    for (int d = 1; d < kWave; d <<= 1) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint64_t o = __shfl_xor(v[k], d);
+        v[k] = (k & 1) ? (v[k] & o) : (v[k] | o);
+      }
+    }
+    if (t == 0)
+      for (int k = 0; k < 4; ++k) sh[k] = v[k];
+  }
+  __syncthreads();
+}
+
+// Whether digit p differs between nodes (orand: the folded words).
 __device__ __forceinline__ bool digit_moves(const uint64_t* orand, int p) {
   const uint64_t x = p < 4 ? (orand[2] ^ orand[3]) >> (8 * p) : (orand[0] ^ orand[1]) >> (8 * (p - 4));
   return (x & 255u) != 0;
@@ -221,6 +244,7 @@ __global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ 
   __shared__ unsigned long long red[4];
   if (threadIdx.x < 4) red[threadIdx.x] = (threadIdx.x & 1) ? ~0ull : 0ull;
   __syncthreads();
+  orand += (blockIdx.x % kOrCopies) * 4;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t waves = (int32_t)(gridDim.x * blockDim.x / kWave);
   uint64_t or_e = 0, and_e = ~uint64_t(0), or_i = 0, and_i = ~uint64_t(0);
@@ -267,10 +291,18 @@ __global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ 
       and_i &= (uint32_t)k.id;
     }
   }
-  atomicOr(&red[0], (unsigned long long)or_e);
-  atomicAnd(&red[1], (unsigned long long)and_e);
-  atomicOr(&red[2], (unsigned long long)or_i);
-  atomicAnd(&red[3], (unsigned long long)and_i);
+  for (int d = 1; d < kWave; d <<= 1) {
+    or_e |= __shfl_xor(or_e, d);
+    and_e &= __shfl_xor(and_e, d);
+    or_i |= __shfl_xor(or_i, d);
+    and_i &= __shfl_xor(and_i, d);
+  }
+  if (lane == 0) {
+    atomicOr(&red[0], (unsigned long long)or_e);
+    atomicAnd(&red[1], (unsigned long long)and_e);
+    atomicOr(&red[2], (unsigned long long)or_i);
+    atomicAnd(&red[3], (unsigned long long)and_i);
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     atomicOr((unsigned long long*)&orand[0], red[0]);
@@ -317,7 +349,9 @@ __global__ __launch_bounds__(kRThreads) void k_radix_count(const VElem* __restri
   __shared__ uint32_t whist[kRWaves][kRadix];
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
   bool from_b;
-  if (!pass_source(rs.orand, p, from_b)) return;
+  __shared__ uint64_t oa[4];
+  fold_orand(rs.orand, oa);
+  if (!pass_source(oa, p, from_b)) return;
   const VElem* __restrict__ src = from_b ? b : a;
   for (int j = t; j < kRWaves * kRadix; j += kRThreads) (&whist[0][0])[j] = 0;
   __syncthreads();
@@ -343,7 +377,9 @@ __global__ __launch_bounds__(kRThreads) void k_radix_count(const VElem* __restri
 __global__ __launch_bounds__(kRThreads) void k_radix_scan(int p, RadixState rs) {
   __shared__ uint32_t sc[kRThreads];
   bool from_b;
-  if (!pass_source(rs.orand, p, from_b)) return;
+  __shared__ uint64_t oa[4];
+  fold_orand(rs.orand, oa);
+  if (!pass_source(oa, p, from_b)) return;
   const int t = threadIdx.x;
   const int64_t row = (int64_t)blockIdx.x * rs.tiles;
   uint32_t run = 0;
@@ -373,7 +409,9 @@ __global__ __launch_bounds__(kRThreads) void k_radix_scatter(VElem* __restrict__
   __shared__ uint32_t scan[kRadix];
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
   bool from_b;
-  if (!pass_source(rs.orand, p, from_b)) return;
+  __shared__ uint64_t oa[4];
+  fold_orand(rs.orand, oa);
+  if (!pass_source(oa, p, from_b)) return;
   const VElem* __restrict__ src = from_b ? b : a;
   VElem* __restrict__ dst = from_b ? a : b;
   for (int j = t; j < kRWaves * kRadix; j += kRThreads) (&whist[0][0])[j] = 0;
@@ -422,8 +460,10 @@ __global__ __launch_bounds__(kRThreads) void k_radix_scatter(VElem* __restrict__
 // The passes that moved data decide the buffer that holds the sorted nodes.
 __global__ void k_evict_out(int32_t nn, const VElem* __restrict__ a, const VElem* __restrict__ b,
                             const uint64_t* __restrict__ orand, int32_t* __restrict__ order) {
+  __shared__ uint64_t oa[4];
+  fold_orand(orand, oa);
   int moved = 0;
-  for (int p = 0; p < kDigits; ++p) moved += digit_moves(orand, p) ? 1 : 0;
+  for (int p = 0; p < kDigits; ++p) moved += digit_moves(oa, p) ? 1 : 0;
   const VElem* el = (moved & 1) ? b : a;
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nn - 1) order[i] = el[i].node;   // the root sorts last and stays
@@ -465,7 +505,7 @@ ELayout elayout(int64_t nn) {
   L.blk = take(sizeof(EKey) * (size_t)L.levels * L.nb);
   L.v_a = take(sizeof(VElem) * n);
   L.v_b = take(sizeof(VElem) * n);
-  L.orand = take(sizeof(uint64_t) * 4);
+  L.orand = take(sizeof(uint64_t) * 4 * kOrCopies);
   L.counts = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
   L.offs = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
   L.tot = take(sizeof(uint32_t) * kRadix);
@@ -502,8 +542,8 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
     rs = RadixState{(uint64_t*)(w + L.orand), (uint32_t*)(w + L.counts), (uint32_t*)(w + L.offs),
                     (uint32_t*)(w + L.tot), L.tiles};
   }
-  hipLaunchKernelGGL(k_evict_init, dim3(blocks_of(std::max<int64_t>(nn, 4))), dim3(256), 0, st, nodes, demand, nn, E,
-                     J, rs.orand);
+  hipLaunchKernelGGL(k_evict_init, dim3(blocks_of(std::max<int64_t>(nn, 4 * kOrCopies))), dim3(256), 0, st, nodes,
+                     demand, nn, E, J, rs.orand);
   // ceil(log2(levels + 1)) rounds cover the longest chain (levels + 1 nodes)
   for (int64_t span = 1; span < (int64_t)c->max_level + 1; span <<= 1) {
     hipLaunchKernelGGL(k_evict_jump, dim3(blocks_of(nn)), dim3(256), 0, st, nn, E, J, E2, J2);
