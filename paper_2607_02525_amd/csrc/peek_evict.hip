@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "peek_internal.h"
+#include "peek_sort.h"
 
 namespace peek {
 namespace {
@@ -457,14 +458,36 @@ __global__ __launch_bounds__(kRThreads) void k_radix_scatter(VElem* __restrict__
   }
 }
 
-// The passes that moved data decide the buffer that holds the sorted nodes.
+// Below kRadixMin nodes the radix passes cost more launches than the
+// library's merge sort of the same keys (ties keep input order there too).
+constexpr int64_t kRadixMin = int64_t(1) << 19;
+struct VLess {
+  __device__ __forceinline__ bool operator()(const VElem& x, const VElem& y) const {
+    return x.ke < y.ke || (x.ke == y.ke && x.kid < y.kid);
+  }
+};
+// The keys padded to the merge sort's power-of-two size (pads sort last:
+// K.e < 2^62).
+struct PaddedKeys {
+  const VElem* v;
+  int32_t nn;
+  __device__ __forceinline__ VElem operator()(size_t i) const {
+    return i < (size_t)nn ? v[i] : VElem{~uint64_t(0), ~0u, -1};
+  }
+};
+
+// The passes that moved data decide the buffer that holds the sorted nodes
+// (orand == NULL: the merge sort's result, in a).
 __global__ void k_evict_out(int32_t nn, const VElem* __restrict__ a, const VElem* __restrict__ b,
                             const uint64_t* __restrict__ orand, int32_t* __restrict__ order) {
-  __shared__ uint64_t oa[4];
-  fold_orand(orand, oa);
-  int moved = 0;
-  for (int p = 0; p < kDigits; ++p) moved += digit_moves(oa, p) ? 1 : 0;
-  const VElem* el = (moved & 1) ? b : a;
+  const VElem* el = a;
+  if (orand != nullptr) {
+    __shared__ uint64_t oa[4];
+    fold_orand(orand, oa);
+    int moved = 0;
+    for (int p = 0; p < kDigits; ++p) moved += digit_moves(oa, p) ? 1 : 0;
+    if (moved & 1) el = b;
+  }
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nn - 1) order[i] = el[i].node;   // the root sorts last and stays
 }
@@ -478,7 +501,8 @@ int levels_for(int64_t nb) {
 }
 
 struct ELayout {
-  size_t e_a, e_b, j_a, j_b, pre, suf, blk, v_a, v_b, orand, counts, offs, tot, total;
+  size_t e_a, e_b, j_a, j_b, pre, suf, blk, v_a, v_b, v_c, orand, counts, offs, tot, total;
+  size_t nv;
   int32_t nb;
   int32_t tiles;
   int levels;
@@ -503,8 +527,16 @@ ELayout elayout(int64_t nn) {
   L.pre = take(sizeof(EKey) * n);
   L.suf = take(sizeof(EKey) * n);
   L.blk = take(sizeof(EKey) * (size_t)L.levels * L.nb);
-  L.v_a = take(sizeof(VElem) * n);
-  L.v_b = take(sizeof(VElem) * n);
+  // the merge sort works on a power of two >= n
+  size_t nv = n;
+  if ((int64_t)n < kRadixMin) {
+    nv = msort::kTile;
+    while (nv < n) nv <<= 1;
+  }
+  L.nv = nv;
+  L.v_a = take(sizeof(VElem) * nv);
+  L.v_b = take(sizeof(VElem) * nv);
+  L.v_c = take((int64_t)n < kRadixMin ? sizeof(VElem) * nv : 0);
   L.orand = take(sizeof(uint64_t) * 4 * kOrCopies);
   L.counts = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
   L.offs = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
@@ -563,14 +595,18 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
     VElem* vb = (VElem*)(w + L.v_b);
     hipLaunchKernelGGL(k_order_keys, dim3((unsigned)std::min<int64_t>(blocks_of(nn), kKeyBlocks)), dim3(256), 0, st,
                        nodes, E, pre, suf, blk, nn, L.nb, va, rs.orand);
-    for (int p = 0; p < kDigits; ++p)
-      if ((live >> p) & 1u)
-      {
+    if (nn < kRadixMin) {
+      const VElem* sorted = msort::sort_from(PaddedKeys{va, nn}, vb, (VElem*)(w + L.v_c), L.nv, VLess{}, st);
+      hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, sorted, sorted, nullptr, order);
+    } else {
+      for (int p = 0; p < kDigits; ++p) {
+        if (((live >> p) & 1u) == 0) continue;
         hipLaunchKernelGGL(k_radix_count, dim3((unsigned)L.tiles), dim3(kRThreads), 0, st, va, vb, nn, p, rs);
         hipLaunchKernelGGL(k_radix_scan, dim3(kRadix), dim3(kRThreads), 0, st, p, rs);
         hipLaunchKernelGGL(k_radix_scatter, dim3((unsigned)L.tiles), dim3(kRThreads), 0, st, va, vb, nn, p, rs);
       }
-    hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, va, vb, rs.orand, order);
+      hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, va, vb, rs.orand, order);
+    }
   }
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;

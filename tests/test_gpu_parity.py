@@ -513,18 +513,42 @@ def test_input_validation_on_request(monkeypatch):
     assert_parity(w, hp.results(), s)
 
 
+def _big_tree(nn: int, seed: int):
+    """A random tree description of nn nodes built with numpy: each node hangs
+    off a recent node (deep paths) or, three times in ten, any earlier node;
+    its first token is its index among its siblings."""
+    rng = np.random.default_rng(seed)
+    i = np.arange(1, nn)
+    near = np.maximum(i - rng.integers(1, 64, size=nn - 1), 0)
+    anywhere = (rng.random(nn - 1) * i).astype(np.int64)
+    par = np.where(rng.random(nn - 1) < 0.3, anywhere, near)
+    order = np.argsort(par, kind="stable")
+    ps = par[order]
+    starts = np.r_[0, np.flatnonzero(np.diff(ps)) + 1]
+    sib = np.empty(nn - 1, np.int64)
+    sib[order] = np.arange(nn - 1) - np.repeat(starts, np.diff(np.r_[starts, nn - 1]))
+    lens = np.r_[0, rng.integers(1, 4, size=nn - 1)]
+    eoff = np.r_[0, np.cumsum(lens)].astype(np.int64)
+    etok = rng.integers(0, 50, size=int(eoff[-1])).astype(np.int32)
+    etok[eoff[1:-1]] = sib.astype(np.int32)
+    parent = np.r_[-1, par].astype(np.int32)
+    return parent, eoff, etok
+
+
+@pytest.mark.parametrize("nn", [70000, 1 << 19, 600001])
 @pytest.mark.parametrize("kind", ["zero", "huge", "signed", "ties"])
-def test_evict_rank_any_demand(kind):
+def test_evict_rank_any_demand(kind, nn):
     """Eviction ranking from demand vectors no queue produces: all zero (only
     the id digits of the sort key vary), up to 2^31 - 1 (scores beyond 2^40),
     negative entries, and a handful of distinct values (many equal keys), on
-    a 70000-node tree (many sort tiles)."""
+    trees below and at or above the size where the victim order switches from
+    the merge sort to the radix sort (2^19 nodes)."""
     import paper_2607_02525_amd as P
     HotPath = _hot()
-    w = W.random_tree_case(5, n_nodes=70000, n=8, vocab=40, max_edge=3, block_size=4, threshold=2)
-    tree = O.cache_tree_of(w)
-    hp = HotPath.from_description(*w.cache_tree)
-    nn = hp.num_nodes
+    parent, eoff, etok = _big_tree(nn, 5)
+    tree = O.Tree.from_description(parent, eoff, etok)
+    hp = HotPath.from_description(parent, eoff, etok)
+    assert hp.num_nodes == nn
     rng = np.random.default_rng(7)
     if kind == "zero":
         d = np.zeros(nn, np.int32)
@@ -545,3 +569,46 @@ def test_evict_rank_any_demand(kind):
         torch.cuda.synchronize()
         assert np.array_equal(score.cpu().numpy(), e.score)
         assert np.array_equal(order.cpu().numpy(), e.order)
+
+
+def _shape_tree(shape: str, nn: int):
+    """Tree descriptions of nn nodes: a chain, a star, or a comb (a chain
+    whose every node also has one leaf)."""
+    parent, edges = [-1], [np.empty(0, np.int32)]
+    for i in range(1, nn):
+        if shape == "chain":
+            parent.append(i - 1)
+            edges.append(np.array([7], np.int32))
+        elif shape == "star":
+            parent.append(0)
+            edges.append(np.array([i, 3], np.int32))
+        else:   # comb: odd nodes extend the spine, each even node is a leaf off the node before it
+            parent.append((i - 2 if i >= 3 else 0) if i % 2 == 1 else i - 1)
+            edges.append(np.array([i % 2, i], np.int32))
+    tok, off = W.pack(edges)
+    return np.array(parent, np.int32), off, tok
+
+
+@pytest.mark.parametrize("shape,nn", [("chain", 2), ("chain", 3), ("star", 2048), ("star", 2049), ("chain", 4097),
+                                      ("comb", 6001)])
+def test_evict_rank_tree_shapes(shape, nn):
+    """Eviction ranking on degenerate trees at the sort's tile edges (2048
+    nodes per tile): one edge, a chain (every node in one group), a star
+    (every node a leaf) and a comb, with random and all-zero demand."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    parent, eoff, etok = _shape_tree(shape, nn)
+    tree = O.Tree.from_description(parent, eoff, etok)
+    hp = HotPath.from_description(parent, eoff, etok)
+    assert hp.num_nodes == nn == tree.num_nodes
+    print(f"[gpu] evict shape={shape} nodes={nn}", flush=True)
+    ws = torch.empty(P.peek_evict_rank_workspace(nn), dtype=torch.uint8, device="cuda")
+    for seed in range(2):
+        d = np.random.default_rng(seed).integers(0, 50, size=nn).astype(np.int32) if seed else np.zeros(nn, np.int32)
+        e = O.evict(tree, d)
+        score = torch.empty(nn, dtype=torch.int64, device="cuda")
+        order = torch.empty(max(nn - 1, 1), dtype=torch.int32, device="cuda")
+        P.peek_evict_rank(hp.cache, torch.from_numpy(d).cuda(), score, order, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(score.cpu().numpy(), e.score)
+        assert np.array_equal(order.cpu().numpy()[:nn - 1], e.order)
