@@ -29,8 +29,9 @@
  *    Offsets and tokens live on the device, so they are preconditions the
  *    library does not re-check. Each prompt must be shorter than 2^31 tokens.
  *  - Debugging aid: with the environment variable PEEK_VALIDATE set (to
- *    anything but 0), peek_lpm_batch, peek_queue_signals, peek_clpm_signals
- *    and peek_offline_order first check their device inputs on the device
+ *    anything but 0), peek_lpm_batch, peek_queue_signals, peek_clpm_signals,
+ *    peek_offline_order and peek_block_lpm_batch first check their device
+ *    inputs on the device
  *    (offsets non-decreasing from >= 0, prompt lengths < 2^31, last nodes
  *    inside the cache, match lengths inside their prompts) and return
  *    INVALID_ARGUMENT before any other work if one fails. The check adds a

@@ -38,6 +38,7 @@
 #include <vector>
 
 #include "peek_internal.h"
+#include "peek_validate.h"
 
 struct peek_block_table {
   int device;
@@ -461,6 +462,8 @@ peek_status peek_block_lpm_batch(const peek_block_table* t, int32_t n, const int
   const int64_t blocks = ((int64_t)n + kWavesPerBlock - 1) / kWavesPerBlock;
   const dim3 grid((unsigned)blocks), block(kWave * kWavesPerBlock);
   hipStream_t st = (hipStream_t)stream;
+  const peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, st);
+  if (vs != PEEK_OK) return vs;
   switch (t->block_size) {
 #define PEEK_BLOCK_CASE(LT, LS)                                                                                \
   case (1 << LT) << LS:                                                                                        \

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "peek_internal.h"
+#include "peek_validate.h"
 
 namespace peek {
 
@@ -241,6 +242,58 @@ peek_status check_device(int* dev_out) {
     return fail(PEEK_ERR_UNSUPPORTED_DEVICE, "device %d is %s; this library is built for gfx950 only", dev,
                 prop.gcnArchName);
   *dev_out = dev;
+  return PEEK_OK;
+}
+
+// Device-side checks of the caller's device-resident inputs (a debugging aid,
+// off unless the environment variable PEEK_VALIDATE is set to a value other
+// than 0): offsets non-decreasing from >= 0 with every prompt shorter than
+// 2^31 tokens, last nodes inside the cache, match lengths inside their
+// prompts. peek_lpm_batch, peek_queue_signals, peek_clpm_signals,
+// peek_offline_order and peek_block_lpm_batch run them. They cost a launch,
+// a small allocation and a host round trip per call, so they are not for
+// graph capture or the hot loop.
+namespace {
+__global__ void k_validate_queue(int32_t n, const int64_t* __restrict__ offsets, const int32_t* __restrict__ last,
+                                 const int32_t* __restrict__ mlen, int32_t num_nodes, int32_t* __restrict__ bad) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int32_t f = 0;
+  if (offsets != nullptr) {
+    const int64_t a = offsets[i], b = offsets[i + 1];
+    if (a < 0 || b < a || b - a > INT32_MAX) f |= 1;
+    if (mlen != nullptr && (mlen[i] < 0 || (int64_t)mlen[i] > b - a)) f |= 4;
+  }
+  if (last != nullptr && (last[i] < 0 || last[i] >= num_nodes)) f |= 2;
+  if (f) atomicOr(bad, f);
+}
+
+}  // namespace
+
+bool validation_enabled() {
+  const char* v = std::getenv("PEEK_VALIDATE");
+  return v != nullptr && v[0] != 0 && !(v[0] == '0' && v[1] == 0);
+}
+
+peek_status validate_queue(int32_t n, const int64_t* d_offsets, const int32_t* d_last, const int32_t* d_mlen,
+                           int32_t num_nodes, hipStream_t st) {
+  if (!validation_enabled() || n <= 0) return PEEK_OK;
+  int32_t* d_bad = nullptr;
+  PEEK_HIP_TRY(hipMalloc((void**)&d_bad, sizeof(int32_t)));
+  int32_t bad = 0;
+  hipError_t e = hipMemsetAsync(d_bad, 0, sizeof(int32_t), st);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_validate_queue, dim3((unsigned)(((int64_t)n + 255) / 256)), dim3(256), 0, st, n, d_offsets,
+                       d_last, d_mlen, num_nodes, d_bad);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_bad, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  (void)hipFree(d_bad);
+  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "input validation failed to run: %s", hipGetErrorString(e));
+  if (bad & 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_offsets must be non-decreasing from 0 or more, prompts < 2^31");
+  if (bad & 2) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_last_node holds ids outside the cache");
+  if (bad & 4) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_match_len holds lengths outside their prompts");
   return PEEK_OK;
 }
 
@@ -557,54 +610,6 @@ peek_status peek_cache_free(peek_cache* c) {
   hipError_t e = hipFree(c->d_base);
   delete c;
   if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
-  return PEEK_OK;
-}
-
-// Device-side checks of the caller's device-resident inputs (a debugging aid,
-// off unless the environment variable PEEK_VALIDATE is set to a value other
-// than 0): offsets non-decreasing from >= 0 with every prompt shorter than
-// 2^31 tokens, last nodes inside the cache, match lengths inside their
-// prompts. peek_lpm_batch, peek_queue_signals, peek_clpm_signals and
-// peek_offline_order run them. They cost a launch, a small allocation and a host round trip per
-// call, so they are not for graph capture or the hot loop.
-__global__ void k_validate_queue(int32_t n, const int64_t* __restrict__ offsets, const int32_t* __restrict__ last,
-                                 const int32_t* __restrict__ mlen, int32_t num_nodes, int32_t* __restrict__ bad) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  int32_t f = 0;
-  if (offsets != nullptr) {
-    const int64_t a = offsets[i], b = offsets[i + 1];
-    if (a < 0 || b < a || b - a > INT32_MAX) f |= 1;
-    if (mlen != nullptr && (mlen[i] < 0 || (int64_t)mlen[i] > b - a)) f |= 4;
-  }
-  if (last != nullptr && (last[i] < 0 || last[i] >= num_nodes)) f |= 2;
-  if (f) atomicOr(bad, f);
-}
-
-static bool validation_enabled() {
-  const char* v = std::getenv("PEEK_VALIDATE");
-  return v != nullptr && v[0] != 0 && !(v[0] == '0' && v[1] == 0);
-}
-
-static peek_status validate_queue(int32_t n, const int64_t* d_offsets, const int32_t* d_last, const int32_t* d_mlen,
-                                  int32_t num_nodes, hipStream_t st) {
-  if (!validation_enabled() || n <= 0) return PEEK_OK;
-  int32_t* d_bad = nullptr;
-  PEEK_HIP_TRY(hipMalloc((void**)&d_bad, sizeof(int32_t)));
-  int32_t bad = 0;
-  hipError_t e = hipMemsetAsync(d_bad, 0, sizeof(int32_t), st);
-  if (e == hipSuccess) {
-    hipLaunchKernelGGL(k_validate_queue, dim3((unsigned)(((int64_t)n + 255) / 256)), dim3(256), 0, st, n, d_offsets,
-                       d_last, d_mlen, num_nodes, d_bad);
-    e = hipGetLastError();
-  }
-  if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_bad, sizeof(int32_t), hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  (void)hipFree(d_bad);
-  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "input validation failed to run: %s", hipGetErrorString(e));
-  if (bad & 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_offsets must be non-decreasing from 0 or more, prompts < 2^31");
-  if (bad & 2) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_last_node holds ids outside the cache");
-  if (bad & 4) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_match_len holds lengths outside their prompts");
   return PEEK_OK;
 }
 

@@ -508,6 +508,11 @@ def test_input_validation_on_request(monkeypatch):
     with pytest.raises(P.PeekError, match="d_offsets"):
         P.peek_offline_order(hp.d_tokens, bad_off, 128, torch.empty(w.n, dtype=torch.int32, device="cuda"),
                              torch.empty(P.peek_offline_order_workspace(w.n), dtype=torch.uint8, device="cuda"))
+    tab = hp.block_table(w.block_size)
+    with pytest.raises(P.PeekError, match="d_offsets"):
+        P.peek_block_lpm_batch(tab, hp.d_tokens, bad_off, torch.empty(w.n, dtype=torch.int32, device="cuda"))
+    hp.block_lpm()
+    assert np.array_equal(hp.results()["block_h"], O.block_lpm(s.tree, w.tokens, w.offsets, w.block_size))
     monkeypatch.delenv("PEEK_VALIDATE")
     hp.step()
     assert_parity(w, hp.results(), s)
