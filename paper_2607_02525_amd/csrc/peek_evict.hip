@@ -17,8 +17,10 @@
 //     leaf. Every node therefore goes right after the largest key of its
 //     subtree, K(c) = max over [c, subtree_end(c)) of (E, id) in preorder, and
 //     nodes that share K leave bottom-up: the order is the nodes sorted by
-//     (K, id descending). K comes from in-block prefix/suffix maxima and a
-//     sparse table over 64-node blocks; the sort is a radix sort (below).
+//     (K, id descending). K comes from a sparse table over 64-node blocks,
+//     in-block prefix/suffix maxima and, inside one block, a sparse table in
+//     a wave's registers. The sort is the library's merge sort below 2^19
+//     nodes and a radix sort above (below).
 #include <algorithm>
 
 #include "peek_internal.h"
@@ -145,15 +147,15 @@ __device__ __forceinline__ EKey subtree_max(const NodeRec* __restrict__ nodes, c
   return k;
 }
 
-// The victim order is a stable least-significant-digit radix sort of the
-// nodes by K: element i of its input is node nn - 1 - i, so nodes that share
-// K keep descending ids. The key is K.id (4 byte digits, least significant
-// first) then K.e (8 digits; E >= 0 since the root, at depth 0, is on every
-// chain). Digits the host can rule out (K.id < nn, K.e < 2^31 * max depth)
-// get no pass. The key pass also ORs and ANDs all keys: a digit on which
-// they agree is the same for every node, and its pass returns at once. The
-// buffer that holds the data before pass p follows from the parity of the
-// earlier passes that moved it.
+// From 2^19 nodes up the victim order is a stable least-significant-digit
+// radix sort of the nodes by K: element i of its input is node nn - 1 - i,
+// so nodes that share K keep descending ids. The key is K.id (4 byte
+// digits, least significant first) then K.e (8 digits; E >= 0 since the
+// root, at depth 0, is on every chain). Digits the host can rule out (K.id <
+// nn, K.e < 2^31 * max depth) get no pass. The key pass also ORs and ANDs
+// all keys: a digit on which they agree is the same for every node, and its
+// pass returns at once. The buffer that holds the data before pass p follows
+// from the parity of the earlier passes that moved it.
 struct VElem {
   uint64_t ke;   // K.e
   uint32_t kid;  // K.id
