@@ -100,11 +100,36 @@ def _np64(a):
     return np.ascontiguousarray(a, dtype=np.int64)
 
 
-def _dptr(t):
-    """Device pointer of a torch tensor (or None)."""
+def _arg(t, name: str, dtype=None, count: int | None = None):
+    """Device pointer of `t` (or None) after checking what the C entry points
+    cannot: element type, contiguity, at least `count` elements, and that it
+    lives on a GPU."""
     if t is None:
         return None
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if count is not None and t.numel() < count:
+        raise ValueError(f"{name} needs at least {count} elements, has {t.numel()}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _queue_n(offsets) -> int:
+    import torch
+    if offsets.dtype != torch.int64 or offsets.dim() != 1 or offsets.numel() < 1:
+        raise TypeError("offsets must be a 1-D int64 tensor of n + 1 entries")
+    return int(offsets.shape[0]) - 1
+
+
+def _num_nodes(cache) -> int:
+    if cache is None:
+        return 0
+    if getattr(cache, "_num_nodes", None) is None:
+        cache._num_nodes = peek_cache_stats(cache)["num_nodes"]
+    return cache._num_nodes
 
 
 def _stream(stream):
@@ -203,9 +228,12 @@ def peek_cache_free(cache: Cache):
 def peek_lpm_batch(cache: Cache, tokens, offsets, block_size: int, h, last_node=None, match_len=None,
                    stream=None):
     """tokens int32[*], offsets int64[n+1], outputs int32[n]: all torch tensors on the device."""
-    n = int(offsets.shape[0]) - 1
-    _check(_lib.peek_lpm_batch(cache.handle, n, _dptr(tokens), _dptr(offsets), int(block_size), _dptr(h),
-                               _dptr(last_node), _dptr(match_len), _stream(stream)))
+    import torch
+    n = _queue_n(offsets)
+    i32 = torch.int32
+    _check(_lib.peek_lpm_batch(cache.handle, n, _arg(tokens, "tokens", i32), _arg(offsets, "offsets"),
+                               int(block_size), _arg(h, "h", i32, n), _arg(last_node, "last_node", i32, n),
+                               _arg(match_len, "match_len", i32, n), _stream(stream)))
 
 
 def peek_queue_signals_workspace(n: int, num_nodes: int) -> int:
@@ -216,24 +244,33 @@ def peek_queue_signals(cache, tokens, offsets, last_node, match_len, threshold: 
                        demand, workspace, stream=None):
     """cluster_id/cluster_size int32[n], demand int32[num_nodes], workspace uint8 tensor; torch tensors.
     last_node/match_len: peek_lpm_batch outputs for the same prompts (or None)."""
-    n = int(offsets.shape[0]) - 1
+    import torch
+    n = _queue_n(offsets)
+    i32 = torch.int32
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
-    _check(_lib.peek_queue_signals(None if cache is None else cache.handle, n, _dptr(tokens), _dptr(offsets),
-                                   _dptr(last_node), _dptr(match_len), int(threshold), _dptr(cluster_id),
-                                   _dptr(cluster_size), _dptr(demand), _dptr(workspace), ws_bytes,
-                                   _stream(stream)))
+    _check(_lib.peek_queue_signals(None if cache is None else cache.handle, n, _arg(tokens, "tokens", i32),
+                                   _arg(offsets, "offsets"), _arg(last_node, "last_node", i32, n),
+                                   _arg(match_len, "match_len", i32, n), int(threshold),
+                                   _arg(cluster_id, "cluster_id", i32, n), _arg(cluster_size, "cluster_size", i32, n),
+                                   _arg(demand, "demand", i32, _num_nodes(cache)), _arg(workspace, "workspace"),
+                                   ws_bytes, _stream(stream)))
 
 
 def peek_clpm_signals(cache, tokens, offsets, h, last_node, match_len, threshold: int, tau: int, theta: int,
                       cluster_id, cluster_size, demand, score, section, has_sharing, workspace, stream=None):
     """peek_queue_signals plus the ancestor score (int64[n]), the section (int32[n]) and has_sharing (int32[1]);
     torch tensors, any of score/section/has_sharing may be None."""
-    n = int(offsets.shape[0]) - 1
+    import torch
+    n = _queue_n(offsets)
+    i32 = torch.int32
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
-    _check(_lib.peek_clpm_signals(None if cache is None else cache.handle, n, _dptr(tokens), _dptr(offsets), _dptr(h),
-                                  _dptr(last_node), _dptr(match_len), int(threshold), int(tau), int(theta),
-                                  _dptr(cluster_id), _dptr(cluster_size), _dptr(demand), _dptr(score),
-                                  _dptr(section), _dptr(has_sharing), _dptr(workspace), ws_bytes, _stream(stream)))
+    _check(_lib.peek_clpm_signals(None if cache is None else cache.handle, n, _arg(tokens, "tokens", i32),
+                                  _arg(offsets, "offsets"), _arg(h, "h", i32, n), _arg(last_node, "last_node", i32, n),
+                                  _arg(match_len, "match_len", i32, n), int(threshold), int(tau), int(theta),
+                                  _arg(cluster_id, "cluster_id", i32, n), _arg(cluster_size, "cluster_size", i32, n),
+                                  _arg(demand, "demand", i32, _num_nodes(cache)), _arg(score, "score", torch.int64, n),
+                                  _arg(section, "section", i32, n), _arg(has_sharing, "has_sharing", i32, 1),
+                                  _arg(workspace, "workspace"), ws_bytes, _stream(stream)))
 
 
 def peek_evict_rank_workspace(num_nodes: int) -> int:
@@ -243,9 +280,12 @@ def peek_evict_rank_workspace(num_nodes: int) -> int:
 def peek_evict_rank(cache, demand, score, order, workspace, stream=None):
     """Eviction score int64[num_nodes] and victim order int32[num_nodes-1] from demand int32[num_nodes];
     torch tensors, score or order may be None."""
+    import torch
+    nn = _num_nodes(cache)
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
-    _check(_lib.peek_evict_rank(cache.handle, _dptr(demand), _dptr(score), _dptr(order), _dptr(workspace), ws_bytes,
-                                _stream(stream)))
+    _check(_lib.peek_evict_rank(cache.handle, _arg(demand, "demand", torch.int32, nn),
+                                _arg(score, "score", torch.int64, nn), _arg(order, "order", torch.int32, nn - 1),
+                                _arg(workspace, "workspace"), ws_bytes, _stream(stream)))
 
 
 class BlockTable:
@@ -294,9 +334,10 @@ def peek_block_table_free(table: BlockTable):
 
 def peek_block_lpm_batch(table, tokens, offsets, h, stream=None):
     """Hashed-block hit int32[n] of every prompt; tokens int32[*], offsets int64[n+1]: torch tensors on the device."""
-    n = int(offsets.shape[0]) - 1
-    _check(_lib.peek_block_lpm_batch(None if table is None else table.handle, n, _dptr(tokens), _dptr(offsets),
-                                     _dptr(h), _stream(stream)))
+    import torch
+    n = _queue_n(offsets)
+    _check(_lib.peek_block_lpm_batch(None if table is None else table.handle, n, _arg(tokens, "tokens", torch.int32),
+                                     _arg(offsets, "offsets"), _arg(h, "h", torch.int32, n), _stream(stream)))
 
 
 def peek_offline_order_workspace(n: int) -> int:
@@ -306,7 +347,9 @@ def peek_offline_order_workspace(n: int) -> int:
 def peek_offline_order(tokens, offsets, depth_limit: int, perm, workspace, stream=None):
     """PEEK-offline Phase 1 permutation int32[n] of the prompts' first depth_limit tokens; torch tensors on the
     device."""
-    n = int(offsets.shape[0]) - 1
+    import torch
+    n = _queue_n(offsets)
     ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
-    _check(_lib.peek_offline_order(n, _dptr(tokens), _dptr(offsets), int(depth_limit), _dptr(perm),
-                                   _dptr(workspace), ws_bytes, _stream(stream)))
+    _check(_lib.peek_offline_order(n, _arg(tokens, "tokens", torch.int32), _arg(offsets, "offsets"), int(depth_limit),
+                                   _arg(perm, "perm", torch.int32, n), _arg(workspace, "workspace"), ws_bytes,
+                                   _stream(stream)))

@@ -8,13 +8,15 @@ then demand and clusters, with device buffers allocated once up front.
 """
 from __future__ import annotations
 
+import ctypes
+
 import numpy as np
 import torch
 
+from . import _check, _lib, _stream
 from . import (Cache, peek_block_lpm_batch, peek_block_table_build, peek_cache_build, peek_offline_order,
                peek_offline_order_workspace, peek_cache_stats, peek_clpm_signals, peek_evict_rank,
-               peek_evict_rank_workspace, peek_lpm_batch, peek_queue_signals, peek_queue_signals_workspace,
-               peek_tree_from_sequences)
+               peek_evict_rank_workspace, peek_queue_signals_workspace, peek_tree_from_sequences)
 
 
 class HotPath:
@@ -59,17 +61,23 @@ class HotPath:
         self.d_sharing = torch.empty(1, dtype=torch.int32, device=dev)
         ws = peek_queue_signals_workspace(self.n, self.num_nodes)
         self.d_ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
+        # The step's C arguments, marshalled once: these buffers are the
+        # runner's own, of the types and sizes the entry points expect.
+        p = lambda t: ctypes.c_void_p(t.data_ptr())
+        self._queue_args = (self.cache.handle, self.n, p(self.d_tokens), p(self.d_offsets))
+        self._lpm_out = (p(self.d_h), p(self.d_last), p(self.d_m))
+        self._sig_last = p(self.d_last)
+        self._sig_out = (p(self.d_cid), p(self.d_csz), p(self.d_demand), p(self.d_ws), int(self.d_ws.numel()))
+        self._sig_m = p(self.d_m)
 
     def lpm(self, stream=None):
-        peek_lpm_batch(self.cache, self.d_tokens, self.d_offsets, self.block_size, self.d_h, self.d_last, self.d_m,
-                       stream=stream)
+        _check(_lib.peek_lpm_batch(*self._queue_args, self.block_size, *self._lpm_out, _stream(stream)))
 
     def signals(self, stream=None, anchored: bool = True):
         self._clpm_valid = False
         self._evict_valid = False
-        peek_queue_signals(self.cache, self.d_tokens, self.d_offsets, self.d_last,
-                           self.d_m if anchored else None, self.threshold, self.d_cid, self.d_csz,
-                           self.d_demand, self.d_ws, stream=stream)
+        _check(_lib.peek_queue_signals(*self._queue_args, self._sig_last, self._sig_m if anchored else None,
+                                       self.threshold, *self._sig_out, _stream(stream)))
 
     def clpm(self, tau: int, theta: int, stream=None, anchored: bool = True):
         """Clusters and demand plus cLPM's ancestor score, section and has_sharing."""

@@ -194,3 +194,26 @@ def test_workspace_grows_with_the_queue_and_the_cache():
     assert P.peek_queue_signals_workspace(2000, 10) > a
     assert P.peek_queue_signals_workspace(1000, 100000) > a
     assert P.peek_queue_signals_workspace(-1, 0) == 0
+
+
+def test_binding_checks_tensors_before_the_call():
+    """The binding refuses what the C entry points cannot check: element
+    type, contiguity and host-resident tensors (the first argument checked
+    here; the GPU tests cover the outputs)."""
+    torch = pytest.importorskip("torch")
+    import paper_2607_02525_amd as P
+
+    class NoCache:
+        handle = None
+
+    tok = torch.zeros(16, dtype=torch.int32)
+    off = torch.arange(0, 20, 4, dtype=torch.int64)
+    h = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(TypeError, match="offsets"):
+        P.peek_lpm_batch(NoCache(), tok, off.to(torch.int32), 4, h)
+    with pytest.raises(TypeError, match="tokens"):
+        P.peek_lpm_batch(NoCache(), tok.to(torch.int64), off, 4, h)
+    with pytest.raises(ValueError, match="contiguous"):
+        P.peek_block_lpm_batch(None, torch.zeros(32, dtype=torch.int32)[::2], off, h)
+    with pytest.raises(ValueError, match="device tensor"):
+        P.peek_offline_order(tok, off, 128, h, None)

@@ -617,3 +617,25 @@ def test_evict_rank_tree_shapes(shape, nn):
         torch.cuda.synchronize()
         assert np.array_equal(score.cpu().numpy(), e.score)
         assert np.array_equal(order.cpu().numpy()[:nn - 1], e.order)
+
+
+def test_binding_refuses_bad_output_tensors():
+    """Output tensors of the wrong type, too small or not contiguous are
+    refused before any launch."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    w = W.make("tiny", 42)
+    hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    n = w.n
+    with pytest.raises(TypeError, match="h must be"):
+        P.peek_lpm_batch(hp.cache, hp.d_tokens, hp.d_offsets, 16, torch.empty(n, dtype=torch.int64, device="cuda"))
+    with pytest.raises(ValueError, match="at least"):
+        P.peek_lpm_batch(hp.cache, hp.d_tokens, hp.d_offsets, 16, torch.empty(n - 1, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError, match="contiguous"):
+        P.peek_lpm_batch(hp.cache, hp.d_tokens, hp.d_offsets, 16,
+                         torch.empty(2 * n, dtype=torch.int32, device="cuda")[::2])
+    with pytest.raises(ValueError, match="demand"):
+        P.peek_evict_rank(hp.cache, torch.empty(hp.num_nodes - 1, dtype=torch.int32, device="cuda"), None, None, None)
+    hp.step()
+    assert_parity(w, hp.results(), O.run(w))
