@@ -27,7 +27,7 @@
 //
 // Kernel: one 64-lane wavefront per request. Each step covers 64 T tokens:
 // lane l compresses the T consecutive tokens [T l, T l + T) of the step
-// (T = 8 for B = 8, else 4, so a block spans B / T lanes), a sum
+// (T = 4 for B = 4, else 8, so a block spans B / T lanes), a sum
 // butterfly over a block's lanes completes its NH values, every lane
 // finishes its block's digest, an inclusive scan over the step's blocks adds
 // the chain, and the step's last block is probed (all of its blocks only
@@ -183,9 +183,10 @@ __device__ __forceinline__ bool block_stored(const uint64_t (&v)[SPL], uint64_t 
 
 // The walk. Lane l holds T consecutive tokens of each step (64 T tokens per
 // step); a block spans LPB = B / T lanes. With one lane per block the
-// position keys are compile-time constants. T = 8 for B = 8 and 4 otherwise
-// (measured: fatter steps hash more tokens past the first miss and load
-// less contiguously).
+// position keys are compile-time constants. T = 8 from B = 8 up (measured:
+// 512-token steps halve the dependent steps per request against T = 4; at
+// T = 16 the two extra 16-byte loads per lane are strided and more tokens
+// are hashed past the first miss).
 //
 // The table holds every full-block prefix of every cached path, so the
 // stored keys along a request's chain form a prefix of it: if a step's last
@@ -472,11 +473,11 @@ peek_status peek_block_lpm_batch(const peek_block_table* t, int32_t n, const int
     break;
     PEEK_BLOCK_CASE(2, 0)
     PEEK_BLOCK_CASE(3, 0)
-    PEEK_BLOCK_CASE(2, 2)
-    PEEK_BLOCK_CASE(2, 3)
-    PEEK_BLOCK_CASE(2, 4)
-    PEEK_BLOCK_CASE(2, 5)
-    PEEK_BLOCK_CASE(2, 6)
+    PEEK_BLOCK_CASE(3, 1)
+    PEEK_BLOCK_CASE(3, 2)
+    PEEK_BLOCK_CASE(3, 3)
+    PEEK_BLOCK_CASE(3, 4)
+    PEEK_BLOCK_CASE(3, 5)
 #undef PEEK_BLOCK_CASE
     default:
       return fail(PEEK_ERR_INVALID_ARGUMENT, "table has an unsupported block size %d", t->block_size);
