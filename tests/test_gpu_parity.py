@@ -639,3 +639,35 @@ def test_binding_refuses_bad_output_tensors():
         P.peek_evict_rank(hp.cache, torch.empty(hp.num_nodes - 1, dtype=torch.int32, device="cuda"), None, None, None)
     hp.step()
     assert_parity(w, hp.results(), O.run(w))
+
+
+def test_randomized_sweep():
+    """150 random queues and caches of varied shapes (sizes, vocabularies,
+    block sizes, thresholds, tau, theta, prompt lengths up to 3000 tokens,
+    caches given as sequences or as trees), each compared on every output."""
+    _hot()
+    rng = np.random.default_rng(2026)
+    for k in range(150):
+        seed = 5000 + k
+        kind = k % 4
+        if kind == 0:
+            w = W.random_case(seed, n=int(rng.integers(1, 3000)), n_cached=int(rng.integers(1, 200)),
+                              vocab=int(rng.choice([2, 3, 5, 50, 32000])), max_len=int(rng.integers(1, 600)),
+                              block_size=int(rng.choice([1, 2, 4, 8, 16, 32, 64, 128, 256])),
+                              threshold=int(rng.integers(1, 40)))
+        elif kind == 1:
+            w = W.random_tree_case(seed, n_nodes=int(rng.integers(2, 20000)), n=int(rng.integers(1, 2500)),
+                                   vocab=int(rng.choice([3, 8, 40, 300])), max_edge=int(rng.integers(1, 30)),
+                                   block_size=int(rng.choice([2, 4, 8, 16, 32, 64])),
+                                   threshold=int(rng.integers(1, 10)))
+        elif kind == 2:
+            w = W.random_case(seed, n=int(rng.integers(2000, 9000)), n_cached=int(rng.integers(5, 60)), vocab=3,
+                              max_len=int(rng.integers(50, 400)), block_size=int(rng.choice([4, 8, 16])),
+                              threshold=int(rng.integers(2, 64)))
+        else:
+            w = W.random_case(seed, n=int(rng.integers(1, 400)), n_cached=int(rng.integers(1, 40)), vocab=3,
+                              max_len=int(rng.integers(500, 3000)), block_size=int(rng.choice([4, 16, 64])),
+                              threshold=int(rng.integers(1, 8)))
+        w.tau = int(rng.integers(-1, 64))
+        w.theta = int(rng.choice([0, 1, 2, 5, 32, 200]))
+        run_and_compare(w)
