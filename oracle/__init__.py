@@ -113,9 +113,13 @@ class Tree:
         return cls(h)
 
     def __del__(self):
-        if getattr(self, "_h", None):
-            _load().oracle_tree_free(self._h)
-            self._h = None
+        # at interpreter exit the module's globals may already be gone
+        try:
+            if getattr(self, "_h", None):
+                _load().oracle_tree_free(self._h)
+                self._h = None
+        except Exception:
+            pass
 
     @property
     def num_nodes(self) -> int:
