@@ -31,12 +31,11 @@
  *  - Debugging aid: with the environment variable PEEK_VALIDATE set (to
  *    anything but 0), peek_lpm_batch, peek_queue_signals, peek_clpm_signals,
  *    peek_offline_order and peek_block_lpm_batch first check their device
- *    inputs on the device
- *    (offsets non-decreasing from >= 0, prompt lengths < 2^31, last nodes
- *    inside the cache, match lengths inside their prompts) and return
- *    INVALID_ARGUMENT before any other work if one fails. The check adds a
- *    small allocation, a launch and a stream synchronization per call, so it
- *    is not for use under graph capture.
+ *    inputs on the device (offsets non-decreasing from >= 0, prompt lengths
+ *    < 2^31, last nodes inside the cache, match lengths inside their
+ *    prompts) and return INVALID_ARGUMENT before any other work if one
+ *    fails. The check adds a small allocation, a launch and a stream
+ *    synchronization per call, so it is not for use under graph capture.
  */
 #ifndef PEEK_H
 #define PEEK_H
