@@ -360,6 +360,8 @@ def main():
         "signals_ms": round(float(sig_ms.mean()), 4),
         "clpm_signals_ms": round(float(np.mean(clpm_ms)), 4),
         "evict_rank_ms": round(float(np.mean(evict_ms)), 4),
+        # algorithmic bytes per cached node: demand 4, record 32, score 8, order 4
+        "evict_rank_gbs": round(48 * hp.num_nodes / (float(np.mean(evict_ms)) / 1e3) / 1e9, 1),
         "block_lpm_ms": round(float(np.mean(block_ms)), 4),
         "block_lpm_gbs": round(block_bytes / (float(np.mean(block_ms)) / 1e3) / 1e9, 1),
         "block_table_build_s": round(table_s, 2),
