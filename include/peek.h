@@ -175,10 +175,11 @@ peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_
  * peek_queue_signals_workspace(n, num_nodes) bytes, num_nodes = 0 without a
  * cache); apart from a few pinned host words allocated once per calling
  * thread the library allocates nothing here. The cluster pass refines a sort
- * in rounds: it runs a few rounds and the final stage, then synchronizes
- * `stream` to read device flags, and synchronizes once more per further
- * round when the queue needs more; this call returns after the stream has
- * finished its work. threshold >= 1.
+ * in rounds: it runs a few rounds and the final stage, then waits for the
+ * device flags that one last small kernel stores into pinned host memory
+ * (polling; after 20 ms it synchronizes `stream` instead), and synchronizes
+ * `stream` once more per further round when the queue needs more. When the
+ * call returns, every kernel it launched has run. threshold >= 1.
  * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
  * ---------------------------------------------------------------------- */
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes);

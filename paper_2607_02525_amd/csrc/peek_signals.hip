@@ -34,6 +34,7 @@
 //     equal keys form the next segment at depth d+l+1. The LCP across a new
 //     boundary is d plus the smaller l. Each prompt byte is read about once.
 #include <algorithm>
+#include <chrono>
 
 #include "peek_compare.h"
 #include "peek_internal.h"
@@ -1167,13 +1168,41 @@ void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
 }
 
-// Pinned host words the flag pairs are read into (one set per host thread,
-// kept for the life of the process).
+// Pinned, coherent host words the flag pairs are published into, followed
+// by a sequence word (one set per host thread, kept for the life of the
+// process).
+constexpr int kHostWords = 2 * kFlagPairs + 1;
 int32_t* host_flags() {
   thread_local int32_t* p = nullptr;
-  if (p == nullptr && hipHostMalloc((void**)&p, sizeof(int32_t) * 2 * kFlagPairs, hipHostMallocDefault) != hipSuccess)
+  if (p == nullptr &&
+      hipHostMalloc((void**)&p, sizeof(int32_t) * kHostWords, hipHostMallocCoherent | hipHostMallocMapped) != hipSuccess)
     p = nullptr;
   return p;
+}
+
+// The first `count` flag words into coherent host memory, then the
+// sequence number `seq` after them; the host reads the flags once it sees
+// `seq`. Stores are system-scope vector stores.
+__global__ void k_publish_flags(const int32_t* __restrict__ flags, int32_t count, int32_t* host, int32_t seq) {
+  const int t = threadIdx.x;
+  if (t < count) __hip_atomic_store(host + t, flags[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __syncthreads();
+  if (t == 0) __hip_atomic_store(host + 2 * kFlagPairs, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Waits until the stream has published `seq`: polls the host word for a
+// short while (a publish lands within microseconds of the work before it),
+// then falls back to synchronizing the stream, which also reports a failed
+// launch.
+hipError_t wait_published(const int32_t* host, int32_t seq, hipStream_t st) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t spin = 0;; ++spin) {
+    if (__atomic_load_n(host + 2 * kFlagPairs, __ATOMIC_ACQUIRE) == seq) return hipSuccess;
+    if ((spin & 255) == 255 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
+  }
+  const hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return e;
+  return __atomic_load_n(host + 2 * kFlagPairs, __ATOMIC_ACQUIRE) == seq ? hipSuccess : hipErrorUnknown;
 }
 
 }  // namespace
@@ -1353,8 +1382,11 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   };
 
   fixed(st);
-  PEEK_HIP_TRY(hipMemcpyAsync(hf, flags, sizeof(int32_t) * 2 * (kSpeculativeRounds + 1), hipMemcpyDeviceToHost, st));
-  PEEK_HIP_TRY(hipStreamSynchronize(st));
+  thread_local int32_t seq = 0;
+  seq = seq == INT32_MAX ? 1 : seq + 1;
+  hipLaunchKernelGGL(k_publish_flags, dim3(1), dim3(kWave), 0, st, flags, 2 * (kSpeculativeRounds + 1), hf, seq);
+  PEEK_HIP_TRY(hipGetLastError());
+  PEEK_HIP_TRY(wait_published(hf, seq, st));
   int64_t r = 0;
   // round 1 ran whatever its segment sizes; a later one only without a
   // segment beyond the segment sort
