@@ -671,3 +671,16 @@ def test_randomized_sweep():
         w.tau = int(rng.integers(-1, 64))
         w.theta = int(rng.choice([0, 1, 2, 5, 32, 200]))
         run_and_compare(w)
+
+
+def test_large_queue_big_sort_tiles():
+    """300000 short prompts: the cluster and offline sorts reach 2^19
+    elements, where the merge sort switches to 1024-element tiles."""
+    w = W.random_case(11, n=300000, n_cached=60, vocab=3, max_len=24, block_size=4, threshold=3)
+    w.tau = 2
+    w.theta = 5
+    hp, res, s = run_and_compare(w)
+    hp.clpm(w.tau, w.theta)
+    got = hp.results()
+    assert np.array_equal(got["score"], s.clpm.score)
+    assert np.array_equal(got["section"], s.clpm.section)
