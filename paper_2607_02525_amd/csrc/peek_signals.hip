@@ -1168,16 +1168,28 @@ void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
 }
 
-// Pinned, coherent host words the flag pairs are published into, followed
-// by a sequence word (one set per host thread, kept for the life of the
-// process).
+// Pinned host words the flag pairs are read into, followed by a sequence
+// word (one set per host thread, kept for the life of the process). They
+// are coherent, mapped memory that a kernel can publish into; where that
+// cannot be had, plain pinned memory that the flags are copied into.
 constexpr int kHostWords = 2 * kFlagPairs + 1;
-int32_t* host_flags() {
-  thread_local int32_t* p = nullptr;
-  if (p == nullptr &&
-      hipHostMalloc((void**)&p, sizeof(int32_t) * kHostWords, hipHostMallocCoherent | hipHostMallocMapped) != hipSuccess)
-    p = nullptr;
-  return p;
+struct HostFlags {
+  int32_t* p;
+  bool coherent;
+};
+HostFlags host_flags() {
+  thread_local HostFlags h{nullptr, false};
+  if (h.p == nullptr) {
+    if (hipHostMalloc((void**)&h.p, sizeof(int32_t) * kHostWords, hipHostMallocCoherent | hipHostMallocMapped) ==
+        hipSuccess) {
+      h.coherent = true;
+    } else {
+      (void)hipGetLastError();
+      h.coherent = false;
+      if (hipHostMalloc((void**)&h.p, sizeof(int32_t) * kHostWords, hipHostMallocDefault) != hipSuccess) h.p = nullptr;
+    }
+  }
+  return h;
 }
 
 // The first `count` flag words into coherent host memory, then the
@@ -1255,7 +1267,8 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
   int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
-  int32_t* hf = host_flags();
+  const HostFlags hflags = host_flags();
+  int32_t* hf = hflags.p;
   if (hf == nullptr) return fail(PEEK_ERR_OUT_OF_MEMORY, "pinned host flag buffer could not be allocated");
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
   ClElem* el = el_a;
@@ -1382,11 +1395,17 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   };
 
   fixed(st);
-  thread_local int32_t seq = 0;
-  seq = seq == INT32_MAX ? 1 : seq + 1;
-  hipLaunchKernelGGL(k_publish_flags, dim3(1), dim3(kWave), 0, st, flags, 2 * (kSpeculativeRounds + 1), hf, seq);
-  PEEK_HIP_TRY(hipGetLastError());
-  PEEK_HIP_TRY(wait_published(hf, seq, st));
+  if (hflags.coherent) {
+    thread_local int32_t seq = 0;
+    seq = seq == INT32_MAX ? 1 : seq + 1;
+    hipLaunchKernelGGL(k_publish_flags, dim3(1), dim3(kWave), 0, st, flags, 2 * (kSpeculativeRounds + 1), hf, seq);
+    PEEK_HIP_TRY(hipGetLastError());
+    PEEK_HIP_TRY(wait_published(hf, seq, st));
+  } else {
+    PEEK_HIP_TRY(hipMemcpyAsync(hf, flags, sizeof(int32_t) * 2 * (kSpeculativeRounds + 1), hipMemcpyDeviceToHost,
+                                st));
+    PEEK_HIP_TRY(hipStreamSynchronize(st));
+  }
   int64_t r = 0;
   // round 1 ran whatever its segment sizes; a later one only without a
   // segment beyond the segment sort
