@@ -301,7 +301,7 @@ peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const
  * Requests that share a truncated prefix are therefore contiguous in d_perm.
  * No cache is involved (the paper's regime is a cold cache). depth_limit >= 0
  * (0: arrival order); n < 2^30. Scratch comes only from d_workspace (device, 256-byte
- * aligned, at least peek_offline_order_workspace(n) bytes). Synchronizes
+ * aligned, at least peek_offline_order_workspace(n) bytes). Waits for
  * `stream` once or a few times, as peek_queue_signals does.
  * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY (pinned host
  * words), DEVICE.
