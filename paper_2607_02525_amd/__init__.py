@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpeek.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_02525_amd.build` "
+    raise ImportError(f"{LIB_PATH} is not built; run `python paper_2607_02525_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
 _lib = ctypes.CDLL(LIB_PATH)

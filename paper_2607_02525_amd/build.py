@@ -1,6 +1,6 @@
 """Builds libpeek.so for gfx950 in-tree with hipcc.
 
-Usage: python -m paper_2607_02525_amd.build
+Usage: python paper_2607_02525_amd/build.py
 """
 from __future__ import annotations
 
