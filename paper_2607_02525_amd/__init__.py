@@ -22,6 +22,12 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python paper_2607_02525_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
+# torch's HIP runtime goes in first: libpeek.so then binds to that same
+# libamdhip64.so.7 (same soname) instead of loading the system copy beside
+# it. Two HIP runtimes in one process do not share the device: the second
+# to initialise reports no device.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 PEEK_OK = 0

@@ -217,3 +217,13 @@ def test_binding_checks_tensors_before_the_call():
         P.peek_block_lpm_batch(None, torch.zeros(32, dtype=torch.int32)[::2], off, h)
     with pytest.raises(ValueError, match="device tensor"):
         P.peek_offline_order(tok, off, 128, h, None)
+
+
+def test_one_hip_runtime_per_process():
+    # the package binds libpeek.so to torch's HIP runtime; a second runtime
+    # loaded beside it finds no device on a GPU machine
+    code = ("import paper_2607_02525_amd\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n")
+    out = subprocess.run(["python", "-c", code], capture_output=True, text=True, cwd=ROOT, check=True).stdout
+    assert out.strip() == "1"
