@@ -21,6 +21,13 @@
 //     in-block prefix/suffix maxima and, inside one block, a sparse table in
 //     a wave's registers. The sort is the library's merge sort below 2^19
 //     nodes and a radix sort above (below).
+//  3. From 2^19 nodes up the ties on K need no sort. K.id is always a leaf
+//     (a child's key exceeds its parent's), and the nodes that share it are
+//     a contiguous run of that leaf's ancestor chain. Laying the nodes out
+//     by (K.id ascending, id descending) therefore takes one scan: a leaf's
+//     run starts after the runs of all smaller leaves, and a node sits
+//     level(K.id) - level(node) places into its run. A stable radix sort by
+//     K.e alone then yields the victim order.
 #include <algorithm>
 
 #include "peek_internal.h"
@@ -42,18 +49,23 @@ __device__ __forceinline__ bool ekey_less(const EKey& a, const EKey& b) {
 }
 __device__ __forceinline__ EKey ekey_max(const EKey& a, const EKey& b) { return ekey_less(a, b) ? b : a; }
 
-// One jump: fold in the chain segment that ends at the current link.
+// One jump: fold in the chain segment that ends at the current link. With
+// Dl, also the number of links from c to its current link (after the last
+// round: c's level, the edges from the root to c).
 __global__ void k_evict_jump(int32_t nn, const int64_t* __restrict__ E, const int32_t* __restrict__ J,
-                             int64_t* __restrict__ E2, int32_t* __restrict__ J2) {
+                             int64_t* __restrict__ E2, int32_t* __restrict__ J2, const int32_t* __restrict__ Dl,
+                             int32_t* __restrict__ Dl2) {
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= nn) return;
   const int32_t j = J[c];
   if (j < 0) {
     E2[c] = E[c];
     J2[c] = -1;
+    if (Dl) Dl2[c] = Dl[c];
   } else {
     E2[c] = max(E[c], E[j]);
     J2[c] = J[j];
+    if (Dl) Dl2[c] = Dl[c] + Dl[j];
   }
 }
 
@@ -148,14 +160,14 @@ __device__ __forceinline__ EKey subtree_max(const NodeRec* __restrict__ nodes, c
 }
 
 // From 2^19 nodes up the victim order is a stable least-significant-digit
-// radix sort of the nodes by K: element i of its input is node nn - 1 - i,
-// so nodes that share K keep descending ids. The key is K.id (4 byte
-// digits, least significant first) then K.e (8 digits; E >= 0 since the
-// root, at depth 0, is on every chain). Digits the host can rule out (K.id <
-// nn, K.e < 2^31 * max depth) get no pass. The key pass also ORs and ANDs
-// all keys: a digit on which they agree is the same for every node, and its
-// pass returns at once. The buffer that holds the data before pass p follows
-// from the parity of the earlier passes that moved it.
+// radix sort of the nodes by K.e (8 byte digits; E >= 0 since the root, at
+// depth 0, is on every chain) over the chain placement, which already
+// orders them by (K.id, id descending). Digits the host can rule out (K.e <
+// 2^31 * max depth) get no pass. The key pass also ORs and ANDs all keys: a
+// digit on which they agree is the same for every node, and its pass
+// returns at once. The buffer that holds the data before pass p follows
+// from the parity of the earlier passes that moved it. (Digits 0-3, the
+// bytes of K.id, are kept for the general key but never move here.)
 struct VElem {
   uint64_t ke;   // K.e
   uint32_t kid;  // K.id
@@ -186,13 +198,15 @@ constexpr int kRWaves = kRThreads / kWave;
 constexpr int64_t kKeyBlocks = 1 << 16;   // grid cap of the key pass (grid-stride beyond it)
 
 __global__ void k_evict_init(const NodeRec* __restrict__ nodes, const int32_t* __restrict__ demand, int32_t nn,
-                             int64_t* __restrict__ E, int32_t* __restrict__ J, uint64_t* __restrict__ orand) {
+                             int64_t* __restrict__ E, int32_t* __restrict__ J, int32_t* __restrict__ Dl,
+                             uint64_t* __restrict__ orand) {
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
   if (orand != nullptr && c < 4 * kOrCopies) orand[c] = (c & 1) ? ~uint64_t(0) : 0;
   if (c >= nn) return;
   const NodeRec r = nodes[c];
   E[c] = (int64_t)demand[c] * r.depth;
   J[c] = r.parent;
+  if (Dl) Dl[c] = r.parent >= 0 ? 1 : 0;
 }
 
 // The OR/AND copies folded into sh[4] (the first wave loads them, every
@@ -235,7 +249,9 @@ __device__ __forceinline__ EKey shfl_key(const EKey& k, int src) {
   return EKey{__shfl(k.e, src), __shfl(k.id, src), 0};
 }
 
-// Sort input, plus the OR and AND of all keys. A wave takes one 64-node
+// Sort input, plus the OR and AND of all keys. With `chain` the keys stay
+// in node order (the chain placement reorders them) and K.id takes no part
+// in the OR and AND, so no radix pass sorts on it. A wave takes one 64-node
 // block: K of a node whose subtree ends inside the block comes from a sparse
 // table over the block held in registers (level k of lane l = max over
 // [l, l + 2^k)), the rest from the in-block prefix/suffix maxima and the
@@ -243,7 +259,8 @@ __device__ __forceinline__ EKey shfl_key(const EKey& k, int src) {
 __global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ nodes, const int64_t* __restrict__ E,
                                                     const EKey* __restrict__ pre, const EKey* __restrict__ suf,
                                                     const EKey* __restrict__ blk, int32_t nn, int32_t nb,
-                                                    VElem* __restrict__ out, uint64_t* __restrict__ orand) {
+                                                    VElem* __restrict__ out, uint64_t* __restrict__ orand,
+                                                    int32_t chain) {
   __shared__ unsigned long long red[4];
   if (threadIdx.x < 4) red[threadIdx.x] = (threadIdx.x & 1) ? ~0ull : 0ull;
   __syncthreads();
@@ -287,11 +304,12 @@ __global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ 
           k = ekey_max(k, ekey_max(blk[(int64_t)l2 * nb + x], blk[(int64_t)l2 * nb + y - (1 << l2) + 1]));
         }
       }
-      out[nn - 1 - c] = VElem{(uint64_t)k.e, (uint32_t)k.id, c};
+      out[chain ? c : nn - 1 - c] = VElem{(uint64_t)k.e, (uint32_t)k.id, c};
       or_e |= (uint64_t)k.e;
       and_e &= (uint64_t)k.e;
-      or_i |= (uint32_t)k.id;
-      and_i &= (uint32_t)k.id;
+      const uint32_t id_bits = chain ? 0u : (uint32_t)k.id;
+      or_i |= id_bits;
+      and_i &= id_bits;
     }
   }
   for (int d = 1; d < kWave; d <<= 1) {
@@ -313,6 +331,88 @@ __global__ __launch_bounds__(256) void k_order_keys(const NodeRec* __restrict__ 
     atomicOr((unsigned long long*)&orand[2], red[2]);
     atomicAnd((unsigned long long*)&orand[3], red[3]);
   }
+}
+
+// Chain placement (radix path). run_len[l] for a leaf l is the number of
+// nodes whose K.id is l: the run from l up to its topmost such ancestor
+// (the node whose parent has another K.id, or the root). An inner node's
+// slot is 0. Every slot has one writer: an inner node writes its own, a
+// run's top node its leaf's.
+__global__ void k_chain_len(const NodeRec* __restrict__ nodes, const VElem* __restrict__ keys,
+                            const int32_t* __restrict__ level, int32_t nn, int32_t* __restrict__ run_len) {
+  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= nn) return;
+  const NodeRec r = nodes[c];
+  const uint32_t l = keys[c].kid;
+  if (r.subtree_end != c + 1) run_len[c] = 0;
+  const bool top = r.parent < 0 || keys[r.parent].kid != l;
+  if (top && l < (uint32_t)nn) run_len[l] = level[l] - level[c] + 1;
+}
+
+constexpr int kChainScan = 1024;   // positions per block of the run-length scan
+
+// Exclusive scan of run_len inside each block of kChainScan slots, and the
+// block totals.
+__global__ __launch_bounds__(kChainScan) void k_chain_scan(const int32_t* __restrict__ run_len, int32_t nn,
+                                                           int32_t* __restrict__ start, int32_t* __restrict__ part) {
+  __shared__ int32_t wsum[kChainScan / kWave];
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int32_t i = (int32_t)blockIdx.x * kChainScan + t;
+  const int32_t mine = i < nn ? run_len[i] : 0;
+  int32_t v = mine;
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int32_t o = __shfl(v, lane >= d ? lane - d : lane);
+    if (lane >= d) v += o;
+  }
+  if (lane == kWave - 1) wsum[wave] = v;
+  __syncthreads();
+  int32_t before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  v += before;
+  if (i < nn) start[i] = v - mine;
+  if (t == kChainScan - 1) part[blockIdx.x] = v;
+}
+
+// Exclusive scan of the block totals in place (one workgroup, chunk by
+// chunk).
+__global__ __launch_bounds__(kChainScan) void k_chain_parts(int32_t* __restrict__ part, int32_t nparts) {
+  __shared__ int32_t wsum[kChainScan / kWave];
+  __shared__ int32_t carry;
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  if (t == 0) carry = 0;
+  __syncthreads();
+  for (int32_t j0 = 0; j0 < nparts; j0 += kChainScan) {
+    const int32_t j = j0 + t;
+    const int32_t mine = j < nparts ? part[j] : 0;
+    int32_t v = mine;
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int32_t o = __shfl(v, lane >= d ? lane - d : lane);
+      if (lane >= d) v += o;
+    }
+    if (lane == kWave - 1) wsum[wave] = v;
+    __syncthreads();
+    int32_t before = carry;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    v += before;
+    if (j < nparts) part[j] = v - mine;
+    __syncthreads();
+    if (t == kChainScan - 1) carry = v;
+    __syncthreads();
+  }
+}
+
+// Node c to place start(K.id) + level(K.id) - level(c): the nodes ordered by
+// (K.id ascending, id descending), the radix sort's input.
+__global__ void k_chain_place(const VElem* __restrict__ keys, const int32_t* __restrict__ level,
+                              const int32_t* __restrict__ start, const int32_t* __restrict__ part, int32_t nn,
+                              VElem* __restrict__ out) {
+  const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= nn) return;
+  const VElem v = keys[c];
+  const uint32_t l = v.kid;
+  if (l >= (uint32_t)nn) return;
+  const int64_t pos = (int64_t)start[l] + part[l / kChainScan] + level[l] - level[c];
+  if (pos >= 0 && pos < nn) out[pos] = v;
 }
 
 // Lanes of the wave whose digit equals this lane's (among the lanes in m).
@@ -503,7 +603,9 @@ int levels_for(int64_t nb) {
 }
 
 struct ELayout {
-  size_t e_a, e_b, j_a, j_b, pre, suf, blk, v_a, v_b, v_c, orand, counts, offs, tot, total;
+  size_t e_a, e_b, j_a, j_b, pre, suf, blk, v_a, v_b, v_c, orand, counts, offs, tot, lv_a, lv_b, run, start, part,
+      total;
+  int32_t nparts;
   size_t nv;
   int32_t nb;
   int32_t tiles;
@@ -543,6 +645,14 @@ ELayout elayout(int64_t nn) {
   L.counts = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
   L.offs = take(sizeof(uint32_t) * kRadix * (size_t)L.tiles);
   L.tot = take(sizeof(uint32_t) * kRadix);
+  // chain placement (radix path only)
+  const bool radix = (int64_t)n >= kRadixMin;
+  L.nparts = (int32_t)((n + kChainScan - 1) / kChainScan);
+  L.lv_a = take(radix ? sizeof(int32_t) * n : 0);
+  L.lv_b = take(radix ? sizeof(int32_t) * n : 0);
+  L.run = take(radix ? sizeof(int32_t) * n : 0);
+  L.start = take(radix ? sizeof(int32_t) * n : 0);
+  L.part = take(radix ? sizeof(int32_t) * (size_t)L.nparts : 0);
   L.total = o;
   return L;
 }
@@ -565,10 +675,13 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
   const NodeRec* nodes = c->tree.nodes;
   const bool ordered = order != nullptr && nn > 1;
   RadixState rs{nullptr, nullptr, nullptr, nullptr, 0};
-  // digits that can differ: bytes of K.id < nn, bytes of K.e < 2^31 * max depth
+  const bool radix = nn >= kRadixMin;
+  // levels ride along the pointer jumping when the chain placement needs them
+  int32_t* Dl = ordered && radix ? (int32_t*)(w + L.lv_a) : nullptr;
+  int32_t* Dl2 = ordered && radix ? (int32_t*)(w + L.lv_b) : nullptr;
+  // digits that can differ: bytes of K.e < 2^31 * max depth (the chain
+  // placement settles K.id)
   uint32_t live = 0;
-  for (int p = 0; p < 4; ++p)
-    if (((uint64_t)(nn - 1) >> (8 * p)) != 0) live |= 1u << p;
   const uint64_t e_bound = (uint64_t)INT32_MAX * (uint64_t)std::max<int64_t>(c->max_depth, 1);
   for (int p = 0; p < 8; ++p)
     if ((e_bound >> (8 * p)) != 0) live |= 1u << (4 + p);
@@ -577,12 +690,13 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
                     (uint32_t*)(w + L.tot), L.tiles};
   }
   hipLaunchKernelGGL(k_evict_init, dim3(blocks_of(std::max<int64_t>(nn, 4 * kOrCopies))), dim3(256), 0, st, nodes,
-                     demand, nn, E, J, rs.orand);
+                     demand, nn, E, J, Dl, rs.orand);
   // ceil(log2(levels + 1)) rounds cover the longest chain (levels + 1 nodes)
   for (int64_t span = 1; span < (int64_t)c->max_level + 1; span <<= 1) {
-    hipLaunchKernelGGL(k_evict_jump, dim3(blocks_of(nn)), dim3(256), 0, st, nn, E, J, E2, J2);
+    hipLaunchKernelGGL(k_evict_jump, dim3(blocks_of(nn)), dim3(256), 0, st, nn, E, J, E2, J2, Dl, Dl2);
     std::swap(E, E2);
     std::swap(J, J2);
+    std::swap(Dl, Dl2);
   }
   EKey* pre = (EKey*)(w + L.pre);
   EKey* suf = (EKey*)(w + L.suf);
@@ -596,11 +710,18 @@ peek_status run_evict(const peek_cache* c, const int32_t* demand, int64_t* score
     VElem* va = (VElem*)(w + L.v_a);
     VElem* vb = (VElem*)(w + L.v_b);
     hipLaunchKernelGGL(k_order_keys, dim3((unsigned)std::min<int64_t>(blocks_of(nn), kKeyBlocks)), dim3(256), 0, st,
-                       nodes, E, pre, suf, blk, nn, L.nb, va, rs.orand);
-    if (nn < kRadixMin) {
+                       nodes, E, pre, suf, blk, nn, L.nb, radix ? vb : va, rs.orand, (int32_t)radix);
+    if (!radix) {
       const VElem* sorted = msort::sort_from(PaddedKeys{va, nn}, vb, (VElem*)(w + L.v_c), L.nv, VLess{}, st);
       hipLaunchKernelGGL(k_evict_out, dim3(blocks_of(nn)), dim3(256), 0, st, nn, sorted, sorted, nullptr, order);
     } else {
+      int32_t* run = (int32_t*)(w + L.run);
+      int32_t* start = (int32_t*)(w + L.start);
+      int32_t* part = (int32_t*)(w + L.part);
+      hipLaunchKernelGGL(k_chain_len, dim3(blocks_of(nn)), dim3(256), 0, st, nodes, vb, Dl, nn, run);
+      hipLaunchKernelGGL(k_chain_scan, dim3((unsigned)L.nparts), dim3(kChainScan), 0, st, run, nn, start, part);
+      hipLaunchKernelGGL(k_chain_parts, dim3(1), dim3(kChainScan), 0, st, part, L.nparts);
+      hipLaunchKernelGGL(k_chain_place, dim3(blocks_of(nn)), dim3(256), 0, st, vb, Dl, start, part, nn, va);
       for (int p = 0; p < kDigits; ++p) {
         if (((live >> p) & 1u) == 0) continue;
         hipLaunchKernelGGL(k_radix_count, dim3((unsigned)L.tiles), dim3(kRThreads), 0, st, va, vb, nn, p, rs);
