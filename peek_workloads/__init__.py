@@ -65,7 +65,7 @@ class Workload:
 
 
 _TAGS = {"tiny": 1, "rag": 2, "agentic": 3, "nosharing": 4, "scale": 5,
-         "random": 6, "randtree": 7}
+         "random": 6, "randtree": 7, "caterpillar": 8}
 
 
 def _rng(seed: int, tag: str) -> np.random.Generator:
@@ -421,12 +421,47 @@ def make_scale(seed: int = 42, n: int = 65536, n_covered: int = 77,
                           "doc_of_rag": live_docs, "doc_len": doc_len, "sys_len": sys_len})
 
 
+def make_caterpillar(seed: int = 42, n: int = 4096) -> Workload:
+    """A deep-branching queue: two spines of shared tokens, each with n/2
+    prompts hanging off it, where prompt i of a spine follows the spine for
+    i tokens and then leaves it (so the pending tree is a caterpillar with a
+    branch node at every depth), and the shallowest leaver is the longest
+    prompt (prompt i is 2n - i + 17 tokens long). The cache holds the first
+    n/4 tokens of spine B only, so half the queue branches below a cached
+    node and half from the root. Spine tokens are drawn from the lower half
+    of the vocabulary, leave tokens from the upper half. Arrival order is a
+    seeded shuffle."""
+    rng = _rng(seed, "caterpillar")
+    V = VOCAB_LARGE
+    half = n // 2
+    depth = 2 * n + 32
+    spines = [rng.integers(0, V // 2, size=depth, dtype=np.int32) for _ in range(2)]
+    spines[1][0] = (int(spines[0][0]) + 1) % (V // 2)     # the two spines differ at their first token
+    prompts = []
+    for s in range(2):
+        for j in range(n - half if s == 0 else half):
+            i = j + 1                                      # leaves after i tokens
+            L = 2 * n - i + 17
+            p = np.empty(L, dtype=np.int32)
+            p[:i] = spines[s][:i]
+            p[i] = int(rng.integers(V // 2, V))
+            p[i + 1:] = rng.integers(0, V, size=L - i - 1, dtype=np.int32)
+            prompts.append(p)
+    order = rng.permutation(len(prompts))
+    tok, off = pack([prompts[k] for k in order])
+    ctok, coff = pack([spines[1][:block_floor(n // 4)]])
+    return Workload("caterpillar", seed, tok, off, 16, 256, cache_sequences=(ctok, coff),
+                    meta={"spine_of": np.array([0 if k < n - half else 1 for k in order]),
+                          "leave_at": np.array([(k if k < n - half else k - (n - half)) + 1 for k in order])})
+
+
 CONFIGS = {
     "tiny": make_tiny,
     "rag": make_rag,
     "agentic": make_agentic,
     "nosharing": make_nosharing,
     "scale": make_scale,
+    "caterpillar": make_caterpillar,
 }
 
 

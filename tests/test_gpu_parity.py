@@ -139,8 +139,9 @@ def test_configs_bit_exact(name, seed):
     checks.check_demand(w.n, parent, res["last_node"], res["demand"])
 
 
-def test_scale_bit_exact_full_size():
-    w = W.make("scale", 42)
+@pytest.mark.parametrize("seed", W.PAPER_SEEDS)
+def test_scale_bit_exact_full_size(seed):
+    w = W.make("scale", seed)
     hp, res, s = run_and_compare(w, repeat=2, block_sample=3000)
     parent, depth, _, _ = s.tree.export()
     checks.check_lpm(w, parent, depth, res["match_len"], res["h"], res["last_node"])
@@ -221,6 +222,15 @@ def test_deep_chain_beyond_64k_tokens():
     cached = [long[:c] for c in cuts]
     prompts = [long[:69000], long[:70000], long[:66000] + [5], long[:100]]
     run_and_compare(_w(prompts, cached=cached, T=256))
+
+
+@pytest.mark.parametrize("seed", W.PAPER_SEEDS)
+def test_caterpillar_deep_branching(seed):
+    # a pending tree with a branch node at every depth along two spines of
+    # 2048 prompts each, where the longest prompt leaves its spine first
+    w = W.make("caterpillar", seed)
+    hp, res, s = run_and_compare(w)
+    checks.check_clusters(w, res["cluster_id"], res["cluster_size"])
 
 
 def test_many_requests_not_multiple_of_the_block():

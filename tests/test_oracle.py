@@ -410,7 +410,6 @@ def test_invariants_hold_on_oracle_outputs(name, seed):
     checks.check_clpm(w, s.lpm.h, s.clpm.score, s.clpm.section, s.clpm.has_sharing, seed=seed)
 
 
-@pytest.mark.slow
 def test_scale_invariants_and_closed_forms():
     w, s = _run("scale", 42)
     parent, depth, _, _ = s.tree.export()
@@ -426,3 +425,39 @@ def test_scale_invariants_and_closed_forms():
     assert np.all((m[cov] == base[cov]) | (m[cov] == base[cov] + 1))
     assert np.all(m[~cov] == 1024)
     assert 0.8e6 <= s.tree.num_nodes <= 1.2e6 and 160e6 <= s.tree.num_edge_tokens <= 240e6
+
+
+@pytest.mark.parametrize("seed", W.PAPER_SEEDS)
+def test_caterpillar_closed_forms(seed):
+    # Prompt i of a spine follows the spine for i tokens, then leaves it with a
+    # token the spine never uses. Two prompts of one spine leaving at i < j
+    # therefore share exactly i tokens, and prompts of different spines share
+    # none. So share_i = i except for the deepest leaver (share = i_max - 1);
+    # the cluster of the leaver at i holds every prompt of its spine leaving
+    # at i or deeper, and each cluster is its own id except the last two
+    # leavers, which share one node at depth i_max - 1 (Sec. 3.1 cluster =
+    # deepest pending node with count >= 2). Only spine B is cached, for its
+    # first n/4 tokens, so m = min(i, n/4) there and 0 on spine A.
+    w, s = _run("caterpillar", seed)
+    spine, i = w.meta["spine_of"], w.meta["leave_at"]
+    n = w.n
+    for sp in (0, 1):
+        on = spine == sp
+        imax = int(i[on].max())
+        share = np.where(i[on] == imax, imax - 1, i[on])
+        np.testing.assert_array_equal(s.clusters.share[on], share)
+        expect_size = np.where(share >= w.threshold, imax - np.minimum(i[on], imax - 1) + 1, 1)
+        np.testing.assert_array_equal(s.clusters.cluster_size[on], expect_size)
+        idx = np.flatnonzero(on)
+        last_two = idx[i[on] >= imax - 1]
+        assert len(last_two) == 2
+        for r, ii in zip(idx, i[on]):
+            if share[np.searchsorted(idx, r)] < w.threshold:
+                assert s.clusters.cluster_id[r] == -1
+            elif ii >= imax - 1:
+                assert s.clusters.cluster_id[r] == last_two.min()
+            else:
+                assert s.clusters.cluster_id[r] == r
+    m_expect = np.where(spine == 1, np.minimum(i, n // 4), 0)
+    np.testing.assert_array_equal(s.lpm.m, m_expect)
+    np.testing.assert_array_equal(s.lpm.h, 16 * (m_expect // 16))
