@@ -173,14 +173,12 @@ peek_status peek_lpm_batch(const peek_cache* cache, int32_t n, const int32_t* d_
  *
  * Scratch comes from d_workspace (device, 256-byte aligned, at least
  * peek_queue_signals_workspace(n, num_nodes) bytes, num_nodes = 0 without a
- * cache); apart from a few pinned host words allocated once per calling
- * thread the library allocates nothing here. The cluster pass refines a sort
- * in rounds: it runs a few rounds and the final stage, then waits for the
- * device flags that one last small kernel stores into pinned host memory
- * (polling; after 20 ms it synchronizes `stream` instead), and synchronizes
- * `stream` once more per further round when the queue needs more. When the
- * call returns, every kernel it launched has run. threshold >= 1.
- * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
+ * cache); the library allocates nothing here. Asynchronous on `stream`: the
+ * call only enqueues kernels and returns without waiting for the device
+ * (however many refinement rounds the queue needs, they run on the device),
+ * so the workspace and every output must stay untouched until `stream` has
+ * run the work. Calls on different streams need distinct workspaces.
+ * threshold >= 1. Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
  * ---------------------------------------------------------------------- */
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes);
 
@@ -207,8 +205,8 @@ peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t
  * vector); it is needed when d_section is given. d_score, d_section and
  * d_has_sharing are each optional (NULL: not written); d_cluster_id and
  * d_cluster_size are required. theta >= 0 (the paper uses 32); tau is any
- * int32 (the paper leaves it unset). Same workspace, synchronization and
- * errors as peek_queue_signals.
+ * int32 (the paper leaves it unset). Same workspace, asynchrony and errors
+ * as peek_queue_signals.
  * ---------------------------------------------------------------------- */
 peek_status peek_clpm_signals(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
                               const int64_t* d_offsets, const int32_t* d_h, const int32_t* d_last_node,
@@ -290,7 +288,7 @@ peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const
 
 /* ------------------------------------------------------------------------
  * peek_offline_order: PEEK-offline Phase 1 (appendix on PEEK-offline,
- * "Phase 1: Prefix trie DFS reordering").
+ * Phase 1).
  *
  * Over the token trie of the prompts' first depth_limit tokens (the paper
  * uses D = 128), a depth-first traversal emits at every node the requests
@@ -301,10 +299,9 @@ peek_status peek_block_lpm_batch(const peek_block_table* table, int32_t n, const
  * Requests that share a truncated prefix are therefore contiguous in d_perm.
  * No cache is involved (the paper's regime is a cold cache). depth_limit >= 0
  * (0: arrival order); n < 2^30. Scratch comes only from d_workspace (device, 256-byte
- * aligned, at least peek_offline_order_workspace(n) bytes). Waits for
- * `stream` once or a few times, as peek_queue_signals does.
- * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, OUT_OF_MEMORY (pinned host
- * words), DEVICE.
+ * aligned, at least peek_offline_order_workspace(n) bytes). Asynchronous on
+ * `stream`, as peek_queue_signals.
+ * Errors: INVALID_ARGUMENT, WORKSPACE_TOO_SMALL, DEVICE.
  * ---------------------------------------------------------------------- */
 size_t peek_offline_order_workspace(int32_t n);
 

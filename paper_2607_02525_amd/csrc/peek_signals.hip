@@ -29,15 +29,23 @@
 //     requests that also share the next token need more work, from m+1 on.
 //  2. Head-path refinement of every group that still has two or more
 //     members. A segment of requests known to share d tokens is compared with
-//     its longest member (the head) from depth d; a member's first mismatch l
-//     and its token there form its key, the head sorts last, and members with
-//     equal keys form the next segment at depth d+l+1. The LCP across a new
-//     boundary is d plus the smaller l. Each prompt byte is read about once.
+//     one of its members (the head) from depth d; a member's key is its first
+//     mismatch l with the head and its own token there (none when it ended
+//     there). Members with equal keys form the next segment at depth d+l+1;
+//     the LCP across a new boundary is d plus the smaller l. Each prompt byte
+//     is read about once.
+// Two refinement rounds run over the whole queue with the longest member as
+// the head: every member that is a prefix of it (the turns of one agentic
+// session) settles in one round. Whatever is still unsettled after them is
+// finished inside single workgroups with a head picked by a hash of the
+// segment's place and depth, which also halves a group whose members leave a
+// shared path one depth after another (where the longest member would peel
+// one request per round). The host never waits for the device.
 #include <algorithm>
-#include <chrono>
 
 #include "peek_compare.h"
 #include "peek_internal.h"
+#include "peek_lds_sort.h"
 #include "peek_sort.h"
 
 namespace peek {
@@ -134,9 +142,10 @@ struct DemandRide {
 // ---------------------------------------------------------------- clusters
 // Sort element. hi = (group << 32) | l, where the group is the anchor node
 // (first stage) or the segment start (refinement), and l the match length /
-// first mismatch with the head (0xFFFFFFFF for the head itself).
-// lo = (next-token code << 31) | (kLenMax - len): code 0 means the prompt
-// ended there; longer prompts first inside a group (the next head).
+// first mismatch with the head. lo = (next-token code << 31) | (kLenMax -
+// len): code 0 means the prompt ended there; longer prompts first inside a
+// group, so a group's first member is its longest (the next head). Sorts
+// are stable, so equal keys keep their order.
 struct ClElem {
   uint64_t hi;
   uint64_t lo;
@@ -151,18 +160,16 @@ struct ClLess {
 };
 
 constexpr uint64_t kLenMax = 0x7FFFFFFFull;
-constexpr uint32_t kHeadL = 0xFFFFFFFFu;
 
-// Largest segment the segment sort ranks inside one workgroup; rounds with
-// a larger active segment sort globally.
-constexpr int kSegSortMax = 512;
+// Largest segment the segment sort orders inside one workgroup. A round
+// that may sort globally does so when some active segment is larger; a
+// round that sorts per segment only leaves such a segment as it is (still
+// active, for the workgroup-local tail).
+constexpr int kSegSortMax = 4096;
 
-// Whether a refinement round has work: flags_in = {any active segment, some
-// active segment larger than kSegSortMax}; only a round that sorts globally
-// takes the latter.
-__device__ __forceinline__ bool round_runs(const int32_t* flags_in, int32_t global) {
-  return flags_in[0] != 0 && (global != 0 || flags_in[1] == 0);
-}
+// flags of a round: {any active segment, some active segment larger than
+// kSegSortMax}.
+__device__ __forceinline__ bool deferred(int32_t size, int32_t global) { return global == 0 && size > kSegSortMax; }
 
 struct AnchorKeys {
   const ClElem* el;
@@ -220,11 +227,11 @@ __device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, 
   return m;
 }
 
-// Anchor element of request i (the tile pass of the anchor sort builds its
-// input with this): key (last node, match length, next token, longest
-// first). Positions past n are padding that sorts last. Building element i
-// also clears lcp[i] (and lcp[n]), the round flags and the has_sharing
-// output, which later kernels of the pass expect zeroed.
+// Anchor element of request i (the anchor sort builds its input with this):
+// key (last node, match length, next token, longest first). Positions past n are
+// padding that sorts last. Building element i also clears lcp[i]; element 0
+// also clears lcp[n], the round flags and the has_sharing output, which
+// later kernels of the pass expect zeroed.
 struct AnchorSource {
   const int32_t* tokens;
   const int64_t* offsets;
@@ -237,9 +244,9 @@ struct AnchorSource {
   int32_t* sharing;   // NULL, or the has_sharing output (cleared here, raised by the final stage)
   uint32_t len_cap;   // prompts are taken as their first len_cap tokens
   __device__ __forceinline__ ClElem operator()(size_t i) const {
-    if (i < (size_t)n_flags) flags[i] = 0;
     if (i <= (size_t)n) lcp[i] = 0;
     if (i == 0) {
+      for (int f = 0; f < n_flags; ++f) flags[f] = 0;
       lcp[n] = 0;
       if (sharing) *sharing = 0;
     }
@@ -338,13 +345,39 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
   }
 }
 
+// Head of a segment in the workgroup-local tail: the member at a hashed
+// offset of the segment's start and depth. Any member works as the head; a
+// hash keeps a long prompt that leaves a shared path early from heading
+// round after round.
+__device__ __forceinline__ int32_t head_pos(int32_t s, int32_t d, int32_t size) {
+  return s + (int32_t)(ldssort::mix32((uint32_t)s * 0x9E3779B9u ^ (uint32_t)d * 0x85EBCA6Bu) % (uint32_t)size);
+}
+
+// Key of a member j (length len_j) of a segment of depth d against the
+// segment's head h (length len_h): l = first mismatch from d, and j's token
+// there, or code 0 if j ended there. j may also run past the head's end.
+// One wavefront; the result is uniform across it.
+__device__ __forceinline__ void member_key(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets,
+                                           uint32_t j, uint32_t len_j, uint32_t h, uint32_t len_h, int32_t d,
+                                           int lane, uint32_t& ell, uint64_t& code) {
+  const int32_t* __restrict__ pj = tokens + offsets[j] + d;
+  const int32_t* __restrict__ ph = tokens + offsets[h] + d;
+  const int32_t lim = (int32_t)min(len_j, len_h) - d;
+  const int32_t l = cmp::first_mismatch(pj, ph, lim, lane);
+  ell = (uint32_t)l;
+  code = (l < lim || (int64_t)len_j > (int64_t)d + l) ? tok_code(pj[l]) : 0;
+}
+
 // One wavefront per position: rewrite every element's key for the next sort;
-// members of active segments are compared with their segment's head.
-// `flags_in` are the previous round's flags: nothing to do when [0] is 0;
-// with [1] raised only a round that sorts globally (`global`) may run.
+// members of active segments are compared with their segment's first member,
+// its longest (the sort keeps the longest first in every group). Nothing to
+// do when the previous round left no active segment (flags_in[0] = 0). In a
+// round that sorts per segment only (global = 0), a segment beyond the
+// segment sort keeps its keys and waits for the tail.
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
+                                                        const int32_t* __restrict__ gsize,
                                                         const int32_t* __restrict__ depth,
                                                         const uint8_t* __restrict__ active,
                                                         const int32_t* __restrict__ flags_in, int32_t global,
@@ -354,7 +387,7 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
                    ((int32_t)blockIdx.x - ride.first_block) * (int32_t)blockDim.x + (int32_t)threadIdx.x);
     return;
   }
-  if (!round_runs(flags_in, global)) return;
+  if (flags_in[0] == 0) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (i >= n) return;
@@ -363,20 +396,11 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
     if (lane == 0) el[i].hi = (uint64_t)(uint32_t)s << 32;
     return;
   }
+  if (deferred(gsize[s], global)) return;
   const uint32_t len_j = el[i].len;
-  uint32_t ell = kHeadL;
+  uint32_t ell = len_j - (uint32_t)depth[s];   // the head (s) itself: ended at its length
   uint64_t code = 0;
-  if (i != s) {
-    const int32_t d = depth[s];
-    const uint32_t j = el[i].req, h = el[s].req;
-    const uint32_t len_h = el[s].len;
-    const int32_t* __restrict__ pj = tokens + offsets[j] + d;
-    const int32_t* __restrict__ ph = tokens + offsets[h] + d;
-    const int32_t lim = (int32_t)min(len_j, len_h) - d;
-    const int32_t l = cmp::first_mismatch(pj, ph, lim, lane);
-    ell = (uint32_t)l;
-    code = l < lim ? tok_code(pj[l]) : 0;   // 0: the member ended (the head is the longest)
-  }
+  if (i != s) member_key(tokens, offsets, el[i].req, len_j, el[s].req, el[s].len, depth[s], lane, ell, code);
   if (lane == 0) {
     el[i].hi = ((uint64_t)(uint32_t)s << 32) | ell;
     el[i].lo = lo_of(code, len_j);
@@ -403,30 +427,47 @@ __device__ __forceinline__ ClElem seg_elem(const SegKey& k, int32_t s) {
   return e;
 }
 
-constexpr int kSegThreads = kSegSortMax;   // one thread per member of a medium segment
-constexpr int kSegRange = 256;             // segment starts owned by one workgroup
+constexpr int kSegThreads = 512;           // one thread per member of a medium segment
+constexpr int kSegMid = kSegThreads;       // members ranked against LDS keys
+constexpr int kSegRange = 256;             // positions (and segment starts) owned by one workgroup
 
-// Sorts every active segment of at most kSegSortMax members in place. Each
-// workgroup owns the segment starts in kSegRange consecutive positions:
+// Sorts every active segment of at most kSegSortMax members from `in` into
+// `out`, stably by key (in place when they are the same buffer; otherwise
+// every position outside a sorted segment is copied across). Each
+// workgroup owns the positions in kSegRange consecutive places and the
+// segments starting there:
 //  - a segment of at most 64 members is ranked by one wavefront;
-//  - a larger one is ranked by the whole workgroup, one member per thread,
-//    against the segment's keys staged in LDS (every read is a broadcast).
-// A member's rank is the number of members that order before it (ties by
-// position), so the sort is stable. Rounds with a larger segment
-// (flags_in[1]) sort globally instead and this kernel does nothing.
-__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClElem* __restrict__ el,
+//  - up to kSegMid members, by the whole workgroup, one member per thread,
+//    against the segment's keys staged in LDS (every read is a broadcast);
+//  - up to kSegSortMax, by the workgroup's LDS merge sort.
+// A member's rank is the number of members that order before it, ties by
+// position. A round that sorts globally (global, with some segment beyond
+// kSegSortMax) leaves everything to the global sort.
+__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, const ClElem* __restrict__ in,
+                                                                 ClElem* __restrict__ out,
                                                                  const int32_t* __restrict__ nseg,
                                                                  const int32_t* __restrict__ gsize,
                                                                  const uint8_t* __restrict__ active,
-                                                                 const int32_t* __restrict__ flags_in) {
-  if (!round_runs(flags_in, 0)) return;
-  __shared__ SegKey sk[kSegSortMax];
+                                                                 const int32_t* __restrict__ flags_in,
+                                                                 int32_t global) {
+  if (global != 0 && flags_in[0] != 0 && flags_in[1] != 0) return;
+  __shared__ SegKey sk[kSegMid];
+  __shared__ uint64_t sa[kSegSortMax];
+  __shared__ uint64_t sb[kSegSortMax];
+  __shared__ uint32_t sp[kSegSortMax];
   __shared__ int32_t mid[kSegRange / 64 + 1];
   __shared__ int32_t n_mid;
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   const int wave = t / kWave;
   const int32_t r0 = (int32_t)blockIdx.x * kSegRange;
+  if (in != out) {
+    for (int32_t p = r0 + t; p < min(n, r0 + kSegRange); p += kSegThreads) {
+      const int32_t q = nseg[p];
+      if (flags_in[0] == 0 || !active[q] || deferred(gsize[q], global)) out[p] = in[p];
+    }
+  }
+  if (flags_in[0] == 0) return;
   if (t == 0) n_mid = 0;
   __syncthreads();
   // small segments: wave w looks at the starts r0 + 32w .. r0 + 32w + 31
@@ -435,7 +476,7 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClEl
   {
     const int32_t p = r0 + wave * kPerWave + lane;
     bool small = false;
-    if (lane < kPerWave && p < n && nseg[p] == p && active[p]) {
+    if (lane < kPerWave && p < n && nseg[p] == p && active[p] && !deferred(gsize[p], global)) {
       if (gsize[p] <= kWave) small = true;
       else mid[atomicAdd(&n_mid, 1)] = p;   // members > 64: at most one start per 64 positions
     }
@@ -446,7 +487,7 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClEl
       const int32_t s = r0 + wave * kPerWave + f;
       const int32_t size = gsize[s];
       ClElem e{};
-      if (lane < size) e = el[s + lane];
+      if (lane < size) e = in[s + lane];
       int rank = 0;
       const ClLess less;
       for (int j = 0; j < size; ++j) {
@@ -455,7 +496,7 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClEl
         o.lo = __shfl(e.lo, j);
         if (less(o, e) || (j < lane && !less(e, o))) ++rank;
       }
-      if (lane < size) el[s + rank] = e;
+      if (lane < size) out[s + rank] = e;
     }
   }
   __syncthreads();
@@ -463,21 +504,54 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClEl
   for (int b = 0; b < nm; ++b) {
     const int32_t s = mid[b];
     const int32_t size = gsize[s];
-    SegKey v{};
-    if (t < size) {
-      v = seg_key(el[s + t]);
-      sk[t] = v;
-    }
-    __syncthreads();
-    if (t < size) {
-      int32_t rank = 0;
-      for (int32_t j = 0; j < size; ++j) {
-        const SegKey o = sk[j];
-        rank += (seg_less(o, v) || (j < t && !seg_less(v, o))) ? 1 : 0;
+    if (size <= kSegMid) {
+      SegKey v{};
+      if (t < size) {
+        v = seg_key(in[s + t]);
+        sk[t] = v;
       }
-      el[s + rank] = seg_elem(v, s);
+      __syncthreads();
+      if (t < size) {
+        int32_t rank = 0;
+        for (int32_t j = 0; j < size; ++j) {
+          const SegKey o = sk[j];
+          rank += (seg_less(o, v) || (j < t && !seg_less(v, o))) ? 1 : 0;
+        }
+        out[s + rank] = seg_elem(v, s);
+      }
+      __syncthreads();
+    } else {
+      const int M = ldssort::pow2_at_least(size);
+      for (int r = t; r < M; r += kSegThreads) {
+        if (r < size) {
+          const ClElem e = in[s + r];
+          sa[r] = ell_of(e.hi);
+          sb[r] = e.lo;
+          sp[r] = (uint32_t)r;
+        } else {
+          sa[r] = ~0ull;
+          sb[r] = ~0ull;
+          sp[r] = 0xFFFFFFFFu;
+        }
+      }
+      __syncthreads();
+      ldssort::lds_sort<kSegThreads>(sa, sb, sp, M);
+      // through registers: in and out may be the same buffer
+      constexpr int kPer = kSegSortMax / kSegThreads;
+      ClElem v[kPer];
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int r = t + q * kSegThreads;
+        if (r < size) v[q] = in[s + sp[r]];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int r = t + q * kSegThreads;
+        if (r < size) out[s + r] = v[q];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
@@ -491,7 +565,7 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
                                                        uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
                                                        const int32_t* __restrict__ flags_in,
                                                        int32_t* __restrict__ flags, int32_t global) {
-  if (!round_runs(flags_in, global)) return;
+  if (flags_in[0] == 0) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -499,11 +573,13 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   const bool valid = i < n;
   ClElem e{};
   int32_t s = 0;
-  bool live = false, start = false;
+  bool live = false, start = false, wait = false;
   if (valid) {
     e = el[i];
-    s = (int32_t)(e.hi >> 32);
+    s = nseg[i];
     live = active_old[s] != 0;
+    wait = live && deferred(gsize[s], global);   // kept whole for the tail
+    live = live && !wait;
     start = live && (i == s || !same_group(el[i - 1], e));
   }
   // lanes of a live group that began before this wave share one search
@@ -513,8 +589,9 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   if (!valid) return;
   if (!live) {
     if (i == s) {
-      active_new[i] = 0;
+      active_new[i] = wait;
       depth_new[i] = depth_old[i];
+      if (wait) flags[0] = 1;
     }
     return;
   }
@@ -523,7 +600,7 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   const uint32_t ell = ell_of(e.hi);
   const uint64_t code = code_of(e.lo);
   const bool last = i + 1 == n || !same_group(e, el[i + 1]);
-  const bool can_split = ell != kHeadL && code != 0;
+  const bool can_split = code != 0;
   if (last) {
     const int32_t size = i - g + 1;
     gsize[g] = size;
@@ -535,8 +612,349 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
     active_new[i] = act;
     depth_new[i] = act ? d + (int32_t)ell + 1 : 0;
     if (act) flags[0] = 1;
-  } else if (code == 0 && ell != kHeadL) {
+  } else if (code == 0) {
     lcp[i] = d + (int32_t)ell;   // identical prompts that ended together
+  }
+}
+
+// ---------------------------------------------------------------- tail
+// Segments still active after the global rounds are finished inside single
+// workgroups. Workgroup g owns the segments that start in positions
+// [g * kTailRange, (g + 1) * kTailRange), whole (wherever they end), and keeps
+// the state of their sub-segments in tail-only arrays indexed by position
+// (tact, tdep, tsize), so no workgroup reads what another one writes. Each
+// pass collects the active sub-segments of its segments:
+//  - one of at most 64 members is settled completely by one wavefront, its
+//    elements held in registers (lane l = position start + l), every round
+//    down to single requests;
+//  - a larger one gets one round from the whole workgroup: 16 wavefronts
+//    compare the members with the head, the keys are sorted in LDS (merge
+//    sort; beyond kTailCap members, ranked in global memory), the
+//    elements are permuted and the new groups marked;
+// and passes repeat until nothing is active. Every round makes each active
+// group strictly deeper or settles it, so the loop ends.
+constexpr int kTailRange = 1024;
+constexpr int kTailThreads = 1024;
+constexpr int kTailWaves = kTailThreads / kWave;
+constexpr int kTailCap = 4096;              // members the workgroup sorts in LDS
+constexpr int kTailList = 1024;              // sub-segments collected per pass and kind
+constexpr int kTailRoots = kTailRange / 2;   // segments of >= 2 members starting in one range
+constexpr uint64_t kCodeMask = (1ull << 33) - 1;
+
+struct TailArgs {
+  const int32_t* tokens;
+  const int64_t* offsets;
+  int32_t n;
+  ClElem* el;                // the order after the global rounds, refined in place
+  ClElem* tmp;               // free element buffer (scratch of the global-memory ranking)
+  const int32_t* nseg;       // state after the last global round (read only here)
+  const int32_t* gsize;
+  const int32_t* depth;
+  const uint8_t* active;
+  int32_t* lcp;
+  uint8_t* tact;             // tail state by position: an active sub-segment starts here
+  int32_t* tdep;             //   its depth
+  int32_t* tsize;            //   its size
+  const int32_t* flags_in;   // the last global round's flags
+};
+
+__device__ __forceinline__ bool tail_key_less(uint32_t ea, uint64_t ca, uint32_t ra, uint32_t eb, uint64_t cb,
+                                              uint32_t rb) {
+  return ea < eb || (ea == eb && (ca < cb || (ca == cb && ra < rb)));
+}
+
+// Settles the segment [s, s + size) of depth d0 (size <= 64) with one
+// wavefront: lane l holds the element at position s + l; each round refines
+// the first active group in the lanes and regroups it.
+__device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int32_t d0, int lane) {
+  const bool in = lane < size;
+  ClElem e{};
+  if (in) e = A.el[s + lane];
+  int32_t g = 0, gsz = size, d = d0;   // this lane's group: first lane, size, depth
+  bool act = true;                     // whether it still needs a round
+  int32_t lv = 0;                      // lcp at this position, once known
+  bool lset = false;
+  // Every round removes at least the head from each active group it
+  // refines, so a group of z members needs at most z rounds and the loop at
+  // most 64 * 64; the bound only guards the device against a broken
+  // invariant.
+  for (int iter = 0; iter < kWave * kWave; ++iter) {
+    const uint64_t am = __ballot(in && act && lane == g);
+    if (am == 0) break;
+    const int gs = __ffsll((unsigned long long)am) - 1;
+    const int32_t gz = __shfl(gsz, gs);
+    const int32_t gd = __shfl(d, gs);
+    const int hl = head_pos(s + gs, gd, gz) - s;
+    const uint32_t hreq = __shfl(e.req, hl), hlen = __shfl(e.len, hl);
+    uint32_t ell = 0;
+    uint64_t code = 0;
+    for (int j = gs; j < gs + gz; ++j) {
+      const uint32_t jreq = __shfl(e.req, j), jlen = __shfl(e.len, j);
+      uint32_t le;
+      uint64_t lc;
+      if (j == hl) {
+        le = jlen - (uint32_t)gd;
+        lc = 0;
+      } else {
+        member_key(A.tokens, A.offsets, jreq, jlen, hreq, hlen, gd, lane, le, lc);
+      }
+      if (lane == j) {
+        ell = le;
+        code = lc;
+      }
+    }
+    const bool mem = in && lane >= gs && lane < gs + gz;
+    int rank = 0;
+    for (int j = gs; j < gs + gz; ++j) {
+      const uint32_t oe = __shfl(ell, j);
+      const uint64_t oc = __shfl(code, j);
+      const uint32_t orq = __shfl(e.req, j);
+      if (mem && tail_key_less(oe, oc, orq, ell, code, e.req)) ++rank;
+    }
+    // lane gs + rank takes this lane's element: each member pulls from the
+    // member whose rank is its own offset in the group
+    int src = lane;
+    for (int j = gs; j < gs + gz; ++j) {
+      const int rj = __shfl(rank, j);
+      if (mem && rj == lane - gs) src = j;
+    }
+    ClElem f;
+    f.hi = __shfl(e.hi, src);
+    f.lo = __shfl(e.lo, src);
+    f.req = __shfl(e.req, src);
+    f.len = __shfl(e.len, src);
+    const uint32_t fe = __shfl(ell, src);
+    const uint64_t fc = __shfl(code, src);
+    if (mem) {
+      e = f;
+      ell = fe;
+      code = fc;
+    }
+    const int prev = lane > 0 ? lane - 1 : 0;
+    const uint32_t pe = __shfl(ell, prev);
+    const uint64_t pc = __shfl(code, prev);
+    const bool gstart = mem && (lane == gs || pe != ell || pc != code);
+    if (mem && lane > gs) {
+      if (gstart) {
+        lv = gd + (int32_t)pe;   // keys ascend, so the previous l is the smaller
+        lset = true;
+      } else if (code == 0) {
+        lv = gd + (int32_t)ell;  // prompts that ended together
+        lset = true;
+      }
+    }
+    const uint64_t sm = __ballot(gstart);
+    const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
+    const uint64_t after = sm & ~upto;
+    if (mem) {
+      const int ng = 63 - __clzll((unsigned long long)(sm & upto));
+      const int nx = after ? __ffsll((unsigned long long)after) - 1 : gs + gz;
+      g = ng;
+      gsz = nx - ng;
+      d = gd + (int32_t)ell + 1;
+      act = code != 0 && gsz >= 2;
+    }
+  }
+  if (in) {
+    A.el[s + lane] = e;
+    if (lset) A.lcp[s + lane] = lv;
+  }
+}
+
+// One round of the segment [s, s + sz) of depth d (sz > 64) by the whole
+// workgroup. Keys are written into the elements' hi/lo fields (hi = l << 33 |
+// code, lo = request), which nothing after the refinement reads.
+__device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t d, uint64_t* sa, uint64_t* sb,
+                              uint32_t* sp, uint64_t* cmask) {
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int32_t hp = head_pos(s, d, sz);
+  const uint32_t hreq = A.el[hp].req, hlen = A.el[hp].len;
+  for (int32_t j = wave; j < sz; j += kTailWaves) {
+    const uint32_t jreq = A.el[s + j].req, jlen = A.el[s + j].len;
+    uint32_t ell;
+    uint64_t code;
+    if (s + j == hp) {
+      ell = jlen - (uint32_t)d;
+      code = 0;
+    } else {
+      member_key(A.tokens, A.offsets, jreq, jlen, hreq, hlen, d, lane, ell, code);
+    }
+    if (lane == 0) {
+      A.el[s + j].hi = ((uint64_t)ell << 33) | code;
+      A.el[s + j].lo = jreq;
+    }
+  }
+  __syncthreads();
+  const bool fits = sz <= kTailCap;
+  if (fits) {
+    const int M = ldssort::pow2_at_least(sz);
+    for (int r = t; r < M; r += kTailThreads) {
+      if (r < sz) {
+        sa[r] = A.el[s + r].hi;
+        sb[r] = A.el[s + r].lo;
+        sp[r] = (uint32_t)r;
+      } else {
+        sa[r] = ~0ull;
+        sb[r] = ~0ull;
+        sp[r] = 0xFFFFFFFFu;
+      }
+    }
+    __syncthreads();
+    ldssort::lds_sort<kTailThreads>(sa, sb, sp, M);
+    constexpr int kPer = kTailCap / kTailThreads;
+    ClElem v[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int r = t + q * kTailThreads;
+      if (r < sz) v[q] = A.el[s + sp[r]];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int r = t + q * kTailThreads;
+      if (r < sz) A.el[s + r] = v[q];
+    }
+  } else {
+    // ranks against every member, then a permutation through the free buffer
+    for (int32_t j = t; j < sz; j += kTailThreads) {
+      const uint64_t xa = A.el[s + j].hi, xb = A.el[s + j].lo;
+      int32_t rank = 0;
+      for (int32_t q = 0; q < sz; ++q) {
+        const uint64_t ya = A.el[s + q].hi, yb = A.el[s + q].lo;
+        rank += (ya < xa || (ya == xa && yb < xb)) ? 1 : 0;
+      }
+      A.tmp[s + rank] = A.el[s + j];
+    }
+    __syncthreads();
+    for (int32_t r = t; r < sz; r += kTailThreads) A.el[s + r] = A.tmp[s + r];
+  }
+  __syncthreads();
+  // groups: boundaries, their lcps, and each new group's size and state
+  const int32_t nchunks = (sz + kWave - 1) / kWave;
+  for (int32_t c = wave; c < (fits ? nchunks : 0); c += kTailWaves) {
+    const int32_t r = c * kWave + lane;
+    const bool st = r < sz && (r == 0 || A.el[s + r].hi != A.el[s + r - 1].hi);
+    const uint64_t m = __ballot(st);
+    if (lane == 0) cmask[c] = m;
+  }
+  __syncthreads();
+  for (int32_t r = t; r < sz; r += kTailThreads) {
+    const uint64_t a = A.el[s + r].hi;
+    const uint32_t ell = (uint32_t)(a >> 33);
+    const uint64_t code = a & kCodeMask;
+    const uint64_t pa = r > 0 ? A.el[s + r - 1].hi : a;
+    const bool st = r == 0 || pa != a;
+    if (r > 0) {
+      if (st) A.lcp[s + r] = d + (int32_t)(uint32_t)(pa >> 33);
+      else if (code == 0) A.lcp[s + r] = d + (int32_t)ell;
+    }
+    if (!st) continue;
+    // next group start after r
+    int32_t nx = sz;
+    if (fits) {
+      const int32_t c = r / kWave;
+      const int b = r % kWave;
+      const uint64_t above = b == 63 ? 0ull : (cmask[c] & ~((2ull << b) - 1));
+      if (above) {
+        nx = c * kWave + __ffsll((unsigned long long)above) - 1;
+      } else {
+        for (int32_t c2 = c + 1; c2 < nchunks; ++c2) {
+          if (cmask[c2]) {
+            nx = c2 * kWave + __ffsll((unsigned long long)cmask[c2]) - 1;
+            break;
+          }
+        }
+      }
+    } else {
+      for (int32_t q = r + 1; q < sz; ++q) {
+        if (A.el[s + q].hi != a) {
+          nx = q;
+          break;
+        }
+      }
+    }
+    const int32_t size = nx - r;
+    const bool act = code != 0 && size >= 2;
+    A.tact[s + r] = act;
+    if (act) {
+      A.tdep[s + r] = d + (int32_t)ell + 1;
+      A.tsize[s + r] = size;
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
+  if (A.flags_in[0] == 0) return;
+  __shared__ uint64_t sa[kTailCap];
+  __shared__ uint64_t sb[kTailCap];
+  __shared__ uint32_t sp[kTailCap];
+  __shared__ uint64_t cmask[kTailCap / kWave];
+  __shared__ int32_t root_s[kTailRoots], root_e[kTailRoots];
+  __shared__ int32_t small_l[kTailList], big_l[kTailList];
+  __shared__ int32_t n_roots, n_small, n_big;
+  const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+  const int32_t p0 = (int32_t)blockIdx.x * kTailRange;
+  const int32_t p1 = min(A.n, p0 + kTailRange);
+  if (t == 0) n_roots = 0;
+  __syncthreads();
+  for (int32_t p = p0 + t; p < p1; p += kTailThreads) {
+    if (A.nseg[p] == p && A.active[p]) {
+      const int k = atomicAdd(&n_roots, 1);
+      root_s[k] = p;
+      root_e[k] = p + A.gsize[p];
+    }
+  }
+  __syncthreads();
+  const int nr = n_roots;
+  if (nr == 0) return;
+  for (int k = 0; k < nr; ++k) {
+    const int32_t s = root_s[k], e = root_e[k];
+    for (int32_t q = s + t; q < e; q += kTailThreads) A.tact[q] = q == s;
+    if (t == 0) {
+      A.tdep[s] = A.depth[s];
+      A.tsize[s] = e - s;
+    }
+  }
+  __syncthreads();
+  // Each pass settles at least one small segment or gives at least one large
+  // one a round, and the sub-segments ever formed are nodes of a tree over
+  // at most n requests (fewer than 2n), so 2n + 2 passes always suffice; the
+  // bound only guards the device against a broken invariant.
+  for (int64_t pass = 0; pass <= 2 * (int64_t)A.n + 2; ++pass) {
+    if (t == 0) {
+      n_small = 0;
+      n_big = 0;
+    }
+    __syncthreads();
+    for (int k = 0; k < nr; ++k) {
+      const int32_t s = root_s[k], e = root_e[k];
+      for (int32_t q = s + t; q < e; q += kTailThreads) {
+        if (A.tact[q]) {
+          if (A.tsize[q] <= kWave) {
+            const int x = atomicAdd(&n_small, 1);
+            if (x < kTailList) small_l[x] = q;
+          } else {
+            const int x = atomicAdd(&n_big, 1);
+            if (x < kTailList) big_l[x] = q;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    const int ns = min(n_small, kTailList), nb = min(n_big, kTailList);
+    if (ns == 0 && nb == 0) break;
+    for (int x = wave; x < ns; x += kTailWaves) {
+      const int32_t q = small_l[x];
+      tail_wave_settle(A, q, A.tsize[q], A.tdep[q], lane);
+      if (lane == 0) A.tact[q] = 0;
+    }
+    __syncthreads();
+    for (int x = 0; x < nb; ++x) {
+      const int32_t q = big_l[x];
+      tail_wg_round(A, q, A.tsize[q], A.tdep[q], sa, sb, sp, cmask);
+    }
+    __syncthreads();
   }
 }
 
@@ -1072,17 +1490,16 @@ int levels_for(int64_t nb) {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Refinement rounds launched before the host reads any flag. Flag pairs:
-// slot 0 for the anchor groups, slot r for round r, two more for rounds the
-// host drives afterwards.
-constexpr int kSpeculativeRounds = 2;
-static_assert(kSpeculativeRounds >= 1, "the first round carries the demand difference");
-constexpr int kFlagPairs = kSpeculativeRounds + 3;
+// Refinement rounds run over the whole queue before the workgroup-local
+// tail. Flag pairs: slot 0 for the anchor groups, slot r for round r.
+constexpr int kGlobalRounds = 2;
+static_assert(kGlobalRounds >= 1, "the first round carries the demand difference");
+constexpr int kFlagPairs = kGlobalRounds + 1;
 
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
   size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
-      keys_b, prefix, diff, pmin, run, local, part, sharing, total, flags_bytes;
+      keys_b, prefix, diff, pmin, run, local, part, sharing, tact, tdep, tsize, total, flags_bytes;
   // PEEK-offline Phase 1 only
   size_t oel_a, oel_b, olocal, opart, obase, start_a, start_b, npar_a, npar_b, rnode, roff, onp;
   int64_t ib_stride;
@@ -1129,6 +1546,9 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.local = take(sizeof(int64_t) * nn);
   L.part = take(sizeof(int64_t) * (((size_t)n + kScanThreads - 1) / kScanThreads + 1));
   L.sharing = take(sizeof(int32_t));
+  L.tact = take(nn);
+  L.tdep = take(sizeof(int32_t) * nn);
+  L.tsize = take(sizeof(int32_t) * nn);
   if (offline) {
     const size_t m2 = 2 * nn;
     size_t onp = msort::kTile;
@@ -1168,61 +1588,13 @@ void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
 }
 
-// Pinned host words the flag pairs are read into, followed by a sequence
-// word (one set per host thread, kept for the life of the process). They
-// are coherent, mapped memory that a kernel can publish into; where that
-// cannot be had, plain pinned memory that the flags are copied into.
-constexpr int kHostWords = 2 * kFlagPairs + 1;
-struct HostFlags {
-  int32_t* p;
-  bool coherent;
-};
-HostFlags host_flags() {
-  thread_local HostFlags h{nullptr, false};
-  if (h.p == nullptr) {
-    if (hipHostMalloc((void**)&h.p, sizeof(int32_t) * kHostWords, hipHostMallocCoherent | hipHostMallocMapped) ==
-        hipSuccess) {
-      h.coherent = true;
-    } else {
-      (void)hipGetLastError();
-      h.coherent = false;
-      if (hipHostMalloc((void**)&h.p, sizeof(int32_t) * kHostWords, hipHostMallocDefault) != hipSuccess) h.p = nullptr;
-    }
-  }
-  return h;
-}
-
-// The first `count` flag words into coherent host memory, then the
-// sequence number `seq` after them; the host reads the flags once it sees
-// `seq`. Stores are system-scope vector stores.
-__global__ void k_publish_flags(const int32_t* __restrict__ flags, int32_t count, int32_t* host, int32_t seq) {
-  const int t = threadIdx.x;
-  if (t < count) __hip_atomic_store(host + t, flags[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  __syncthreads();
-  if (t == 0) __hip_atomic_store(host + 2 * kFlagPairs, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-}
-
-// Waits until the stream has published `seq`: polls the host word for a
-// short while (a publish lands within microseconds of the work before it),
-// then falls back to synchronizing the stream, which also reports a failed
-// launch.
-hipError_t wait_published(const int32_t* host, int32_t seq, hipStream_t st) {
-  const auto t0 = std::chrono::steady_clock::now();
-  for (uint32_t spin = 0;; ++spin) {
-    if (__atomic_load_n(host + 2 * kFlagPairs, __ATOMIC_ACQUIRE) == seq) return hipSuccess;
-    if ((spin & 255) == 255 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
-  }
-  const hipError_t e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return e;
-  return __atomic_load_n(host + 2 * kFlagPairs, __ATOMIC_ACQUIRE) == seq ? hipSuccess : hipErrorUnknown;
-}
-
 }  // namespace
 
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
                         int32_t* csz, int32_t* demand, const ClpmRequest* clpm, const OfflineRequest* off,
                         void* ws, size_t ws_bytes, hipStream_t st) {
+  (void)ws_bytes;
   const DeviceTree* t = c != nullptr ? &c->tree : nullptr;
   const int64_t num_nodes = t ? t->num_nodes : 0;
   const Layout L = layout(n, num_nodes, off != nullptr);
@@ -1253,8 +1625,7 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
     return PEEK_OK;
   }
 
-  ClElem* el_a = (ClElem*)(w + L.el_a);
-  ClElem* el_b = (ClElem*)(w + L.el_b);
+  ClElem* bufs[2] = {(ClElem*)(w + L.el_a), (ClElem*)(w + L.el_b)};
   int32_t* nseg = (int32_t*)(w + L.nseg);
   int32_t* gsize = (int32_t*)(w + L.gsize);
   // segment depth and activity after round r live in slot r & 1
@@ -1267,12 +1638,8 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
   int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
-  const HostFlags hflags = host_flags();
-  int32_t* hf = hflags.p;
-  if (hf == nullptr) return fail(PEEK_ERR_OUT_OF_MEMORY, "pinned host flag buffer could not be allocated");
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
-  ClElem* el = el_a;
-  ClElem* other = el_b;
+  int cur = 0;   // bufs[cur] holds the current order
   ClpmArgs cl{};
   if (clpm != nullptr) {
     cl.h = clpm->h;
@@ -1290,151 +1657,104 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   int64_t* local = (int64_t*)(w + L.local);
   const LcpIndex ix{ib1, L.ib_stride, st1, L.nb1, L.levels, n};
 
-  // Round r compares every member of an active segment with its head, sorts
-  // each segment by the new keys and splits it into the next segments.
-  // kind: kSeg sorts in segments only (the round idles if a segment is too
-  // large), kGlobal sorts globally, kEither lets the device choose (both
-  // sorts are launched, each gated on the flag that selects it).
-  enum Kind { kSeg, kGlobal, kEither };
+  // 1. Anchor order: sorted by (last node, match length, next token).
+  const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
+                         flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr,
+                         off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
+  cur = msort::sort_from(src, bufs[0], bufs[1], np, ClLess{}, st) == bufs[0] ? 0 : 1;
+  // The anchor order is sorted by last node first, so demand reads it
+  // directly: the prefix P rides along with the anchor groups, the
+  // difference along with the first round's compare.
   const bool ride_demand = demand != nullptr && anchored;
-  const DemandRide no_ride{nullptr, nullptr, nullptr, 0, INT32_MAX};
-  auto round = [&](int64_t r, const int32_t* fin, int32_t* fout, Kind kind, hipStream_t q,
-                   DemandRide ride, unsigned ride_blocks) {
+  DemandRide ride{nullptr, nullptr, nullptr, 0, INT32_MAX};
+  unsigned prefix_blocks = 0, diff_blocks = 0;
+  if (ride_demand) {
+    ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
+    prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
+    diff_blocks = blocks_for(t->num_nodes);
+  }
+  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, bufs[cur],
+                     anchored ? *t : DeviceTree{}, nseg, gsize, depth[0], active[0], lcp, flags, ride);
+
+  // 2. Refinement rounds over the whole queue. Round r compares every member
+  // of an active segment with its head, sorts by the new keys and splits the
+  // segments. The first round sorts globally when some segment is larger
+  // than the segment sort takes (both sorts are launched, each gated on the
+  // flag that selects it); later ones sort per segment and leave a larger
+  // segment to the tail. A round whose flags say nothing is active only
+  // carries the order into its output buffer.
+  for (int r = 1; r <= kGlobalRounds; ++r) {
+    const int32_t global = r == 1;
+    const int32_t* fin = flags + 2 * (r - 1);
+    int32_t* fout = flags + 2 * r;
     const int32_t* dep = depth[(r - 1) & 1];
     const uint8_t* act = active[(r - 1) & 1];
-    const int32_t any = kind != kSeg;
+    ClElem* in = bufs[cur];
     const unsigned cmp_blocks = blocks_for(n, 4);
-    ride.first_block = ride_blocks ? (int32_t)cmp_blocks : INT32_MAX;
-    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks + ride_blocks), dim3(256), 0, q, tokens, offsets, n, el,
-                       nseg, dep, act, fin, any, ride);
-    if (kind != kSeg) {
-      ClElem* sorted = msort::sort(el, other, np, ClLess{}, q, kind == kEither ? fin + 1 : nullptr);
-      other = sorted == el ? other : el;
-      el = sorted;
-    }
-    if (kind != kGlobal)
-      hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, q, n, el, nseg,
-                         gsize, act, fin);
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, q, n, el, nseg, gsize, dep, act,
-                       depth[r & 1], active[r & 1], lcp, fin, fout, any);
-  };
-  // PEEK-offline Phase 1 from the settled order (see OffSource).
-  auto offline_stage = [&](hipStream_t q) {
+    const unsigned ride_blocks = r == 1 ? diff_blocks : 0;
+    DemandRide rr = ride;
+    rr.first_block = ride_blocks ? (int32_t)cmp_blocks : INT32_MAX;
+    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks + ride_blocks), dim3(256), 0, st, tokens, offsets, n, in,
+                       nseg, gsize, dep, act, fin, global, rr);
+    ClElem* out = global ? msort::sort(in, bufs[cur ^ 1], np, ClLess{}, st, fin + 1) : bufs[cur ^ 1];
+    hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, in, out, nseg,
+                       gsize, act, fin, global);
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, out, nseg, gsize, dep, act,
+                       depth[r & 1], active[r & 1], lcp, fin, fout, global);
+    cur = out == bufs[0] ? 0 : 1;
+  }
+
+  // 3. Whatever is still active is settled inside single workgroups.
+  ClElem* el = bufs[cur];
+  const TailArgs ta{tokens, offsets, n, el, bufs[cur ^ 1], nseg, gsize, depth[kGlobalRounds & 1],
+                    active[kGlobalRounds & 1], lcp, (uint8_t*)(w + L.tact), (int32_t*)(w + L.tdep),
+                    (int32_t*)(w + L.tsize), flags + 2 * kGlobalRounds};
+  hipLaunchKernelGGL(k_refine_tail, dim3(blocks_for(n, kTailRange)), dim3(kTailThreads), 0, st, ta);
+
+  // 4. Range queries over the settled order: share, size, id (and the cLPM
+  // signals), or the offline order.
+  hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
+                     ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr);
+  hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
+  if (off != nullptr) {
+    // PEEK-offline Phase 1 from the settled order (see OffSource).
     int64_t* start[2] = {(int64_t*)(w + L.start_a), (int64_t*)(w + L.start_b)};
     int32_t* npar[2] = {(int32_t*)(w + L.npar_a), (int32_t*)(w + L.npar_b)};
     int32_t* rnode = (int32_t*)(w + L.rnode);
     int64_t* roff = (int64_t*)(w + L.roff);
-    int cur = 0;
+    int pc = 0;
     if (n >= 2) {
       const OffArgs oa{n, lcp, el, ix, ib2, st2, L.nb2, npar[0], start[0], rnode, roff};
       const OffElem* sorted = msort::sort_from(OffSource{oa}, (OffElem*)(w + L.oel_a), (OffElem*)(w + L.oel_b),
-                                               L.onp, OffLess{}, q);
+                                               L.onp, OffLess{}, st);
       const int32_t m2 = 2 * n;
       int64_t* olocal = (int64_t*)(w + L.olocal);
       int64_t* opart = (int64_t*)(w + L.opart);
       int64_t* obase = (int64_t*)(w + L.obase);
       const unsigned sb = blocks_for(m2, kScanThreads);
-      hipLaunchKernelGGL(k_off_scan, dim3(sb), dim3(kScanThreads), 0, q, m2, n, sorted, olocal, opart);
-      hipLaunchKernelGGL(k_off_prefix, dim3(sb), dim3(kScanThreads), 0, q, m2, n, sorted, olocal, opart, obase);
-      hipLaunchKernelGGL(k_off_scatter, dim3(blocks_for(m2)), dim3(256), 0, q, m2, sorted, olocal, obase, start[0],
+      hipLaunchKernelGGL(k_off_scan, dim3(sb), dim3(kScanThreads), 0, st, m2, n, sorted, olocal, opart);
+      hipLaunchKernelGGL(k_off_prefix, dim3(sb), dim3(kScanThreads), 0, st, m2, n, sorted, olocal, opart, obase);
+      hipLaunchKernelGGL(k_off_scatter, dim3(blocks_for(m2)), dim3(256), 0, st, m2, sorted, olocal, obase, start[0],
                          roff);
       // a node's chain to the top has at most min(D, n) + 1 links
       const int64_t links = (int64_t)std::min(off->depth_limit, n) + 2;
       for (int64_t span = 1; span < links; span <<= 1) {
-        hipLaunchKernelGGL(k_off_jump, dim3(blocks_for(n)), dim3(256), 0, q, n, start[cur], npar[cur],
-                           start[cur ^ 1], npar[cur ^ 1]);
-        cur ^= 1;
+        hipLaunchKernelGGL(k_off_jump, dim3(blocks_for(n)), dim3(256), 0, st, n, start[pc], npar[pc],
+                           start[pc ^ 1], npar[pc ^ 1]);
+        pc ^= 1;
       }
     }
-    hipLaunchKernelGGL(k_off_place, dim3(blocks_for(n)), dim3(256), 0, q, n, el, rnode, roff, start[cur], off->perm);
-  };
-  auto final_stage = [&](hipStream_t q) {
-    hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, q, n, el, lcp, key2,
-                       ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr);
-    hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, q, st1, st2, L.nb1, L.nb2, L.levels);
-    if (off != nullptr) {
-      offline_stage(q);
-      return;
-    }
-    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, q, n, threshold, key2, lcp, el, ix, ib2, st2,
-                       L.nb2, cid, csz, cl);
+    hipLaunchKernelGGL(k_off_place, dim3(blocks_for(n)), dim3(256), 0, st, n, el, rnode, roff, start[pc], off->perm);
+  } else {
+    hipLaunchKernelGGL(k_final_query, dim3(blocks_for(n)), dim3(256), 0, st, n, threshold, key2, lcp, el, ix, ib2,
+                       st2, L.nb2, cid, csz, cl);
     if (cl.on) {
       const unsigned sb = blocks_for(n, kScanThreads);
-      hipLaunchKernelGGL(k_clpm_scan, dim3(sb), dim3(kScanThreads), 0, q, n, key2, local, cl);
+      hipLaunchKernelGGL(k_clpm_scan, dim3(sb), dim3(kScanThreads), 0, st, n, key2, local, cl);
       if (cl.score != nullptr)
-        hipLaunchKernelGGL(k_clpm_score, dim3(sb), dim3(kScanThreads), 0, q, n, key2, el, local, cl);
+        hipLaunchKernelGGL(k_clpm_score, dim3(sb), dim3(kScanThreads), 0, st, n, key2, el, local, cl);
     }
-  };
-  // The fixed part: anchor order and groups, a few refinement rounds and the
-  // final stage, all before the host looks at any flag. Each round's kernels
-  // read the previous round's flags and do nothing once the segments are
-  // settled. The first round picks its sort on the device (anchor groups are
-  // often large); later ones idle when a segment is too large for the
-  // segment sort, and the host then takes over from that round.
-  auto fixed = [&](hipStream_t q) {
-    const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
-                           flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr,
-                           off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
-    el = msort::sort_from(src, el_a, el_b, np, ClLess{}, q);
-    other = el == el_a ? el_b : el_a;
-    // The anchor order is sorted by last node first, so demand reads it
-    // directly: the prefix P rides along with the anchor groups, the
-    // difference along with the first round's compare.
-    DemandRide ride = no_ride;
-    unsigned prefix_blocks = 0, diff_blocks = 0;
-    if (ride_demand) {
-      ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
-      prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
-      diff_blocks = blocks_for(t->num_nodes);
-    }
-    hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, q, n, el,
-                       anchored ? *t : DeviceTree{}, nseg, gsize, depth[0], active[0], lcp, flags, ride);
-    for (int r = 1; r <= kSpeculativeRounds; ++r)
-      round(r, flags + 2 * (r - 1), flags + 2 * r, r == 1 ? kEither : kSeg, q, ride, r == 1 ? diff_blocks : 0);
-    final_stage(q);
-  };
-
-  fixed(st);
-  if (hflags.coherent) {
-    thread_local int32_t seq = 0;
-    seq = seq == INT32_MAX ? 1 : seq + 1;
-    hipLaunchKernelGGL(k_publish_flags, dim3(1), dim3(kWave), 0, st, flags, 2 * (kSpeculativeRounds + 1), hf, seq);
-    PEEK_HIP_TRY(hipGetLastError());
-    PEEK_HIP_TRY(wait_published(hf, seq, st));
-  } else {
-    PEEK_HIP_TRY(hipMemcpyAsync(hf, flags, sizeof(int32_t) * 2 * (kSpeculativeRounds + 1), hipMemcpyDeviceToHost,
-                                st));
-    PEEK_HIP_TRY(hipStreamSynchronize(st));
   }
-  int64_t r = 0;
-  // round 1 ran whatever its segment sizes; a later one only without a
-  // segment beyond the segment sort
-  while (r < kSpeculativeRounds && hf[2 * r] && (r == 0 || !hf[2 * r + 1])) ++r;
-  if (!hf[2 * r]) {
-    PEEK_HIP_TRY(hipGetLastError());
-    return PEEK_OK;   // settled after round r; the final stage saw the settled order
-  }
-  // The host drives the remaining rounds from the state after round r.
-  // Every round makes each still-active segment strictly deeper, so the loop
-  // ends after at most (longest prompt + 1) rounds; the cap only turns a
-  // broken invariant into an error instead of an endless loop.
-  const int32_t* fin = flags + 2 * r;
-  int32_t* spare[2] = {flags + 2 * (kSpeculativeRounds + 1), flags + 2 * (kSpeculativeRounds + 2)};
-  int32_t cur[2] = {hf[2 * r], hf[2 * r + 1]};
-  constexpr int64_t kMaxRounds = int64_t(1) << 31;
-  while (cur[0]) {
-    if (r > kMaxRounds) return fail(PEEK_ERR_DEVICE, "cluster refinement did not converge");
-    ++r;
-    int32_t* fout = spare[r & 1];
-    PEEK_HIP_TRY(hipMemsetAsync(fout, 0, sizeof(int32_t) * 2, st));
-    round(r, fin, fout, cur[1] != 0 ? kGlobal : kSeg, st, no_ride, 0);
-    fin = fout;
-    PEEK_HIP_TRY(hipMemcpyAsync(hf, fout, sizeof(int32_t) * 2, hipMemcpyDeviceToHost, st));
-    PEEK_HIP_TRY(hipStreamSynchronize(st));
-    cur[0] = hf[0];
-    cur[1] = hf[1];
-  }
-  final_stage(st);
   PEEK_HIP_TRY(hipGetLastError());
   return PEEK_OK;
 }
