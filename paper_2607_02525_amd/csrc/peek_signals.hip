@@ -159,22 +159,17 @@ struct ClLess {
   }
 };
 
-constexpr uint64_t kLenMax = 0x7FFFFFFFull;
+constexpr uint64_t kLenMax = 0x7FFFFFFFull;   // also the mask of a request in a key's low 31 bits
 
-// Largest segment the segment sort orders inside one workgroup. A round
-// that may sort globally does so when some active segment is larger; a
-// round that sorts per segment only leaves such a segment as it is (still
-// active, for the workgroup-local tail).
+// Largest segment the second round orders inside one workgroup.
 constexpr int kSegSortMax = 4096;
 
-// flags of a round: {any active segment, some active segment larger than
-// kSegSortMax}.
-__device__ __forceinline__ bool deferred(int32_t size, int32_t global) { return global == 0 && size > kSegSortMax; }
-
-struct AnchorKeys {
-  const ClElem* el;
-  __device__ __forceinline__ uint32_t operator()(int32_t i) const { return (uint32_t)(el[i].hi >> 32); }
-};
+// The second round takes the active segments of at most kSegSortMax
+// members: their members are compared in parallel, one wavefront each.
+// Larger segments wait, whole, for the tail. Flags after the first round:
+// {any active segment, some segment the second round takes}; the second
+// round runs only when the latter is set.
+__device__ __forceinline__ bool round_takes(int32_t size) { return size <= kSegSortMax; }
 
 __device__ __forceinline__ uint64_t tok_code(int32_t x) { return (uint64_t)((uint32_t)x ^ 0x80000000u) + 1; }
 __device__ __forceinline__ uint64_t lo_of(uint64_t code, uint32_t len) { return (code << 31) | (kLenMax - len); }
@@ -227,49 +222,255 @@ __device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, 
   return m;
 }
 
-// Anchor element of request i (the anchor sort builds its input with this):
-// key (last node, match length, next token, longest first). Positions past n are
-// padding that sorts last. Building element i also clears lcp[i]; element 0
-// also clears lcp[n], the round flags and the has_sharing output, which
-// later kernels of the pass expect zeroed.
-struct AnchorSource {
+// ---------------------------------------------------------------- first round
+// The first round starts from the walk: request r agrees with the cached
+// path of last_node[r] for match_len[r] = m tokens, so requests with equal
+// (last node c, m, next token) form an anchor group known to share m + 1
+// tokens (the "code" of a request that ended at m is 0). Each anchor group
+// is compared with its longest member from depth m + 1, and one sort by
+// (c, m, code, l, code after l, longest first) then gives the order after
+// that first round: a depth-first order of the cache tree with the queue
+// grafted on and every anchor group split by its head. Groups and heads
+// come from a hash table, so no sort precedes the compare:
+//  - k_first_clear empties the table (and clears the lcp array, the round
+//    flags and the has_sharing output);
+//  - k_first_insert puts every request's key into the table. A workgroup
+//    first groups its own 1024 requests in an LDS table, so a group of
+//    thousands touches the global table once per workgroup, not once per
+//    member (accesses to one global word serialize, atomic or not). Then
+//    each local group's representative inserts it globally: a slot holds
+//    the request that claimed it, and a probe compares keys by recomputing
+//    that request's key from the inputs, so no key is stored; an atomic
+//    maximum over (length, -request) picks the longest member, earliest on
+//    ties, and a second member anywhere marks the slot as shared. None of
+//    this depends on the order of the atomics.
+//  - k_first_compare (one wavefront per request, arrival order) compares
+//    every member of a group of two or more with the head.
+
+// Inputs of the first round: a request's anchor key is recomputed from them.
+struct AnchorIn {
   const int32_t* tokens;
   const int64_t* offsets;
-  const int32_t* last;   // NULL: unanchored (every request at the root)
+  const int32_t* last;   // NULL: unanchored (every request at the root, m = 0)
   const int32_t* mlen;
-  int32_t n;
-  int32_t* lcp;
-  int32_t* flags;
-  int32_t n_flags;
-  int32_t* sharing;   // NULL, or the has_sharing output (cleared here, raised by the final stage)
-  uint32_t len_cap;   // prompts are taken as their first len_cap tokens
-  __device__ __forceinline__ ClElem operator()(size_t i) const {
-    if (i <= (size_t)n) lcp[i] = 0;
-    if (i == 0) {
-      for (int f = 0; f < n_flags; ++f) flags[f] = 0;
-      lcp[n] = 0;
-      if (sharing) *sharing = 0;
-    }
-    ClElem e;
-    if (i < (size_t)n) {
-      const int64_t o = offsets[i];
-      const uint32_t len = min((uint32_t)(offsets[i + 1] - o), len_cap);
-      const uint32_t c = last ? (uint32_t)last[i] : 0u;
-      const uint32_t m = mlen ? (uint32_t)mlen[i] : 0u;
-      const uint64_t code = m < len ? tok_code(tokens[o + m]) : 0;
-      e.hi = ((uint64_t)c << 32) | m;
-      e.lo = lo_of(code, len);
-      e.req = (uint32_t)i;
-      e.len = len;
-    } else {
-      e.hi = ~0ull;
-      e.lo = ~0ull;
-      e.req = 0xFFFFFFFFu;
-      e.len = 0;
-    }
-    return e;
+  uint32_t len_cap;      // prompts are taken as their first len_cap tokens
+  __device__ __forceinline__ void key(uint32_t i, uint32_t& c, uint32_t& m, uint64_t& code, uint32_t& len) const {
+    const int64_t o = offsets[i];
+    len = min((uint32_t)(offsets[i + 1] - o), len_cap);
+    c = last ? (uint32_t)last[i] : 0u;
+    m = mlen ? (uint32_t)mlen[i] : 0u;
+    code = m < len ? tok_code(tokens[o + m]) : 0;
   }
 };
+
+// Hash table of anchor groups (capacity mask + 1, a power of two >= 2n).
+struct HeadTable {
+  uint32_t* rep;     // 0: empty; else the representative request + 1
+  uint64_t* best;    // max over the group of (len << 32) | (~request)
+  uint32_t* multi;   // nonzero once a second member has found the slot
+  int32_t* slot;     // [n] each request's slot
+  uint32_t mask;
+};
+
+__device__ __forceinline__ uint32_t group_hash(uint32_t c, uint32_t m, uint64_t code) {
+  uint64_t z = (((uint64_t)c << 32) | m) * 0x9E3779B97F4A7C15ull ^ code * 0xC2B2AE3D27D4EB4Full;
+  z ^= z >> 29;
+  z *= 0xBF58476D1CE4E5B9ull;
+  z ^= z >> 32;
+  return (uint32_t)z;
+}
+
+// Element of the first round's sort: hi = (c << 32) | m, mid = (code << 31) |
+// l, lo = (code after l << 31) | request. l and the request are below 2^31,
+// so the fields fit, and the request makes every key distinct.
+struct AncElem {
+  uint64_t hi, mid, lo;
+};
+struct AncLess {
+  __device__ __forceinline__ bool operator()(const AncElem& a, const AncElem& b) const {
+    return a.hi < b.hi || (a.hi == b.hi && (a.mid < b.mid || (a.mid == b.mid && a.lo < b.lo)));
+  }
+};
+// the compare's output as the sort's input, padded past n with keys that sort last
+struct AncSrc {
+  const AncElem* p;
+  int32_t n;
+  __device__ __forceinline__ AncElem operator()(size_t i) const {
+    if (i < (size_t)n) return p[i];
+    return AncElem{~0ull, ~0ull, ~0ull};
+  }
+};
+struct AncKeys {   // sorted last nodes, for the demand prefix
+  const AncElem* el;
+  __device__ __forceinline__ uint32_t operator()(int32_t i) const { return (uint32_t)(el[i].hi >> 32); }
+};
+__device__ __forceinline__ bool same_sub(const AncElem& a, const AncElem& b) {
+  return a.hi == b.hi && a.mid == b.mid && code_of(a.lo) == code_of(b.lo);
+}
+__device__ __forceinline__ bool sub_less(const AncElem& a, const AncElem& b) {
+  return a.hi < b.hi || (a.hi == b.hi && (a.mid < b.mid || (a.mid == b.mid && code_of(a.lo) < code_of(b.lo))));
+}
+
+__global__ void k_first_clear(HeadTable T, int32_t n, int32_t* __restrict__ lcp, uint64_t* __restrict__ head,
+                              int32_t* __restrict__ flags, int32_t n_flags, int32_t* sharing) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= (int64_t)T.mask) {
+    T.rep[i] = 0;
+    T.best[i] = 0;
+    T.multi[i] = 0;
+  }
+  if (i < n) head[i] = 0;
+  if (i <= n) lcp[i] = 0;
+  if (i < n_flags) flags[i] = 0;
+  if (i == 0 && sharing != nullptr) *sharing = 0;
+}
+
+constexpr int kInsThreads = 1024;
+constexpr int kInsSlots = 2 * kInsThreads;   // the workgroup's LDS table
+
+__global__ __launch_bounds__(kInsThreads) void k_first_insert(AnchorIn in, HeadTable T, int32_t n) {
+  __shared__ uint32_t lrep[kInsSlots];            // 0: empty; else the local representative + 1
+  __shared__ unsigned long long lbest[kInsSlots];
+  __shared__ uint32_t lcnt[kInsSlots];
+  __shared__ int32_t lglob[kInsSlots];            // the local group's global slot
+  __shared__ uint32_t kc[kInsThreads], km[kInsThreads];
+  __shared__ unsigned long long kcode[kInsThreads];
+  const int t = threadIdx.x;
+  for (int q = t; q < kInsSlots; q += kInsThreads) {
+    lrep[q] = 0;
+    lbest[q] = 0;
+    lcnt[q] = 0;
+  }
+  const int32_t i = (int32_t)blockIdx.x * kInsThreads + t;
+  const bool valid = i < n;
+  uint32_t c = 0, m = 0, len = 0;
+  uint64_t code = 0;
+  if (valid) {
+    in.key((uint32_t)i, c, m, code, len);
+    kc[t] = c;
+    km[t] = m;
+    kcode[t] = code;
+  }
+  __syncthreads();
+  uint32_t ls = 0;
+  if (valid) {
+    ls = group_hash(c, m, code) & (kInsSlots - 1);
+    // at most kInsThreads keys in 2 * kInsThreads slots
+    for (int probe = 0; probe < kInsSlots; ++probe) {
+      const uint32_t v = atomicCAS(&lrep[ls], 0u, (uint32_t)t + 1);
+      if (v == 0) break;
+      const uint32_t o = v - 1;
+      if (kc[o] == c && km[o] == m && kcode[o] == code) break;
+      ls = (ls + 1) & (kInsSlots - 1);
+    }
+    atomicMax(&lbest[ls], (unsigned long long)(((uint64_t)len << 32) | (0xFFFFFFFFu - (uint32_t)i)));
+    atomicAdd(&lcnt[ls], 1u);
+  }
+  __syncthreads();
+  if (valid && lrep[ls] == (uint32_t)t + 1) {
+    uint32_t h = group_hash(c, m, code) & T.mask;
+    bool first = false;
+    // at most n keys in more than 2n slots: an empty slot or the key is found
+    for (uint32_t probe = 0; probe <= T.mask; ++probe) {
+      uint32_t v = __hip_atomic_load(&T.rep[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (v == 0) {
+        v = atomicCAS(&T.rep[h], 0u, (uint32_t)i + 1);
+        if (v == 0) {
+          first = true;   // this workgroup's group represents the group
+          break;
+        }
+      }
+      uint32_t c2, m2, len2;
+      uint64_t code2;
+      in.key(v - 1, c2, m2, code2, len2);
+      if (c2 == c && m2 == m && code2 == code) break;
+      h = (h + 1) & T.mask;
+    }
+    lglob[ls] = (int32_t)h;
+    if (!first || lcnt[ls] >= 2) __hip_atomic_store(&T.multi[h], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t mine = lbest[ls];
+    if (__hip_atomic_load(&T.best[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < mine)
+      atomicMax((unsigned long long*)&T.best[h], (unsigned long long)mine);
+  }
+  __syncthreads();
+  if (valid) T.slot[i] = lglob[ls];
+}
+
+// Keys of a member j (length len_j) of a segment of depth d against the
+// segment's head h (length len_h): l = first mismatch from d, and j's token
+// there, or code 0 if j ended there. j may also run past the head's end.
+// One wavefront; the result is uniform across it.
+__device__ __forceinline__ void member_key(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets,
+                                           uint32_t j, uint32_t len_j, uint32_t h, uint32_t len_h, int32_t d,
+                                           int lane, uint32_t& ell, uint64_t& code) {
+  const int32_t* __restrict__ pj = tokens + offsets[j] + d;
+  const int32_t* __restrict__ ph = tokens + offsets[h] + d;
+  const int32_t lim = (int32_t)min(len_j, len_h) - d;
+  const int32_t l = cmp::first_mismatch(pj, ph, lim, lane);
+  ell = (uint32_t)l;
+  code = (l < lim || (int64_t)len_j > (int64_t)d + l) ? tok_code(pj[l]) : 0;
+}
+
+// The same key decided by one lane alone when the first mismatch (or an
+// end) comes within the first kShortKey tokens from d: the lane loads that
+// many tokens of both prompts at once. Returns false when they all agree,
+// and the whole wavefront then compares further (member_key).
+constexpr int kShortKey = 8;
+__device__ __forceinline__ bool short_key(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets,
+                                          uint32_t j, uint32_t len_j, uint32_t h, uint32_t len_h, int32_t d,
+                                          uint32_t& ell, uint64_t& code) {
+  const int32_t lim = (int32_t)min(len_j, len_h) - d;
+  const int32_t* __restrict__ pj = tokens + offsets[j] + d;
+  const int32_t* __restrict__ ph = tokens + offsets[h] + d;
+  int32_t a[kShortKey], b[kShortKey];
+#pragma unroll
+  for (int q = 0; q < kShortKey; ++q) {
+    a[q] = q < lim ? pj[q] : 0;
+    b[q] = q < lim ? ph[q] : 0;
+  }
+  int32_t l = min(lim, kShortKey), tok = 0;
+#pragma unroll
+  for (int q = kShortKey - 1; q >= 0; --q) {
+    if (q < lim && a[q] != b[q]) {
+      l = q;
+      tok = a[q];
+    }
+  }
+  if (l < min(lim, kShortKey)) {
+    ell = (uint32_t)l;
+    code = tok_code(tok);
+    return true;
+  }
+  if (lim > kShortKey) return false;
+  ell = (uint32_t)lim;   // agrees up to the shorter end
+  code = (int64_t)len_j > (int64_t)d + lim ? tok_code(pj[lim]) : 0;
+  return true;
+}
+
+// One wavefront per request, in arrival order: the request's sort element
+// after the first round. Members of a group of two or more that continues
+// past m are compared with the group's head from m + 1.
+__global__ __launch_bounds__(256) void k_first_compare(AnchorIn in, HeadTable T, int32_t n,
+                                                       AncElem* __restrict__ out) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
+  if (i >= n) return;
+  uint32_t c, m, len;
+  uint64_t code;
+  in.key((uint32_t)i, c, m, code, len);
+  uint32_t ell = 0;
+  uint64_t code1 = 0;
+  const int32_t h = T.slot[i];
+  if (code != 0 && T.multi[h] != 0) {
+    const uint64_t b = T.best[h];
+    const uint32_t head = 0xFFFFFFFFu - (uint32_t)b, hlen = (uint32_t)(b >> 32);
+    const int32_t d = (int32_t)m + 1;
+    if ((uint32_t)i == head) ell = len - (uint32_t)d;
+    else member_key(in.tokens, in.offsets, (uint32_t)i, len, head, hlen, d, lane, ell, code1);
+  }
+  if (lane == 0)
+    out[i] = AncElem{((uint64_t)c << 32) | m, (code << 31) | ell, (code1 << 31) | (uint32_t)i};
+}
 
 // Start of every lane's group, for the 64 sorted positions base..base+63 of
 // this wavefront: the nearest group start at or before the lane inside the
@@ -288,18 +489,27 @@ __device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ e
   return below ? base + (63 - __clzll((unsigned long long)below)) : g0;
 }
 
-// Groups of equal (node, match length, next token) after the anchor sort.
-// flags[0] is raised if any group needs refinement, flags[1] if such a
-// group is too large for the in-LDS segment sort. gsize[g] is written at
-// every group start g.
-// Extra blocks (ride) compute the demand prefix P from the same sorted order.
-__global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* __restrict__ el, DeviceTree t,
-                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
-                                                       int32_t* __restrict__ depth, uint8_t* __restrict__ active,
-                                                       int32_t* __restrict__ lcp, int32_t* __restrict__ flags,
-                                                       DemandRide ride) {
+// Segments after the first round's sort: a segment is a run of equal
+// (c, m, code, l, code after l); requests of different anchor groups share
+// what the cache tree says (the same node: the smaller m; an ancestor's
+// group first: its m; otherwise the depth of the nodes' lowest common
+// ancestor), members of one anchor group split by the head share m + 1 plus
+// the smaller l. A segment of two or more that still continues (both codes
+// nonzero) is active at depth m + l + 2, and its longest member (the next
+// round's head) goes to head[start] as max (len << 32 | ~request): a
+// segmented maximum across each wavefront, then one atomic per wavefront
+// and segment. The elements are written out as the refinement's (request,
+// length) pairs. flags[0] is raised if a segment is active, flags[1] if one
+// of them is one the second round takes. Extra blocks (ride) compute the
+// demand prefix P from the same order (sorted by last node first).
+__global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* __restrict__ sd, AnchorIn in,
+                                                      DeviceTree t, ClElem* __restrict__ el,
+                                                      int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
+                                                      int32_t* __restrict__ depth, uint8_t* __restrict__ active,
+                                                      uint64_t* __restrict__ head, int32_t* __restrict__ lcp,
+                                                      int32_t* __restrict__ flags, DemandRide ride) {
   if ((int32_t)blockIdx.x >= ride.first_block) {
-    demand_prefix_block(AnchorKeys{el}, n, ride.nn, ride.P, (int32_t)blockIdx.x - ride.first_block);
+    demand_prefix_block(AncKeys{sd}, n, ride.nn, ride.P, (int32_t)blockIdx.x - ride.first_block);
     return;
   }
   const int lane = threadIdx.x & (kWave - 1);
@@ -307,41 +517,73 @@ __global__ __launch_bounds__(256) void k_anchor_groups(int32_t n, const ClElem* 
   if (base >= n) return;
   const int32_t i = base + lane;
   const bool valid = i < n;
-  ClElem e{};
+  AncElem e{};
   bool start = false;
   if (valid) {
-    e = el[i];
-    start = i == 0 || !same_group(el[i - 1], e);
+    e = sd[i];
+    start = i == 0 || !same_sub(sd[i - 1], e);
   }
-  const bool lane0_start = __ballot(start) & 1ull;
-  const int32_t g = lane_group_start(el, base, lane, start, !lane0_start, 0);
+  // the start of every lane's segment: inside the wave from the ballot, else
+  // one shared wave search back from the wave's first position
+  const uint64_t mask = __ballot(start);
+  const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
+  const uint64_t below = mask & upto;
+  int32_t g0 = base;
+  if (!(mask & 1ull)) {
+    const AncElem b0 = sd[base];
+    g0 = wave_first_true(0, base, lane, [&](int32_t q) { return !sub_less(sd[q], b0); });
+  }
+  const int32_t g = below ? base + (63 - __clzll((unsigned long long)below)) : g0;
+  const uint32_t req = (uint32_t)(e.lo & kLenMax);
+  uint32_t len = 0;
+  if (valid) {
+    const int64_t o = in.offsets[req];
+    len = min((uint32_t)(in.offsets[req + 1] - o), in.len_cap);
+  }
+  // longest member of each segment: segmented maximum over the wave's lanes
+  uint64_t best = valid ? (((uint64_t)len << 32) | (0xFFFFFFFFu - req)) : 0;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint64_t ob = __shfl_down(best, off);
+    const int32_t og = __shfl_down(g, off);
+    if (lane + off < kWave && og == g && best < ob) best = ob;
+  }
   if (!valid) return;
-  nseg[i] = g;
   const uint32_t m = (uint32_t)e.hi;
-  const uint64_t code = code_of(e.lo);
-  const bool last = i + 1 == n || !same_group(e, el[i + 1]);
+  const uint64_t code = e.mid >> 31;
+  const uint32_t ell = (uint32_t)(e.mid & kLenMax);
+  const uint64_t code1 = code_of(e.lo);
+  const bool act_seg = code != 0 && code1 != 0;   // continues past the split (if it has two members)
+  if (act_seg && (lane == 0 || i == g)) atomicMax((unsigned long long*)&head[g], (unsigned long long)best);
+  el[i] = ClElem{0, 0, req, len};
+  nseg[i] = g;
+  const bool last = i + 1 == n || !same_sub(e, sd[i + 1]);
   if (last) {
-    const int32_t size = i - g + 1;
-    gsize[g] = size;
-    if (code != 0 && size >= 2 && size > kSegSortMax) flags[1] = 1;
+    gsize[g] = i - g + 1;
+    if (act_seg && i > g && round_takes(i - g + 1)) flags[1] = 1;
   }
   if (i == g) {
     if (i > 0) {
-      const ClElem p = el[i - 1];
-      const uint32_t c1 = (uint32_t)(p.hi >> 32), m1 = (uint32_t)p.hi;
-      const uint32_t c2 = (uint32_t)(e.hi >> 32);
+      const AncElem p = sd[i - 1];
       int32_t v;
-      if (c1 == c2) v = (int32_t)min(m1, m);
-      else if (c2 < (uint32_t)t.nodes[c1].subtree_end) v = (int32_t)m1;
-      else v = lca_depth(t, (int32_t)c1, (int32_t)c2);
+      if (p.hi == e.hi && (p.mid >> 31) == code) {
+        v = (int32_t)(m + 1 + (uint32_t)(p.mid & kLenMax));   // split by the head: the smaller l is p's
+      } else {
+        const uint32_t c1 = (uint32_t)(p.hi >> 32), m1 = (uint32_t)p.hi;
+        const uint32_t c2 = (uint32_t)(e.hi >> 32);
+        if (c1 == c2) v = (int32_t)min(m1, m);
+        else if (c2 < (uint32_t)t.nodes[c1].subtree_end) v = (int32_t)m1;
+        else v = lca_depth(t, (int32_t)c1, (int32_t)c2);
+      }
       lcp[i] = v;
     }
-    const bool act = code != 0 && !last;
+    const bool act = act_seg && !last;
     active[i] = act;
-    depth[i] = act ? (int32_t)m + 1 : 0;
+    depth[i] = act ? (int32_t)(m + ell + 2) : 0;
     if (act) flags[0] = 1;
   } else if (code == 0) {
-    lcp[i] = (int32_t)m;   // identical prompts of length m
+    lcp[i] = (int32_t)m;             // identical prompts that ended at m
+  } else if (code1 == 0) {
+    lcp[i] = (int32_t)(m + 1 + ell); // identical prompts that ended together after m
   }
 }
 
@@ -353,57 +595,37 @@ __device__ __forceinline__ int32_t head_pos(int32_t s, int32_t d, int32_t size) 
   return s + (int32_t)(ldssort::mix32((uint32_t)s * 0x9E3779B9u ^ (uint32_t)d * 0x85EBCA6Bu) % (uint32_t)size);
 }
 
-// Key of a member j (length len_j) of a segment of depth d against the
-// segment's head h (length len_h): l = first mismatch from d, and j's token
-// there, or code 0 if j ended there. j may also run past the head's end.
-// One wavefront; the result is uniform across it.
-__device__ __forceinline__ void member_key(const int32_t* __restrict__ tokens, const int64_t* __restrict__ offsets,
-                                           uint32_t j, uint32_t len_j, uint32_t h, uint32_t len_h, int32_t d,
-                                           int lane, uint32_t& ell, uint64_t& code) {
-  const int32_t* __restrict__ pj = tokens + offsets[j] + d;
-  const int32_t* __restrict__ ph = tokens + offsets[h] + d;
-  const int32_t lim = (int32_t)min(len_j, len_h) - d;
-  const int32_t l = cmp::first_mismatch(pj, ph, lim, lane);
-  ell = (uint32_t)l;
-  code = (l < lim || (int64_t)len_j > (int64_t)d + l) ? tok_code(pj[l]) : 0;
-}
-
-// One wavefront per position: rewrite every element's key for the next sort;
-// members of active segments are compared with their segment's first member,
-// its longest (the sort keeps the longest first in every group). Nothing to
-// do when the previous round left no active segment (flags_in[0] = 0). In a
-// round that sorts per segment only (global = 0), a segment beyond the
-// segment sort keeps its keys and waits for the tail.
+// Second round, a wavefront per position (grid-stride, so a skipped round
+// costs few workgroups): members of the segments the round takes are
+// compared with their segment's first member, its longest
+// (the first round's sort keeps the longest first in every segment), and
+// get their keys for the segment sort. Nothing to do unless the first round
+// left such a segment (flags_in[1]).
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
                                                         const int32_t* __restrict__ gsize,
                                                         const int32_t* __restrict__ depth,
                                                         const uint8_t* __restrict__ active,
-                                                        const int32_t* __restrict__ flags_in, int32_t global,
-                                                        DemandRide ride) {
-  if ((int32_t)blockIdx.x >= ride.first_block) {
-    demand_diff_at(ride.nodes, ride.nn, ride.P, ride.demand,
-                   ((int32_t)blockIdx.x - ride.first_block) * (int32_t)blockDim.x + (int32_t)threadIdx.x);
-    return;
-  }
-  if (flags_in[0] == 0) return;
+                                                        const uint64_t* __restrict__ head,
+                                                        const int32_t* __restrict__ flags_in) {
+  if (flags_in[1] == 0) return;
   const int lane = threadIdx.x & (kWave - 1);
-  const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
-  if (i >= n) return;
-  const int32_t s = nseg[i];
-  if (!active[s]) {
-    if (lane == 0) el[i].hi = (uint64_t)(uint32_t)s << 32;
-    return;
-  }
-  if (deferred(gsize[s], global)) return;
-  const uint32_t len_j = el[i].len;
-  uint32_t ell = len_j - (uint32_t)depth[s];   // the head (s) itself: ended at its length
-  uint64_t code = 0;
-  if (i != s) member_key(tokens, offsets, el[i].req, len_j, el[s].req, el[s].len, depth[s], lane, ell, code);
-  if (lane == 0) {
-    el[i].hi = ((uint64_t)(uint32_t)s << 32) | ell;
-    el[i].lo = lo_of(code, len_j);
+  const int32_t waves = (int32_t)gridDim.x * 4;
+  for (int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)); i < n;
+       i += waves) {
+    const int32_t s = nseg[i];
+    if (!active[s] || !round_takes(gsize[s])) continue;
+    const uint64_t hb = head[s];
+    const uint32_t hreq = 0xFFFFFFFFu - (uint32_t)hb, hlen = (uint32_t)(hb >> 32);
+    const uint32_t req = el[i].req, len_j = el[i].len;
+    uint32_t ell = len_j - (uint32_t)depth[s];   // the head itself: ended at its length
+    uint64_t code = 0;
+    if (req != hreq) member_key(tokens, offsets, req, len_j, hreq, hlen, depth[s], lane, ell, code);
+    if (lane == 0) {
+      el[i].hi = ((uint64_t)(uint32_t)s << 32) | ell;
+      el[i].lo = lo_of(code, len_j);
+    }
   }
 }
 
@@ -431,54 +653,43 @@ constexpr int kSegThreads = 512;           // one thread per member of a medium 
 constexpr int kSegMid = kSegThreads;       // members ranked against LDS keys
 constexpr int kSegRange = 256;             // positions (and segment starts) owned by one workgroup
 
-// Sorts every active segment of at most kSegSortMax members from `in` into
-// `out`, stably by key (in place when they are the same buffer; otherwise
-// every position outside a sorted segment is copied across). Each
-// workgroup owns the positions in kSegRange consecutive places and the
-// segments starting there:
-//  - a segment of at most 64 members is ranked by one wavefront;
-//  - up to kSegMid members, by the whole workgroup, one member per thread,
-//    against the segment's keys staged in LDS (every read is a broadcast);
-//  - up to kSegSortMax, by the workgroup's LDS merge sort.
-// A member's rank is the number of members that order before it, ties by
-// position. A round that sorts globally (global, with some segment beyond
-// kSegSortMax) leaves everything to the global sort.
-__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, const ClElem* __restrict__ in,
-                                                                 ClElem* __restrict__ out,
+// Second round: sorts, in place and stably by key, every segment the round
+// takes. Each workgroup owns the segments starting in kSegRange
+// consecutive positions: one of at most 64 members is ranked by one
+// wavefront; one of at most kSegMid members by the whole workgroup, one
+// member per thread, against its keys staged in LDS (every read is a
+// broadcast); a larger one is sorted by the workgroup's LDS merge sort. A
+// member's rank counts the members before it, ties by position. Elements
+// move through registers, so reading and writing one buffer is safe.
+__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClElem* __restrict__ el,
                                                                  const int32_t* __restrict__ nseg,
                                                                  const int32_t* __restrict__ gsize,
                                                                  const uint8_t* __restrict__ active,
-                                                                 const int32_t* __restrict__ flags_in,
-                                                                 int32_t global) {
-  if (global != 0 && flags_in[0] != 0 && flags_in[1] != 0) return;
+                                                                 const int32_t* __restrict__ flags_in) {
+  if (flags_in[1] == 0) return;
   __shared__ SegKey sk[kSegMid];
   __shared__ uint64_t sa[kSegSortMax];
   __shared__ uint64_t sb[kSegSortMax];
   __shared__ uint32_t sp[kSegSortMax];
-  __shared__ int32_t mid[kSegRange / 64 + 1];
-  __shared__ int32_t n_mid;
+  __shared__ int32_t take[kSegRange / 64 + 1];
+  __shared__ int32_t n_take;
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   const int wave = t / kWave;
   const int32_t r0 = (int32_t)blockIdx.x * kSegRange;
-  if (in != out) {
-    for (int32_t p = r0 + t; p < min(n, r0 + kSegRange); p += kSegThreads) {
-      const int32_t q = nseg[p];
-      if (flags_in[0] == 0 || !active[q] || deferred(gsize[q], global)) out[p] = in[p];
-    }
-  }
-  if (flags_in[0] == 0) return;
-  if (t == 0) n_mid = 0;
+  if (t == 0) n_take = 0;
   __syncthreads();
-  // small segments: wave w looks at the starts r0 + 32w .. r0 + 32w + 31
+  // segments of at most 64 members: wave w looks at the starts r0 + 32w ..
+  // r0 + 32w + 31; larger ones (at most one start per 64 positions) are
+  // listed for the whole workgroup
   constexpr int kPerWave = kSegRange / (kSegThreads / kWave);
   static_assert(kPerWave <= kWave, "one start per lane");
   {
     const int32_t p = r0 + wave * kPerWave + lane;
     bool small = false;
-    if (lane < kPerWave && p < n && nseg[p] == p && active[p] && !deferred(gsize[p], global)) {
+    if (lane < kPerWave && p < n && nseg[p] == p && active[p] && round_takes(gsize[p])) {
       if (gsize[p] <= kWave) small = true;
-      else mid[atomicAdd(&n_mid, 1)] = p;   // members > 64: at most one start per 64 positions
+      else take[atomicAdd(&n_take, 1)] = p;
     }
     uint64_t todo = __ballot(small);
     while (todo) {
@@ -487,7 +698,7 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, cons
       const int32_t s = r0 + wave * kPerWave + f;
       const int32_t size = gsize[s];
       ClElem e{};
-      if (lane < size) e = in[s + lane];
+      if (lane < size) e = el[s + lane];
       int rank = 0;
       const ClLess less;
       for (int j = 0; j < size; ++j) {
@@ -496,18 +707,18 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, cons
         o.lo = __shfl(e.lo, j);
         if (less(o, e) || (j < lane && !less(e, o))) ++rank;
       }
-      if (lane < size) out[s + rank] = e;
+      if (lane < size) el[s + rank] = e;
     }
   }
   __syncthreads();
-  const int32_t nm = n_mid;
-  for (int b = 0; b < nm; ++b) {
-    const int32_t s = mid[b];
+  const int32_t nt = n_take;
+  for (int b = 0; b < nt; ++b) {
+    const int32_t s = take[b];
     const int32_t size = gsize[s];
     if (size <= kSegMid) {
       SegKey v{};
       if (t < size) {
-        v = seg_key(in[s + t]);
+        v = seg_key(el[s + t]);
         sk[t] = v;
       }
       __syncthreads();
@@ -517,14 +728,14 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, cons
           const SegKey o = sk[j];
           rank += (seg_less(o, v) || (j < t && !seg_less(v, o))) ? 1 : 0;
         }
-        out[s + rank] = seg_elem(v, s);
+        el[s + rank] = seg_elem(v, s);
       }
       __syncthreads();
     } else {
       const int M = ldssort::pow2_at_least(size);
       for (int r = t; r < M; r += kSegThreads) {
         if (r < size) {
-          const ClElem e = in[s + r];
+          const ClElem e = el[s + r];
           sa[r] = ell_of(e.hi);
           sb[r] = e.lo;
           sp[r] = (uint32_t)r;
@@ -536,27 +747,28 @@ __global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, cons
       }
       __syncthreads();
       ldssort::lds_sort<kSegThreads>(sa, sb, sp, M);
-      // through registers: in and out may be the same buffer
       constexpr int kPer = kSegSortMax / kSegThreads;
       ClElem v[kPer];
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int r = t + q * kSegThreads;
-        if (r < size) v[q] = in[s + sp[r]];
+        if (r < size) v[q] = el[s + sp[r]];
       }
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int r = t + q * kSegThreads;
-        if (r < size) out[s + r] = v[q];
+        if (r < size) el[s + r] = v[q];
       }
       __syncthreads();
     }
   }
 }
 
-// After the refinement sort: new groups, their LCPs, depths, sizes and
-// activity.
+// Second round, after the segment sort: new groups of the segments the
+// round took, their LCPs, depths, sizes and activity; every other segment
+// start carries its state over (a segment the round did not take stays
+// active for the tail). flags[0] is raised if any segment is still active.
 __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* __restrict__ el,
                                                        int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
                                                        const int32_t* __restrict__ depth_old,
@@ -564,8 +776,8 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
                                                        int32_t* __restrict__ depth_new,
                                                        uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
                                                        const int32_t* __restrict__ flags_in,
-                                                       int32_t* __restrict__ flags, int32_t global) {
-  if (flags_in[0] == 0) return;
+                                                       int32_t* __restrict__ flags) {
+  if (flags_in[1] == 0) return;
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -578,7 +790,7 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
     e = el[i];
     s = nseg[i];
     live = active_old[s] != 0;
-    wait = live && deferred(gsize[s], global);   // kept whole for the tail
+    wait = live && !round_takes(gsize[s]);   // kept whole for the tail
     live = live && !wait;
     start = live && (i == s || !same_group(el[i - 1], e));
   }
@@ -601,11 +813,7 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
   const uint64_t code = code_of(e.lo);
   const bool last = i + 1 == n || !same_group(e, el[i + 1]);
   const bool can_split = code != 0;
-  if (last) {
-    const int32_t size = i - g + 1;
-    gsize[g] = size;
-    if (can_split && size >= 2 && size > kSegSortMax) flags[1] = 1;
-  }
+  if (last) gsize[g] = i - g + 1;
   if (i == g) {
     if (i > s) lcp[i] = d + (int32_t)min(ell_of(el[i - 1].hi), ell);
     const bool act = can_split && !last;
@@ -634,7 +842,7 @@ __global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* 
 // and passes repeat until nothing is active. Every round makes each active
 // group strictly deeper or settles it, so the loop ends.
 constexpr int kTailRange = 1024;
-constexpr int kTailThreads = 1024;
+constexpr int kTailThreads = 512;
 constexpr int kTailWaves = kTailThreads / kWave;
 constexpr int kTailCap = 4096;              // members the workgroup sorts in LDS
 constexpr int kTailList = 1024;              // sub-segments collected per pass and kind
@@ -645,17 +853,17 @@ struct TailArgs {
   const int32_t* tokens;
   const int64_t* offsets;
   int32_t n;
-  ClElem* el;                // the order after the global rounds, refined in place
+  ClElem* el;                // the order after the queue-wide rounds, refined in place
   ClElem* tmp;               // free element buffer (scratch of the global-memory ranking)
-  const int32_t* nseg;       // state after the last global round (read only here)
+  const int32_t* nseg;       // state after the queue-wide rounds (read only here)
   const int32_t* gsize;
-  const int32_t* depth;
-  const uint8_t* active;
+  const int32_t* depth[2];   // segment depth and activity after the first round [0] or the second [1]
+  const uint8_t* active[2];
+  const int32_t* flags[2];   // flags after the first round [0] and after the second [1]
   int32_t* lcp;
   uint8_t* tact;             // tail state by position: an active sub-segment starts here
   int32_t* tdep;             //   its depth
   int32_t* tsize;            //   its size
-  const int32_t* flags_in;   // the last global round's flags
 };
 
 __device__ __forceinline__ bool tail_key_less(uint32_t ea, uint64_t ca, uint32_t ra, uint32_t eb, uint64_t cb,
@@ -686,24 +894,27 @@ __device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int
     const int32_t gd = __shfl(d, gs);
     const int hl = head_pos(s + gs, gd, gz) - s;
     const uint32_t hreq = __shfl(e.req, hl), hlen = __shfl(e.len, hl);
+    const bool mem = in && lane >= gs && lane < gs + gz;
+    // every member's key: each lane first checks its own member's first
+    // tokens; members that agree on all of them are compared by the whole
+    // wavefront, one after another
     uint32_t ell = 0;
     uint64_t code = 0;
-    for (int j = gs; j < gs + gz; ++j) {
-      const uint32_t jreq = __shfl(e.req, j), jlen = __shfl(e.len, j);
+    bool need = false;
+    if (mem) {
+      if (lane == hl) ell = e.len - (uint32_t)gd;
+      else need = !short_key(A.tokens, A.offsets, e.req, e.len, hreq, hlen, gd, ell, code);
+    }
+    for (uint64_t todo = __ballot(need); todo; todo &= todo - 1) {
+      const int j = __ffsll((unsigned long long)todo) - 1;
       uint32_t le;
       uint64_t lc;
-      if (j == hl) {
-        le = jlen - (uint32_t)gd;
-        lc = 0;
-      } else {
-        member_key(A.tokens, A.offsets, jreq, jlen, hreq, hlen, gd, lane, le, lc);
-      }
+      member_key(A.tokens, A.offsets, __shfl(e.req, j), __shfl(e.len, j), hreq, hlen, gd, lane, le, lc);
       if (lane == j) {
         ell = le;
         code = lc;
       }
     }
-    const bool mem = in && lane >= gs && lane < gs + gz;
     int rank = 0;
     for (int j = gs; j < gs + gz; ++j) {
       const uint32_t oe = __shfl(ell, j);
@@ -769,17 +980,30 @@ __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t 
   const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
   const int32_t hp = head_pos(s, d, sz);
   const uint32_t hreq = A.el[hp].req, hlen = A.el[hp].len;
-  for (int32_t j = wave; j < sz; j += kTailWaves) {
-    const uint32_t jreq = A.el[s + j].req, jlen = A.el[s + j].len;
-    uint32_t ell;
-    uint64_t code;
-    if (s + j == hp) {
-      ell = jlen - (uint32_t)d;
-      code = 0;
-    } else {
-      member_key(A.tokens, A.offsets, jreq, jlen, hreq, hlen, d, lane, ell, code);
+  // 64 members per wavefront at a time: each lane checks its member's first
+  // tokens, the wavefront compares the rest one member after another
+  for (int32_t b0 = wave * kWave; b0 < sz; b0 += kTailWaves * kWave) {
+    const int32_t j = b0 + lane;
+    uint32_t jreq = 0, jlen = 0, ell = 0;
+    uint64_t code = 0;
+    bool need = false;
+    if (j < sz) {
+      jreq = A.el[s + j].req;
+      jlen = A.el[s + j].len;
+      if (s + j == hp) ell = jlen - (uint32_t)d;
+      else need = !short_key(A.tokens, A.offsets, jreq, jlen, hreq, hlen, d, ell, code);
     }
-    if (lane == 0) {
+    for (uint64_t todo = __ballot(need); todo; todo &= todo - 1) {
+      const int f = __ffsll((unsigned long long)todo) - 1;
+      uint32_t le;
+      uint64_t lc;
+      member_key(A.tokens, A.offsets, __shfl(jreq, f), __shfl(jlen, f), hreq, hlen, d, lane, le, lc);
+      if (lane == f) {
+        ell = le;
+        code = lc;
+      }
+    }
+    if (j < sz) {
       A.el[s + j].hi = ((uint64_t)ell << 33) | code;
       A.el[s + j].lo = jreq;
     }
@@ -885,7 +1109,11 @@ __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t 
 }
 
 __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
-  if (A.flags_in[0] == 0) return;
+  // the state the second round left, or the first round's when it did not run
+  const int r2 = A.flags[0][1] != 0 ? 1 : 0;
+  if (A.flags[r2][0] == 0) return;
+  const int32_t* depth = A.depth[r2];
+  const uint8_t* active = A.active[r2];
   __shared__ uint64_t sa[kTailCap];
   __shared__ uint64_t sb[kTailCap];
   __shared__ uint32_t sp[kTailCap];
@@ -899,7 +1127,7 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
   if (t == 0) n_roots = 0;
   __syncthreads();
   for (int32_t p = p0 + t; p < p1; p += kTailThreads) {
-    if (A.nseg[p] == p && A.active[p]) {
+    if (A.nseg[p] == p && active[p]) {
       const int k = atomicAdd(&n_roots, 1);
       root_s[k] = p;
       root_e[k] = p + A.gsize[p];
@@ -912,7 +1140,7 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
     const int32_t s = root_s[k], e = root_e[k];
     for (int32_t q = s + t; q < e; q += kTailThreads) A.tact[q] = q == s;
     if (t == 0) {
-      A.tdep[s] = A.depth[s];
+      A.tdep[s] = depth[s];
       A.tsize[s] = e - s;
     }
   }
@@ -1000,7 +1228,12 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
                                                       int32_t* __restrict__ ib1, uint64_t* __restrict__ ib2,
                                                       int64_t ib_stride, int32_t* __restrict__ st1,
                                                       uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2,
-                                                      ClpmArgs cl, bool key_is_request) {
+                                                      ClpmArgs cl, bool key_is_request, DemandRide ride) {
+  if ((int32_t)blockIdx.x >= ride.first_block) {
+    demand_diff_at(ride.nodes, ride.nn, ride.P, ride.demand,
+                   ((int32_t)blockIdx.x - ride.first_block) * (int32_t)blockDim.x + (int32_t)threadIdx.x);
+    return;
+  }
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
   const int32_t i = b * kWave + lane;
@@ -1490,16 +1723,14 @@ int levels_for(int64_t nb) {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Refinement rounds run over the whole queue before the workgroup-local
-// tail. Flag pairs: slot 0 for the anchor groups, slot r for round r.
-constexpr int kGlobalRounds = 2;
-static_assert(kGlobalRounds >= 1, "the first round carries the demand difference");
-constexpr int kFlagPairs = kGlobalRounds + 1;
+// Flag pairs: slot 0 after the first round, slot 1 after the second.
+constexpr int kFlagPairs = 2;
 
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
   size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
-      keys_b, prefix, diff, pmin, run, local, part, sharing, tact, tdep, tsize, total, flags_bytes;
+      keys_b, prefix, diff, pmin, run, local, part, sharing, anc_a, anc_b, hrep, hbest, hmulti, hslot, hcap, head, tact,
+      tdep, tsize, total, flags_bytes;
   // PEEK-offline Phase 1 only
   size_t oel_a, oel_b, olocal, opart, obase, start_a, start_b, npar_a, npar_b, rnode, roff, onp;
   int64_t ib_stride;
@@ -1546,6 +1777,15 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.local = take(sizeof(int64_t) * nn);
   L.part = take(sizeof(int64_t) * (((size_t)n + kScanThreads - 1) / kScanThreads + 1));
   L.sharing = take(sizeof(int32_t));
+  L.anc_a = take(sizeof(AncElem) * np);
+  L.anc_b = take(sizeof(AncElem) * np);
+  L.hcap = 256;
+  while (L.hcap < 2 * nn) L.hcap <<= 1;
+  L.hrep = take(sizeof(uint32_t) * L.hcap);
+  L.hbest = take(sizeof(uint64_t) * L.hcap);
+  L.hmulti = take(sizeof(uint32_t) * L.hcap);
+  L.hslot = take(sizeof(int32_t) * nn);
+  L.head = take(sizeof(uint64_t) * nn);
   L.tact = take(nn);
   L.tdep = take(sizeof(int32_t) * nn);
   L.tsize = take(sizeof(int32_t) * nn);
@@ -1639,7 +1879,6 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   uint64_t* st2 = (uint64_t*)(w + L.st2);
   int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
-  int cur = 0;   // bufs[cur] holds the current order
   ClpmArgs cl{};
   if (clpm != nullptr) {
     cl.h = clpm->h;
@@ -1657,64 +1896,62 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   int64_t* local = (int64_t*)(w + L.local);
   const LcpIndex ix{ib1, L.ib_stride, st1, L.nb1, L.levels, n};
 
-  // 1. Anchor order: sorted by (last node, match length, next token).
-  const AnchorSource src{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr, n, lcp,
-                         flags, (int32_t)(L.flags_bytes / sizeof(int32_t)), cl.on ? cl.sharing : nullptr,
-                         off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
-  cur = msort::sort_from(src, bufs[0], bufs[1], np, ClLess{}, st) == bufs[0] ? 0 : 1;
-  // The anchor order is sorted by last node first, so demand reads it
-  // directly: the prefix P rides along with the anchor groups, the
-  // difference along with the first round's compare.
+  // 1. The first round: anchor groups and their heads from a hash table,
+  // every member compared with its head, one sort, then the segments.
+  const HeadTable T{(uint32_t*)(w + L.hrep), (uint64_t*)(w + L.hbest), (uint32_t*)(w + L.hmulti),
+                    (int32_t*)(w + L.hslot), (uint32_t)(L.hcap - 1)};
+  const AnchorIn ain{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr,
+                     off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
+  const int32_t n_flags = (int32_t)(L.flags_bytes / sizeof(int32_t));
+  const int64_t clear_span = std::max<int64_t>(std::max<int64_t>((int64_t)L.hcap, (int64_t)n + 1), n_flags);
+  uint64_t* head = (uint64_t*)(w + L.head);
+  hipLaunchKernelGGL(k_first_clear, dim3(blocks_for(clear_span)), dim3(256), 0, st, T, n, lcp, head, flags, n_flags,
+                     cl.on ? cl.sharing : nullptr);
+  hipLaunchKernelGGL(k_first_insert, dim3(blocks_for(n, kInsThreads)), dim3(kInsThreads), 0, st, ain, T, n);
+  AncElem* anc_a = (AncElem*)(w + L.anc_a);
+  AncElem* anc_b = (AncElem*)(w + L.anc_b);
+  hipLaunchKernelGGL(k_first_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, ain, T, n, anc_a);
+  const AncElem* sorted = msort::sort_from(AncSrc{anc_a, n}, anc_a, anc_b, np, AncLess{}, st);
+  // The order is sorted by last node first, so demand reads it directly: the
+  // prefix P rides along with the segment kernel, the difference along with
+  // the final stage's first kernel.
   const bool ride_demand = demand != nullptr && anchored;
   DemandRide ride{nullptr, nullptr, nullptr, 0, INT32_MAX};
-  unsigned prefix_blocks = 0, diff_blocks = 0;
+  unsigned prefix_blocks = 0;
   if (ride_demand) {
     ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
     prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
-    diff_blocks = blocks_for(t->num_nodes);
   }
-  hipLaunchKernelGGL(k_anchor_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, bufs[cur],
-                     anchored ? *t : DeviceTree{}, nseg, gsize, depth[0], active[0], lcp, flags, ride);
+  hipLaunchKernelGGL(k_first_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, sorted, ain,
+                     anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth[0], active[0], head, lcp, flags, ride);
 
-  // 2. Refinement rounds over the whole queue. Round r compares every member
-  // of an active segment with its head, sorts by the new keys and splits the
-  // segments. The first round sorts globally when some segment is larger
-  // than the segment sort takes (both sorts are launched, each gated on the
-  // flag that selects it); later ones sort per segment and leave a larger
-  // segment to the tail. A round whose flags say nothing is active only
-  // carries the order into its output buffer.
-  for (int r = 1; r <= kGlobalRounds; ++r) {
-    const int32_t global = r == 1;
-    const int32_t* fin = flags + 2 * (r - 1);
-    int32_t* fout = flags + 2 * r;
-    const int32_t* dep = depth[(r - 1) & 1];
-    const uint8_t* act = active[(r - 1) & 1];
-    ClElem* in = bufs[cur];
-    const unsigned cmp_blocks = blocks_for(n, 4);
-    const unsigned ride_blocks = r == 1 ? diff_blocks : 0;
-    DemandRide rr = ride;
-    rr.first_block = ride_blocks ? (int32_t)cmp_blocks : INT32_MAX;
-    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks + ride_blocks), dim3(256), 0, st, tokens, offsets, n, in,
-                       nseg, gsize, dep, act, fin, global, rr);
-    ClElem* out = global ? msort::sort(in, bufs[cur ^ 1], np, ClLess{}, st, fin + 1) : bufs[cur ^ 1];
-    hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, in, out, nseg,
-                       gsize, act, fin, global);
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, out, nseg, gsize, dep, act,
-                       depth[r & 1], active[r & 1], lcp, fin, fout, global);
-    cur = out == bufs[0] ? 0 : 1;
+  // 2. The second round, over the whole queue but only for segments of 65
+  // to kSegSortMax members (skipped when there are none): every member is
+  // compared with its segment's head (its longest member) by a wavefront of
+  // its own, the segments are sorted in place and split.
+  ClElem* el = bufs[0];
+  {
+    const unsigned cmp_blocks = std::min(blocks_for(n, 4), 2048u);
+    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks), dim3(256), 0, st, tokens, offsets, n, el, nseg, gsize,
+                       depth[0], active[0], head, flags);
+    hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, el, nseg,
+                       gsize, active[0], flags);
+    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, gsize, depth[0], active[0],
+                       depth[1], active[1], lcp, flags, flags + 2);
   }
 
   // 3. Whatever is still active is settled inside single workgroups.
-  ClElem* el = bufs[cur];
-  const TailArgs ta{tokens, offsets, n, el, bufs[cur ^ 1], nseg, gsize, depth[kGlobalRounds & 1],
-                    active[kGlobalRounds & 1], lcp, (uint8_t*)(w + L.tact), (int32_t*)(w + L.tdep),
-                    (int32_t*)(w + L.tsize), flags + 2 * kGlobalRounds};
+  TailArgs ta{tokens, offsets, n, el, bufs[1], nseg, gsize, {depth[0], depth[1]}, {active[0], active[1]},
+              {flags, flags + 2}, lcp, (uint8_t*)(w + L.tact), (int32_t*)(w + L.tdep), (int32_t*)(w + L.tsize)};
   hipLaunchKernelGGL(k_refine_tail, dim3(blocks_for(n, kTailRange)), dim3(kTailThreads), 0, st, ta);
 
   // 4. Range queries over the settled order: share, size, id (and the cLPM
   // signals), or the offline order.
-  hipLaunchKernelGGL(k_final_blocks, dim3(blocks_for((int64_t)L.nb1 * kWave)), dim3(256), 0, st, n, el, lcp, key2,
-                     ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr);
+  const unsigned fb_blocks = blocks_for((int64_t)L.nb1 * kWave);
+  DemandRide fr = ride;
+  fr.first_block = ride_demand ? (int32_t)fb_blocks : INT32_MAX;
+  hipLaunchKernelGGL(k_final_blocks, dim3(fb_blocks + (ride_demand ? blocks_for(t->num_nodes) : 0)), dim3(256), 0,
+                     st, n, el, lcp, key2, ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr, fr);
   hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
   if (off != nullptr) {
     // PEEK-offline Phase 1 from the settled order (see OffSource).
