@@ -189,6 +189,31 @@ peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t
                                void* d_workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * peek_queue_signals_noalloc: peek_queue_signals without a workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc). Same arguments,
+ * outputs and errors as peek_queue_signals minus the workspace pair. The
+ * call allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine) and is asynchronous on `stream`.
+ * Its scratch is a static device array of PEEK_NOALLOC_SCRATCH_BYTES per
+ * GPU, reserved when the library is loaded onto that GPU and held until the
+ * process ends. A call that needs more (peek_queue_signals_workspace(n,
+ * num_nodes) > PEEK_NOALLOC_SCRATCH_BYTES, e.g. 64K requests against a cache
+ * of about 3.6M nodes) fails with WORKSPACE_TOO_SMALL before any launch.
+ * Every call on one GPU shares that GPU's array: calls whose work may
+ * overlap on the device (different streams, host threads racing) race on it
+ * and must not be issued; calls ordered on one stream are safe. The array
+ * keeps the last call's contents; each call clears what it needs.
+ * PEEK_VALIDATE has no effect here (its checks allocate).
+ * ---------------------------------------------------------------------- */
+#define PEEK_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+peek_status peek_queue_signals_noalloc(const peek_cache* cache, int32_t n, const int32_t* d_tokens,
+                                       const int64_t* d_offsets, const int32_t* d_last_node,
+                                       const int32_t* d_match_len, int32_t threshold, int32_t* d_cluster_id,
+                                       int32_t* d_cluster_size, int32_t* d_demand, void* stream);
+
+/* ------------------------------------------------------------------------
  * peek_clpm_signals: everything peek_queue_signals computes plus the rest
  * of cLPM's per-request signal vector (Sec. 3.2 signals (2)-(3); Alg. 2,
  * which reads them as section, score and cluster info):

@@ -58,6 +58,8 @@ EXPORTS = [
     ("peek_queue_signals_workspace", ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int64]),
     ("peek_queue_signals", ctypes.c_int,
      [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
+    ("peek_queue_signals_noalloc", ctypes.c_int,
+     [_vp, ctypes.c_int32, _vp, _vp, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp, _vp]),
     ("peek_evict_rank_workspace", ctypes.c_size_t, [ctypes.c_int64]),
     ("peek_evict_rank", ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     ("peek_clpm_signals", ctypes.c_int,
@@ -260,6 +262,23 @@ def peek_queue_signals(cache, tokens, offsets, last_node, match_len, threshold: 
                                    _arg(cluster_id, "cluster_id", i32, n), _arg(cluster_size, "cluster_size", i32, n),
                                    _arg(demand, "demand", i32, _num_nodes(cache)), _arg(workspace, "workspace"),
                                    ws_bytes, _stream(stream)))
+
+
+PEEK_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def peek_queue_signals_noalloc(cache, tokens, offsets, last_node, match_len, threshold: int, cluster_id,
+                               cluster_size, demand, stream=None):
+    """peek_queue_signals with the library's static scratch instead of a workspace (allocates nothing)."""
+    import torch
+    n = _queue_n(offsets)
+    i32 = torch.int32
+    _check(_lib.peek_queue_signals_noalloc(None if cache is None else cache.handle, n, _arg(tokens, "tokens", i32),
+                                           _arg(offsets, "offsets"), _arg(last_node, "last_node", i32, n),
+                                           _arg(match_len, "match_len", i32, n), int(threshold),
+                                           _arg(cluster_id, "cluster_id", i32, n),
+                                           _arg(cluster_size, "cluster_size", i32, n),
+                                           _arg(demand, "demand", i32, _num_nodes(cache)), _stream(stream)))
 
 
 def peek_clpm_signals(cache, tokens, offsets, h, last_node, match_len, threshold: int, tau: int, theta: int,

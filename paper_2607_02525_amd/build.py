@@ -15,7 +15,8 @@ LIB = os.path.join(HERE, "libpeek.so")
 CALIB_LIB = os.path.join(HERE, "libpeek_calib.so")   # measurement helper for bench.py
 BUILD_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["peek_host.hip", "peek_walk.hip", "peek_signals.hip", "peek_evict.hip", "peek_blocks.hip"]
+SOURCES = ["peek_host.hip", "peek_walk.hip", "peek_signals.hip", "peek_evict.hip", "peek_blocks.hip",
+           "peek_noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

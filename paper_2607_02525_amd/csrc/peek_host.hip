@@ -665,10 +665,17 @@ peek_status peek_evict_rank(const peek_cache* c, const int32_t* d_demand, int64_
   return run_evict(c, d_demand, d_score, d_order, d_workspace, workspace_bytes, (hipStream_t)stream);
 }
 
-static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
-                                 const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
-                                 int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
-                                 const ClpmRequest* clpm, void* d_workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace peek {
+
+// Argument checks and the cluster / demand pass of peek_queue_signals and
+// peek_clpm_signals. may_allocate = false skips the opt-in input
+// validation, which allocates (the allocation-free entry point).
+peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                          const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
+                          int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand, const ClpmRequest* clpm,
+                          void* d_workspace, size_t workspace_bytes, void* stream, bool may_allocate) {
   if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
   if (threshold < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "threshold must be >= 1 (got %d)", threshold);
   const bool want_demand = d_demand != nullptr;
@@ -698,7 +705,7 @@ static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* 
     peek_status s = check_same_device(c);
     if (s != PEEK_OK) return s;
   }
-  if (want_demand || want_clusters) {
+  if ((want_demand || want_clusters) && may_allocate) {
     const bool anchored = want_clusters && c != nullptr && d_last_node != nullptr && d_match_len != nullptr;
     const int32_t* last = (c != nullptr && (want_demand || anchored)) ? d_last_node : nullptr;
     peek_status s = validate_queue(n, want_clusters ? d_offsets : nullptr, last,
@@ -711,13 +718,17 @@ static peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* 
                      (hipStream_t)stream);
 }
 
+}  // namespace peek
+
+extern "C" {
+
 peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
                                const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
                                int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
                                size_t workspace_bytes, void* stream) {
   clear_error();
   return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
-                       d_demand, nullptr, d_workspace, workspace_bytes, stream);
+                       d_demand, nullptr, d_workspace, workspace_bytes, stream, true);
 }
 
 peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
@@ -728,7 +739,7 @@ peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_t
   clear_error();
   const ClpmRequest req{d_h, tau, theta, d_score, d_section, d_has_sharing};
   return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
-                       d_demand, &req, d_workspace, workspace_bytes, stream);
+                       d_demand, &req, d_workspace, workspace_bytes, stream, true);
 }
 
 size_t peek_offline_order_workspace(int32_t n) { return n < 0 ? 0 : offline_workspace_bytes(n); }

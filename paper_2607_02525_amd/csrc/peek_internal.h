@@ -142,6 +142,13 @@ struct OfflineRequest {
 };
 size_t offline_workspace_bytes(int32_t n);
 
+// Argument checks plus run_signals for the queue-signal entry points (see
+// peek_host.hip); may_allocate = false skips the opt-in input validation.
+peek_status signals_entry(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
+                          const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
+                          int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand, const ClpmRequest* clpm,
+                          void* d_workspace, size_t workspace_bytes, void* stream, bool may_allocate);
+
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cluster_id,
                         int32_t* cluster_size, int32_t* demand, const ClpmRequest* clpm,

@@ -147,6 +147,25 @@ def test_argument_errors_before_any_gpu_work():
                                  fake, fake, need - 1, None) == P.PEEK_ERR_WORKSPACE_TOO_SMALL
 
 
+def test_noalloc_signals_errors_before_any_gpu_work():
+    lib = P._lib
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.peek_queue_signals_noalloc(None, -1, None, None, None, None, 8, None, None, None, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+    assert lib.peek_queue_signals_noalloc(None, 4, fake, fake, None, None, 0, fake, fake, None, None) \
+        == P.PEEK_ERR_INVALID_ARGUMENT
+    # a queue whose scratch exceeds the static array is refused with its size
+    n = 300000
+    assert P.peek_queue_signals_workspace(n, 0) > P.PEEK_NOALLOC_SCRATCH_BYTES
+    assert lib.peek_queue_signals_noalloc(None, n, fake, fake, None, None, 8, fake, fake, None, None) \
+        == P.PEEK_ERR_WORKSPACE_TOO_SMALL
+    assert "static scratch" in P.peek_last_error()
+    # the header's maximum and the binding's agree
+    with open(HEADER) as f:
+        assert "#define PEEK_NOALLOC_SCRATCH_BYTES (32u << 20)" in f.read()
+    assert P.PEEK_NOALLOC_SCRATCH_BYTES == 32 << 20
+
+
 def test_block_table_argument_errors_before_any_gpu_work():
     lib = P._lib
     parent = np.array([-1, 0, 0], dtype=np.int32)
