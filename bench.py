@@ -120,6 +120,9 @@ def walk_traffic(config: str):
 
 
 def cpu_baseline(w, budget_s: float):
+    """The oracle on one host core: LPM + demand + clusters over the whole
+    queue, repeated for about budget_s seconds. Also returns the oracle's
+    outputs of one pass (they fix the algorithmic byte counts)."""
     import oracle as O
     O.build(force=False)
     t0 = time.perf_counter()
@@ -129,42 +132,79 @@ def cpu_baseline(w, budget_s: float):
     while total < budget_s or reps == 0:
         t = time.perf_counter()
         l = O.lpm(tree, w.tokens, w.offsets, w.block_size)
-        O.demand(tree, l.last_node)
-        O.clusters(w.tokens, w.offsets, w.threshold)
+        d = O.demand(tree, l.last_node)
+        c = O.clusters(w.tokens, w.offsets, w.threshold)
         total += time.perf_counter() - t
         reps += 1
-    return {"value": w.n * reps / total, "unit": "LPM queries/s", "cores": 1, "kind": "oracle",
+    base = {"value": w.n * reps / total, "unit": "LPM queries/s", "cores": 1, "kind": "oracle",
             "sample": f"whole {w.name} queue ({w.n} requests): LPM + demand + clusters, single thread, "
                       f"{reps} passes in {total:.1f} s; cache-tree ingest {ingest:.1f} s not counted",
-            "cpu": _cpu_model()}
+            "cpu": _cpu_model(), "host_logical_cpus": os.cpu_count()}
+    return base, tree, (l, d, c)
 
 
-def cpu_all_cores_lpm(w, budget_s: float, threads: int):
-    """The oracle's LPM walk over the whole queue split into request chunks,
-    one per host thread (the walk only reads the tree; the C call releases
-    the interpreter lock). Context beside the single-thread cpu_baseline."""
+def cpu_all_cores(w, tree, budget_s: float, threads: int):
+    """The oracle's LPM + demand + clusters over the whole queue on `threads`
+    host threads: the walk and the demand climb in request chunks (partial
+    demands summed), the clusters per group of requests with the same first
+    token (requests with different first tokens share nothing), groups dealt
+    out largest first. The C calls release the interpreter lock."""
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle as O
-    tree = O.cache_tree_of(w)
     bounds = np.linspace(0, w.n, threads + 1).astype(np.int64)
     chunks = []
     for a, b in zip(bounds[:-1], bounds[1:]):
         off = w.offsets[a:b + 1]
         chunks.append((w.tokens[off[0]:off[-1]], off - off[0]))
-    reps, total = 0, 0.0
+    lens = np.diff(w.offsets)
+    first = np.where(lens > 0, w.tokens[np.minimum(w.offsets[:-1], max(len(w.tokens) - 1, 0))], np.iinfo(np.int64).min)
+    order = np.argsort(first, kind="stable")
+    cuts = np.flatnonzero(np.diff(first[order])) + 1
+    groups = sorted(np.split(order, cuts), key=len, reverse=True)
+    group_queues = []
+    for g in groups:
+        g = np.sort(g)
+        glen = lens[g]
+        goff = np.zeros(len(g) + 1, np.int64)
+        np.cumsum(glen, out=goff[1:])
+        gtok = np.concatenate([w.tokens[w.offsets[i]:w.offsets[i + 1]] for i in g]) if len(g) > 1 else \
+            w.tokens[w.offsets[g[0]]:w.offsets[g[0] + 1]]
+        group_queues.append((gtok.astype(np.int32), goff))
+
+    def walk_and_demand(cq):
+        l = O.lpm(tree, cq[0], cq[1], w.block_size)
+        return O.demand(tree, l.last_node)
+
+    def cluster(gq):
+        return O.clusters(gq[0], gq[1], w.threshold)
+
+    reps, total, largest = 0, 0.0, 0.0
     with ThreadPoolExecutor(max_workers=threads) as ex:
         while total < budget_s or reps == 0:
             t = time.perf_counter()
-            list(ex.map(lambda c: O.lpm(tree, c[0], c[1], w.block_size), chunks))
+            parts = list(ex.map(walk_and_demand, chunks))
+            sum(parts)
+            list(ex.map(cluster, group_queues))
             total += time.perf_counter() - t
             reps += 1
-    return {"value": w.n * reps / total, "unit": "LPM queries/s", "threads": threads, "kind": "oracle",
-            "sample": f"whole {w.name} queue ({w.n} requests): LPM walk only, {threads} request chunks on "
-                      f"{threads} threads, {reps} passes in {total:.1f} s"}
+    return {"value": w.n * reps / total, "unit": "LPM queries/s", "cores": threads, "kind": "oracle",
+            "sample": f"whole {w.name} queue ({w.n} requests): LPM + demand in {threads} request chunks, clusters "
+                      f"in {len(groups)} first-token groups (largest {len(groups[0])} requests), {threads} threads, "
+                      f"{reps} passes in {total:.1f} s",
+            "host_logical_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu": _cpu_model()}
 
 
 def _cpu_model():
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
@@ -172,6 +212,21 @@ def _cpu_model():
     except OSError:
         pass
     return "unknown"
+
+
+def signals_algorithmic_bytes(lengths, share, m, n_nodes, passes):
+    """The signals pass's bytes as the survey's byte accounting counts them:
+    every prompt up to and including the token after its share (what a
+    plain pending-tree build reads), 16 bytes per request per sort pass, 4
+    of outputs, 16 per cache node (demand). Also the part of the prompt
+    bytes the walk had already proven (up to the match length), which the
+    pass here does not read again."""
+    prompt = 4 * int(np.minimum(lengths, share + 1).sum())
+    proven = 4 * int(np.minimum(np.minimum(lengths, share + 1), m).sum())
+    n = len(lengths)
+    parts = {"prompt_bytes": prompt, "sort_bytes": 16 * n * passes, "io_bytes": 4 * n,
+             "node_bytes": 16 * n_nodes, "prompt_bytes_proven_by_the_walk": proven}
+    return prompt + 16 * n * passes + 4 * n + 16 * n_nodes, parts
 
 
 def main():
@@ -313,6 +368,7 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": walk_traffic(args.config),
                 "kernel": "k_lpm_walk", "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
+                "bytes_from": "GPU outputs (no oracle run)",
                 "avg_launch_ms": round(float(lpm_ms.mean()), 4), "min_launch_ms": round(float(lpm_ms.min()), 4)}
 
     if args.calibrate_copy:
@@ -331,12 +387,38 @@ def main():
     log(f"streaming read of 4 GiB: {read_peak:.0f} GB/s")
 
     cpu = cpu_all = None
+    signals_roofline = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host for cpu_baseline")
-        cpu = cpu_baseline(w, args.cpu_budget)
-        threads = max(1, min(16, os.cpu_count() or 1))
-        cpu_all = cpu_all_cores_lpm(w, args.cpu_budget / 2, threads)
-        log(f"oracle LPM walk on {threads} threads: {cpu_all['value']:.0f} queries/s")
+        cpu, tree, (ol, od, oc) = cpu_baseline(w, args.cpu_budget)
+        # the byte counts come from the oracle's outputs; the GPU's agree
+        assert np.array_equal(ol.m, res["match_len"]) and np.array_equal(ol.last_node, res["last_node"])
+        assert np.array_equal(od, res["demand"])
+        b_alg, parts = walk_algorithmic_bytes(w.lengths.astype(np.int64), ol.m.astype(np.int64),
+                                              ol.last_node.astype(np.int64), od.astype(np.int64), exp)
+        roofline.update({"achieved": round(b_alg / lpm_avg_s / 1e9, 1),
+                         "frac": round(b_alg / lpm_avg_s / 1e9 / HBM_PEAK_GBS, 4),
+                         "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
+                         "bytes_from": "oracle outputs"})
+        # sort passes over the queue in one signals call: the first round's
+        # merge sort (tile pass + merge passes) and the second round's
+        # segment sort
+        np2 = 256
+        while np2 < w.n:
+            np2 <<= 1
+        passes = 1 + int(np.log2(np2 // 256)) + 1
+        sb, sparts = signals_algorithmic_bytes(w.lengths.astype(np.int64), oc.share.astype(np.int64),
+                                               ol.m.astype(np.int64), hp.num_nodes, passes)
+        sig_s = float(sig_ms.mean()) / 1e3
+        signals_roofline = {"bound": "hbm", "achieved": round(sb / sig_s / 1e9, 1), "peak": HBM_PEAK_GBS,
+                            "unit": "GB/s", "frac": round(sb / sig_s / 1e9 / HBM_PEAK_GBS, 4),
+                            "call": "peek_queue_signals", "algorithmic_bytes_per_call": sb,
+                            "bytes_breakdown": sparts, "sort_passes": passes,
+                            "avg_call_ms": round(float(sig_ms.mean()), 4), "host_round_trips": 0}
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        cpu_all = cpu_all_cores(w, tree, args.cpu_budget / 2, threads)
+        log(f"oracle LPM + demand + clusters on {threads} threads: {cpu_all['value']:.0f} queries/s "
+            f"(host shows {os.cpu_count()} logical CPUs)")
 
     out = {
         "metric": METRIC,
@@ -369,6 +451,7 @@ def main():
         "offline_order_5000_ms": round(offline5k_ms, 4),
         "cache_build_s": round(build_s, 2),
         "roofline": roofline,
+        "signals_roofline": signals_roofline,
         "cpu_baseline": cpu,
         "cpu_baseline_all_cores": cpu_all,
     }
