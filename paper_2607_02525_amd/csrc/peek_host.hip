@@ -44,6 +44,13 @@ struct Flat {
   std::vector<int32_t> pdep_pre;   // minimum of pdep from the start of c's 64-node block to c
   std::vector<int32_t> pdep_suf;   // minimum of pdep from c to the end of its block
   int32_t pdep_nb = 0;
+  std::vector<EvNode> evn;         // eviction fields per node
+  std::vector<int32_t> leaf_rank;  // leaves before c in preorder
+  std::vector<int32_t> pend;       // subtree end of the parent
+  std::vector<int32_t> ep_level;   // shallow trees: level of the parent of c's topmost in-block ancestor
+  std::vector<int32_t> anc;        // shallow trees: [blocks][kEvAncMax] proper ancestors of each block's first node
+  int32_t n_leaves = 0;
+  bool ev_shallow = false;
   int64_t edge_tokens = 0;
   int32_t max_fanout = 0;
   int64_t max_depth = 0;
@@ -206,6 +213,48 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     for (int32_t b = 0; b + (1 << k) <= nb; ++b)
       f->pdep_st[(size_t)k * nb + b] =
           std::min(f->pdep_st[(size_t)(k - 1) * nb + b], f->pdep_st[(size_t)(k - 1) * nb + b + (1 << (k - 1))]);
+
+  // Eviction tables (see EvictTree).
+  try {
+    f->evn.resize(num_nodes);
+    f->leaf_rank.resize(num_nodes);
+    f->pend.resize(num_nodes);
+  } catch (const std::bad_alloc&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation for the flattened tree failed");
+  }
+  int32_t leaves = 0;
+  bool shallow = true;
+  for (int32_t c = 0; c < num_nodes; ++c) {
+    const NodeRec& r = f->recs[c];
+    f->evn[c] = EvNode{r.parent, r.depth, r.subtree_end, level_in[order[c]]};
+    f->pend[c] = r.parent >= 0 ? f->recs[r.parent].subtree_end : num_nodes;
+    f->leaf_rank[c] = leaves;
+    if (r.subtree_end == c + 1) ++leaves;
+    if ((c & 63) == 0 && f->evn[c].level > kEvAncMax) shallow = false;
+  }
+  f->n_leaves = leaves;
+  f->ev_shallow = shallow;
+  if (shallow) {
+    try {
+      f->ep_level.resize(num_nodes);
+      f->anc.assign((size_t)nb * kEvAncMax, -1);
+    } catch (const std::bad_alloc&) {
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation for the flattened tree failed");
+    }
+    std::vector<int32_t> top(num_nodes);   // topmost ancestor of c inside c's 64-node block
+    for (int32_t c = 0; c < num_nodes; ++c) {
+      const int32_t p = f->evn[c].parent;
+      top[c] = (p >= 0 && p >= (c & ~63)) ? top[p] : c;
+      const int32_t ep = f->evn[top[c]].parent;
+      f->ep_level[c] = ep >= 0 ? f->evn[ep].level : -1;
+    }
+    for (int32_t b = 0; b < nb; ++b) {
+      const int32_t first = b * 64;
+      int32_t* list = f->anc.data() + (size_t)b * kEvAncMax;
+      for (int32_t a = f->evn[first].parent, k = f->evn[first].level - 1; a >= 0; a = f->evn[a].parent, --k)
+        list[k] = a;
+    }
+  }
   return PEEK_OK;
 }
 
@@ -521,6 +570,11 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
       {f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(), 0},
       {f.pdep_pre.data(), sizeof(int32_t) * f.pdep_pre.size(), 0},
       {f.pdep_suf.data(), sizeof(int32_t) * f.pdep_suf.size(), 0},
+      {f.evn.data(), sizeof(EvNode) * f.evn.size(), 0},
+      {f.leaf_rank.data(), sizeof(int32_t) * f.leaf_rank.size(), 0},
+      {f.pend.data(), sizeof(int32_t) * f.pend.size(), 0},
+      {f.ep_level.data(), sizeof(int32_t) * f.ep_level.size(), 0},
+      {f.anc.data(), sizeof(int32_t) * f.anc.size(), 0},
   };
   size_t total = 0;
   for (Part& q : parts) {
@@ -537,6 +591,7 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   hipStream_t st = (hipStream_t)stream;
   hipError_t first_err = hipSuccess;
   for (const Part& q : parts) {
+    if (q.bytes == 0) continue;
     const hipError_t ee = hipMemcpyAsync(p + q.at, q.src, q.bytes, hipMemcpyHostToDevice, st);
     if (ee != hipSuccess && first_err == hipSuccess) first_err = ee;
   }
@@ -572,6 +627,13 @@ peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int
   c->tree.pdep_suf = (const int32_t*)(p + parts[8].at);
   c->tree.pdep_nb = f.pdep_nb;
   c->tree.num_nodes = num_nodes;
+  c->evict.nodes = (const EvNode*)(p + parts[9].at);
+  c->evict.leaf_rank = (const int32_t*)(p + parts[10].at);
+  c->evict.pend = (const int32_t*)(p + parts[11].at);
+  c->evict.ep_level = f.ev_shallow ? (const int32_t*)(p + parts[12].at) : nullptr;
+  c->evict.anc = f.ev_shallow ? (const int32_t*)(p + parts[13].at) : nullptr;
+  c->evict.n_leaves = f.n_leaves;
+  c->evict.shallow = f.ev_shallow ? 1 : 0;
   if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
   *out = c;
   return PEEK_OK;

@@ -75,6 +75,33 @@ struct DeviceTree {
   int32_t num_nodes;
 };
 
+// What the eviction ranking reads per node (16 bytes, canonical order).
+struct EvNode {
+  int32_t parent;   // -1 for the root
+  int32_t depth;    // tokens from the root to the end of the edge
+  int32_t end;      // subtree = [c, end)
+  int32_t level;    // edges from the root
+};
+
+// Static tables of the eviction ranking, built with the cache. A tree is
+// shallow when the first node of every 64-node block sits at most
+// kEvAncMax levels below the root; then each block keeps the list of that
+// first node's proper ancestors (by level, kEvAncMax slots, -1 past the
+// end) and every node the level of the parent of its topmost ancestor
+// inside its own block (-1 when that ancestor is the root): a node's
+// ancestors outside its block are exactly the list's entries down to that
+// level.
+constexpr int32_t kEvAncMax = 64;
+struct EvictTree {
+  const EvNode* nodes;       // [num_nodes]
+  const int32_t* leaf_rank;  // [num_nodes] leaves before c in preorder
+  const int32_t* pend;       // [num_nodes] subtree end of the parent (num_nodes for the root)
+  const int32_t* ep_level;   // [num_nodes], shallow trees only
+  const int32_t* anc;        // [blocks][kEvAncMax], shallow trees only
+  int32_t n_leaves;
+  int32_t shallow;
+};
+
 // Host-side result of validating and flattening a description.
 struct HostFlat;
 
@@ -91,6 +118,7 @@ struct peek_cache {
   int64_t device_bytes;
   void* d_base;             // one allocation holding every array below
   peek::DeviceTree tree;
+  peek::EvictTree evict;
 };
 
 namespace peek {
