@@ -629,6 +629,31 @@ def test_evict_rank_tree_shapes(shape, nn):
         assert np.array_equal(order.cpu().numpy()[:nn - 1], e.order)
 
 
+@pytest.mark.parametrize("leaves,run", [(8192, 2), (8194, 2), (8192, 8192), (24577, 2)])
+def test_evict_rank_segment_counts(leaves, run):
+    """A star whose leaves take two demands in alternating runs, so the
+    leaves' scores form exactly ceil(leaves / run) runs of equal score in
+    leaf order: 4096 (the most one workgroup sorts), 4097 (two tiles), one,
+    and 12289 (four tiles)."""
+    import paper_2607_02525_amd as P
+    HotPath = _hot()
+    nn = leaves + 1
+    parent, eoff, etok = _shape_tree("star", nn)
+    tree = O.Tree.from_description(parent, eoff, etok)
+    hp = HotPath.from_description(parent, eoff, etok)
+    d = np.zeros(nn, np.int32)
+    d[1:] = 1 + (np.arange(leaves) // run) % 2
+    e = O.evict(tree, d)
+    print(f"[gpu] evict star leaves={leaves} run={run}", flush=True)
+    score = torch.empty(nn, dtype=torch.int64, device="cuda")
+    order = torch.empty(nn - 1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(P.peek_evict_rank_workspace(nn), dtype=torch.uint8, device="cuda")
+    P.peek_evict_rank(hp.cache, torch.from_numpy(d).cuda(), score, order, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(score.cpu().numpy(), e.score)
+    assert np.array_equal(order.cpu().numpy(), e.order)
+
+
 def test_binding_refuses_bad_output_tensors():
     """Output tensors of the wrong type, too small or not contiguous are
     refused before any launch."""
