@@ -319,171 +319,179 @@ extern "C" {
 peek_status peek_block_table_build(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
                                    const int32_t* edge_tokens, int32_t block_size, void* stream,
                                    peek_block_table** out) {
-  clear_error();
-  if (!out) return fail(PEEK_ERR_INVALID_ARGUMENT, "out is NULL");
-  *out = nullptr;
-  if (block_size < 4 || block_size > 256 || (block_size & (block_size - 1)) != 0)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "block_size must be a power of two in [4, 256] (got %d)", block_size);
-  // validation (structure, sibling tokens, reachability) as for peek_cache_build
-  std::vector<int32_t> canon(num_nodes > 0 ? num_nodes : 1);
-  peek_status vs = peek_tree_canonical_ids(num_nodes, parent, edge_offsets, edge_tokens, canon.data());
-  if (vs != PEEK_OK) return vs;
-  int device = 0;
-  vs = check_device(&device);
-  if (vs != PEEK_OK) return vs;
-  // children lists, then a depth-first pass carrying the chain state
-  int32_t root = 0;
-  std::vector<int32_t> kbeg(num_nodes + 1, 0), kids(num_nodes > 0 ? num_nodes - 1 : 0);
-  for (int32_t i = 0; i < num_nodes; ++i) {
-    if (parent[i] < 0) root = i;
-    else kbeg[parent[i] + 1] += 1;
-  }
-  for (int32_t i = 0; i < num_nodes; ++i) kbeg[i + 1] += kbeg[i];
-  {
-    std::vector<int32_t> fill(kbeg.begin(), kbeg.end() - 1);
-    for (int32_t i = 0; i < num_nodes; ++i)
-      if (parent[i] >= 0) kids[fill[parent[i]]++] = i;
-  }
-  // position keys of one block
-  std::vector<uint32_t> ka(block_size), kb(block_size);
-  for (int32_t j = 0; j < block_size; ++j) {
-    const uint64_t w = pos_key((uint32_t)j);
-    ka[j] = (uint32_t)w;
-    kb[j] = (uint32_t)(w >> 32);
-  }
-  // depth first, carrying the chain value, the full blocks so far and the
-  // block in progress (its NH sums, position and an unpaired even token)
-  struct State {
-    int32_t node;
-    int32_t pos;
-    uint32_t pend;
-    uint64_t k, na, nb, blocks;
-  };
-  std::vector<uint64_t> keys;
-  std::vector<State> stack{{root, 0, 0, kChainStart, 0, 0, 0}};
-  while (!stack.empty()) {
-    State st = stack.back();
-    stack.pop_back();
-    for (int64_t q = edge_offsets[st.node]; q < edge_offsets[st.node + 1]; ++q) {
-      const uint32_t u = (uint32_t)edge_tokens[q];
-      if ((st.pos & 1) == 0) {
-        st.pend = u;
-      } else {
-        st.na += nh_pair(st.pend + ka[st.pos - 1], u + ka[st.pos]);
-        st.nb += nh_pair(st.pend + kb[st.pos - 1], u + kb[st.pos]);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!out) return fail(PEEK_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    if (block_size < 4 || block_size > 256 || (block_size & (block_size - 1)) != 0)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "block_size must be a power of two in [4, 256] (got %d)", block_size);
+    // validation (structure, sibling tokens, reachability) as for peek_cache_build
+    std::vector<int32_t> canon(num_nodes > 0 ? num_nodes : 1);
+    peek_status vs = peek_tree_canonical_ids(num_nodes, parent, edge_offsets, edge_tokens, canon.data());
+    if (vs != PEEK_OK) return vs;
+    int device = 0;
+    vs = check_device(&device);
+    if (vs != PEEK_OK) return vs;
+    // children lists, then a depth-first pass carrying the chain state
+    int32_t root = 0;
+    std::vector<int32_t> kbeg(num_nodes + 1, 0), kids(num_nodes > 0 ? num_nodes - 1 : 0);
+    for (int32_t i = 0; i < num_nodes; ++i) {
+      if (parent[i] < 0) root = i;
+      else kbeg[parent[i] + 1] += 1;
+    }
+    for (int32_t i = 0; i < num_nodes; ++i) kbeg[i + 1] += kbeg[i];
+    {
+      std::vector<int32_t> fill(kbeg.begin(), kbeg.end() - 1);
+      for (int32_t i = 0; i < num_nodes; ++i)
+        if (parent[i] >= 0) kids[fill[parent[i]]++] = i;
+    }
+    // position keys of one block
+    std::vector<uint32_t> ka(block_size), kb(block_size);
+    for (int32_t j = 0; j < block_size; ++j) {
+      const uint64_t w = pos_key((uint32_t)j);
+      ka[j] = (uint32_t)w;
+      kb[j] = (uint32_t)(w >> 32);
+    }
+    // depth first, carrying the chain value, the full blocks so far and the
+    // block in progress (its NH sums, position and an unpaired even token)
+    struct State {
+      int32_t node;
+      int32_t pos;
+      uint32_t pend;
+      uint64_t k, na, nb, blocks;
+    };
+    std::vector<uint64_t> keys;
+    std::vector<State> stack{{root, 0, 0, kChainStart, 0, 0, 0}};
+    while (!stack.empty()) {
+      State st = stack.back();
+      stack.pop_back();
+      for (int64_t q = edge_offsets[st.node]; q < edge_offsets[st.node + 1]; ++q) {
+        const uint32_t u = (uint32_t)edge_tokens[q];
+        if ((st.pos & 1) == 0) {
+          st.pend = u;
+        } else {
+          st.na += nh_pair(st.pend + ka[st.pos - 1], u + ka[st.pos]);
+          st.nb += nh_pair(st.pend + kb[st.pos - 1], u + kb[st.pos]);
+        }
+        if (++st.pos == block_size) {
+          st.k += finish_digest(st.na, st.nb, kGamma * (st.blocks + 1));
+          keys.push_back(st.k);
+          st.blocks += 1;
+          st.na = st.nb = 0;
+          st.pos = 0;
+        }
       }
-      if (++st.pos == block_size) {
-        st.k += finish_digest(st.na, st.nb, kGamma * (st.blocks + 1));
-        keys.push_back(st.k);
-        st.blocks += 1;
-        st.na = st.nb = 0;
-        st.pos = 0;
+      for (int32_t q = kbeg[st.node]; q < kbeg[st.node + 1]; ++q) {
+        State c = st;
+        c.node = kids[q];
+        stack.push_back(c);
       }
     }
-    for (int32_t q = kbeg[st.node]; q < kbeg[st.node + 1]; ++q) {
-      State c = st;
-      c.node = kids[q];
-      stack.push_back(c);
+    std::sort(keys.begin(), keys.end());
+    keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
+    const int64_t num_blocks = (int64_t)keys.size();
+    const bool zero_stored = !keys.empty() && keys.front() == 0;
+    if (zero_stored) keys.erase(keys.begin());
+    int32_t bucket_bits = 3;
+    while ((int64_t(kBucketSlots) << bucket_bits) < 2 * (int64_t)keys.size()) ++bucket_bits;
+    const uint64_t buckets = uint64_t(1) << bucket_bits;
+    const uint64_t slots_n = buckets * kBucketSlots;
+    std::vector<uint64_t> table(slots_n, 0);
+    std::vector<uint8_t> used(buckets, 0);
+    for (uint64_t key : keys) {
+      uint64_t b = key >> (64 - bucket_bits);
+      while (used[b] == kBucketSlots) b = (b + 1) & (buckets - 1);
+      table[b * kBucketSlots + used[b]++] = key;
     }
-  }
-  std::sort(keys.begin(), keys.end());
-  keys.erase(std::unique(keys.begin(), keys.end()), keys.end());
-  const int64_t num_blocks = (int64_t)keys.size();
-  const bool zero_stored = !keys.empty() && keys.front() == 0;
-  if (zero_stored) keys.erase(keys.begin());
-  int32_t bucket_bits = 3;
-  while ((int64_t(kBucketSlots) << bucket_bits) < 2 * (int64_t)keys.size()) ++bucket_bits;
-  const uint64_t buckets = uint64_t(1) << bucket_bits;
-  const uint64_t slots_n = buckets * kBucketSlots;
-  std::vector<uint64_t> table(slots_n, 0);
-  std::vector<uint8_t> used(buckets, 0);
-  for (uint64_t key : keys) {
-    uint64_t b = key >> (64 - bucket_bits);
-    while (used[b] == kBucketSlots) b = (b + 1) & (buckets - 1);
-    table[b * kBucketSlots + used[b]++] = key;
-  }
-  uint64_t* d = nullptr;
-  hipError_t e = hipMalloc((void**)&d, sizeof(uint64_t) * slots_n);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "hipMalloc of the block table failed: %s", hipGetErrorString(e));
-  }
-  hipStream_t st = (hipStream_t)stream;
-  e = hipMemcpyAsync(d, table.data(), sizeof(uint64_t) * slots_n, hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e != hipSuccess) {
-    (void)hipFree(d);
-    return fail(PEEK_ERR_DEVICE, "uploading the block table failed: %s", hipGetErrorString(e));
-  }
-  peek_block_table* t = new (std::nothrow) peek_block_table();
-  if (!t) {
-    (void)hipFree(d);
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "out of host memory");
-  }
-  t->device = device;
-  t->block_size = block_size;
-  t->bucket_bits = bucket_bits;
-  t->zero_stored = zero_stored ? 1 : 0;
-  t->num_blocks = num_blocks;
-  t->d_slots = d;
-  *out = t;
-  return PEEK_OK;
+    uint64_t* d = nullptr;
+    hipError_t e = hipMalloc((void**)&d, sizeof(uint64_t) * slots_n);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "hipMalloc of the block table failed: %s", hipGetErrorString(e));
+    }
+    hipStream_t st = (hipStream_t)stream;
+    e = hipMemcpyAsync(d, table.data(), sizeof(uint64_t) * slots_n, hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+      (void)hipFree(d);
+      return fail(PEEK_ERR_DEVICE, "uploading the block table failed: %s", hipGetErrorString(e));
+    }
+    peek_block_table* t = new (std::nothrow) peek_block_table();
+    if (!t) {
+      (void)hipFree(d);
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "out of host memory");
+    }
+    t->device = device;
+    t->block_size = block_size;
+    t->bucket_bits = bucket_bits;
+    t->zero_stored = zero_stored ? 1 : 0;
+    t->num_blocks = num_blocks;
+    t->d_slots = d;
+    *out = t;
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_block_table_stats(const peek_block_table* t, int64_t* num_blocks, int64_t* num_slots,
                                    int32_t* block_size) {
-  clear_error();
-  if (!t) return fail(PEEK_ERR_INVALID_ARGUMENT, "table is NULL");
-  if (num_blocks) *num_blocks = t->num_blocks;
-  if (num_slots) *num_slots = int64_t(kBucketSlots) << t->bucket_bits;
-  if (block_size) *block_size = t->block_size;
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!t) return fail(PEEK_ERR_INVALID_ARGUMENT, "table is NULL");
+    if (num_blocks) *num_blocks = t->num_blocks;
+    if (num_slots) *num_slots = int64_t(kBucketSlots) << t->bucket_bits;
+    if (block_size) *block_size = t->block_size;
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_block_table_free(peek_block_table* t) {
-  clear_error();
-  if (!t) return PEEK_OK;
-  const hipError_t e = hipFree(t->d_slots);
-  delete t;
-  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!t) return PEEK_OK;
+    const hipError_t e = hipFree(t->d_slots);
+    delete t;
+    if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_block_lpm_batch(const peek_block_table* t, int32_t n, const int32_t* d_tokens,
                                  const int64_t* d_offsets, int32_t* d_h, void* stream) {
-  clear_error();
-  if (!t) return fail(PEEK_ERR_INVALID_ARGUMENT, "table is NULL");
-  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
-  if (n == 0) return PEEK_OK;
-  if (!d_tokens || !d_offsets || !d_h) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h are required");
-  int dev = 0;
-  PEEK_HIP_TRY(hipGetDevice(&dev));
-  if (dev != t->device)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "table lives on device %d, current device is %d", t->device, dev);
-  const int64_t blocks = ((int64_t)n + kWavesPerBlock - 1) / kWavesPerBlock;
-  const dim3 grid((unsigned)blocks), block(kWave * kWavesPerBlock);
-  hipStream_t st = (hipStream_t)stream;
-  const peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, st);
-  if (vs != PEEK_OK) return vs;
-  switch (t->block_size) {
-#define PEEK_BLOCK_CASE(LT, LS)                                                                                \
-  case (1 << LT) << LS:                                                                                        \
-    hipLaunchKernelGGL((k_block_lpm<LT, LS>), grid, block, 0, st, d_tokens, d_offsets, n, t->d_slots,          \
-                       t->bucket_bits, t->zero_stored, d_h);                                                   \
-    break;
-    PEEK_BLOCK_CASE(2, 0)
-    PEEK_BLOCK_CASE(3, 0)
-    PEEK_BLOCK_CASE(3, 1)
-    PEEK_BLOCK_CASE(3, 2)
-    PEEK_BLOCK_CASE(3, 3)
-    PEEK_BLOCK_CASE(3, 4)
-    PEEK_BLOCK_CASE(3, 5)
-#undef PEEK_BLOCK_CASE
-    default:
-      return fail(PEEK_ERR_INVALID_ARGUMENT, "table has an unsupported block size %d", t->block_size);
-  }
-  PEEK_HIP_TRY(hipGetLastError());
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!t) return fail(PEEK_ERR_INVALID_ARGUMENT, "table is NULL");
+    if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+    if (n == 0) return PEEK_OK;
+    if (!d_tokens || !d_offsets || !d_h) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h are required");
+    int dev = 0;
+    PEEK_HIP_TRY(hipGetDevice(&dev));
+    if (dev != t->device)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "table lives on device %d, current device is %d", t->device, dev);
+    const int64_t blocks = ((int64_t)n + kWavesPerBlock - 1) / kWavesPerBlock;
+    const dim3 grid((unsigned)blocks), block(kWave * kWavesPerBlock);
+    hipStream_t st = (hipStream_t)stream;
+    const peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, st);
+    if (vs != PEEK_OK) return vs;
+    switch (t->block_size) {
+  #define PEEK_BLOCK_CASE(LT, LS)                                                                                \
+    case (1 << LT) << LS:                                                                                        \
+      hipLaunchKernelGGL((k_block_lpm<LT, LS>), grid, block, 0, st, d_tokens, d_offsets, n, t->d_slots,          \
+                         t->bucket_bits, t->zero_stored, d_h);                                                   \
+      break;
+      PEEK_BLOCK_CASE(2, 0)
+      PEEK_BLOCK_CASE(3, 0)
+      PEEK_BLOCK_CASE(3, 1)
+      PEEK_BLOCK_CASE(3, 2)
+      PEEK_BLOCK_CASE(3, 3)
+      PEEK_BLOCK_CASE(3, 4)
+      PEEK_BLOCK_CASE(3, 5)
+  #undef PEEK_BLOCK_CASE
+      default:
+        return fail(PEEK_ERR_INVALID_ARGUMENT, "table has an unsupported block size %d", t->block_size);
+    }
+    PEEK_HIP_TRY(hipGetLastError());
+    return PEEK_OK;
+  });
 }
 
 }  // extern "C"

@@ -15,20 +15,22 @@
 namespace peek {
 
 namespace {
-thread_local std::string g_last_error;
+// A fixed buffer: reporting an error never allocates (it may be reporting
+// an allocation failure).
+thread_local char g_last_error[512];
 }
 
 peek_status fail(peek_status s, const char* fmt, ...) {
-  char buf[512];
+  char buf[sizeof(g_last_error)];
   va_list ap;
   va_start(ap, fmt);
   std::vsnprintf(buf, sizeof(buf), fmt, ap);
   va_end(ap);
-  g_last_error = buf;
+  std::memcpy(g_last_error, buf, sizeof(buf));
   return s;
 }
 
-void clear_error() { g_last_error.clear(); }
+void clear_error() { g_last_error[0] = 0; }
 
 namespace {
 
@@ -105,10 +107,10 @@ peek_status flatten(int32_t num_nodes, const int32_t* parent, const int64_t* eof
     int32_t* b = kids.data() + kbeg[v];
     int32_t* e = kids.data() + kbeg[v + 1];
     std::sort(b, e, [&](int32_t x, int32_t y) { return first_tok(x) < first_tok(y); });
-    for (int32_t* q = b + 1; q < e; ++q)
-      if (first_tok(q[-1]) == first_tok(q[0]))
-        return fail(PEEK_ERR_INVALID_TREE, "siblings %d and %d (parent %d) share first token %d", q[-1], q[0], v,
-                    first_tok(q[0]));
+    for (int32_t k = kbeg[v] + 1; k < kbeg[v + 1]; ++k)   // indices: kids may be empty (no pointer past null)
+      if (first_tok(kids[k - 1]) == first_tok(kids[k]))
+        return fail(PEEK_ERR_INVALID_TREE, "siblings %d and %d (parent %d) share first token %d", kids[k - 1], kids[k],
+                    v, first_tok(kids[k]));
     max_fanout = std::max<int32_t>(max_fanout, (int32_t)(e - b));
   }
 
@@ -354,17 +356,19 @@ extern "C" {
 
 int32_t peek_abi_version(void) { return PEEK_ABI_VERSION; }
 
-const char* peek_last_error(void) { return g_last_error.c_str(); }
+const char* peek_last_error(void) { return g_last_error; }
 
 peek_status peek_tree_canonical_ids(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
                                     const int32_t* edge_tokens, int32_t* canon_id) {
-  clear_error();
-  if (!canon_id) return fail(PEEK_ERR_INVALID_ARGUMENT, "canon_id must not be NULL");
-  Flat f;
-  peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, false);
-  if (s != PEEK_OK) return s;
-  std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!canon_id) return fail(PEEK_ERR_INVALID_ARGUMENT, "canon_id must not be NULL");
+    Flat f;
+    peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, false);
+    if (s != PEEK_OK) return s;
+    std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
+    return PEEK_OK;
+  });
 }
 
 void peek_free_host(void* p) { std::free(p); }
@@ -378,301 +382,315 @@ void peek_free_host(void* p) { std::free(p); }
 peek_status peek_tree_from_sequences(const int32_t* tokens, const int64_t* offsets, int64_t num_seqs,
                                      int32_t* num_nodes_out, int32_t** parent_out,
                                      int64_t** edge_offsets_out, int32_t** edge_tokens_out) {
-  clear_error();
-  if (num_seqs < 0 || !offsets || !num_nodes_out || !parent_out || !edge_offsets_out || !edge_tokens_out)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "invalid arguments to peek_tree_from_sequences");
-  if (offsets[num_seqs] > offsets[0] && !tokens) return fail(PEEK_ERR_INVALID_ARGUMENT, "tokens is NULL");
-  std::vector<SeqRef> seqs;
-  seqs.reserve(num_seqs);
-  for (int64_t s = 0; s < num_seqs; ++s) {
-    if (offsets[s + 1] < offsets[s]) return fail(PEEK_ERR_INVALID_ARGUMENT, "offsets decrease at %lld", (long long)s);
-    seqs.push_back({tokens + offsets[s], offsets[s + 1] - offsets[s]});
-  }
-  std::sort(seqs.begin(), seqs.end(), seq_less);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (num_seqs < 0 || !offsets || !num_nodes_out || !parent_out || !edge_offsets_out || !edge_tokens_out)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "invalid arguments to peek_tree_from_sequences");
+    if (offsets[num_seqs] > offsets[0] && !tokens) return fail(PEEK_ERR_INVALID_ARGUMENT, "tokens is NULL");
+    std::vector<SeqRef> seqs;
+    seqs.reserve(num_seqs);
+    for (int64_t s = 0; s < num_seqs; ++s) {
+      if (offsets[s + 1] < offsets[s]) return fail(PEEK_ERR_INVALID_ARGUMENT, "offsets decrease at %lld", (long long)s);
+      seqs.push_back({tokens + offsets[s], offsets[s + 1] - offsets[s]});
+    }
+    std::sort(seqs.begin(), seqs.end(), seq_less);
 
-  struct TNode {
-    int64_t depth;
-    int32_t parent;
-    int32_t witness;   // index into seqs
-  };
-  std::vector<TNode> nodes{{0, -1, -1}};
-  std::vector<int32_t> stack{0};
-  int32_t prev = -1;
-  for (int32_t i = 0; i < (int32_t)seqs.size(); ++i) {
-    const SeqRef& s = seqs[i];
-    if (s.len == 0) continue;                       // ends at the root
-    int64_t l = 0;
-    if (prev >= 0) {
-      l = seq_lcp(seqs[prev], s);
-      if (l == s.len && l == seqs[prev].len) continue;   // duplicate
+    struct TNode {
+      int64_t depth;
+      int32_t parent;
+      int32_t witness;   // index into seqs
+    };
+    std::vector<TNode> nodes{{0, -1, -1}};
+    std::vector<int32_t> stack{0};
+    int32_t prev = -1;
+    for (int32_t i = 0; i < (int32_t)seqs.size(); ++i) {
+      const SeqRef& s = seqs[i];
+      if (s.len == 0) continue;                       // ends at the root
+      int64_t l = 0;
+      if (prev >= 0) {
+        l = seq_lcp(seqs[prev], s);
+        if (l == s.len && l == seqs[prev].len) continue;   // duplicate
+      }
+      int32_t popped = -1;
+      while (nodes[stack.back()].depth > l) {
+        popped = stack.back();
+        stack.pop_back();
+      }
+      if (nodes[stack.back()].depth < l) {
+        // branch point inside the edge into `popped`
+        TNode b{l, stack.back(), i};
+        nodes.push_back(b);
+        const int32_t bid = (int32_t)nodes.size() - 1;
+        nodes[popped].parent = bid;
+        stack.push_back(bid);
+      }
+      if (s.len > l) {
+        nodes.push_back({s.len, stack.back(), i});
+        stack.push_back((int32_t)nodes.size() - 1);
+      }
+      prev = i;
     }
-    int32_t popped = -1;
-    while (nodes[stack.back()].depth > l) {
-      popped = stack.back();
-      stack.pop_back();
+    if (nodes.size() > (size_t)INT32_MAX) return fail(PEEK_ERR_INVALID_ARGUMENT, "too many nodes");
+    const int32_t nn = (int32_t)nodes.size();
+    int64_t total = 0;
+    for (int32_t v = 1; v < nn; ++v) total += nodes[v].depth - nodes[nodes[v].parent].depth;
+    std::vector<int32_t> par(nn);
+    std::vector<int64_t> eoff(nn + 1);
+    std::vector<int32_t> etok(std::max<int64_t>(total, 1));
+    int64_t pos = 0;
+    for (int32_t v = 0; v < nn; ++v) {
+      par[v] = nodes[v].parent;
+      eoff[v] = pos;
+      if (v > 0) {
+        const int64_t d0 = nodes[nodes[v].parent].depth;
+        const SeqRef& w = seqs[nodes[v].witness];
+        std::memcpy(etok.data() + pos, w.p + d0, sizeof(int32_t) * (nodes[v].depth - d0));
+        pos += nodes[v].depth - d0;
+      }
     }
-    if (nodes[stack.back()].depth < l) {
-      // branch point inside the edge into `popped`
-      TNode b{l, stack.back(), i};
-      nodes.push_back(b);
-      const int32_t bid = (int32_t)nodes.size() - 1;
-      nodes[popped].parent = bid;
-      stack.push_back(bid);
+    eoff[nn] = pos;
+    // emit in canonical order
+    Flat f;
+    peek_status st = flatten(nn, par.data(), eoff.data(), etok.data(), &f, false);
+    if (st != PEEK_OK) {
+      char why[sizeof(g_last_error)];
+      std::memcpy(why, g_last_error, sizeof(why));
+      return fail(st == PEEK_ERR_OUT_OF_MEMORY ? st : PEEK_ERR_INVALID_TREE, "internal: built tree is invalid: %s", why);
     }
-    if (s.len > l) {
-      nodes.push_back({s.len, stack.back(), i});
-      stack.push_back((int32_t)nodes.size() - 1);
+    std::vector<int32_t> order(nn);
+    for (int32_t v = 0; v < nn; ++v) order[f.canon[v]] = v;
+    int32_t* P = (int32_t*)std::malloc(sizeof(int32_t) * nn);
+    int64_t* O = (int64_t*)std::malloc(sizeof(int64_t) * (nn + 1));
+    int32_t* T = (int32_t*)std::malloc(sizeof(int32_t) * std::max<int64_t>(total, 1));
+    if (!P || !O || !T) {
+      std::free(P);
+      std::free(O);
+      std::free(T);
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
     }
-    prev = i;
-  }
-  if (nodes.size() > (size_t)INT32_MAX) return fail(PEEK_ERR_INVALID_ARGUMENT, "too many nodes");
-  const int32_t nn = (int32_t)nodes.size();
-  int64_t total = 0;
-  for (int32_t v = 1; v < nn; ++v) total += nodes[v].depth - nodes[nodes[v].parent].depth;
-  std::vector<int32_t> par(nn);
-  std::vector<int64_t> eoff(nn + 1);
-  std::vector<int32_t> etok(std::max<int64_t>(total, 1));
-  int64_t pos = 0;
-  for (int32_t v = 0; v < nn; ++v) {
-    par[v] = nodes[v].parent;
-    eoff[v] = pos;
-    if (v > 0) {
-      const int64_t d0 = nodes[nodes[v].parent].depth;
-      const SeqRef& w = seqs[nodes[v].witness];
-      std::memcpy(etok.data() + pos, w.p + d0, sizeof(int32_t) * (nodes[v].depth - d0));
-      pos += nodes[v].depth - d0;
+    int64_t q = 0;
+    for (int32_t c = 0; c < nn; ++c) {
+      const int32_t v = order[c];
+      P[c] = par[v] == -1 ? -1 : f.canon[par[v]];
+      O[c] = q;
+      const int64_t len = eoff[v + 1] - eoff[v];
+      if (len) std::memcpy(T + q, etok.data() + eoff[v], sizeof(int32_t) * len);
+      q += len;
     }
-  }
-  eoff[nn] = pos;
-  // emit in canonical order
-  Flat f;
-  peek_status st = flatten(nn, par.data(), eoff.data(), etok.data(), &f, false);
-  if (st != PEEK_OK) return fail(PEEK_ERR_INVALID_TREE, "internal: built tree is invalid: %s", g_last_error.c_str());
-  std::vector<int32_t> order(nn);
-  for (int32_t v = 0; v < nn; ++v) order[f.canon[v]] = v;
-  int32_t* P = (int32_t*)std::malloc(sizeof(int32_t) * nn);
-  int64_t* O = (int64_t*)std::malloc(sizeof(int64_t) * (nn + 1));
-  int32_t* T = (int32_t*)std::malloc(sizeof(int32_t) * std::max<int64_t>(total, 1));
-  if (!P || !O || !T) {
-    std::free(P);
-    std::free(O);
-    std::free(T);
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
-  }
-  int64_t q = 0;
-  for (int32_t c = 0; c < nn; ++c) {
-    const int32_t v = order[c];
-    P[c] = par[v] == -1 ? -1 : f.canon[par[v]];
-    O[c] = q;
-    const int64_t len = eoff[v + 1] - eoff[v];
-    if (len) std::memcpy(T + q, etok.data() + eoff[v], sizeof(int32_t) * len);
-    q += len;
-  }
-  O[nn] = q;
-  *num_nodes_out = nn;
-  *parent_out = P;
-  *edge_offsets_out = O;
-  *edge_tokens_out = T;
-  return PEEK_OK;
+    O[nn] = q;
+    *num_nodes_out = nn;
+    *parent_out = P;
+    *edge_offsets_out = O;
+    *edge_tokens_out = T;
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_cache_build(int32_t num_nodes, const int32_t* parent, const int64_t* edge_offsets,
                              const int32_t* edge_tokens, void* stream, peek_cache** out, int32_t* canon_id) {
-  clear_error();
-  if (!out) return fail(PEEK_ERR_INVALID_ARGUMENT, "out must not be NULL");
-  Flat f;
-  peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, true);
-  if (s != PEEK_OK) return s;
-  int dev = 0;
-  s = check_device(&dev);
-  if (s != PEEK_OK) return s;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!out) return fail(PEEK_ERR_INVALID_ARGUMENT, "out must not be NULL");
+    Flat f;
+    peek_status s = flatten(num_nodes, parent, edge_offsets, edge_tokens, &f, true);
+    if (s != PEEK_OK) return s;
+    int dev = 0;
+    s = check_device(&dev);
+    if (s != PEEK_OK) return s;
 
-  // Maximal unary runs: a node with exactly one child is followed in
-  // preorder by that child, and their edges are adjacent in the pool, so
-  // the walk compares the whole run c .. run_last[c] in one sweep.
-  std::vector<int32_t> run_len, run_last, hash_off, depth_by_id;
-  std::vector<WalkRec> wrec, htab;
-  try {
-    run_len.resize(num_nodes);
-    run_last.resize(num_nodes);
-    hash_off.assign(num_nodes, -1);
-    depth_by_id.resize(num_nodes);
-    wrec.resize(num_nodes);
-  } catch (const std::bad_alloc&) {
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
-  }
-  for (int32_t c = num_nodes - 1; c >= 0; --c) {
-    const NodeRec& r = f.recs[c];
-    const bool unary = c > 0 && r.n_child == 1;   // the root is never merged
-    const int64_t len = (int64_t)r.edge_len + (unary ? run_len[c + 1] : 0);
-    if (len > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "unary chain longer than 2^31-1 tokens");
-    run_len[c] = (int32_t)len;
-    run_last[c] = unary ? run_last[c + 1] : c;
-    depth_by_id[c] = r.depth;
-  }
-  // open-addressing tables (linear probing) for nodes with many children
-  int64_t htotal = 0;
-  for (int32_t c = 0; c < num_nodes; ++c) {
-    if (f.recs[c].n_child <= kHashMin) continue;
-    hash_off[c] = (int32_t)htotal;
-    htotal += int64_t(1) << hash_bits(f.recs[c].n_child);
-  }
-  if (htotal > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "too many children for the lookup tables");
-  // walk records in slot order: slot 0 = root, slot 1 + j = child-table entry j
-  auto walk_rec = [&](int32_t c, int32_t first_tok) {
-    const int32_t last = c == 0 ? 0 : run_last[c];
-    const NodeRec& e = f.recs[last];
-    WalkRec w{};
-    w.edge_off = f.recs[c].edge_off;
-    w.run_len = c == 0 ? 0 : run_len[c];
-    w.n_child = e.n_child;
-    w.child_ref = e.n_child > kHashMin ? hash_off[last] : e.child_beg;
-    w.id = c;
-    w.last_id = last;
-    w.first_tok = first_tok;
-    return w;
-  };
-  wrec[0] = walk_rec(0, 0);
-  for (int32_t j = 0; j + 1 < num_nodes; ++j) wrec[1 + j] = walk_rec(f.child_id[j], f.child_tok[j]);
-  try {
-    WalkRec empty{};
-    empty.id = -1;
-    htab.assign(std::max<int64_t>(htotal, 1), empty);
-  } catch (const std::bad_alloc&) {
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
-  }
-  for (int32_t c = 0; c < num_nodes; ++c) {
-    const NodeRec& r = f.recs[c];
-    if (r.n_child <= kHashMin) continue;
-    const int32_t bits = hash_bits(r.n_child);
-    const uint32_t mask = (1u << bits) - 1;
-    WalkRec* table = htab.data() + hash_off[c];
-    for (int32_t i = 0; i < r.n_child; ++i) {
-      const WalkRec& ch = wrec[1 + r.child_beg + i];
-      uint32_t pos = hash_slot(ch.first_tok, bits);
-      while (table[pos].id >= 0) pos = (pos + 1) & mask;
-      table[pos] = ch;
+    // Maximal unary runs: a node with exactly one child is followed in
+    // preorder by that child, and their edges are adjacent in the pool, so
+    // the walk compares the whole run c .. run_last[c] in one sweep.
+    std::vector<int32_t> run_len, run_last, hash_off, depth_by_id;
+    std::vector<WalkRec> wrec, htab;
+    try {
+      run_len.resize(num_nodes);
+      run_last.resize(num_nodes);
+      hash_off.assign(num_nodes, -1);
+      depth_by_id.resize(num_nodes);
+      wrec.resize(num_nodes);
+    } catch (const std::bad_alloc&) {
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
     }
-  }
+    for (int32_t c = num_nodes - 1; c >= 0; --c) {
+      const NodeRec& r = f.recs[c];
+      const bool unary = c > 0 && r.n_child == 1;   // the root is never merged
+      const int64_t len = (int64_t)r.edge_len + (unary ? run_len[c + 1] : 0);
+      if (len > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "unary chain longer than 2^31-1 tokens");
+      run_len[c] = (int32_t)len;
+      run_last[c] = unary ? run_last[c + 1] : c;
+      depth_by_id[c] = r.depth;
+    }
+    // open-addressing tables (linear probing) for nodes with many children
+    int64_t htotal = 0;
+    for (int32_t c = 0; c < num_nodes; ++c) {
+      if (f.recs[c].n_child <= kHashMin) continue;
+      hash_off[c] = (int32_t)htotal;
+      htotal += int64_t(1) << hash_bits(f.recs[c].n_child);
+    }
+    if (htotal > INT32_MAX) return fail(PEEK_ERR_INVALID_TREE, "too many children for the lookup tables");
+    // walk records in slot order: slot 0 = root, slot 1 + j = child-table entry j
+    auto walk_rec = [&](int32_t c, int32_t first_tok) {
+      const int32_t last = c == 0 ? 0 : run_last[c];
+      const NodeRec& e = f.recs[last];
+      WalkRec w{};
+      w.edge_off = f.recs[c].edge_off;
+      w.run_len = c == 0 ? 0 : run_len[c];
+      w.n_child = e.n_child;
+      w.child_ref = e.n_child > kHashMin ? hash_off[last] : e.child_beg;
+      w.id = c;
+      w.last_id = last;
+      w.first_tok = first_tok;
+      return w;
+    };
+    wrec[0] = walk_rec(0, 0);
+    for (int32_t j = 0; j + 1 < num_nodes; ++j) wrec[1 + j] = walk_rec(f.child_id[j], f.child_tok[j]);
+    try {
+      WalkRec empty{};
+      empty.id = -1;
+      htab.assign(std::max<int64_t>(htotal, 1), empty);
+    } catch (const std::bad_alloc&) {
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+    }
+    for (int32_t c = 0; c < num_nodes; ++c) {
+      const NodeRec& r = f.recs[c];
+      if (r.n_child <= kHashMin) continue;
+      const int32_t bits = hash_bits(r.n_child);
+      const uint32_t mask = (1u << bits) - 1;
+      WalkRec* table = htab.data() + hash_off[c];
+      for (int32_t i = 0; i < r.n_child; ++i) {
+        const WalkRec& ch = wrec[1 + r.child_beg + i];
+        uint32_t pos = hash_slot(ch.first_tok, bits);
+        while (table[pos].id >= 0) pos = (pos + 1) & mask;
+        table[pos] = ch;
+      }
+    }
 
-  struct Part {
-    const void* src;
-    size_t bytes;
-    size_t at;
-  };
-  Part parts[] = {
-      {f.recs.data(), sizeof(NodeRec) * (size_t)num_nodes, 0},
-      {wrec.data(), sizeof(WalkRec) * (size_t)num_nodes, 0},
-      {htab.data(), sizeof(WalkRec) * htab.size(), 0},
-      {depth_by_id.data(), sizeof(int32_t) * depth_by_id.size(), 0},
-      {f.pool.data(), sizeof(int32_t) * f.pool.size(), 0},
-      {f.pdep.data(), sizeof(int32_t) * f.pdep.size(), 0},
-      {f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(), 0},
-      {f.pdep_pre.data(), sizeof(int32_t) * f.pdep_pre.size(), 0},
-      {f.pdep_suf.data(), sizeof(int32_t) * f.pdep_suf.size(), 0},
-      {f.evn.data(), sizeof(EvNode) * f.evn.size(), 0},
-      {f.leaf_rank.data(), sizeof(int32_t) * f.leaf_rank.size(), 0},
-      {f.pend.data(), sizeof(int32_t) * f.pend.size(), 0},
-      {f.ep_level.data(), sizeof(int32_t) * f.ep_level.size(), 0},
-      {f.anc.data(), sizeof(int32_t) * f.anc.size(), 0},
-  };
-  size_t total = 0;
-  for (Part& q : parts) {
-    q.at = total;
-    total += align256(q.bytes);
-  }
-  void* base = nullptr;
-  hipError_t e = hipMalloc(&base, total);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
-  }
-  char* p = (char*)base;
-  hipStream_t st = (hipStream_t)stream;
-  hipError_t first_err = hipSuccess;
-  for (const Part& q : parts) {
-    if (q.bytes == 0) continue;
-    const hipError_t ee = hipMemcpyAsync(p + q.at, q.src, q.bytes, hipMemcpyHostToDevice, st);
-    if (ee != hipSuccess && first_err == hipSuccess) first_err = ee;
-  }
-  const hipError_t es = hipStreamSynchronize(st);
-  if (first_err == hipSuccess) first_err = es;
-  if (first_err != hipSuccess) {
-    (void)hipFree(base);
-    return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(first_err));
-  }
-  peek_cache* c = new (std::nothrow) peek_cache();
-  if (!c) {
-    (void)hipFree(base);
-    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
-  }
-  c->device = dev;
-  c->num_nodes = num_nodes;
-  c->num_edge_tokens = f.edge_tokens;
-  c->pool_tokens = (int64_t)f.pool.size();
-  c->max_fanout = f.max_fanout;
-  c->max_depth = f.max_depth;
-  c->max_level = f.max_level;
-  c->device_bytes = (int64_t)total;
-  c->d_base = base;
-  c->tree.nodes = (const NodeRec*)(p + parts[0].at);
-  c->tree.walk.recs = (const WalkRec*)(p + parts[1].at);
-  c->tree.walk.hash = (const WalkRec*)(p + parts[2].at);
-  c->tree.walk.depth = (const int32_t*)(p + parts[3].at);
-  c->tree.walk.pool = (const int32_t*)(p + parts[4].at);
-  c->tree.pool = c->tree.walk.pool;
-  c->tree.pdep = (const int32_t*)(p + parts[5].at);
-  c->tree.pdep_st = (const int32_t*)(p + parts[6].at);
-  c->tree.pdep_pre = (const int32_t*)(p + parts[7].at);
-  c->tree.pdep_suf = (const int32_t*)(p + parts[8].at);
-  c->tree.pdep_nb = f.pdep_nb;
-  c->tree.num_nodes = num_nodes;
-  c->evict.nodes = (const EvNode*)(p + parts[9].at);
-  c->evict.leaf_rank = (const int32_t*)(p + parts[10].at);
-  c->evict.pend = (const int32_t*)(p + parts[11].at);
-  c->evict.ep_level = f.ev_shallow ? (const int32_t*)(p + parts[12].at) : nullptr;
-  c->evict.anc = f.ev_shallow ? (const int32_t*)(p + parts[13].at) : nullptr;
-  c->evict.n_leaves = f.n_leaves;
-  c->evict.shallow = f.ev_shallow ? 1 : 0;
-  if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
-  *out = c;
-  return PEEK_OK;
+    struct Part {
+      const void* src;
+      size_t bytes;
+      size_t at;
+    };
+    Part parts[] = {
+        {f.recs.data(), sizeof(NodeRec) * (size_t)num_nodes, 0},
+        {wrec.data(), sizeof(WalkRec) * (size_t)num_nodes, 0},
+        {htab.data(), sizeof(WalkRec) * htab.size(), 0},
+        {depth_by_id.data(), sizeof(int32_t) * depth_by_id.size(), 0},
+        {f.pool.data(), sizeof(int32_t) * f.pool.size(), 0},
+        {f.pdep.data(), sizeof(int32_t) * f.pdep.size(), 0},
+        {f.pdep_st.data(), sizeof(int32_t) * f.pdep_st.size(), 0},
+        {f.pdep_pre.data(), sizeof(int32_t) * f.pdep_pre.size(), 0},
+        {f.pdep_suf.data(), sizeof(int32_t) * f.pdep_suf.size(), 0},
+        {f.evn.data(), sizeof(EvNode) * f.evn.size(), 0},
+        {f.leaf_rank.data(), sizeof(int32_t) * f.leaf_rank.size(), 0},
+        {f.pend.data(), sizeof(int32_t) * f.pend.size(), 0},
+        {f.ep_level.data(), sizeof(int32_t) * f.ep_level.size(), 0},
+        {f.anc.data(), sizeof(int32_t) * f.anc.size(), 0},
+    };
+    size_t total = 0;
+    for (Part& q : parts) {
+      q.at = total;
+      total += align256(q.bytes);
+    }
+    void* base = nullptr;
+    hipError_t e = hipMalloc(&base, total);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "hipMalloc(%zu) failed: %s", total, hipGetErrorString(e));
+    }
+    char* p = (char*)base;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t first_err = hipSuccess;
+    for (const Part& q : parts) {
+      if (q.bytes == 0) continue;
+      const hipError_t ee = hipMemcpyAsync(p + q.at, q.src, q.bytes, hipMemcpyHostToDevice, st);
+      if (ee != hipSuccess && first_err == hipSuccess) first_err = ee;
+    }
+    const hipError_t es = hipStreamSynchronize(st);
+    if (first_err == hipSuccess) first_err = es;
+    if (first_err != hipSuccess) {
+      (void)hipFree(base);
+      return fail(PEEK_ERR_DEVICE, "uploading the cache tree failed: %s", hipGetErrorString(first_err));
+    }
+    peek_cache* c = new (std::nothrow) peek_cache();
+    if (!c) {
+      (void)hipFree(base);
+      return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+    }
+    c->device = dev;
+    c->num_nodes = num_nodes;
+    c->num_edge_tokens = f.edge_tokens;
+    c->pool_tokens = (int64_t)f.pool.size();
+    c->max_fanout = f.max_fanout;
+    c->max_depth = f.max_depth;
+    c->max_level = f.max_level;
+    c->device_bytes = (int64_t)total;
+    c->d_base = base;
+    c->tree.nodes = (const NodeRec*)(p + parts[0].at);
+    c->tree.walk.recs = (const WalkRec*)(p + parts[1].at);
+    c->tree.walk.hash = (const WalkRec*)(p + parts[2].at);
+    c->tree.walk.depth = (const int32_t*)(p + parts[3].at);
+    c->tree.walk.pool = (const int32_t*)(p + parts[4].at);
+    c->tree.pool = c->tree.walk.pool;
+    c->tree.pdep = (const int32_t*)(p + parts[5].at);
+    c->tree.pdep_st = (const int32_t*)(p + parts[6].at);
+    c->tree.pdep_pre = (const int32_t*)(p + parts[7].at);
+    c->tree.pdep_suf = (const int32_t*)(p + parts[8].at);
+    c->tree.pdep_nb = f.pdep_nb;
+    c->tree.num_nodes = num_nodes;
+    c->evict.nodes = (const EvNode*)(p + parts[9].at);
+    c->evict.leaf_rank = (const int32_t*)(p + parts[10].at);
+    c->evict.pend = (const int32_t*)(p + parts[11].at);
+    c->evict.ep_level = f.ev_shallow ? (const int32_t*)(p + parts[12].at) : nullptr;
+    c->evict.anc = f.ev_shallow ? (const int32_t*)(p + parts[13].at) : nullptr;
+    c->evict.n_leaves = f.n_leaves;
+    c->evict.shallow = f.ev_shallow ? 1 : 0;
+    if (canon_id) std::memcpy(canon_id, f.canon.data(), sizeof(int32_t) * num_nodes);
+    *out = c;
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_cache_stats(const peek_cache* c, int64_t* num_nodes, int64_t* num_edge_tokens, int32_t* max_fanout,
                              int64_t* max_depth, int64_t* device_bytes) {
-  clear_error();
-  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
-  if (num_nodes) *num_nodes = c->num_nodes;
-  if (num_edge_tokens) *num_edge_tokens = c->num_edge_tokens;
-  if (max_fanout) *max_fanout = c->max_fanout;
-  if (max_depth) *max_depth = c->max_depth;
-  if (device_bytes) *device_bytes = c->device_bytes;
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (num_nodes) *num_nodes = c->num_nodes;
+    if (num_edge_tokens) *num_edge_tokens = c->num_edge_tokens;
+    if (max_fanout) *max_fanout = c->max_fanout;
+    if (max_depth) *max_depth = c->max_depth;
+    if (device_bytes) *device_bytes = c->device_bytes;
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_cache_export(const peek_cache* c, int32_t* parent, int32_t* depth, int32_t* edge_len,
                               int32_t* subtree_end) {
-  clear_error();
-  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
-  std::vector<NodeRec> recs(c->num_nodes);
-  PEEK_HIP_TRY(hipMemcpy(recs.data(), c->tree.nodes, sizeof(NodeRec) * c->num_nodes, hipMemcpyDeviceToHost));
-  for (int32_t i = 0; i < c->num_nodes; ++i) {
-    if (parent) parent[i] = recs[i].parent;
-    if (depth) depth[i] = recs[i].depth;
-    if (edge_len) edge_len[i] = recs[i].edge_len;
-    if (subtree_end) subtree_end[i] = recs[i].subtree_end;
-  }
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+    std::vector<NodeRec> recs(c->num_nodes);
+    PEEK_HIP_TRY(hipMemcpy(recs.data(), c->tree.nodes, sizeof(NodeRec) * c->num_nodes, hipMemcpyDeviceToHost));
+    for (int32_t i = 0; i < c->num_nodes; ++i) {
+      if (parent) parent[i] = recs[i].parent;
+      if (depth) depth[i] = recs[i].depth;
+      if (edge_len) edge_len[i] = recs[i].edge_len;
+      if (subtree_end) subtree_end[i] = recs[i].subtree_end;
+    }
+    return PEEK_OK;
+  });
 }
 
 peek_status peek_cache_free(peek_cache* c) {
-  clear_error();
-  if (!c) return PEEK_OK;
-  hipError_t e = hipFree(c->d_base);
-  delete c;
-  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!c) return PEEK_OK;
+    hipError_t e = hipFree(c->d_base);
+    delete c;
+    if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "hipFree failed: %s", hipGetErrorString(e));
+    return PEEK_OK;
+  });
 }
 
 static peek_status check_same_device(const peek_cache* c) {
@@ -686,21 +704,23 @@ static peek_status check_same_device(const peek_cache* c) {
 peek_status peek_lpm_batch(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
                            int32_t block_size, int32_t* d_h, int32_t* d_last_node, int32_t* d_match_len,
                            void* stream) {
-  clear_error();
-  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
-  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
-  if (block_size < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "block_size must be >= 1 (got %d)", block_size);
-  if (n == 0) return PEEK_OK;
-  if (!d_tokens || !d_offsets || !d_h)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h must not be NULL");
-  peek_status s = check_same_device(c);
-  if (s != PEEK_OK) return s;
-  s = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
-  if (s != PEEK_OK) return s;
-  hipError_t e = launch_lpm_walk(c->tree, n, d_tokens, d_offsets, block_size, d_h, d_last_node, d_match_len,
-                                 (hipStream_t)stream);
-  if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "lpm walk launch failed: %s", hipGetErrorString(e));
-  return PEEK_OK;
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+    if (block_size < 1) return fail(PEEK_ERR_INVALID_ARGUMENT, "block_size must be >= 1 (got %d)", block_size);
+    if (n == 0) return PEEK_OK;
+    if (!d_tokens || !d_offsets || !d_h)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_h must not be NULL");
+    peek_status s = check_same_device(c);
+    if (s != PEEK_OK) return s;
+    s = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
+    if (s != PEEK_OK) return s;
+    hipError_t e = launch_lpm_walk(c->tree, n, d_tokens, d_offsets, block_size, d_h, d_last_node, d_match_len,
+                                   (hipStream_t)stream);
+    if (e != hipSuccess) return fail(PEEK_ERR_DEVICE, "lpm walk launch failed: %s", hipGetErrorString(e));
+    return PEEK_OK;
+  });
 }
 
 size_t peek_queue_signals_workspace(int32_t n, int64_t num_nodes) {
@@ -712,19 +732,21 @@ size_t peek_evict_rank_workspace(int64_t num_nodes) { return evict_workspace_byt
 
 peek_status peek_evict_rank(const peek_cache* c, const int32_t* d_demand, int64_t* d_score, int32_t* d_order,
                             void* d_workspace, size_t workspace_bytes, void* stream) {
-  clear_error();
-  if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
-  if (!d_demand) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_demand is NULL");
-  if (!d_score && !d_order) return fail(PEEK_ERR_INVALID_ARGUMENT, "nothing to compute: d_score and d_order are NULL");
-  const size_t need = evict_workspace_bytes(c->num_nodes);
-  if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
-  if (workspace_bytes < need)
-    return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
-  peek_status s = check_same_device(c);
-  if (s != PEEK_OK) return s;
-  return run_evict(c, d_demand, d_score, d_order, d_workspace, workspace_bytes, (hipStream_t)stream);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (!c) return fail(PEEK_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (!d_demand) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_demand is NULL");
+    if (!d_score && !d_order) return fail(PEEK_ERR_INVALID_ARGUMENT, "nothing to compute: d_score and d_order are NULL");
+    const size_t need = evict_workspace_bytes(c->num_nodes);
+    if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
+    if (workspace_bytes < need)
+      return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+    if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+    peek_status s = check_same_device(c);
+    if (s != PEEK_OK) return s;
+    return run_evict(c, d_demand, d_score, d_order, d_workspace, workspace_bytes, (hipStream_t)stream);
+  });
 }
 
 }  // extern "C"
@@ -788,9 +810,11 @@ peek_status peek_queue_signals(const peek_cache* c, int32_t n, const int32_t* d_
                                const int32_t* d_last_node, const int32_t* d_match_len, int32_t threshold,
                                int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand, void* d_workspace,
                                size_t workspace_bytes, void* stream) {
-  clear_error();
-  return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
-                       d_demand, nullptr, d_workspace, workspace_bytes, stream, true);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
+                         d_demand, nullptr, d_workspace, workspace_bytes, stream, true);
+  });
 }
 
 peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_tokens, const int64_t* d_offsets,
@@ -798,35 +822,39 @@ peek_status peek_clpm_signals(const peek_cache* c, int32_t n, const int32_t* d_t
                               int32_t threshold, int32_t tau, int32_t theta, int32_t* d_cluster_id,
                               int32_t* d_cluster_size, int32_t* d_demand, int64_t* d_score, int32_t* d_section,
                               int32_t* d_has_sharing, void* d_workspace, size_t workspace_bytes, void* stream) {
-  clear_error();
-  const ClpmRequest req{d_h, tau, theta, d_score, d_section, d_has_sharing};
-  return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
-                       d_demand, &req, d_workspace, workspace_bytes, stream, true);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    const ClpmRequest req{d_h, tau, theta, d_score, d_section, d_has_sharing};
+    return signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id, d_cluster_size,
+                         d_demand, &req, d_workspace, workspace_bytes, stream, true);
+  });
 }
 
 size_t peek_offline_order_workspace(int32_t n) { return n < 0 ? 0 : offline_workspace_bytes(n); }
 
 peek_status peek_offline_order(int32_t n, const int32_t* d_tokens, const int64_t* d_offsets, int32_t depth_limit,
                                int32_t* d_perm, void* d_workspace, size_t workspace_bytes, void* stream) {
-  clear_error();
-  if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
-  if (depth_limit < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "depth_limit must be >= 0 (got %d)", depth_limit);
-  if (n > (INT32_MAX - 1) / 2)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be below 2^30 for the offline order (got %d)", n);
-  if (n == 0) return PEEK_OK;
-  if (!d_tokens || !d_offsets || !d_perm)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_perm must not be NULL");
-  const size_t need = offline_workspace_bytes(n);
-  if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
-  if (workspace_bytes < need)
-    return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
-    return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
-  peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
-  if (vs != PEEK_OK) return vs;
-  const OfflineRequest off{depth_limit, d_perm};
-  return run_signals(nullptr, n, d_tokens, d_offsets, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, &off,
-                     d_workspace, workspace_bytes, (hipStream_t)stream);
+  return guarded([&]() -> peek_status {
+    clear_error();
+    if (n < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+    if (depth_limit < 0) return fail(PEEK_ERR_INVALID_ARGUMENT, "depth_limit must be >= 0 (got %d)", depth_limit);
+    if (n > (INT32_MAX - 1) / 2)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "n must be below 2^30 for the offline order (got %d)", n);
+    if (n == 0) return PEEK_OK;
+    if (!d_tokens || !d_offsets || !d_perm)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "d_tokens, d_offsets and d_perm must not be NULL");
+    const size_t need = offline_workspace_bytes(n);
+    if (!d_workspace) return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace is NULL");
+    if (workspace_bytes < need)
+      return fail(PEEK_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+    if ((reinterpret_cast<uintptr_t>(d_workspace) & 255) != 0)
+      return fail(PEEK_ERR_INVALID_ARGUMENT, "d_workspace must be 256-byte aligned");
+    peek_status vs = validate_queue(n, d_offsets, nullptr, nullptr, 0, (hipStream_t)stream);
+    if (vs != PEEK_OK) return vs;
+    const OfflineRequest off{depth_limit, d_perm};
+    return run_signals(nullptr, n, d_tokens, d_offsets, nullptr, nullptr, 1, nullptr, nullptr, nullptr, nullptr, &off,
+                       d_workspace, workspace_bytes, (hipStream_t)stream);
+  });
 }
 
 }  // extern "C"

@@ -5,6 +5,8 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <new>
+#include <stdexcept>
 
 #include "../../include/peek.h"
 
@@ -126,6 +128,22 @@ namespace peek {
 // Thread-local error reporting.
 peek_status fail(peek_status s, const char* fmt, ...);
 void clear_error();
+
+// Runs an entry point's body so that no C++ exception leaves the C ABI: a
+// failed host allocation (std::bad_alloc, or std::length_error from an
+// oversized container) is reported as OUT_OF_MEMORY.
+template <typename F>
+peek_status guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed");
+  } catch (const std::length_error&) {
+    return fail(PEEK_ERR_OUT_OF_MEMORY, "host allocation failed (size beyond the container limit)");
+  } catch (...) {
+    return fail(PEEK_ERR_DEVICE, "unexpected host exception");
+  }
+}
 
 // Current device id if it is a gfx950, else UNSUPPORTED_DEVICE.
 peek_status check_device(int* dev_out);

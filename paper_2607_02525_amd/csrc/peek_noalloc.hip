@@ -48,19 +48,21 @@ extern "C" peek_status peek_queue_signals_noalloc(const peek_cache* c, int32_t n
                                                   const int32_t* d_match_len, int32_t threshold,
                                                   int32_t* d_cluster_id, int32_t* d_cluster_size, int32_t* d_demand,
                                                   void* stream) {
-  peek::clear_error();
-  if (n < 0) return peek::fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
-  if (threshold < 1) return peek::fail(PEEK_ERR_INVALID_ARGUMENT, "threshold must be >= 1 (got %d)", threshold);
-  const int64_t nn = c ? c->num_nodes : 0;
-  const size_t need = peek::signals_workspace_bytes(n, nn);
-  if (need > (size_t)PEEK_NOALLOC_SCRATCH_BYTES)
-    return peek::fail(PEEK_ERR_WORKSPACE_TOO_SMALL,
-                      "%d requests against %lld cache nodes need %zu bytes of scratch; the static scratch holds %zu "
-                      "(use peek_queue_signals with a workspace)",
-                      n, (long long)nn, need, (size_t)PEEK_NOALLOC_SCRATCH_BYTES);
-  void* ws = nullptr;
-  const peek_status s = scratch_here(&ws);
-  if (s != PEEK_OK) return s;
-  return peek::signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id,
-                             d_cluster_size, d_demand, nullptr, ws, PEEK_NOALLOC_SCRATCH_BYTES, stream, false);
+  return peek::guarded([&]() -> peek_status {
+    peek::clear_error();
+    if (n < 0) return peek::fail(PEEK_ERR_INVALID_ARGUMENT, "n must be >= 0 (got %d)", n);
+    if (threshold < 1) return peek::fail(PEEK_ERR_INVALID_ARGUMENT, "threshold must be >= 1 (got %d)", threshold);
+    const int64_t nn = c ? c->num_nodes : 0;
+    const size_t need = peek::signals_workspace_bytes(n, nn);
+    if (need > (size_t)PEEK_NOALLOC_SCRATCH_BYTES)
+      return peek::fail(PEEK_ERR_WORKSPACE_TOO_SMALL,
+                        "%d requests against %lld cache nodes need %zu bytes of scratch; the static scratch holds %zu "
+                        "(use peek_queue_signals with a workspace)",
+                        n, (long long)nn, need, (size_t)PEEK_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    const peek_status s = scratch_here(&ws);
+    if (s != PEEK_OK) return s;
+    return peek::signals_entry(c, n, d_tokens, d_offsets, d_last_node, d_match_len, threshold, d_cluster_id,
+                               d_cluster_size, d_demand, nullptr, ws, PEEK_NOALLOC_SCRATCH_BYTES, stream, false);
+  });
 }
