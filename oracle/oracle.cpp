@@ -538,13 +538,14 @@ void oracle_evict(const oracle_tree* t, const int64_t* demand, int64_t* score_ou
   }
 }
 
-// The rest of the cLPM signal vector. score_out[r]: walk r's path in the
-// pending tree and add pending_count * edge length of every node on it.
-// section_out[r]: 0 warm (h[r] > tau); else, scanning requests in arrival
-// order, 1 if the token string prompt[:theta] (the whole prompt when it is
-// shorter) has not been claimed by an earlier cold request (it is claimed
-// now), 2 otherwise. *has_sharing_out: 1 if a child of the pending root has
-// pending_count >= 2, else 0.
+// The rest of the cLPM signal vector (Sec. 3.2). score_out[r]: walk r's
+// path in the pending tree and add pending_count * edge length of every node
+// on it. section_out[r] (signal 2): 0 for a warm request (h[r] > tau); a
+// cold request is the pioneer of its theta-prefix (prompt[:theta], the whole
+// prompt when shorter) when it is the earliest cold request with that
+// prefix (1), otherwise a cold sibling of that pioneer (2).
+// *has_sharing_out: 1 if a child of the pending root has pending_count >= 2,
+// else 0.
 void oracle_clpm(int64_t n, const int32_t* tokens, const int64_t* offsets, const int64_t* h, int64_t tau,
                  int64_t theta, int64_t* score_out, int32_t* section_out, int32_t* has_sharing_out) {
   PendingTree T;
@@ -563,22 +564,20 @@ void oracle_clpm(int64_t n, const int32_t* tokens, const int64_t* offsets, const
     }
     score_out[r] = score;
   }
-  std::set<std::vector<int32_t>> seen;
-  for (int64_t r = 0; r < n; ++r) {
-    if (h[r] > tau) {
-      section_out[r] = 0;
-      continue;
-    }
+  // the earliest cold request of every theta-prefix, then each request's section
+  auto theta_prefix = [&](int64_t r) {
     const int64_t len = offsets[r + 1] - offsets[r];
     const int64_t k = len < theta ? len : theta;
-    std::vector<int32_t> prefix(tokens + offsets[r], tokens + offsets[r] + k);
-    if (seen.count(prefix)) {
-      section_out[r] = 2;
-    } else {
-      section_out[r] = 1;
-      seen.insert(prefix);
-    }
+    return std::vector<int32_t>(tokens + offsets[r], tokens + offsets[r] + k);
+  };
+  std::map<std::vector<int32_t>, int64_t> pioneer;
+  for (int64_t r = 0; r < n; ++r) {
+    if (h[r] > tau) continue;
+    auto it = pioneer.emplace(theta_prefix(r), r).first;
+    it->second = std::min(it->second, r);
   }
+  for (int64_t r = 0; r < n; ++r)
+    section_out[r] = h[r] > tau ? 0 : (pioneer.at(theta_prefix(r)) == r ? 1 : 2);
   int32_t sharing = 0;
   for (const auto& kv : T.root->kids)
     if (kv.second->pending_count >= 2) sharing = 1;

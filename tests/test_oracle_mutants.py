@@ -51,7 +51,8 @@ MUTANTS = {
                                      "      score += (node->pending_count - 1) * node->elen;"),
     "score_weights_by_depth": ("      score += node->pending_count * node->elen;",
                                "      score += node->pending_count * node->depth;"),
-    "warm_is_at_least_tau": ("    if (h[r] > tau) {", "    if (h[r] >= tau) {"),
+    "warm_is_at_least_tau": ("section_out[r] = h[r] > tau ? 0", "section_out[r] = h[r] >= tau ? 0"),
+    "pioneer_is_the_latest": ("it->second = std::min(it->second, r);", "it->second = std::max(it->second, r);"),
     "section_prefix_too_short": ("const int64_t k = len < theta ? len : theta;",
                                  "const int64_t k = len < theta - 1 ? len : theta - 1;"),
     "sharing_counts_single_requests": ("if (kv.second->pending_count >= 2) sharing = 1;",
