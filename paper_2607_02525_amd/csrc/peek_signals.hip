@@ -1427,46 +1427,65 @@ __device__ __forceinline__ uint64_t key_range_min(const uint64_t* __restrict__ i
 // One thread per sorted position i: cluster id and size of its request;
 // with cLPM signals requested also the weight of the pending-tree node
 // whose leftmost inner position is i, and the section run of position i.
-__global__ void k_final_query(int32_t n, int32_t threshold, const uint64_t* __restrict__ key2,
-                              const int32_t* __restrict__ lcp, const ClElem* __restrict__ el, LcpIndex ix,
-                              const uint64_t* __restrict__ ib2, const uint64_t* __restrict__ st2, int32_t nb2,
-                              int32_t* __restrict__ cid, int32_t* __restrict__ csz, ClpmArgs cl) {
+__global__ __launch_bounds__(256) void k_final_query(int32_t n, int32_t threshold, const uint64_t* __restrict__ key2,
+                                                    const int32_t* __restrict__ lcp, const ClElem* __restrict__ el,
+                                                    LcpIndex ix, const uint64_t* __restrict__ ib2,
+                                                    const uint64_t* __restrict__ st2, int32_t nb2,
+                                                    int32_t* __restrict__ cid, int32_t* __restrict__ csz, ClpmArgs cl) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint64_t own = key2[i];
-  const int32_t s = (int32_t)(own >> 32);
-  const uint32_t req = (uint32_t)own;
-  if (s < threshold) {
-    cid[req] = -1;
-    csz[req] = 1;
-  } else {
-    // [L, R): the widest range around i whose inner lcps are >= s
-    const int32_t L = ix.last_below_from(i, s);
-    const int32_t R = ix.first_below_from(i + 1, s);
-    // id: minimum of (share, request) over [L, R)
-    const uint64_t m = key_range_min(ib2, ix.stride, st2, nb2, L, R - 1);
-    cid[req] = (int32_t)(uint32_t)m;
-    csz[req] = R - L;
-  }
-  if (!cl.on) return;
-  // the node of depth D = lcp[i] > 0 is counted once, at its leftmost inner
-  // position: the previous position with lcp <= D must have lcp < D
-  const int32_t D = i >= 1 ? lcp[i] : 0;
-  if (D > 0) {
-    const int32_t L = ix.last_below_from(i - 1, D + 1);
-    const int32_t lL = lcp[L];
-    if (lL < D) {
-      const int32_t R = ix.first_below_from(i + 1, D);
-      const int64_t wgt = (int64_t)(R - L) * (D - max(lL, lcp[R]));
-      atomicAdd((unsigned long long*)&cl.diff[L], (unsigned long long)wgt);
-      atomicAdd((unsigned long long*)&cl.diff[R], (unsigned long long)(-wgt));
+  const bool valid = i < n;
+  uint32_t req = 0;
+  if (valid) {
+    const uint64_t own = key2[i];
+    const int32_t s = (int32_t)(own >> 32);
+    req = (uint32_t)own;
+    if (s < threshold) {
+      cid[req] = -1;
+      csz[req] = 1;
+    } else {
+      // [L, R): the widest range around i whose inner lcps are >= s
+      const int32_t L = ix.last_below_from(i, s);
+      const int32_t R = ix.first_below_from(i + 1, s);
+      // id: minimum of (share, request) over [L, R)
+      const uint64_t m = key_range_min(ib2, ix.stride, st2, nb2, L, R - 1);
+      cid[req] = (int32_t)(uint32_t)m;
+      csz[req] = R - L;
     }
   }
-  const int32_t len = (int32_t)el[i].len;
-  const int32_t cut = min(cl.theta, len);
-  const int32_t start = cut <= 0 ? 0 : ix.last_below_from(i, cut);
-  cl.run[i] = start;
-  if (cl.h[req] <= cl.tau) atomicMin(&cl.pmin[start], (int32_t)req);
+  if (!cl.on) return;
+  int32_t start = 0, cold = INT32_MAX;
+  if (valid) {
+    // the node of depth D = lcp[i] > 0 is counted once, at its leftmost
+    // inner position: the previous position with lcp <= D must have lcp < D
+    const int32_t D = i >= 1 ? lcp[i] : 0;
+    if (D > 0) {
+      const int32_t L = ix.last_below_from(i - 1, D + 1);
+      const int32_t lL = lcp[L];
+      if (lL < D) {
+        const int32_t R = ix.first_below_from(i + 1, D);
+        const int64_t wgt = (int64_t)(R - L) * (D - max(lL, lcp[R]));
+        atomicAdd((unsigned long long*)&cl.diff[L], (unsigned long long)wgt);
+        atomicAdd((unsigned long long*)&cl.diff[R], (unsigned long long)(-wgt));
+      }
+    }
+    const int32_t len = (int32_t)el[i].len;
+    const int32_t cut = min(cl.theta, len);
+    start = cut <= 0 ? 0 : ix.last_below_from(i, cut);
+    cl.run[i] = start;
+    if (cl.h[req] <= cl.tau) cold = (int32_t)req;
+  }
+  // The smallest cold request of each run: a minimum over the wavefront's
+  // lanes of equal run start first, then one atomic per run and wavefront
+  // (a run of thousands of cold requests would otherwise serialize as many
+  // atomics on one word).
+  const int lane = threadIdx.x & (kWave - 1);
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int32_t oc = __shfl_down(cold, off);
+    const int32_t os = __shfl_down(start, off);
+    if (lane + off < kWave && os == start) cold = min(cold, oc);
+  }
+  const int32_t prev = __shfl_up(start, 1);
+  if (valid && (lane == 0 || prev != start) && cold != INT32_MAX) atomicMin(&cl.pmin[start], cold);
 }
 
 constexpr int kScanThreads = 1024;
@@ -1680,19 +1699,26 @@ __global__ void k_off_scatter(int32_t m, const OffElem* __restrict__ el, const i
 }
 
 // One pointer-jumping round over the interval tree: each node adds the
-// offset accumulated at its current link and jumps past it.
+// offsets accumulated at its next kJump - 1 links and jumps past them, so
+// every round multiplies the links a node has summed by kJump (a few more
+// dependent loads per round, a quarter of the rounds of plain doubling).
+constexpr int kJump = 4;
+
 __global__ void k_off_jump(int32_t n, const int64_t* __restrict__ A, const int32_t* __restrict__ P,
                            int64_t* __restrict__ A2, int32_t* __restrict__ P2) {
   const int32_t c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= n) return;
-  const int32_t p = P[c];
-  if (p >= 0) {
-    A2[c] = A[c] + A[p];
-    P2[c] = P[p];
-  } else {
-    A2[c] = A[c];
-    P2[c] = -1;
+  int64_t a = A[c];
+  int32_t p = P[c];
+#pragma unroll
+  for (int q = 1; q < kJump; ++q) {
+    if (p >= 0) {
+      a += A[p];
+      p = P[p];
+    }
   }
+  A2[c] = a;
+  P2[c] = p;
 }
 
 // perm[start of the request's node + its offset] = request.
@@ -1975,7 +2001,7 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
                          roff);
       // a node's chain to the top has at most min(D, n) + 1 links
       const int64_t links = (int64_t)std::min(off->depth_limit, n) + 2;
-      for (int64_t span = 1; span < links; span <<= 1) {
+      for (int64_t span = 1; span < links; span *= kJump) {
         hipLaunchKernelGGL(k_off_jump, dim3(blocks_for(n)), dim3(256), 0, st, n, start[pc], npar[pc],
                            start[pc ^ 1], npar[pc ^ 1]);
         pc ^= 1;

@@ -150,6 +150,30 @@ def test_scale_bit_exact_full_size(seed):
     assert exp["num_nodes"] == s.tree.num_nodes
 
 
+@pytest.mark.parametrize("name,theta", [("rag", 32), ("agentic", 64), ("scale", 32)])
+def test_clpm_every_request_cold(name, theta):
+    # tau above every hit: every request is cold, so a theta-prefix run holds
+    # thousands of cold requests across many wavefronts (the pioneer is the
+    # smallest of them) and the section is pioneer or sibling throughout
+    w = W.make(name, 42)
+    tau = 1 << 30
+    HotPath = _hot()
+    print(f"[gpu] clpm all cold {name} n={w.n} theta={theta}", flush=True)
+    if w.cache_tree is not None:
+        hp = HotPath.from_description(*w.cache_tree)
+    else:
+        hp = HotPath.from_sequences(*w.cache_sequences)
+    hp.load_queue(w.tokens, w.offsets, w.block_size, w.threshold)
+    hp.lpm()
+    hp.clpm(tau, theta)
+    got = hp.results()
+    exp = O.clpm(w.tokens, w.offsets, got["h"], tau, theta)
+    assert np.array_equal(got["section"], exp.section), "section"
+    assert np.array_equal(got["score"], exp.score), "score"
+    assert got["has_sharing"] == exp.has_sharing, "has_sharing"
+    assert set(np.unique(got["section"]).tolist()) <= {1, 2}
+
+
 @pytest.mark.parametrize("seed", range(16))
 @pytest.mark.parametrize("vocab,B,T", [(2, 1, 1), (3, 2, 2), (4, 4, 8), (32000, 16, 4)])
 def test_random_sequence_cases(seed, vocab, B, T):
