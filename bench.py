@@ -401,8 +401,8 @@ def main():
                          "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
                          "bytes_from": "oracle outputs"})
         # sort passes over the queue in one signals call: the first round's
-        # merge sort (tile pass + merge passes) and the second round's
-        # segment sort
+        # merge sort (tile pass + merge passes) and the sort of the second
+        # round's segments
         np2 = 256
         while np2 < w.n:
             np2 <<= 1

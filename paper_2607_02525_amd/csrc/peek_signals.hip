@@ -34,13 +34,15 @@
 //     there). Members with equal keys form the next segment at depth d+l+1;
 //     the LCP across a new boundary is d plus the smaller l. Each prompt byte
 //     is read about once.
-// Two refinement rounds run over the whole queue with the longest member as
-// the head: every member that is a prefix of it (the turns of one agentic
-// session) settles in one round. Whatever is still unsettled after them is
-// finished inside single workgroups with a head picked by a hash of the
-// segment's place and depth, which also halves a group whose members leave a
-// shared path one depth after another (where the longest member would peel
-// one request per round). The host never waits for the device.
+// Two refinement rounds compare over the whole queue with the longest member
+// as the head (the second round's segments are then sorted and split by the
+// workgroups that finish the refinement): every member that is a prefix of
+// it (the turns of one agentic session) settles in one round. Whatever is
+// still unsettled after them is finished inside single workgroups, with a
+// head picked by a hash of the segment's place and depth, which also halves
+// a group whose members leave a shared path one depth after another (where
+// the longest member would peel one request per round). The host never
+// waits for the device.
 #include <algorithm>
 
 #include "peek_compare.h"
@@ -153,12 +155,6 @@ struct ClElem {
   uint32_t len;
 };
 
-struct ClLess {
-  __device__ __forceinline__ bool operator()(const ClElem& a, const ClElem& b) const {
-    return a.hi < b.hi || (a.hi == b.hi && a.lo < b.lo);
-  }
-};
-
 constexpr uint64_t kLenMax = 0x7FFFFFFFull;   // also the mask of a request in a key's low 31 bits
 
 // Largest segment the second round orders inside one workgroup.
@@ -175,13 +171,6 @@ __device__ __forceinline__ uint64_t tok_code(int32_t x) { return (uint64_t)((uin
 __device__ __forceinline__ uint64_t lo_of(uint64_t code, uint32_t len) { return (code << 31) | (kLenMax - len); }
 __device__ __forceinline__ uint64_t code_of(uint64_t lo) { return lo >> 31; }
 __device__ __forceinline__ uint32_t ell_of(uint64_t hi) { return (uint32_t)hi; }
-__device__ __forceinline__ bool same_group(const ClElem& a, const ClElem& b) {
-  return a.hi == b.hi && code_of(a.lo) == code_of(b.lo);
-}
-__device__ __forceinline__ bool group_less(const ClElem& a, uint64_t hi, uint64_t code) {
-  return a.hi < hi || (a.hi == hi && code_of(a.lo) < code);
-}
-
 // Depth of the lowest common ancestor of preorder nodes c1 < c2 that are
 // not ancestor-related: the minimum parent depth over (c1, c2], from the
 // in-block suffix/prefix minima and the sparse table over 64-node blocks.
@@ -472,23 +461,6 @@ __global__ __launch_bounds__(256) void k_first_compare(AnchorIn in, HeadTable T,
     out[i] = AncElem{((uint64_t)c << 32) | m, (code << 31) | ell, (code1 << 31) | (uint32_t)i};
 }
 
-// Start of every lane's group, for the 64 sorted positions base..base+63 of
-// this wavefront: the nearest group start at or before the lane inside the
-// wave, or, for lanes whose group began earlier, one shared wave search
-// over [search_lo, base]. `start` marks lanes whose position opens a group.
-__device__ __forceinline__ int32_t lane_group_start(const ClElem* __restrict__ el, int32_t base, int lane, bool start,
-                                                    bool need_search, int32_t search_lo) {
-  const uint64_t mask = __ballot(start);
-  const uint64_t upto = lane == 63 ? ~0ull : ((2ull << lane) - 1);
-  const uint64_t below = mask & upto;
-  int32_t g0 = base;
-  if (need_search) {
-    const uint64_t h = el[base].hi, c = code_of(el[base].lo);
-    g0 = wave_first_true(search_lo, base, lane, [&](int32_t p) { return !group_less(el[p], h, c); });
-  }
-  return below ? base + (63 - __clzll((unsigned long long)below)) : g0;
-}
-
 // Segments after the first round's sort: a segment is a run of equal
 // (c, m, code, l, code after l); requests of different anchor groups share
 // what the cache tree says (the same node: the smaller m; an ancestor's
@@ -597,10 +569,10 @@ __device__ __forceinline__ int32_t head_pos(int32_t s, int32_t d, int32_t size) 
 
 // Second round, a wavefront per position (grid-stride, so a skipped round
 // costs few workgroups): members of the segments the round takes are
-// compared with their segment's first member, its longest
-// (the first round's sort keeps the longest first in every segment), and
-// get their keys for the segment sort. Nothing to do unless the first round
-// left such a segment (flags_in[1]).
+// compared with their segment's longest member, and get their keys in the
+// form the tail sorts by (hi = l << 33 | code, lo = request); the tail then
+// sorts and splits those segments without comparing again. Nothing to do
+// unless the first round left such a segment (flags_in[1]).
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
@@ -611,243 +583,65 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
                                                         const int32_t* __restrict__ flags_in) {
   if (flags_in[1] == 0) return;
   const int lane = threadIdx.x & (kWave - 1);
+  const int32_t wv = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   const int32_t waves = (int32_t)gridDim.x * 4;
-  for (int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)); i < n;
-       i += waves) {
-    const int32_t s = nseg[i];
-    if (!active[s] || !round_takes(gsize[s])) continue;
-    const uint64_t hb = head[s];
-    const uint32_t hreq = 0xFFFFFFFFu - (uint32_t)hb, hlen = (uint32_t)(hb >> 32);
-    const uint32_t req = el[i].req, len_j = el[i].len;
-    uint32_t ell = len_j - (uint32_t)depth[s];   // the head itself: ended at its length
-    uint64_t code = 0;
-    if (req != hreq) member_key(tokens, offsets, req, len_j, hreq, hlen, depth[s], lane, ell, code);
-    if (lane == 0) {
-      el[i].hi = ((uint64_t)(uint32_t)s << 32) | ell;
-      el[i].lo = lo_of(code, len_j);
-    }
-  }
-}
-
-// Sort key of a segment member inside the segment sort: the segment start
-// is common to all members, so (l, lo) order them as ClLess does.
-struct SegKey {
-  uint32_t ell;
-  uint32_t req;
-  uint64_t lo;
-};
-__device__ __forceinline__ bool seg_less(const SegKey& a, const SegKey& b) {
-  return a.ell < b.ell || (a.ell == b.ell && a.lo < b.lo);
-}
-__device__ __forceinline__ SegKey seg_key(const ClElem& e) { return SegKey{ell_of(e.hi), e.req, e.lo}; }
-__device__ __forceinline__ ClElem seg_elem(const SegKey& k, int32_t s) {
-  ClElem e;
-  e.hi = ((uint64_t)(uint32_t)s << 32) | k.ell;
-  e.lo = k.lo;
-  e.req = k.req;
-  e.len = (uint32_t)(kLenMax - (k.lo & kLenMax));
-  return e;
-}
-
-constexpr int kSegThreads = 512;           // one thread per member of a medium segment
-constexpr int kSegMid = kSegThreads;       // members ranked against LDS keys
-constexpr int kSegRange = 256;             // positions (and segment starts) owned by one workgroup
-
-// Second round: sorts, in place and stably by key, every segment the round
-// takes. Each workgroup owns the segments starting in kSegRange
-// consecutive positions: one of at most 64 members is ranked by one
-// wavefront; one of at most kSegMid members by the whole workgroup, one
-// member per thread, against its keys staged in LDS (every read is a
-// broadcast); a larger one is sorted by the workgroup's LDS merge sort. A
-// member's rank counts the members before it, ties by position. Elements
-// move through registers, so reading and writing one buffer is safe.
-__global__ __launch_bounds__(kSegThreads) void k_refine_seg_sort(int32_t n, ClElem* __restrict__ el,
-                                                                 const int32_t* __restrict__ nseg,
-                                                                 const int32_t* __restrict__ gsize,
-                                                                 const uint8_t* __restrict__ active,
-                                                                 const int32_t* __restrict__ flags_in) {
-  if (flags_in[1] == 0) return;
-  __shared__ SegKey sk[kSegMid];
-  __shared__ uint64_t sa[kSegSortMax];
-  __shared__ uint64_t sb[kSegSortMax];
-  __shared__ uint32_t sp[kSegSortMax];
-  __shared__ int32_t take[kSegRange / 64 + 1];
-  __shared__ int32_t n_take;
-  const int t = threadIdx.x;
-  const int lane = t & (kWave - 1);
-  const int wave = t / kWave;
-  const int32_t r0 = (int32_t)blockIdx.x * kSegRange;
-  if (t == 0) n_take = 0;
-  __syncthreads();
-  // segments of at most 64 members: wave w looks at the starts r0 + 32w ..
-  // r0 + 32w + 31; larger ones (at most one start per 64 positions) are
-  // listed for the whole workgroup
-  constexpr int kPerWave = kSegRange / (kSegThreads / kWave);
-  static_assert(kPerWave <= kWave, "one start per lane");
-  {
-    const int32_t p = r0 + wave * kPerWave + lane;
-    bool small = false;
-    if (lane < kPerWave && p < n && nseg[p] == p && active[p] && round_takes(gsize[p])) {
-      if (gsize[p] <= kWave) small = true;
-      else take[atomicAdd(&n_take, 1)] = p;
-    }
-    uint64_t todo = __ballot(small);
-    while (todo) {
+  // each wavefront takes `per` consecutive positions at a time and checks
+  // them in parallel, one lane each (the loads of one check depend on each
+  // other, so checking them one after another would chain them), then
+  // compares the members among them one after another
+  const int32_t per = min(kWave, max(1, (n + waves - 1) / waves));
+  for (int32_t base = wv * per; base < n; base += waves * per) {
+    const int32_t i = base + lane;
+    const bool in = lane < per && i < n;
+    const int32_t s = in ? nseg[i] : 0;
+    const uint8_t ac = active[s];
+    const int32_t gz = gsize[s];
+    for (uint64_t todo = __ballot(in && ac && round_takes(gz)); todo; todo &= todo - 1) {
       const int f = __ffsll((unsigned long long)todo) - 1;
-      todo &= todo - 1;
-      const int32_t s = r0 + wave * kPerWave + f;
-      const int32_t size = gsize[s];
-      ClElem e{};
-      if (lane < size) e = el[s + lane];
-      int rank = 0;
-      const ClLess less;
-      for (int j = 0; j < size; ++j) {
-        ClElem o;
-        o.hi = __shfl(e.hi, j);
-        o.lo = __shfl(e.lo, j);
-        if (less(o, e) || (j < lane && !less(e, o))) ++rank;
+      const int32_t im = base + f;
+      const int32_t sm = __shfl(s, f);
+      const uint64_t hb = head[sm];
+      const uint32_t hreq = 0xFFFFFFFFu - (uint32_t)hb, hlen = (uint32_t)(hb >> 32);
+      const int32_t d = depth[sm];
+      const uint32_t req = el[im].req, len_j = el[im].len;
+      uint32_t ell = len_j - (uint32_t)d;   // the head itself: ended at its length
+      uint64_t code = 0;
+      if (req != hreq) member_key(tokens, offsets, req, len_j, hreq, hlen, d, lane, ell, code);
+      if (lane == 0) {
+        el[im].hi = ((uint64_t)ell << 33) | code;
+        el[im].lo = req;
       }
-      if (lane < size) el[s + rank] = e;
     }
-  }
-  __syncthreads();
-  const int32_t nt = n_take;
-  for (int b = 0; b < nt; ++b) {
-    const int32_t s = take[b];
-    const int32_t size = gsize[s];
-    if (size <= kSegMid) {
-      SegKey v{};
-      if (t < size) {
-        v = seg_key(el[s + t]);
-        sk[t] = v;
-      }
-      __syncthreads();
-      if (t < size) {
-        int32_t rank = 0;
-        for (int32_t j = 0; j < size; ++j) {
-          const SegKey o = sk[j];
-          rank += (seg_less(o, v) || (j < t && !seg_less(v, o))) ? 1 : 0;
-        }
-        el[s + rank] = seg_elem(v, s);
-      }
-      __syncthreads();
-    } else {
-      const int M = ldssort::pow2_at_least(size);
-      for (int r = t; r < M; r += kSegThreads) {
-        if (r < size) {
-          const ClElem e = el[s + r];
-          sa[r] = ell_of(e.hi);
-          sb[r] = e.lo;
-          sp[r] = (uint32_t)r;
-        } else {
-          sa[r] = ~0ull;
-          sb[r] = ~0ull;
-          sp[r] = 0xFFFFFFFFu;
-        }
-      }
-      __syncthreads();
-      ldssort::lds_sort<kSegThreads>(sa, sb, sp, M);
-      constexpr int kPer = kSegSortMax / kSegThreads;
-      ClElem v[kPer];
-#pragma unroll
-      for (int q = 0; q < kPer; ++q) {
-        const int r = t + q * kSegThreads;
-        if (r < size) v[q] = el[s + sp[r]];
-      }
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < kPer; ++q) {
-        const int r = t + q * kSegThreads;
-        if (r < size) el[s + r] = v[q];
-      }
-      __syncthreads();
-    }
-  }
-}
-
-// Second round, after the segment sort: new groups of the segments the
-// round took, their LCPs, depths, sizes and activity; every other segment
-// start carries its state over (a segment the round did not take stays
-// active for the tail). flags[0] is raised if any segment is still active.
-__global__ __launch_bounds__(256) void k_refine_groups(int32_t n, const ClElem* __restrict__ el,
-                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
-                                                       const int32_t* __restrict__ depth_old,
-                                                       const uint8_t* __restrict__ active_old,
-                                                       int32_t* __restrict__ depth_new,
-                                                       uint8_t* __restrict__ active_new, int32_t* __restrict__ lcp,
-                                                       const int32_t* __restrict__ flags_in,
-                                                       int32_t* __restrict__ flags) {
-  if (flags_in[1] == 0) return;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
-  if (base >= n) return;
-  const int32_t i = base + lane;
-  const bool valid = i < n;
-  ClElem e{};
-  int32_t s = 0;
-  bool live = false, start = false, wait = false;
-  if (valid) {
-    e = el[i];
-    s = nseg[i];
-    live = active_old[s] != 0;
-    wait = live && !round_takes(gsize[s]);   // kept whole for the tail
-    live = live && !wait;
-    start = live && (i == s || !same_group(el[i - 1], e));
-  }
-  // lanes of a live group that began before this wave share one search
-  const bool lane0_needs = __shfl(live && !start, 0);
-  const int32_t s0 = __shfl(s, 0);
-  const int32_t g = lane_group_start(el, base, lane, start, lane0_needs, s0);
-  if (!valid) return;
-  if (!live) {
-    if (i == s) {
-      active_new[i] = wait;
-      depth_new[i] = depth_old[i];
-      if (wait) flags[0] = 1;
-    }
-    return;
-  }
-  const int32_t d = depth_old[s];
-  nseg[i] = g;
-  const uint32_t ell = ell_of(e.hi);
-  const uint64_t code = code_of(e.lo);
-  const bool last = i + 1 == n || !same_group(e, el[i + 1]);
-  const bool can_split = code != 0;
-  if (last) gsize[g] = i - g + 1;
-  if (i == g) {
-    if (i > s) lcp[i] = d + (int32_t)min(ell_of(el[i - 1].hi), ell);
-    const bool act = can_split && !last;
-    active_new[i] = act;
-    depth_new[i] = act ? d + (int32_t)ell + 1 : 0;
-    if (act) flags[0] = 1;
-  } else if (code == 0) {
-    lcp[i] = d + (int32_t)ell;   // identical prompts that ended together
   }
 }
 
 // ---------------------------------------------------------------- tail
-// Segments still active after the global rounds are finished inside single
+// Segments still active after the first round are finished inside single
 // workgroups. Workgroup g owns the segments that start in positions
 // [g * kTailRange, (g + 1) * kTailRange), whole (wherever they end), and keeps
 // the state of their sub-segments in tail-only arrays indexed by position
-// (tact, tdep, tsize), so no workgroup reads what another one writes. Each
-// pass collects the active sub-segments of its segments:
+// (tact, tdep, tsize), so no workgroup reads what another one writes. A
+// segment the queue-wide second round compared (2 to kSegSortMax members)
+// already has its keys: a larger one is sorted and split by the workgroup
+// at once (a smaller one is settled below like any other). Then each pass
+// collects the active sub-segments of its segments:
 //  - one of at most 64 members is settled completely by one wavefront, its
 //    elements held in registers (lane l = position start + l), every round
 //    down to single requests;
-//  - a larger one gets one round from the whole workgroup: 16 wavefronts
+//  - a larger one gets one round from the whole workgroup: 8 wavefronts
 //    compare the members with the head, the keys are sorted in LDS (merge
 //    sort; beyond kTailCap members, ranked in global memory), the
 //    elements are permuted and the new groups marked;
 // and passes repeat until nothing is active. Every round makes each active
 // group strictly deeper or settles it, so the loop ends.
-constexpr int kTailRange = 1024;
+constexpr int kTailRange = 256;
 constexpr int kTailThreads = 512;
 constexpr int kTailWaves = kTailThreads / kWave;
 constexpr int kTailCap = 4096;              // members the workgroup sorts in LDS
 constexpr int kTailList = 1024;              // sub-segments collected per pass and kind
 constexpr int kTailRoots = kTailRange / 2;   // segments of >= 2 members starting in one range
 constexpr uint64_t kCodeMask = (1ull << 33) - 1;
+static_assert(kSegSortMax <= kTailCap, "the second round's segments are sorted in LDS");
 
 struct TailArgs {
   const int32_t* tokens;
@@ -855,11 +649,11 @@ struct TailArgs {
   int32_t n;
   ClElem* el;                // the order after the queue-wide rounds, refined in place
   ClElem* tmp;               // free element buffer (scratch of the global-memory ranking)
-  const int32_t* nseg;       // state after the queue-wide rounds (read only here)
+  const int32_t* nseg;       // state after the first round (read only here)
   const int32_t* gsize;
-  const int32_t* depth[2];   // segment depth and activity after the first round [0] or the second [1]
-  const uint8_t* active[2];
-  const int32_t* flags[2];   // flags after the first round [0] and after the second [1]
+  const int32_t* depth;      // segment depth and activity after the first round
+  const uint8_t* active;
+  const int32_t* flags;      // [any active segment, the second round compared]
   int32_t* lcp;
   uint8_t* tact;             // tail state by position: an active sub-segment starts here
   int32_t* tdep;             //   its depth
@@ -873,8 +667,10 @@ __device__ __forceinline__ bool tail_key_less(uint32_t ea, uint64_t ca, uint32_t
 
 // Settles the segment [s, s + size) of depth d0 (size <= 64) with one
 // wavefront: lane l holds the element at position s + l; each round refines
-// the first active group in the lanes and regroups it.
-__device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int32_t d0, int lane) {
+// the first active group in the lanes and regroups it. `keyed`: the first
+// round's keys are in the elements already (hi = l << 33 | code), written
+// by the second round against its own head.
+__device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int32_t d0, int lane, bool keyed) {
   const bool in = lane < size;
   ClElem e{};
   if (in) e = A.el[s + lane];
@@ -902,8 +698,14 @@ __device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int
     uint64_t code = 0;
     bool need = false;
     if (mem) {
-      if (lane == hl) ell = e.len - (uint32_t)gd;
-      else need = !short_key(A.tokens, A.offsets, e.req, e.len, hreq, hlen, gd, ell, code);
+      if (keyed && iter == 0) {
+        ell = (uint32_t)(e.hi >> 33);
+        code = e.hi & kCodeMask;
+      } else if (lane == hl) {
+        ell = e.len - (uint32_t)gd;
+      } else {
+        need = !short_key(A.tokens, A.offsets, e.req, e.len, hreq, hlen, gd, ell, code);
+      }
     }
     for (uint64_t todo = __ballot(need); todo; todo &= todo - 1) {
       const int j = __ffsll((unsigned long long)todo) - 1;
@@ -974,15 +776,16 @@ __device__ void tail_wave_settle(const TailArgs& A, int32_t s, int32_t size, int
 
 // One round of the segment [s, s + sz) of depth d (sz > 64) by the whole
 // workgroup. Keys are written into the elements' hi/lo fields (hi = l << 33 |
-// code, lo = request), which nothing after the refinement reads.
+// code, lo = request), which nothing after the refinement reads; `keyed`:
+// the second round has written them already.
 __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t d, uint64_t* sa, uint64_t* sb,
-                              uint32_t* sp, uint64_t* cmask) {
+                              uint32_t* sp, uint64_t* cmask, bool keyed) {
   const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
   const int32_t hp = head_pos(s, d, sz);
   const uint32_t hreq = A.el[hp].req, hlen = A.el[hp].len;
   // 64 members per wavefront at a time: each lane checks its member's first
   // tokens, the wavefront compares the rest one member after another
-  for (int32_t b0 = wave * kWave; b0 < sz; b0 += kTailWaves * kWave) {
+  for (int32_t b0 = wave * kWave; b0 < (keyed ? 0 : sz); b0 += kTailWaves * kWave) {
     const int32_t j = b0 + lane;
     uint32_t jreq = 0, jlen = 0, ell = 0;
     uint64_t code = 0;
@@ -1025,18 +828,33 @@ __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t 
     }
     __syncthreads();
     ldssort::lds_sort<kTailThreads>(sa, sb, sp, M);
+    // the permutation goes through registers, field by field (an array of
+    // whole elements would be kept in scratch memory)
     constexpr int kPer = kTailCap / kTailThreads;
-    ClElem v[kPer];
+    uint64_t vh[kPer], vl[kPer];
+    uint32_t vr[kPer], vn[kPer];
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int r = t + q * kTailThreads;
-      if (r < sz) v[q] = A.el[s + sp[r]];
+      if (r < sz) {
+        const ClElem* x = A.el + s + sp[r];
+        vh[q] = x->hi;
+        vl[q] = x->lo;
+        vr[q] = x->req;
+        vn[q] = x->len;
+      }
     }
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
       const int r = t + q * kTailThreads;
-      if (r < sz) A.el[s + r] = v[q];
+      if (r < sz) {
+        ClElem* x = A.el + s + r;
+        x->hi = vh[q];
+        x->lo = vl[q];
+        x->req = vr[q];
+        x->len = vn[q];
+      }
     }
   } else {
     // ranks against every member, then a permutation through the free buffer
@@ -1109,11 +927,10 @@ __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t 
 }
 
 __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
-  // the state the second round left, or the first round's when it did not run
-  const int r2 = A.flags[0][1] != 0 ? 1 : 0;
-  if (A.flags[r2][0] == 0) return;
-  const int32_t* depth = A.depth[r2];
-  const uint8_t* active = A.active[r2];
+  if (A.flags[0] == 0) return;
+  const bool keyed = A.flags[1] != 0;   // the second round compared its segments
+  const int32_t* depth = A.depth;
+  const uint8_t* active = A.active;
   __shared__ uint64_t sa[kTailCap];
   __shared__ uint64_t sb[kTailCap];
   __shared__ uint32_t sp[kTailCap];
@@ -1126,25 +943,51 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
   const int32_t p1 = min(A.n, p0 + kTailRange);
   if (t == 0) n_roots = 0;
   __syncthreads();
+  // (the three loads are issued together: a load behind a branch on another
+  // one would wait for it)
   for (int32_t p = p0 + t; p < p1; p += kTailThreads) {
-    if (A.nseg[p] == p && active[p]) {
+    const int32_t sg = A.nseg[p];
+    const uint8_t ac = active[p];
+    const int32_t gz = A.gsize[p];
+    if (sg == p && ac) {
       const int k = atomicAdd(&n_roots, 1);
       root_s[k] = p;
-      root_e[k] = p + A.gsize[p];
+      root_e[k] = p + gz;
     }
   }
   __syncthreads();
   const int nr = n_roots;
   if (nr == 0) return;
+  // the second round's segments of at most 64 members, from the keys it
+  // wrote: each is settled completely by one wavefront and leaves the list
+  // (its range is emptied)
+  if (keyed) {
+    for (int k = wave; k < nr; k += kTailWaves) {
+      const int32_t s = root_s[k], sz = root_e[k] - s;
+      if (sz <= kWave) {
+        tail_wave_settle(A, s, sz, depth[s], lane, true);
+        if (lane == 0) root_e[k] = s;
+      }
+    }
+    __syncthreads();
+  }
   for (int k = 0; k < nr; ++k) {
     const int32_t s = root_s[k], e = root_e[k];
     for (int32_t q = s + t; q < e; q += kTailThreads) A.tact[q] = q == s;
-    if (t == 0) {
+    if (t == 0 && e > s) {
       A.tdep[s] = depth[s];
       A.tsize[s] = e - s;
     }
   }
   __syncthreads();
+  // its larger segments: sorted by those keys and split by the workgroup
+  // (their parts are then collected by the passes below)
+  if (keyed) {
+    for (int k = 0; k < nr; ++k) {
+      const int32_t s = root_s[k], sz = root_e[k] - s;
+      if (sz > kWave && round_takes(sz)) tail_wg_round(A, s, sz, depth[s], sa, sb, sp, cmask, true);
+    }
+  }
   // Each pass settles at least one small segment or gives at least one large
   // one a round, and the sub-segments ever formed are nodes of a tree over
   // at most n requests (fewer than 2n), so 2n + 2 passes always suffice; the
@@ -1158,8 +1001,10 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
     for (int k = 0; k < nr; ++k) {
       const int32_t s = root_s[k], e = root_e[k];
       for (int32_t q = s + t; q < e; q += kTailThreads) {
-        if (A.tact[q]) {
-          if (A.tsize[q] <= kWave) {
+        const uint8_t ac = A.tact[q];
+        const int32_t z = A.tsize[q];
+        if (ac) {
+          if (z <= kWave) {
             const int x = atomicAdd(&n_small, 1);
             if (x < kTailList) small_l[x] = q;
           } else {
@@ -1174,13 +1019,13 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
     if (ns == 0 && nb == 0) break;
     for (int x = wave; x < ns; x += kTailWaves) {
       const int32_t q = small_l[x];
-      tail_wave_settle(A, q, A.tsize[q], A.tdep[q], lane);
+      tail_wave_settle(A, q, A.tsize[q], A.tdep[q], lane, false);
       if (lane == 0) A.tact[q] = 0;
     }
     __syncthreads();
     for (int x = 0; x < nb; ++x) {
       const int32_t q = big_l[x];
-      tail_wg_round(A, q, A.tsize[q], A.tdep[q], sa, sb, sp, cmask);
+      tail_wg_round(A, q, A.tsize[q], A.tdep[q], sa, sb, sp, cmask, false);
     }
     __syncthreads();
   }
@@ -1749,12 +1594,13 @@ int levels_for(int64_t nb) {
 
 size_t a256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Flag pairs: slot 0 after the first round, slot 1 after the second.
-constexpr int kFlagPairs = 2;
+// Flags after the first round: [any active segment, a segment the second
+// round takes].
+constexpr int kFlags = 2;
 
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
-  size_t el_a, el_b, nseg, gsize, depth_a, depth_b, active_a, active_b, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
+  size_t el_a, el_b, nseg, gsize, depth_a, active_a, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
       keys_b, prefix, diff, pmin, run, local, part, sharing, anc_a, anc_b, hrep, hbest, hmulti, hslot, hcap, head, tact,
       tdep, tsize, total, flags_bytes;
   // PEEK-offline Phase 1 only
@@ -1782,9 +1628,7 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.nseg = take(sizeof(int32_t) * nn);
   L.gsize = take(sizeof(int32_t) * nn);
   L.depth_a = take(sizeof(int32_t) * nn);
-  L.depth_b = take(sizeof(int32_t) * nn);
   L.active_a = take(nn);
-  L.active_b = take(nn);
   L.lcp = take(sizeof(int32_t) * ((size_t)n + 1));
   L.key2 = take(sizeof(uint64_t) * nn);
   L.ib_stride = (int64_t)L.nb1 * 64;
@@ -1792,7 +1636,7 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.ib2 = take(sizeof(uint64_t) * kInBlockLevels * (size_t)L.ib_stride);
   L.st1 = take(sizeof(int32_t) * (size_t)L.levels * L.nb1);
   L.st2 = take(sizeof(uint64_t) * (size_t)L.levels * L.nb2);
-  L.flags_bytes = sizeof(int32_t) * 2 * kFlagPairs;
+  L.flags_bytes = sizeof(int32_t) * kFlags;
   L.flags = take(L.flags_bytes);
   L.keys_a = take(sizeof(uint32_t) * np);
   L.keys_b = take(sizeof(uint32_t) * np);
@@ -1895,15 +1739,15 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   int32_t* nseg = (int32_t*)(w + L.nseg);
   int32_t* gsize = (int32_t*)(w + L.gsize);
   // segment depth and activity after round r live in slot r & 1
-  int32_t* depth[2] = {(int32_t*)(w + L.depth_a), (int32_t*)(w + L.depth_b)};
-  uint8_t* active[2] = {(uint8_t*)(w + L.active_a), (uint8_t*)(w + L.active_b)};
+  int32_t* depth = (int32_t*)(w + L.depth_a);
+  uint8_t* active = (uint8_t*)(w + L.active_a);
   int32_t* lcp = (int32_t*)(w + L.lcp);
   uint64_t* key2 = (uint64_t*)(w + L.key2);
   int32_t* ib1 = (int32_t*)(w + L.ib1);
   uint64_t* ib2 = (uint64_t*)(w + L.ib2);
   int32_t* st1 = (int32_t*)(w + L.st1);
   uint64_t* st2 = (uint64_t*)(w + L.st2);
-  int32_t* flags = (int32_t*)(w + L.flags);   // pairs: [any active segment, some active segment too large]
+  int32_t* flags = (int32_t*)(w + L.flags);   // [any active segment, a segment the second round takes]
   const unsigned wave_blocks = blocks_for(n, 4 * kWave);
   ClpmArgs cl{};
   if (clpm != nullptr) {
@@ -1949,26 +1793,23 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
     prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
   }
   hipLaunchKernelGGL(k_first_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, sorted, ain,
-                     anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth[0], active[0], head, lcp, flags, ride);
+                     anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth, active, head, lcp, flags, ride);
 
-  // 2. The second round, over the whole queue but only for segments of 65
-  // to kSegSortMax members (skipped when there are none): every member is
+  // 2. The second round, over the whole queue but only for segments of 2 to
+  // kSegSortMax members (skipped when there are none): every member is
   // compared with its segment's head (its longest member) by a wavefront of
-  // its own, the segments are sorted in place and split.
+  // its own.
   ClElem* el = bufs[0];
   {
     const unsigned cmp_blocks = std::min(blocks_for(n, 4), 2048u);
     hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks), dim3(256), 0, st, tokens, offsets, n, el, nseg, gsize,
-                       depth[0], active[0], head, flags);
-    hipLaunchKernelGGL(k_refine_seg_sort, dim3(blocks_for(n, kSegRange)), dim3(kSegThreads), 0, st, n, el, nseg,
-                       gsize, active[0], flags);
-    hipLaunchKernelGGL(k_refine_groups, dim3(wave_blocks), dim3(256), 0, st, n, el, nseg, gsize, depth[0], active[0],
-                       depth[1], active[1], lcp, flags, flags + 2);
+                       depth, active, head, flags);
   }
 
-  // 3. Whatever is still active is settled inside single workgroups.
-  TailArgs ta{tokens, offsets, n, el, bufs[1], nseg, gsize, {depth[0], depth[1]}, {active[0], active[1]},
-              {flags, flags + 2}, lcp, (uint8_t*)(w + L.tact), (int32_t*)(w + L.tdep), (int32_t*)(w + L.tsize)};
+  // 3. Everything still active (with the second round's keys where it ran)
+  // is settled inside single workgroups.
+  TailArgs ta{tokens, offsets, n, el, bufs[1], nseg, gsize, depth, active, flags, lcp, (uint8_t*)(w + L.tact),
+              (int32_t*)(w + L.tdep), (int32_t*)(w + L.tsize)};
   hipLaunchKernelGGL(k_refine_tail, dim3(blocks_for(n, kTailRange)), dim3(kTailThreads), 0, st, ta);
 
   // 4. Range queries over the settled order: share, size, id (and the cLPM
