@@ -337,23 +337,45 @@ def make_scale(seed: int = 42, n: int = 65536, n_covered: int = 77,
     q_tok_all = rng.integers(0, V, size=int(q_lens_all.sum()), dtype=np.int32)
     pos = 0
     qi = 0
+    n_branch = 0
     for k in covered:
         parents.append(sys_node)
         edges.append(docs[k])
         doc_node = len(parents) - 1
         base = len(system) + len(docs[k])
-        firsts = _distinct(rng, V, queries_per_doc)
-        pairs = set()
+        # Query tokens are i.i.d., first tokens included, so about 560 of a
+        # document's 12168 queries share their first token with another one
+        # (the survey's first-token-collision branch nodes). Their second
+        # tokens are made distinct, so such queries branch right after the
+        # shared token: a one-token branch node under the document.
+        by_first = {}
         for j in range(queries_per_doc):
             ql = int(q_lens_all[qi])
             q = q_tok_all[pos:pos + ql]
-            q[0] = firsts[j]
             pos += ql
             qi += 1
-            keep = block_floor(base + ql) - base
+            by_first.setdefault(int(q[0]), []).append((q, block_floor(base + ql) - base))
+        pairs = set()
+        for t0, group in by_first.items():
+            if len(group) == 1:
+                q, keep = group[0]
+                parents.append(doc_node)
+                edges.append(q[:keep])
+                pairs.add(t0 * V + int(q[1]))
+                continue
             parents.append(doc_node)
-            edges.append(q[:keep])
-            pairs.add(int(q[0]) * V + int(q[1]))
+            edges.append(group[0][0][:1])
+            branch = len(parents) - 1
+            n_branch += 1
+            seconds = set()
+            for q, keep in group:
+                while int(q[1]) in seconds:
+                    q[1] = rng.integers(0, V)
+                seconds.add(int(q[1]))
+                pairs.add(t0 * V + int(q[1]))
+                if keep > 1:
+                    parents.append(branch)
+                    edges.append(q[1:keep])
         doc_pairs[int(k)] = pairs
     for s in cached_sessions:
         prev_end, parent = 0, 0
@@ -418,7 +440,8 @@ def make_scale(seed: int = 42, n: int = 65536, n_covered: int = 77,
     return Workload("scale", seed, tokens, offsets, 16, 256,
                     cache_tree=(parent_arr, eoff, etok),
                     meta={"kind": kinds, "index": index, "covered": is_cov,
-                          "doc_of_rag": live_docs, "doc_len": doc_len, "sys_len": sys_len})
+                          "doc_of_rag": live_docs, "doc_len": doc_len, "sys_len": sys_len,
+                          "branch_nodes": n_branch})
 
 
 def make_caterpillar(seed: int = 42, n: int = 4096) -> Workload:

@@ -425,6 +425,18 @@ def test_scale_invariants_and_closed_forms():
     assert np.all((m[cov] == base[cov]) | (m[cov] == base[cov] + 1))
     assert np.all(m[~cov] == 1024)
     assert 0.8e6 <= s.tree.num_nodes <= 1.2e6 and 160e6 <= s.tree.num_edge_tokens <= 240e6
+    # cached queries sharing a first token under a document branch right after
+    # it: about 45K one-token branch nodes under the document nodes (+-20%)
+    nb = w.meta["branch_nodes"]
+    assert 36000 <= nb <= 54000
+    nchild = np.bincount(parent[1:], minlength=len(parent))
+    sys_node = np.unique(s.lpm.last_node[rag][~cov])   # where prompts on uncovered documents stop
+    assert len(sys_node) == 1 and depth[sys_node[0]] == w.meta["sys_len"]
+    doc_nodes = np.flatnonzero(parent == sys_node[0])
+    assert len(doc_nodes) == int(w.meta["covered"].sum())
+    under_doc = np.isin(parent, doc_nodes)
+    one = under_doc & (depth - depth[np.maximum(parent, 0)] == 1) & (nchild >= 1)
+    assert nb - nb // 100 <= int(one.sum()) <= nb
 
 
 @pytest.mark.parametrize("seed", W.PAPER_SEEDS)
