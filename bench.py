@@ -98,10 +98,11 @@ WALK_SOURCES = ("peek_walk.hip", "peek_compare.h", "peek_internal.h")
 WALK_COUNTERS = os.path.join(ROOT, "profiles", "k_lpm_walk_scale_counters.txt")
 
 
-def walk_traffic(config: str):
+def walk_traffic(config: str, nodes: int, tokens: int):
     """HBM bytes per walk launch from the committed counter summary (FETCH_SIZE
     and WRITE_SIZE scaled by a plain-copy calibration), or None when the walk
-    sources changed since the counters were taken or another config runs."""
+    sources or the workload (cache nodes, queue tokens) changed since the
+    counters were taken, or another config runs."""
     import hashlib
     if config != "scale" or not os.path.exists(WALK_COUNTERS):
         return None
@@ -115,6 +116,8 @@ def walk_traffic(config: str):
         with open(os.path.join(ROOT, "paper_2607_02525_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     if kv.get("source_sha256") != h.hexdigest():
+        return None
+    if kv.get("workload_nodes") != str(nodes) or kv.get("workload_tokens") != str(tokens):
         return None
     return int(kv["traffic_bytes_per_dispatch"])
 
@@ -366,7 +369,7 @@ def main():
     lpm_avg_s = float(lpm_ms.mean()) / 1e3
     achieved = b_alg / lpm_avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": walk_traffic(args.config),
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": walk_traffic(args.config, hp.num_nodes, len(w.tokens)),
                 "kernel": "k_lpm_walk", "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
                 "bytes_from": "GPU outputs (no oracle run)",
                 "avg_launch_ms": round(float(lpm_ms.mean()), 4), "min_launch_ms": round(float(lpm_ms.min()), 4)}

@@ -1126,54 +1126,70 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
   }
 }
 
-// Sparse tables over the block minima, one workgroup, level by level. Up to
-// kTabLds blocks the previous level is read from LDS (each level costs a
-// barrier, not a round trip to memory); beyond that from memory.
-constexpr int kTabLds = 4096;
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 
-__global__ __launch_bounds__(1024) void k_final_tables(int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
-                                                       int32_t nb1, int32_t nb2, int levels) {
-  if (nb1 <= kTabLds && nb2 <= kTabLds) {
-    __shared__ int32_t a1[2][kTabLds];
-    __shared__ uint64_t a2[2][kTabLds];
-    for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) a1[0][b] = st1[b];
-    for (int32_t b = threadIdx.x; b < nb2; b += blockDim.x) a2[0][b] = st2[b];
-    __syncthreads();
-    for (int k = 1; k < levels; ++k) {
-      const int32_t h = 1 << (k - 1);
-      const int cur = k & 1, prev = cur ^ 1;
-      for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) {
-        if (b + 2 * h <= nb1) {
-          const int32_t v = min(a1[prev][b], a1[prev][b + h]);
-          a1[cur][b] = v;
-          st1[(int64_t)k * nb1 + b] = v;
-        }
-        if (b + 2 * h <= nb2) {
-          const uint64_t x = a2[prev][b], y = a2[prev][b + h];
-          const uint64_t v = x < y ? x : y;
-          a2[cur][b] = v;
-          st2[(int64_t)k * nb2 + b] = v;
-        }
-      }
-      __syncthreads();
-    }
-    return;
+// Sparse tables over the block minima (level k, entry b: the minimum over
+// blocks [b, b + 2^k), stored while b + 2^k <= the block count).
+// Levels 1..kTabLow: each workgroup owns kTabChunk consecutive entries and
+// loads their level-0 values plus the kTabChunk - 1 that follow into LDS,
+// where the levels are built one after another (a barrier per level, no
+// round trip to memory); every window of those levels lies inside what it
+// loaded. Levels above kTabLow (from 2 * kTabChunk blocks on, queues of
+// about 131K requests and more) come from level kTabLow directly: entry b
+// of level k is the minimum of 2^(k - kTabLow) level-kTabLow entries spaced
+// kTabChunk apart, in one more launch.
+constexpr int kTabChunk = 1024;
+constexpr int kTabLow = 10;   // 2^kTabLow == kTabChunk
+static_assert((1 << kTabLow) == kTabChunk, "a level-kTabLow window spans one chunk");
+
+__global__ __launch_bounds__(kTabChunk) void k_final_tables(int32_t* __restrict__ st1, uint64_t* __restrict__ st2,
+                                                            int32_t nb1, int32_t nb2, int levels) {
+  __shared__ int32_t a1[2][2 * kTabChunk];   // two buffers: one barrier per level
+  __shared__ uint64_t a2[2][2 * kTabChunk];
+  const int t = threadIdx.x;
+  const int32_t b0 = (int32_t)blockIdx.x * kTabChunk;
+  for (int q = t; q < 2 * kTabChunk; q += kTabChunk) {
+    const int32_t b = b0 + q;
+    a1[0][q] = b < nb1 ? st1[b] : INT32_MAX;
+    a2[0][q] = b < nb2 ? st2[b] : ~0ull;
   }
-  for (int k = 1; k < levels; ++k) {
-    const int32_t h = 1 << (k - 1);
-    for (int32_t b = threadIdx.x; b < nb1; b += blockDim.x) {
-      if (b + 2 * h <= nb1)
-        st1[(int64_t)k * nb1 + b] = min(st1[(int64_t)(k - 1) * nb1 + b], st1[(int64_t)(k - 1) * nb1 + b + h]);
-      if (b + 2 * h <= nb2) {
-        const uint64_t x = st2[(int64_t)(k - 1) * nb2 + b], y = st2[(int64_t)(k - 1) * nb2 + b + h];
-        st2[(int64_t)k * nb2 + b] = x < y ? x : y;
-      }
+  __syncthreads();
+  const int top = min(levels - 1, kTabLow);
+  for (int k = 1; k <= top; ++k) {
+    const int h = 1 << (k - 1);
+    const int prev = (k - 1) & 1, cur = k & 1;
+    // positions a later level reads: q < kTabChunk + (kTabChunk - 2^k)
+    for (int q = t; q < 2 * kTabChunk - (1 << k); q += kTabChunk) {
+      a1[cur][q] = min(a1[prev][q], a1[prev][q + h]);
+      a2[cur][q] = umin64(a2[prev][q], a2[prev][q + h]);
     }
     __syncthreads();
+    const int32_t b = b0 + t;
+    if (b + 2 * h <= nb1) st1[(int64_t)k * nb1 + b] = a1[cur][t];
+    if (b + 2 * h <= nb2) st2[(int64_t)k * nb2 + b] = a2[cur][t];
   }
 }
 
-__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+// Levels above kTabLow, from level kTabLow (one thread per entry).
+__global__ void k_final_tables_high(int32_t* __restrict__ st1, uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2,
+                                    int levels) {
+  const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t* l1 = st1 + (int64_t)kTabLow * nb1;
+  const uint64_t* l2 = st2 + (int64_t)kTabLow * nb2;
+  for (int k = kTabLow + 1; k < levels; ++k) {
+    const int32_t w = 1 << k;
+    if (b + w <= nb1) {
+      int32_t m = INT32_MAX;
+      for (int32_t j = b; j < b + w; j += kTabChunk) m = min(m, l1[j]);
+      st1[(int64_t)k * nb1 + b] = m;
+    }
+    if (b + w <= nb2) {
+      uint64_t m = ~0ull;
+      for (int32_t j = b; j < b + w; j += kTabChunk) m = umin64(m, l2[j]);
+      st2[(int64_t)k * nb2 + b] = m;
+    }
+  }
+}
 
 // Minimum of a[lo..hi] inside one 64-block, from the in-block table: two
 // windows of the largest stored width (at most 32) that cover the range.
@@ -1819,7 +1835,14 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   fr.first_block = ride_demand ? (int32_t)fb_blocks : INT32_MAX;
   hipLaunchKernelGGL(k_final_blocks, dim3(fb_blocks + (ride_demand ? blocks_for(t->num_nodes) : 0)), dim3(256), 0,
                      st, n, el, lcp, key2, ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr, fr);
-  hipLaunchKernelGGL(k_final_tables, dim3(1), dim3(1024), 0, st, st1, st2, L.nb1, L.nb2, L.levels);
+  {
+    const int32_t nbm = std::max(L.nb1, L.nb2);
+    hipLaunchKernelGGL(k_final_tables, dim3(blocks_for(nbm, kTabChunk)), dim3(kTabChunk), 0, st, st1, st2, L.nb1,
+                       L.nb2, L.levels);
+    if (L.levels > kTabLow + 1)
+      hipLaunchKernelGGL(k_final_tables_high, dim3(blocks_for(nbm)), dim3(256), 0, st, st1, st2, L.nb1, L.nb2,
+                         L.levels);
+  }
   if (off != nullptr) {
     // PEEK-offline Phase 1 from the settled order (see OffSource).
     int64_t* start[2] = {(int64_t*)(w + L.start_a), (int64_t*)(w + L.start_b)};
