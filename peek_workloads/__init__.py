@@ -65,7 +65,7 @@ class Workload:
 
 
 _TAGS = {"tiny": 1, "rag": 2, "agentic": 3, "nosharing": 4, "scale": 5,
-         "random": 6, "randtree": 7, "caterpillar": 8}
+         "random": 6, "randtree": 7, "caterpillar": 8, "long": 9}
 
 
 def _rng(seed: int, tag: str) -> np.random.Generator:
@@ -490,6 +490,31 @@ CONFIGS = {
 
 def make(name: str, seed: int = 42) -> Workload:
     return CONFIGS[name](seed)
+
+
+def long_queue(seed: int = 42, n: int = 140000, n_prefix: int = 512, prefix_len: int = 512,
+               n_cached: int = 256) -> Workload:
+    """A long queue of short prompts (64-256 tokens of their own): 70% of them
+    start with one of n_prefix shared prefixes of prefix_len tokens (chat
+    system prompts), the first n_cached of which are cached. Built with
+    vectorized draws, for queues of a few hundred thousand requests."""
+    rng = _rng(seed, "long")
+    V = VOCAB_LARGE
+    pre = rng.integers(0, V, size=(n_prefix, prefix_len), dtype=np.int32)
+    pre[:, 0] = _distinct(rng, V, n_prefix)
+    own = rng.integers(64, 257, size=n)
+    shared = rng.random(n) < 0.7
+    which = rng.integers(0, n_prefix, size=n)
+    lens = own + np.where(shared, prefix_len, 0)
+    off = np.zeros(n + 1, np.int64)
+    np.cumsum(lens, out=off[1:])
+    tok = rng.integers(0, V, size=int(off[-1]), dtype=np.int32)
+    rows = np.flatnonzero(shared)
+    idx = off[rows][:, None] + np.arange(prefix_len)[None, :]
+    tok[idx] = pre[which[rows]]
+    ctok, coff = pack([pre[j] for j in range(n_cached)])
+    return Workload("long", seed, tok, off, 16, 4, cache_sequences=(ctok, coff),
+                    meta={"shared": shared, "prefix": which})
 
 
 # --------------------------------------------------------------------------

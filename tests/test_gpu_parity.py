@@ -150,6 +150,15 @@ def test_scale_bit_exact_full_size(seed):
     assert exp["num_nodes"] == s.tree.num_nodes
 
 
+def test_long_queue_bit_exact():
+    # 140,000 requests: 2188 position blocks of 64, so the range tables over
+    # the blocks need levels above 10 (built from level 10 by the second
+    # table kernel), and every output is compared element by element
+    w = W.long_queue(42)
+    assert (w.n + 64) // 64 > 2048
+    run_and_compare(w)
+
+
 @pytest.mark.parametrize("name,theta", [("rag", 32), ("agentic", 64), ("scale", 32)])
 def test_clpm_every_request_cold(name, theta):
     # tau above every hit: every request is cold, so a theta-prefix run holds
