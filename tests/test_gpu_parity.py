@@ -142,7 +142,11 @@ def test_configs_bit_exact(name, seed):
 @pytest.mark.parametrize("seed", W.PAPER_SEEDS)
 def test_scale_bit_exact_full_size(seed):
     w = W.make("scale", seed)
-    hp, res, s = run_and_compare(w, repeat=2, block_sample=3000)
+    # the hashed-block hit against the oracle on the whole queue at seed 42
+    # (the oracle hashes the cache's 193M edge tokens first: about a minute),
+    # on 3000 sampled requests at the other seeds; every seed also compares
+    # it on the whole queue with the radix path's block-floored hit
+    hp, res, s = run_and_compare(w, repeat=2, block_sample=None if seed == 42 else 3000)
     parent, depth, _, _ = s.tree.export()
     checks.check_lpm(w, parent, depth, res["match_len"], res["h"], res["last_node"])
     checks.check_demand(w.n, parent, res["last_node"], res["demand"])
