@@ -307,12 +307,15 @@ def test_segment_sizes_at_the_anchor(copies):
     run_and_compare(_w(prompts, cached=[base[:150]], T=16))
 
 
-@pytest.mark.parametrize("copies,fan", [(600, 2), (1500, 2), (2000, 1), (9300, 2), (20000, 3)])
+@pytest.mark.parametrize("copies,fan", [(64, 1), (65, 1), (600, 2), (1500, 2), (2000, 1), (4096, 1), (4097, 1),
+                                        (9300, 2), (20000, 3)])
 def test_large_segments_in_later_rounds(copies, fan):
     # the anchor group splits into `fan` groups in the first round, each into
-    # four in the second and into single requests in the third; a group above
-    # 512 members after the first round makes the host drive the next round
-    # with a global sort
+    # four in the second and into single requests in the third. The second
+    # round compares the groups of at most 4096 members queue-wide and the
+    # tail sorts them from its keys (a wavefront up to 64 members, the
+    # workgroup above); a larger group goes to the tail whole: sizes on both
+    # sides of 64 and of 4096
     rng = np.random.default_rng(copies + fan)
     base = rng.integers(0, 1000, size=200).tolist()
     mid = rng.integers(0, 1000, size=100).tolist()
