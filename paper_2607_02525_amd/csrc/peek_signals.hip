@@ -361,13 +361,10 @@ __global__ __launch_bounds__(kInsThreads) void k_first_insert(AnchorIn in, HeadT
     bool first = false;
     // at most n keys in more than 2n slots: an empty slot or the key is found
     for (uint32_t probe = 0; probe <= T.mask; ++probe) {
-      uint32_t v = __hip_atomic_load(&T.rep[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t v = atomicCAS(&T.rep[h], 0u, (uint32_t)i + 1);
       if (v == 0) {
-        v = atomicCAS(&T.rep[h], 0u, (uint32_t)i + 1);
-        if (v == 0) {
-          first = true;   // this workgroup's group represents the group
-          break;
-        }
+        first = true;   // this workgroup's group represents the group
+        break;
       }
       uint32_t c2, m2, len2;
       uint64_t code2;
@@ -378,8 +375,7 @@ __global__ __launch_bounds__(kInsThreads) void k_first_insert(AnchorIn in, HeadT
     lglob[ls] = (int32_t)h;
     if (!first || lcnt[ls] >= 2) __hip_atomic_store(&T.multi[h], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint64_t mine = lbest[ls];
-    if (__hip_atomic_load(&T.best[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < mine)
-      atomicMax((unsigned long long*)&T.best[h], (unsigned long long)mine);
+    atomicMax((unsigned long long*)&T.best[h], (unsigned long long)mine);
   }
   __syncthreads();
   if (valid) T.slot[i] = lglob[ls];
