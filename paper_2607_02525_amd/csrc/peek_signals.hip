@@ -485,12 +485,16 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
   if (base >= n) return;
   const int32_t i = base + lane;
   const bool valid = i < n;
-  AncElem e{};
-  bool start = false;
-  if (valid) {
-    e = sd[i];
-    start = i == 0 || !same_sub(sd[i - 1], e);
-  }
+  // this position and both neighbours, loaded together (clamped indices; a
+  // load behind a branch on another one would wait for it)
+  const AncElem e = sd[min(i, n - 1)];
+  const AncElem p = sd[max(min(i, n - 1) - 1, 0)];
+  const AncElem nx = sd[min(i + 1, n - 1)];
+  const bool start = valid && (i == 0 || !same_sub(p, e));
+  const bool last = i + 1 >= n || !same_sub(e, nx);
+  // the end of the previous position's node, for the lcp across a group
+  // start (anchored passes only: unanchored ones put every request at the root)
+  const int32_t p_end = t.nodes != nullptr ? t.nodes[(uint32_t)(p.hi >> 32)].subtree_end : 0;
   // the start of every lane's segment: inside the wave from the ballot, else
   // one shared wave search back from the wave's first position
   const uint64_t mask = __ballot(start);
@@ -503,11 +507,8 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
   }
   const int32_t g = below ? base + (63 - __clzll((unsigned long long)below)) : g0;
   const uint32_t req = (uint32_t)(e.lo & kLenMax);
-  uint32_t len = 0;
-  if (valid) {
-    const int64_t o = in.offsets[req];
-    len = min((uint32_t)(in.offsets[req + 1] - o), in.len_cap);
-  }
+  const int64_t o0 = in.offsets[req], o1 = in.offsets[req + 1];
+  const uint32_t len = valid ? min((uint32_t)(o1 - o0), in.len_cap) : 0u;
   // longest member of each segment: segmented maximum over the wave's lanes
   uint64_t best = valid ? (((uint64_t)len << 32) | (0xFFFFFFFFu - req)) : 0;
   for (int off = 1; off < kWave; off <<= 1) {
@@ -524,14 +525,12 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
   if (act_seg && (lane == 0 || i == g)) atomicMax((unsigned long long*)&head[g], (unsigned long long)best);
   el[i] = ClElem{0, 0, req, len};
   nseg[i] = g;
-  const bool last = i + 1 == n || !same_sub(e, sd[i + 1]);
   if (last) {
     gsize[g] = i - g + 1;
     if (act_seg && i > g && round_takes(i - g + 1)) flags[1] = 1;
   }
   if (i == g) {
     if (i > 0) {
-      const AncElem p = sd[i - 1];
       int32_t v;
       if (p.hi == e.hi && (p.mid >> 31) == code) {
         v = (int32_t)(m + 1 + (uint32_t)(p.mid & kLenMax));   // split by the head: the smaller l is p's
@@ -539,7 +538,7 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
         const uint32_t c1 = (uint32_t)(p.hi >> 32), m1 = (uint32_t)p.hi;
         const uint32_t c2 = (uint32_t)(e.hi >> 32);
         if (c1 == c2) v = (int32_t)min(m1, m);
-        else if (c2 < (uint32_t)t.nodes[c1].subtree_end) v = (int32_t)m1;
+        else if (c2 < (uint32_t)p_end) v = (int32_t)m1;
         else v = lca_depth(t, (int32_t)c1, (int32_t)c2);
       }
       lcp[i] = v;
