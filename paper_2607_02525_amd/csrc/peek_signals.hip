@@ -440,14 +440,17 @@ __global__ __launch_bounds__(256) void k_first_compare(AnchorIn in, HeadTable T,
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t i = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   if (i >= n) return;
+  // the slot with the key's loads, then the group's state with the key's
+  // token (loads behind a branch on another one would wait for it)
+  const int32_t h = T.slot[i];
   uint32_t c, m, len;
   uint64_t code;
   in.key((uint32_t)i, c, m, code, len);
+  const uint32_t multi = T.multi[h];
+  const uint64_t b = T.best[h];
   uint32_t ell = 0;
   uint64_t code1 = 0;
-  const int32_t h = T.slot[i];
-  if (code != 0 && T.multi[h] != 0) {
-    const uint64_t b = T.best[h];
+  if (code != 0 && multi != 0) {
     const uint32_t head = 0xFFFFFFFFu - (uint32_t)b, hlen = (uint32_t)(b >> 32);
     const int32_t d = (int32_t)m + 1;
     if ((uint32_t)i == head) ell = len - (uint32_t)d;
@@ -1195,31 +1198,64 @@ __device__ __forceinline__ T in_block_min(const T* __restrict__ ib, int64_t stri
   return x < y ? x : y;
 }
 
+// In-block searches in two rounds of independent loads (lifting through the
+// levels would chain six dependent loads): the minima of the 8-position
+// windows (level 3) pick the window that holds the answer, then that
+// window's 8 values pick the position. Windows are laid from the search's
+// own end, so all of them are whole except one short window at the far
+// side. Loads use clamped in-range addresses and their values are selected
+// afterwards.
+constexpr int kWin = 8;
+static_assert(kInBlockLevels > 3 && (1 << 3) == kWin, "level 3 holds the 8-position window minima");
+
 // Last j in [lo, hi] (one block, at most 64 positions) with lcp[j] < s, or
-// lo - 1 if none. Lifting by 32, 16, .., 1 skips up to 63 positions; a
-// final single step covers a block that is >= s throughout.
+// lo - 1 if none.
 __device__ __forceinline__ int32_t last_below(const int32_t* __restrict__ ib1, int64_t stride, int32_t lo, int32_t hi,
                                               int32_t s) {
-  int32_t pos = hi;   // lcp[pos+1..hi] >= s
-  for (int k = kInBlockLevels - 1; k >= 0; --k) {
-    const int32_t w = 1 << k;
-    if (pos - w + 1 >= lo && ib1[k * stride + pos - w + 1] >= s) pos -= w;
-  }
-  if (pos >= lo && ib1[pos] >= s) --pos;
-  return pos;
+  const int32_t full = (hi - lo + 1) / kWin;   // whole windows ending at hi, hi - 8, ...
+  const int32_t* __restrict__ l3 = ib1 + 3 * stride;
+  int32_t mv[kWin];
+#pragma unroll
+  for (int t = 0; t < kWin; ++t) mv[t] = l3[t < full ? hi - kWin * t - (kWin - 1) : lo];
+  int win = -1;
+#pragma unroll
+  for (int t = kWin - 1; t >= 0; --t)
+    if (t < full && mv[t] < s) win = t;   // the window nearest hi
+  const int32_t whi = win >= 0 ? hi - kWin * win : hi - kWin * full;
+  const int32_t wlo = win >= 0 ? whi - (kWin - 1) : lo;   // the short window: [lo, whi], possibly empty
+  int32_t v[kWin];
+#pragma unroll
+  for (int q = 0; q < kWin; ++q) v[q] = ib1[max(whi - q, lo)];
+  int32_t ans = lo - 1;
+#pragma unroll
+  for (int q = kWin - 1; q >= 0; --q)
+    if (whi - q >= wlo && v[q] < s) ans = whi - q;   // the largest position
+  return ans;
 }
 
 // First j in [lo, hi] (one block, at most 64 positions) with lcp[j] < s, or
 // hi + 1 if none.
 __device__ __forceinline__ int32_t first_below(const int32_t* __restrict__ ib1, int64_t stride, int32_t lo, int32_t hi,
                                                int32_t s) {
-  int32_t pos = lo;   // lcp[lo..pos-1] >= s
-  for (int k = kInBlockLevels - 1; k >= 0; --k) {
-    const int32_t w = 1 << k;
-    if (pos + w - 1 <= hi && ib1[k * stride + pos] >= s) pos += w;
-  }
-  if (pos <= hi && ib1[pos] >= s) ++pos;
-  return pos;
+  const int32_t full = (hi - lo + 1) / kWin;   // whole windows starting at lo, lo + 8, ...
+  const int32_t* __restrict__ l3 = ib1 + 3 * stride;
+  int32_t mv[kWin];
+#pragma unroll
+  for (int t = 0; t < kWin; ++t) mv[t] = l3[t < full ? lo + kWin * t : lo];
+  int win = -1;
+#pragma unroll
+  for (int t = kWin - 1; t >= 0; --t)
+    if (t < full && mv[t] < s) win = t;   // the window nearest lo
+  const int32_t wlo = win >= 0 ? lo + kWin * win : lo + kWin * full;
+  const int32_t whi = win >= 0 ? wlo + (kWin - 1) : hi;   // the short window: [wlo, hi], possibly empty
+  int32_t v[kWin];
+#pragma unroll
+  for (int q = 0; q < kWin; ++q) v[q] = ib1[min(wlo + q, hi)];
+  int32_t ans = hi + 1;
+#pragma unroll
+  for (int q = kWin - 1; q >= 0; --q)
+    if (wlo + q <= whi && v[q] < s) ans = wlo + q;   // the smallest position
+  return ans;
 }
 
 // Range queries over lcp[0..n] from the in-block tables and the sparse
