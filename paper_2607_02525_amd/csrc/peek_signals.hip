@@ -275,9 +275,13 @@ __device__ __forceinline__ uint32_t group_hash(uint32_t c, uint32_t m, uint64_t 
 struct AncElem {
   uint64_t hi, mid, lo;
 };
+// Every field is compared without short-circuit branches: with || and &&
+// the compiler loads the later fields of both elements only after the
+// earlier ones compare equal, one dependent round trip per field, in the
+// sort's LDS searches and in its global diagonal searches alike.
 struct AncLess {
   __device__ __forceinline__ bool operator()(const AncElem& a, const AncElem& b) const {
-    return a.hi < b.hi || (a.hi == b.hi && (a.mid < b.mid || (a.mid == b.mid && a.lo < b.lo)));
+    return (a.hi < b.hi) | ((a.hi == b.hi) & ((a.mid < b.mid) | ((a.mid == b.mid) & (a.lo < b.lo))));
   }
 };
 // the compare's output as the sort's input, padded past n with keys that sort last
@@ -1454,9 +1458,9 @@ struct OffElem {
   int32_t k2;      // the request, or the child's earliest request
   int32_t owner;   // the child's node id (> 0), or -(position + 1) for a request
 };
-struct OffLess {
+struct OffLess {   // branch-free, as AncLess
   __device__ __forceinline__ bool operator()(const OffElem& a, const OffElem& b) const {
-    return a.node < b.node || (a.node == b.node && (a.k1 < b.k1 || (a.k1 == b.k1 && a.k2 < b.k2)));
+    return (a.node < b.node) | ((a.node == b.node) & ((a.k1 < b.k1) | ((a.k1 == b.k1) & (a.k2 < b.k2))));
   }
 };
 

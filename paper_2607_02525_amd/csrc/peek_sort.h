@@ -56,6 +56,24 @@ __device__ __forceinline__ void merge_seq(const T* A, int la, const T* B, int lb
   }
 }
 
+// The same steps with both candidates loaded up front (indices clamped into
+// the runs, the choice made by selects). The tile pass's merge levels run
+// faster this way (8.9 -> 8.1 us for a 64K-element tile pass); the global
+// merge passes run slower with it (5.9 -> 7.4 us), so they keep merge_seq.
+template <int I, typename T, typename Less>
+__device__ __forceinline__ void merge_seq_flat(const T* A, int la, const T* B, int lb, int i, int j, T (&out)[I],
+                                               Less less) {
+#pragma unroll
+  for (int q = 0; q < I; ++q) {
+    const T a = A[max(min(i, la - 1), 0)];
+    const T b = B[max(min(j, lb - 1), 0)];
+    const bool take_a = (i < la) & ((j >= lb) | !less(b, a));
+    out[q] = take_a ? a : b;
+    i += take_a;
+    j += !take_a;
+  }
+}
+
 // Element source of the tile pass: a plain array, or a functor that builds
 // element i on the fly (saves a pass that would only write the input).
 template <typename T>
@@ -107,7 +125,7 @@ __global__ __launch_bounds__(kThreads) void k_tile_sort(Src src, T* __restrict__
     const T* A = s + pair;
     const T* B = A + w;
     const int i = merge_path(A, w, B, w, k, less);
-    merge_seq<I>(A, w, B, w, i, k - i, v, less);
+    merge_seq_flat<I>(A, w, B, w, i, k - i, v, less);
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < I; ++q) s[o + q] = v[q];
