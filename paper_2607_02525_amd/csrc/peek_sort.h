@@ -1,17 +1,19 @@
 // Stable merge sort for the queue-signal kernels (device templates).
 //
-// Tile pass: 128 threads x ITEMS items per workgroup; each thread orders its
+// Tile pass: 256 threads x ITEMS items per workgroup; each thread orders its
 // items in registers, then runs are merged in LDS with merge-path
 // partitioning (every thread produces its outputs after a binary search on
 // its diagonal).
 // Global passes: each workgroup emits a tile's worth of outputs of a pair of
 // sorted runs; its start and end diagonals are found by a wave-wide 64-ary
 // search, the two input slices are staged in LDS and merged as above.
-// Tile size: 256 elements (2 items) keeps a 64K-element sort spread over all
-// 256 CUs; from 512K elements up, 1024-element tiles (8 items) save two
-// passes and amortize each workgroup's dependent diagonal searches over
-// more outputs (measured: a 1M-element sort goes from 0.33 to 0.28 ms,
-// while 64K-element sorts get slower with the larger tiles).
+// Tile size: 512 elements (2 items) keeps a 64K-element sort spread over
+// 128 workgroups; from 512K elements up, 1024-element tiles (4 items) save a
+// pass and amortize each workgroup's dependent diagonal searches over more
+// outputs. Measured on the 64K-element anchor sort: 256-element tiles (128
+// threads) take 8.0 us for the tile pass and 8 x 5.8 us for the merge
+// passes, 512-element tiles 10.4 + 7 x 5.9 us; more items per thread (4
+// or 8) are slower (12.2 + 7 x 6.9 us and 20.6 + 6 x 9.1 us).
 // Ties keep input order (stable), so results are deterministic.
 #pragma once
 
@@ -23,10 +25,10 @@
 namespace peek {
 namespace msort {
 
-constexpr int kThreads = 128;
+constexpr int kThreads = 256;
 constexpr int kItems = 2;
-constexpr int kTile = kThreads * kItems;            // 256: the smallest tile, so np is a multiple of it
-constexpr int kBigItems = 8;                        // 1024-element tiles
+constexpr int kTile = kThreads * kItems;            // 512: the smallest tile, so np is a multiple of it
+constexpr int kBigItems = 4;                        // 1024-element tiles
 constexpr size_t kBigSort = size_t(1) << 19;        // sorts of at least this many elements use them
 
 // Number of items taken from A among the first k outputs of a stable merge
