@@ -91,28 +91,118 @@ struct PlainKeys {
   __device__ __forceinline__ uint32_t operator()(int32_t i) const { return k[i]; }
 };
 
-// P[c] for c in [0, nn], one node per lane: a wave-wide search brackets the
-// keys of the wave's 64 nodes once, then each lane binary-searches inside
-// the bracket (usually a handful of keys), so no lane waits on a chain.
+// P[c] for c in [0, nn]: a wavefront covers kPrefixNodes x 64 consecutive
+// nodes (node wbase + 64 r + lane is lane's r-th). A wave-wide search
+// brackets the keys of the wave's nodes once (both ends of the bracket
+// narrowed in the same rounds), then every lane searches for all of its
+// nodes in lockstep: 8-ary steps (the probes of all its nodes loaded
+// together) while a node's interval holds more than 8 keys, which only
+// happens around a node with many requests, then one round that loads the
+// last 8 keys of each interval and counts those below the node. Each wave
+// thus waits on a few rounds only, and the grid has a quarter of the
+// workgroups it would with one node per lane: in the rides, the launch's
+// time went mostly into dispatching 4,000 small workgroups for the 1M
+// nodes of the scale cache.
 // `block` is the 256-thread block's index among the blocks doing this.
+constexpr int kPrefixNodes = 4;
+constexpr int64_t kPrefixBlockNodes = 256 * kPrefixNodes;   // nodes per 256-thread block
 template <typename Keys>
 __device__ __forceinline__ void demand_prefix_block(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P,
                                                     int32_t block) {
+  constexpr int R = kPrefixNodes;
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wbase = (int64_t)__builtin_amdgcn_readfirstlane(block * 4 + (int32_t)(threadIdx.x / kWave)) * kWave;
+  const int64_t wbase =
+      (int64_t)__builtin_amdgcn_readfirstlane(block * 4 + (int32_t)(threadIdx.x / kWave)) * (kWave * R);
   if (wbase > nn) return;
-  const int64_t wend = wbase + kWave;   // exclusive
-  const int32_t lo = n == 0 ? 0 : wave_first_true(0, n, lane, [&](int32_t p) { return p >= n || (int64_t)keys(p) >= wbase; });
-  const int32_t hi = n == 0 ? 0 : wave_first_true(lo, n, lane, [&](int32_t p) { return p >= n || (int64_t)keys(p) >= wend; });
-  const int64_t c = wbase + lane;
-  if (c > nn) return;
-  int32_t a = lo, b = hi;
-  while (a < b) {
-    const int32_t mid = a + ((b - a) >> 1);
-    if ((int64_t)keys(mid) < c) a = mid + 1;
-    else b = mid;
+  if (n == 0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (wbase + r * kWave + lane <= nn) P[wbase + r * kWave + lane] = 0;
+    return;
   }
-  P[c] = a;
+  const int64_t wend = wbase + kWave * R;   // exclusive
+  // first position with key >= wbase in [alo, ahi], with key >= wend in [blo, bhi]
+  int32_t alo = 0, ahi = n, blo = 0, bhi = n;
+  while (ahi - alo >= kWave || bhi - blo >= kWave) {
+    const int64_t sa = (int64_t)ahi - alo, sb = (int64_t)bhi - blo;
+    const int32_t pa = alo + (int32_t)((sa * lane) / kWave);
+    const int32_t pb = blo + (int32_t)((sb * lane) / kWave);
+    const int64_t ka = pa < n ? (int64_t)keys(pa) : INT64_MAX;
+    const int64_t kb = pb < n ? (int64_t)keys(pb) : INT64_MAX;
+    if (sa >= kWave) {
+      const uint64_t bt = __ballot(ka >= wbase);
+      const int f = bt ? __ffsll((unsigned long long)bt) - 1 : kWave;
+      const int32_t nlo = f == 0 ? alo : alo + (int32_t)((sa * (f - 1)) / kWave) + 1;
+      const int32_t nhi = f == kWave ? ahi : alo + (int32_t)((sa * f) / kWave);
+      alo = __builtin_amdgcn_readfirstlane(nlo);
+      ahi = __builtin_amdgcn_readfirstlane(nhi);
+    }
+    if (sb >= kWave) {
+      const uint64_t bt = __ballot(kb >= wend);
+      const int f = bt ? __ffsll((unsigned long long)bt) - 1 : kWave;
+      const int32_t nlo = f == 0 ? blo : blo + (int32_t)((sb * (f - 1)) / kWave) + 1;
+      const int32_t nhi = f == kWave ? bhi : blo + (int32_t)((sb * f) / kWave);
+      blo = __builtin_amdgcn_readfirstlane(nlo);
+      bhi = __builtin_amdgcn_readfirstlane(nhi);
+    }
+  }
+  int32_t lo, hi;
+  {
+    const int32_t pa = alo + lane, pb = blo + lane;
+    const int64_t ka = pa < n ? (int64_t)keys(pa) : INT64_MAX;
+    const int64_t kb = pb < n ? (int64_t)keys(pb) : INT64_MAX;
+    const uint64_t ba = __ballot(pa <= ahi && (pa >= n || ka >= wbase));
+    const uint64_t bb = __ballot(pb <= bhi && (pb >= n || kb >= wend));
+    lo = alo + (__ffsll((unsigned long long)ba) - 1);
+    hi = blo + (__ffsll((unsigned long long)bb) - 1);
+  }
+  // per node: the first position in [a, b) with key >= c (b if none)
+  int64_t c[R];
+  int32_t a[R], b[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    c[r] = wbase + r * kWave + lane;
+    a[r] = lo;
+    b[r] = hi;
+  }
+  while (true) {
+    bool wide = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) wide |= b[r] - a[r] > 8;
+    if (!__ballot(wide)) break;
+    int64_t k[R][7];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int q = 0; q < 7; ++q)
+        k[r][q] = (int64_t)keys(min(a[r] + (int32_t)(((int64_t)(b[r] - a[r]) * (q + 1)) >> 3), n - 1));
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int32_t span = b[r] - a[r];
+      if (span <= 8) continue;
+      int32_t na = a[r], nb = b[r];
+#pragma unroll
+      for (int q = 6; q >= 0; --q)
+        if (k[r][q] >= c[r]) nb = a[r] + (int32_t)(((int64_t)span * (q + 1)) >> 3);   // the smallest probe at or above c
+#pragma unroll
+      for (int q = 0; q < 7; ++q)
+        if (k[r][q] < c[r]) na = a[r] + (int32_t)(((int64_t)span * (q + 1)) >> 3) + 1;   // past the largest probe below c
+      a[r] = na;
+      b[r] = nb;
+    }
+  }
+  int64_t k[R][8];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) k[r][q] = (int64_t)keys(min(a[r] + q, n - 1));
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    int32_t cnt = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) cnt += (q < b[r] - a[r] && k[r][q] < c[r]) ? 1 : 0;
+    if (c[r] <= nn) P[c[r]] = a[r] + cnt;
+  }
 }
 
 template <typename Keys>
@@ -133,6 +223,7 @@ __global__ void k_demand_diff(const NodeRec* __restrict__ nodes, int32_t nn, con
 
 // Demand work that rides along in a cluster kernel's launch: the blocks past
 // the kernel's own run one step of the demand computation.
+constexpr int kDiffNodes = 4;   // nodes per thread of the demand difference riding in k_final_blocks
 struct DemandRide {
   const NodeRec* nodes;
   int32_t* P;
@@ -178,8 +269,26 @@ __device__ __forceinline__ int32_t lca_depth(const DeviceTree& t, int32_t c1, in
   const int32_t lo = c1 + 1, hi = c2;
   const int32_t bl = lo >> 6, bh = hi >> 6;
   if (bl == bh) {
+    // the 4-value groups of the block that overlap [lo, hi], eight at a
+    // time, each eight loaded together (one load after another would wait
+    // for each; a block starts 256-byte aligned and the array is padded to
+    // 256 bytes, so every group of the block lies inside it)
+    const int4* __restrict__ pb = reinterpret_cast<const int4*>(t.pdep + (bl << 6));
+    const int32_t g0 = (lo & 63) >> 2, g1 = (hi & 63) >> 2;
     int32_t m = INT32_MAX;
-    for (int32_t v = lo; v <= hi; ++v) m = min(m, t.pdep[v]);
+    for (int32_t gb = g0; gb <= g1; gb += 8) {
+      int4 v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = pb[min(gb + q, g1)];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int32_t e = (bl << 6) + 4 * min(gb + q, g1);
+        m = min(m, e + 0 >= lo && e + 0 <= hi ? v[q].x : INT32_MAX);
+        m = min(m, e + 1 >= lo && e + 1 <= hi ? v[q].y : INT32_MAX);
+        m = min(m, e + 2 >= lo && e + 2 <= hi ? v[q].z : INT32_MAX);
+        m = min(m, e + 3 >= lo && e + 3 <= hi ? v[q].w : INT32_MAX);
+      }
+    }
     return m;
   }
   int32_t m = min(t.pdep_suf[lo], t.pdep_pre[hi]);
@@ -187,26 +296,6 @@ __device__ __forceinline__ int32_t lca_depth(const DeviceTree& t, int32_t c1, in
     const int32_t x = bl + 1, y = bh - 1;
     const int k = 31 - __clz(y - x + 1);
     m = min(m, min(t.pdep_st[(int64_t)k * t.pdep_nb + x], t.pdep_st[(int64_t)k * t.pdep_nb + y - (1 << k) + 1]));
-  }
-  return m;
-}
-
-// Minimum of a[lo..hi] (inclusive) using 64-wide block minima and a sparse
-// table over the blocks (levels of nb entries each).
-__device__ __forceinline__ int32_t range_min_i32(const int32_t* __restrict__ a, const int32_t* __restrict__ st,
-                                                 int32_t nb, int32_t lo, int32_t hi) {
-  int32_t m = INT32_MAX;
-  const int32_t bl = lo >> 6, bh = hi >> 6;
-  if (bl == bh) {
-    for (int32_t v = lo; v <= hi; ++v) m = min(m, a[v]);
-    return m;
-  }
-  for (int32_t v = lo; v < (bl + 1) << 6; ++v) m = min(m, a[v]);
-  for (int32_t v = bh << 6; v <= hi; ++v) m = min(m, a[v]);
-  if (bh - bl >= 2) {
-    const int32_t x = bl + 1, y = bh - 1;
-    const int k = 31 - __clz(y - x + 1);
-    m = min(m, min(st[(int64_t)k * nb + x], st[(int64_t)k * nb + y - (1 << k) + 1]));
   }
   return m;
 }
@@ -300,8 +389,8 @@ struct AncKeys {   // sorted last nodes, for the demand prefix
 __device__ __forceinline__ bool same_sub(const AncElem& a, const AncElem& b) {
   return a.hi == b.hi && a.mid == b.mid && code_of(a.lo) == code_of(b.lo);
 }
-__device__ __forceinline__ bool sub_less(const AncElem& a, const AncElem& b) {
-  return a.hi < b.hi || (a.hi == b.hi && (a.mid < b.mid || (a.mid == b.mid && code_of(a.lo) < code_of(b.lo))));
+__device__ __forceinline__ bool sub_less(const AncElem& a, const AncElem& b) {   // branch-free, as AncLess
+  return (a.hi < b.hi) | ((a.hi == b.hi) & ((a.mid < b.mid) | ((a.mid == b.mid) & (code_of(a.lo) < code_of(b.lo)))));
 }
 
 __global__ void k_first_clear(HeadTable T, int32_t n, int32_t* __restrict__ lcp, uint64_t* __restrict__ head,
@@ -502,6 +591,10 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
   // the end of the previous position's node, for the lcp across a group
   // start (anchored passes only: unanchored ones put every request at the root)
   const int32_t p_end = t.nodes != nullptr ? t.nodes[(uint32_t)(p.hi >> 32)].subtree_end : 0;
+  // the request's length, also before the search below
+  const uint32_t req = (uint32_t)(e.lo & kLenMax);
+  const int64_t o0 = in.offsets[req], o1 = in.offsets[req + 1];
+  const uint32_t len = valid ? min((uint32_t)(o1 - o0), in.len_cap) : 0u;
   // the start of every lane's segment: inside the wave from the ballot, else
   // one shared wave search back from the wave's first position
   const uint64_t mask = __ballot(start);
@@ -509,13 +602,12 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
   const uint64_t below = mask & upto;
   int32_t g0 = base;
   if (!(mask & 1ull)) {
-    const AncElem b0 = sd[base];
+    // the wave's first element is lane 0's e
+    const AncElem b0{(uint64_t)__shfl((long long)e.hi, 0), (uint64_t)__shfl((long long)e.mid, 0),
+                     (uint64_t)__shfl((long long)e.lo, 0)};
     g0 = wave_first_true(0, base, lane, [&](int32_t q) { return !sub_less(sd[q], b0); });
   }
   const int32_t g = below ? base + (63 - __clzll((unsigned long long)below)) : g0;
-  const uint32_t req = (uint32_t)(e.lo & kLenMax);
-  const int64_t o0 = in.offsets[req], o1 = in.offsets[req + 1];
-  const uint32_t len = valid ? min((uint32_t)(o1 - o0), in.len_cap) : 0u;
   // longest member of each segment: segmented maximum over the wave's lanes
   uint64_t best = valid ? (((uint64_t)len << 32) | (0xFFFFFFFFu - req)) : 0;
   for (int off = 1; off < kWave; off <<= 1) {
@@ -1077,8 +1169,21 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
                                                       uint64_t* __restrict__ st2, int32_t nb1, int32_t nb2,
                                                       ClpmArgs cl, bool key_is_request, DemandRide ride) {
   if ((int32_t)blockIdx.x >= ride.first_block) {
-    demand_diff_at(ride.nodes, ride.nn, ride.P, ride.demand,
-                   ((int32_t)blockIdx.x - ride.first_block) * (int32_t)blockDim.x + (int32_t)threadIdx.x);
+    // kDiffNodes nodes per thread (fewer workgroups to dispatch), their
+    // loads issued together with clamped indices
+    const int32_t c0 = ((int32_t)blockIdx.x - ride.first_block) * (256 * kDiffNodes) + (int32_t)threadIdx.x;
+    int32_t end[kDiffNodes], pc[kDiffNodes], pe[kDiffNodes];
+#pragma unroll
+    for (int r = 0; r < kDiffNodes; ++r) {
+      const int32_t c = max(min(c0 + 256 * r, ride.nn - 1), 0);
+      end[r] = ride.nodes[c].subtree_end;
+      pc[r] = ride.P[c];
+    }
+#pragma unroll
+    for (int r = 0; r < kDiffNodes; ++r) pe[r] = ride.P[end[r]];
+#pragma unroll
+    for (int r = 0; r < kDiffNodes; ++r)
+      if (c0 + 256 * r < ride.nn) ride.demand[c0 + 256 * r] = pe[r] - pc[r];
     return;
   }
   const int lane = threadIdx.x & (kWave - 1);
@@ -1745,7 +1850,8 @@ template <typename Keys>
 void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_t* P, int32_t* demand,
                                hipStream_t st) {
   const int32_t nn = t.num_nodes;
-  hipLaunchKernelGGL((k_demand_prefix<Keys>), dim3(blocks_for((int64_t)nn + 1)), dim3(256), 0, st, keys, n, nn, P);
+  hipLaunchKernelGGL((k_demand_prefix<Keys>), dim3(blocks_for((int64_t)nn + 1, kPrefixBlockNodes)), dim3(256), 0, st,
+                     keys, n, nn, P);
   hipLaunchKernelGGL(k_demand_diff, dim3(blocks_for(nn)), dim3(256), 0, st, t.nodes, nn, P, demand);
 }
 
@@ -1841,7 +1947,7 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   unsigned prefix_blocks = 0;
   if (ride_demand) {
     ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
-    prefix_blocks = blocks_for((int64_t)t->num_nodes + 1);
+    prefix_blocks = blocks_for((int64_t)t->num_nodes + 1, kPrefixBlockNodes);
   }
   hipLaunchKernelGGL(k_first_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, sorted, ain,
                      anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth, active, head, lcp, flags, ride);
@@ -1868,7 +1974,8 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   const unsigned fb_blocks = blocks_for((int64_t)L.nb1 * kWave);
   DemandRide fr = ride;
   fr.first_block = ride_demand ? (int32_t)fb_blocks : INT32_MAX;
-  hipLaunchKernelGGL(k_final_blocks, dim3(fb_blocks + (ride_demand ? blocks_for(t->num_nodes) : 0)), dim3(256), 0,
+  hipLaunchKernelGGL(k_final_blocks, dim3(fb_blocks + (ride_demand ? blocks_for(t->num_nodes, 256 * kDiffNodes) : 0)),
+                     dim3(256), 0,
                      st, n, el, lcp, key2, ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr, fr);
   {
     const int32_t nbm = std::max(L.nb1, L.nb2);
