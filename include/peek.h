@@ -199,7 +199,7 @@ peek_status peek_queue_signals(const peek_cache* cache, int32_t n, const int32_t
  * GPU, reserved when the library is loaded onto that GPU and held until the
  * process ends. A call that needs more (peek_queue_signals_workspace(n,
  * num_nodes) > PEEK_NOALLOC_SCRATCH_BYTES, e.g. 64K requests against a cache
- * of more than about 3.8M nodes) fails with WORKSPACE_TOO_SMALL before any
+ * of more than about 3.6M nodes) fails with WORKSPACE_TOO_SMALL before any
  * launch.
  * Every call on one GPU shares that GPU's array: calls whose work may
  * overlap on the device (different streams, host threads racing) race on it

@@ -343,19 +343,23 @@ struct AnchorIn {
 
 // Hash table of anchor groups (capacity mask + 1, a power of two >= 2n).
 struct HeadTable {
-  uint32_t* rep;     // 0: empty; else the representative request + 1
+  uint64_t* rep;     // 0: empty; else (fingerprint << 32) | (the representative request + 1)
   uint64_t* best;    // max over the group of (len << 32) | (~request)
   uint32_t* multi;   // nonzero once a second member has found the slot
   int32_t* slot;     // [n] each request's slot
   uint32_t mask;
 };
 
-__device__ __forceinline__ uint32_t group_hash(uint32_t c, uint32_t m, uint64_t code) {
+__device__ __forceinline__ uint64_t group_hash64(uint32_t c, uint32_t m, uint64_t code) {
   uint64_t z = (((uint64_t)c << 32) | m) * 0x9E3779B97F4A7C15ull ^ code * 0xC2B2AE3D27D4EB4Full;
   z ^= z >> 29;
   z *= 0xBF58476D1CE4E5B9ull;
   z ^= z >> 32;
-  return (uint32_t)z;
+  return z;
+}
+// slot hash (low half) and the fingerprint kept in a slot (high half)
+__device__ __forceinline__ uint32_t group_hash(uint32_t c, uint32_t m, uint64_t code) {
+  return (uint32_t)group_hash64(c, m, code);
 }
 
 // Element of the first round's sort: hi = (c << 32) | m, mid = (code << 31) |
@@ -450,19 +454,26 @@ __global__ __launch_bounds__(kInsThreads) void k_first_insert(AnchorIn in, HeadT
   }
   __syncthreads();
   if (valid && lrep[ls] == (uint32_t)t + 1) {
-    uint32_t h = group_hash(c, m, code) & T.mask;
+    const uint64_t z = group_hash64(c, m, code);
+    uint32_t h = (uint32_t)z & T.mask;
+    const uint32_t fp = (uint32_t)(z >> 32);
     bool first = false;
-    // at most n keys in more than 2n slots: an empty slot or the key is found
+    // at most n keys in more than 2n slots: an empty slot or the key is
+    // found. A slot whose fingerprint differs holds another key, so only a
+    // matching fingerprint costs the occupant's key (two dependent loads).
     for (uint32_t probe = 0; probe <= T.mask; ++probe) {
-      const uint32_t v = atomicCAS(&T.rep[h], 0u, (uint32_t)i + 1);
+      const uint64_t v = atomicCAS((unsigned long long*)&T.rep[h], 0ull,
+                                   (unsigned long long)(((uint64_t)fp << 32) | ((uint32_t)i + 1)));
       if (v == 0) {
         first = true;   // this workgroup's group represents the group
         break;
       }
-      uint32_t c2, m2, len2;
-      uint64_t code2;
-      in.key(v - 1, c2, m2, code2, len2);
-      if (c2 == c && m2 == m && code2 == code) break;
+      if ((uint32_t)(v >> 32) == fp) {
+        uint32_t c2, m2, len2;
+        uint64_t code2;
+        in.key((uint32_t)v - 1, c2, m2, code2, len2);
+        if (c2 == c && m2 == m && code2 == code) break;
+      }
       h = (h + 1) & T.mask;
     }
     lglob[ls] = (int32_t)h;
@@ -1807,7 +1818,7 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.anc_b = take(sizeof(AncElem) * np);
   L.hcap = 256;
   while (L.hcap < 2 * nn) L.hcap <<= 1;
-  L.hrep = take(sizeof(uint32_t) * L.hcap);
+  L.hrep = take(sizeof(uint64_t) * L.hcap);
   L.hbest = take(sizeof(uint64_t) * L.hcap);
   L.hmulti = take(sizeof(uint32_t) * L.hcap);
   L.hslot = take(sizeof(int32_t) * nn);
@@ -1925,7 +1936,7 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
 
   // 1. The first round: anchor groups and their heads from a hash table,
   // every member compared with its head, one sort, then the segments.
-  const HeadTable T{(uint32_t*)(w + L.hrep), (uint64_t*)(w + L.hbest), (uint32_t*)(w + L.hmulti),
+  const HeadTable T{(uint64_t*)(w + L.hrep), (uint64_t*)(w + L.hbest), (uint32_t*)(w + L.hmulti),
                     (int32_t*)(w + L.hslot), (uint32_t)(L.hcap - 1)};
   const AnchorIn ain{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr,
                      off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
