@@ -1403,6 +1403,36 @@ struct LcpIndex {
     return L;
   }
 
+  // last_below_from(iL, sL) and first_below_from(iR, sR) (iL < n, iR <= n)
+  // computed together: the two chains of dependent loads (in-block rounds,
+  // then the lifting over the sparse table, then the in-block rounds of the
+  // block found) advance in the same steps, so the pair waits about as long
+  // as one of them. Indices are clamped so that the side that needs no
+  // lifting still loads inside the tables; its results are not used.
+  __device__ __forceinline__ void pair_from(int32_t iL, int32_t sL, int32_t iR, int32_t sR, int32_t& L,
+                                            int32_t& R) const {
+    const int32_t bL = iL >> 6, bR = iR >> 6;
+    const int32_t bendR = min((bR << 6) + 63, n);
+    L = last_below(ib1, stride, bL << 6, iL, sL);
+    R = first_below(ib1, stride, iR, bendR, sR);
+    const bool needL = L < (bL << 6), needR = R > bendR;
+    if (needL || needR) {
+      int32_t pl = bL - 1, pr = bR + 1;   // as in the single searches
+      for (int k = levels - 1; k >= 0; --k) {
+        const int32_t w = 1 << k;
+        const int32_t vl = st1[(int64_t)k * nb1 + max(pl - w + 1, 0)];
+        const int32_t vr = st1[(int64_t)k * nb1 + max(min(pr, nb1 - 1), 0)];
+        if (needL && pl - w + 1 >= 0 && vl >= sL) pl -= w;
+        if (needR && pr + w <= nb1 && vr >= sR) pr += w;
+      }
+      const int32_t ql = max(pl, 0), qr = max(min(pr, nb1 - 1), 0);
+      const int32_t l2 = last_below(ib1, stride, ql << 6, min((ql << 6) + 63, n), sL);
+      const int32_t r2 = first_below(ib1, stride, qr << 6, min((qr << 6) + 63, n), sR);
+      if (needL) L = l2;
+      if (needR) R = r2;
+    }
+  }
+
   // First j >= i (i <= n) with lcp[j] < s, for s >= 1 (lcp[n] = 0).
   __device__ __forceinline__ int32_t first_below_from(int32_t i, int32_t s) const {
     const int32_t bi = i >> 6;
@@ -1456,8 +1486,8 @@ __global__ __launch_bounds__(256) void k_final_query(int32_t n, int32_t threshol
       csz[req] = 1;
     } else {
       // [L, R): the widest range around i whose inner lcps are >= s
-      const int32_t L = ix.last_below_from(i, s);
-      const int32_t R = ix.first_below_from(i + 1, s);
+      int32_t L, R;
+      ix.pair_from(i, s, i + 1, s, L, R);
       // id: minimum of (share, request) over [L, R)
       const uint64_t m = key_range_min(ib2, ix.stride, st2, nb2, L, R - 1);
       cid[req] = (int32_t)(uint32_t)m;
@@ -1471,10 +1501,10 @@ __global__ __launch_bounds__(256) void k_final_query(int32_t n, int32_t threshol
     // inner position: the previous position with lcp <= D must have lcp < D
     const int32_t D = i >= 1 ? lcp[i] : 0;
     if (D > 0) {
-      const int32_t L = ix.last_below_from(i - 1, D + 1);
+      int32_t L, R;   // R is only used when L is the node's leftmost position
+      ix.pair_from(i - 1, D + 1, i + 1, D, L, R);
       const int32_t lL = lcp[L];
       if (lL < D) {
-        const int32_t R = ix.first_below_from(i + 1, D);
         const int64_t wgt = (int64_t)(R - L) * (D - max(lL, lcp[R]));
         atomicAdd((unsigned long long*)&cl.diff[L], (unsigned long long)wgt);
         atomicAdd((unsigned long long*)&cl.diff[R], (unsigned long long)(-wgt));
