@@ -686,7 +686,7 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
                                                         const uint8_t* __restrict__ active,
                                                         const uint64_t* __restrict__ head,
                                                         const int32_t* __restrict__ flags_in) {
-  if (flags_in[1] == 0) return;
+  const int32_t gate = flags_in[1];   // tested after the first positions' loads are issued
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t wv = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
   const int32_t waves = (int32_t)gridDim.x * 4;
@@ -698,7 +698,8 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
   for (int32_t base = wv * per; base < n; base += waves * per) {
     const int32_t i = base + lane;
     const bool in = lane < per && i < n;
-    const int32_t s = in ? nseg[i] : 0;
+    const int32_t s = nseg[min(i, n - 1)];
+    if (gate == 0) return;
     const uint8_t ac = active[s];
     const int32_t gz = gsize[s];
     for (uint64_t todo = __ballot(in && ac && round_takes(gz)); todo; todo &= todo - 1) {
@@ -1200,17 +1201,20 @@ __global__ __launch_bounds__(256) void k_final_blocks(int32_t n, const ClElem* _
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t b = (int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave);
   const int32_t i = b * kWave + lane;
-  int32_t v1 = INT32_MAX;
+  // both lcps and the element loaded together (clamped indices; loads
+  // behind the range checks would wait one after another)
+  const int32_t l0 = lcp[min(i, n)], l1 = lcp[min(i + 1, n)];
+  const uint32_t ereq = el[max(min(i, n - 1), 0)].req;
+  const int32_t v1 = i <= n ? l0 : INT32_MAX;
   uint64_t v2 = ~0ull;
-  if (i <= n) v1 = lcp[i];
   if (cl.on) {
     if (i <= n) cl.diff[i] = 0;
     if (i < n) cl.pmin[i] = INT32_MAX;
     if (i >= 1 && i < n && v1 > 0) *cl.sharing = 1;
   }
   if (i < n) {
-    const int32_t share = max(lcp[i], lcp[i + 1]);
-    v2 = key_is_request ? (uint64_t)el[i].req : ((uint64_t)(uint32_t)share << 32) | el[i].req;
+    const int32_t share = max(l0, l1);
+    v2 = key_is_request ? (uint64_t)ereq : ((uint64_t)(uint32_t)share << 32) | ereq;
     key2[i] = v2;
   }
   int32_t m1 = v1;
