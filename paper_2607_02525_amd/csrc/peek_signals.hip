@@ -1661,13 +1661,14 @@ struct OffSource {
     if (j >= (size_t)2 * n) return pad;
     const int32_t i = (int32_t)(j - n);
     const int32_t d = a.lcp[i];
-    const int32_t L = d == 0 ? 0 : a.ix.last_below_from(i - 1, d);
+    // the interval's two ends, searched together (R is wasted on padding)
+    int32_t L = 0, R = n;
+    if (d != 0) a.ix.pair_from(i - 1, d, i + 1, d, L, R);
     a.start[i] = 0;
     if (a.ix.first_below_from(L + 1, d + 1) != i) {
       a.nparent[i] = -1;
       return pad;
     }
-    const int32_t R = d == 0 ? n : a.ix.first_below_from(i + 1, d);
     const int32_t lL = L >= 1 ? a.lcp[L] : -1, lR = R <= n - 1 ? a.lcp[R] : -1;
     if (lL < 0 && lR < 0) {   // the top interval
       a.nparent[i] = -1;
