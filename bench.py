@@ -404,12 +404,13 @@ def main():
                          "algorithmic_bytes_per_launch": b_alg, "bytes_breakdown": parts,
                          "bytes_from": "oracle outputs"})
         # sort passes over the queue in one signals call: the first round's
-        # merge sort (tile pass + merge passes) and the sort of the second
-        # round's segments
-        np2 = 256
+        # merge sort (a tile pass over 512-element tiles, then merge passes)
+        # and the sort of the second round's segments
+        np2 = 512
         while np2 < w.n:
             np2 <<= 1
-        passes = 1 + int(np.log2(np2 // 256)) + 1
+        tile = 1024 if np2 >= (1 << 19) else 512   # sorts of 512K elements and up use 1024-element tiles
+        passes = 1 + int(np.log2(np2 // tile)) + 1
         sb, sparts = signals_algorithmic_bytes(w.lengths.astype(np.int64), oc.share.astype(np.int64),
                                                ol.m.astype(np.int64), hp.num_nodes, passes)
         sig_s = float(sig_ms.mean()) / 1e3
