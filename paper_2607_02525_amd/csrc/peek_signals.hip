@@ -1032,8 +1032,9 @@ __device__ void tail_wg_round(const TailArgs& A, int32_t s, int32_t sz, int32_t 
   __syncthreads();
 }
 
+static_assert(kTailRange <= kTailThreads, "one position per thread in the root scan");
 __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
-  if (A.flags[0] == 0) return;
+  const int32_t f0 = A.flags[0];        // tested once the root loads below are issued
   const bool keyed = A.flags[1] != 0;   // the second round compared its segments
   const int32_t* depth = A.depth;
   const uint8_t* active = A.active;
@@ -1047,19 +1048,19 @@ __global__ __launch_bounds__(kTailThreads) void k_refine_tail(TailArgs A) {
   const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
   const int32_t p0 = (int32_t)blockIdx.x * kTailRange;
   const int32_t p1 = min(A.n, p0 + kTailRange);
+  // the three loads of this thread's position are issued with the gate's (a
+  // load behind a branch on another one would wait for it)
+  const int32_t p = p0 + t, pc = min(p, A.n - 1);
+  const int32_t sg = A.nseg[pc];
+  const uint8_t ac = active[pc];
+  const int32_t gz = A.gsize[pc];
+  if (f0 == 0) return;
   if (t == 0) n_roots = 0;
   __syncthreads();
-  // (the three loads are issued together: a load behind a branch on another
-  // one would wait for it)
-  for (int32_t p = p0 + t; p < p1; p += kTailThreads) {
-    const int32_t sg = A.nseg[p];
-    const uint8_t ac = active[p];
-    const int32_t gz = A.gsize[p];
-    if (sg == p && ac) {
-      const int k = atomicAdd(&n_roots, 1);
-      root_s[k] = p;
-      root_e[k] = p + gz;
-    }
+  if (p < p1 && sg == p && ac) {
+    const int k = atomicAdd(&n_roots, 1);
+    root_s[k] = p;
+    root_e[k] = p + gz;
   }
   __syncthreads();
   const int nr = n_roots;
