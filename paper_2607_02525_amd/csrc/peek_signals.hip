@@ -740,7 +740,7 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
 //    elements are permuted and the new groups marked;
 // and passes repeat until nothing is active. Every round makes each active
 // group strictly deeper or settles it, so the loop ends.
-constexpr int kTailRange = 256;
+constexpr int kTailRange = 64;
 constexpr int kTailThreads = 512;
 constexpr int kTailWaves = kTailThreads / kWave;
 constexpr int kTailCap = 4096;              // members the workgroup sorts in LDS
