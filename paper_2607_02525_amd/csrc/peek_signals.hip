@@ -205,6 +205,66 @@ __device__ __forceinline__ void demand_prefix_block(Keys keys, int32_t n, int32_
   }
 }
 
+// P[c] for c in [0, nn] once the run starts are known: the segment kernel
+// wrote P[c] = (start of c's run) for every node c that is some request's
+// last node and set its bit in `keyed`. Any other node's prefix is that of
+// the first keyed node after it (no key lies in between), or n past the
+// last one. A wavefront covers kPrefixNodes x 64 consecutive nodes (node
+// wbase + 64 r + lane is lane's r-th): it loads their bits and marked
+// values with one search for the first key at or past its range (the value
+// that carries in from the right), then takes suffix minima across lanes,
+// row by row from the right. Unlike searching every node's prefix, no lane
+// waits on a search inside a node that holds thousands of requests.
+template <typename Keys>
+__device__ __forceinline__ void demand_fill_block(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P,
+                                                  const uint32_t* __restrict__ keyed, int32_t block) {
+  constexpr int R = kPrefixNodes;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wbase =
+      (int64_t)__builtin_amdgcn_readfirstlane(block * 4 + (int32_t)(threadIdx.x / kWave)) * (kWave * R);
+  if (wbase > nn) return;
+  const int64_t wend = wbase + kWave * R;   // exclusive
+  int32_t v[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int32_t c = (int32_t)min(wbase + r * kWave + lane, (int64_t)nn);
+    const bool k = (keyed[c >> 5] >> (c & 31)) & 1u;
+    const int32_t pv = P[c];
+    v[r] = k ? pv : INT32_MAX;
+  }
+  // first position with key >= wend (n if none)
+  int32_t lo = 0, hi = n;
+  while (hi - lo >= kWave) {
+    const int64_t span = (int64_t)hi - lo;
+    const int32_t probe = lo + (int32_t)((span * lane) / kWave);
+    const uint64_t b = __ballot((int64_t)keys(probe) >= wend);
+    const int f = b ? __ffsll((unsigned long long)b) - 1 : kWave;
+    const int32_t nlo = f == 0 ? lo : lo + (int32_t)((span * (f - 1)) / kWave) + 1;
+    const int32_t nhi = f == kWave ? hi : lo + (int32_t)((span * f) / kWave);
+    lo = __builtin_amdgcn_readfirstlane(nlo);
+    hi = __builtin_amdgcn_readfirstlane(nhi);
+  }
+  int32_t carry;
+  {
+    const int32_t probe = lo + lane;
+    const bool pr = probe <= hi && (probe >= n || (int64_t)keys(min(probe, n - 1)) >= wend);
+    const uint64_t b = __ballot(pr);
+    carry = lo + (__ffsll((unsigned long long)b) - 1);
+  }
+#pragma unroll
+  for (int r = R - 1; r >= 0; --r) {
+    int32_t x = v[r];
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int32_t y = __shfl_down(x, off);
+      if (lane + off < kWave) x = min(x, y);
+    }
+    x = min(x, carry);
+    const int64_t c = wbase + r * kWave + lane;
+    if (c <= nn) P[c] = x;
+    carry = __shfl(x, 0);
+  }
+}
+
 template <typename Keys>
 __global__ __launch_bounds__(256) void k_demand_prefix(Keys keys, int32_t n, int32_t nn, int32_t* __restrict__ P) {
   demand_prefix_block(keys, n, nn, P, (int32_t)blockIdx.x);
@@ -230,6 +290,7 @@ struct DemandRide {
   int32_t* demand;
   int32_t nn;
   int32_t first_block;   // blocks >= first_block do demand work; INT32_MAX for none
+  uint32_t* keyed;       // bit c: some request's last node is c (anchored cluster pass)
 };
 
 // ---------------------------------------------------------------- clusters
@@ -398,8 +459,10 @@ __device__ __forceinline__ bool sub_less(const AncElem& a, const AncElem& b) {  
 }
 
 __global__ void k_first_clear(HeadTable T, int32_t n, int32_t* __restrict__ lcp, uint64_t* __restrict__ head,
-                              int32_t* __restrict__ flags, int32_t n_flags, int32_t* sharing) {
+                              int32_t* __restrict__ flags, int32_t n_flags, int32_t* sharing,
+                              uint32_t* __restrict__ keyed, int32_t n_keyed) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_keyed) keyed[i] = 0;
   if (i <= (int64_t)T.mask) {
     T.rep[i] = 0;
     T.best[i] = 0;
@@ -583,10 +646,6 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
                                                       int32_t* __restrict__ depth, uint8_t* __restrict__ active,
                                                       uint64_t* __restrict__ head, int32_t* __restrict__ lcp,
                                                       int32_t* __restrict__ flags, DemandRide ride) {
-  if ((int32_t)blockIdx.x >= ride.first_block) {
-    demand_prefix_block(AncKeys{sd}, n, ride.nn, ride.P, (int32_t)blockIdx.x - ride.first_block);
-    return;
-  }
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t base = __builtin_amdgcn_readfirstlane(((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave)) * kWave);
   if (base >= n) return;
@@ -627,6 +686,15 @@ __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* 
     if (lane + off < kWave && og == g && best < ob) best = ob;
   }
   if (!valid) return;
+  if (ride.P != nullptr) {
+    // demand: where each last node's run starts is its prefix P[c] (the
+    // fill that rides in the second round's compare completes the rest)
+    const uint32_t c = (uint32_t)(e.hi >> 32);
+    if (i == 0 || (uint32_t)(p.hi >> 32) != c) {
+      ride.P[c] = i;
+      atomicOr(&ride.keyed[c >> 5], 1u << (c & 31));
+    }
+  }
   const uint32_t m = (uint32_t)e.hi;
   const uint64_t code = e.mid >> 31;
   const uint32_t ell = (uint32_t)(e.mid & kLenMax);
@@ -685,11 +753,16 @@ __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restric
                                                         const int32_t* __restrict__ depth,
                                                         const uint8_t* __restrict__ active,
                                                         const uint64_t* __restrict__ head,
-                                                        const int32_t* __restrict__ flags_in) {
+                                                        const int32_t* __restrict__ flags_in, DemandRide ride,
+                                                        const AncElem* __restrict__ sd) {
+  if ((int32_t)blockIdx.x >= ride.first_block) {
+    demand_fill_block(AncKeys{sd}, n, ride.nn, ride.P, ride.keyed, (int32_t)blockIdx.x - ride.first_block);
+    return;
+  }
   const int32_t gate = flags_in[1];   // tested after the first positions' loads are issued
   const int lane = threadIdx.x & (kWave - 1);
   const int32_t wv = __builtin_amdgcn_readfirstlane((int32_t)blockIdx.x * 4 + (int32_t)(threadIdx.x / kWave));
-  const int32_t waves = (int32_t)gridDim.x * 4;
+  const int32_t waves = (int32_t)min(gridDim.x, (unsigned)ride.first_block) * 4;
   // each wavefront takes `per` consecutive positions at a time and checks
   // them in parallel, one lane each (the loads of one check depend on each
   // other, so checking them one after another would chain them), then
@@ -1804,8 +1877,8 @@ constexpr int kFlags = 2;
 // Workspace layout (each region 256-byte aligned).
 struct Layout {
   size_t el_a, el_b, nseg, gsize, depth_a, active_a, lcp, key2, ib1, ib2, st1, st2, flags, keys_a,
-      keys_b, prefix, diff, pmin, run, local, part, sharing, anc_a, anc_b, hrep, hbest, hmulti, hslot, hcap, head, tact,
-      tdep, tsize, total, flags_bytes;
+      keys_b, prefix, keyed, diff, pmin, run, local, part, sharing, anc_a, anc_b, hrep, hbest, hmulti, hslot, hcap,
+      head, tact, tdep, tsize, total, flags_bytes;
   // PEEK-offline Phase 1 only
   size_t oel_a, oel_b, olocal, opart, obase, start_a, start_b, npar_a, npar_b, rnode, roff, onp;
   int64_t ib_stride;
@@ -1844,6 +1917,7 @@ Layout layout(int32_t n, int64_t num_nodes, bool offline = false) {
   L.keys_a = take(sizeof(uint32_t) * np);
   L.keys_b = take(sizeof(uint32_t) * np);
   L.prefix = take(sizeof(int32_t) * (size_t)(num_nodes + 1));
+  L.keyed = take(sizeof(uint32_t) * (size_t)((num_nodes + 1 + 31) / 32));
   L.diff = take(sizeof(int64_t) * ((size_t)n + 1));
   L.pmin = take(sizeof(int32_t) * nn);
   L.run = take(sizeof(int32_t) * nn);
@@ -1977,27 +2051,27 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   const AnchorIn ain{tokens, offsets, anchored ? last_node : nullptr, anchored ? match_len : nullptr,
                      off != nullptr ? (uint32_t)off->depth_limit : UINT32_MAX};
   const int32_t n_flags = (int32_t)(L.flags_bytes / sizeof(int32_t));
-  const int64_t clear_span = std::max<int64_t>(std::max<int64_t>((int64_t)L.hcap, (int64_t)n + 1), n_flags);
+  const bool ride_demand = demand != nullptr && anchored;
+  uint32_t* keyed = (uint32_t*)(w + L.keyed);
+  const int32_t n_keyed = ride_demand ? (int32_t)((t->num_nodes + 1 + 31) / 32) : 0;
+  const int64_t clear_span =
+      std::max<int64_t>(std::max<int64_t>(std::max<int64_t>((int64_t)L.hcap, (int64_t)n + 1), n_flags), n_keyed);
   uint64_t* head = (uint64_t*)(w + L.head);
   hipLaunchKernelGGL(k_first_clear, dim3(blocks_for(clear_span)), dim3(256), 0, st, T, n, lcp, head, flags, n_flags,
-                     cl.on ? cl.sharing : nullptr);
+                     cl.on ? cl.sharing : nullptr, keyed, n_keyed);
   hipLaunchKernelGGL(k_first_insert, dim3(blocks_for(n, kInsThreads)), dim3(kInsThreads), 0, st, ain, T, n);
   AncElem* anc_a = (AncElem*)(w + L.anc_a);
   AncElem* anc_b = (AncElem*)(w + L.anc_b);
   hipLaunchKernelGGL(k_first_compare, dim3(blocks_for(n, 4)), dim3(256), 0, st, ain, T, n, anc_a);
   const AncElem* sorted = msort::sort_from(AncSrc{anc_a, n}, anc_a, anc_b, np, AncLess{}, st);
-  // The order is sorted by last node first, so demand reads it directly: the
-  // prefix P rides along with the segment kernel, the difference along with
-  // the final stage's first kernel.
-  const bool ride_demand = demand != nullptr && anchored;
-  DemandRide ride{nullptr, nullptr, nullptr, 0, INT32_MAX};
-  unsigned prefix_blocks = 0;
-  if (ride_demand) {
-    ride = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)wave_blocks};
-    prefix_blocks = blocks_for((int64_t)t->num_nodes + 1, kPrefixBlockNodes);
-  }
-  hipLaunchKernelGGL(k_first_groups, dim3(wave_blocks + prefix_blocks), dim3(256), 0, st, n, sorted, ain,
-                     anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth, active, head, lcp, flags, ride);
+  // The order is sorted by last node first, so demand reads it directly:
+  // the segment kernel marks where each last node's run starts, the second
+  // round's compare carries the fill of the prefix P over all nodes, the
+  // final stage's first kernel the difference.
+  const DemandRide no_ride{nullptr, nullptr, nullptr, 0, INT32_MAX, nullptr};
+  const DemandRide marks = ride_demand ? DemandRide{t->nodes, P, demand, t->num_nodes, INT32_MAX, keyed} : no_ride;
+  hipLaunchKernelGGL(k_first_groups, dim3(wave_blocks), dim3(256), 0, st, n, sorted, ain,
+                     anchored ? *t : DeviceTree{}, bufs[0], nseg, gsize, depth, active, head, lcp, flags, marks);
 
   // 2. The second round, over the whole queue but only for segments of 2 to
   // kSegSortMax members (skipped when there are none): every member is
@@ -2006,8 +2080,14 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   ClElem* el = bufs[0];
   {
     const unsigned cmp_blocks = std::min(blocks_for(n, 4), 2048u);
-    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks), dim3(256), 0, st, tokens, offsets, n, el, nseg, gsize,
-                       depth, active, head, flags);
+    DemandRide fill = no_ride;
+    unsigned fill_blocks = 0;
+    if (ride_demand) {
+      fill = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)cmp_blocks, keyed};
+      fill_blocks = blocks_for((int64_t)t->num_nodes + 1, kPrefixBlockNodes);
+    }
+    hipLaunchKernelGGL(k_refine_compare, dim3(cmp_blocks + fill_blocks), dim3(256), 0, st, tokens, offsets, n, el,
+                       nseg, gsize, depth, active, head, flags, fill, sorted);
   }
 
   // 3. Everything still active (with the second round's keys where it ran)
@@ -2019,8 +2099,8 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   // 4. Range queries over the settled order: share, size, id (and the cLPM
   // signals), or the offline order.
   const unsigned fb_blocks = blocks_for((int64_t)L.nb1 * kWave);
-  DemandRide fr = ride;
-  fr.first_block = ride_demand ? (int32_t)fb_blocks : INT32_MAX;
+  DemandRide fr = no_ride;
+  if (ride_demand) fr = DemandRide{t->nodes, P, demand, t->num_nodes, (int32_t)fb_blocks, nullptr};
   hipLaunchKernelGGL(k_final_blocks, dim3(fb_blocks + (ride_demand ? blocks_for(t->num_nodes, 256 * kDiffNodes) : 0)),
                      dim3(256), 0,
                      st, n, el, lcp, key2, ib1, ib2, L.ib_stride, st1, st2, L.nb1, L.nb2, cl, off != nullptr, fr);
