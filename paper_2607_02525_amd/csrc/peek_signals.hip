@@ -100,9 +100,9 @@ struct PlainKeys {
 // happens around a node with many requests, then one round that loads the
 // last 8 keys of each interval and counts those below the node. Each wave
 // thus waits on a few rounds only, and the grid has a quarter of the
-// workgroups it would with one node per lane: in the rides, the launch's
-// time went mostly into dispatching 4,000 small workgroups for the 1M
-// nodes of the scale cache.
+// workgroups it would with one node per lane (dispatching 4,000 small
+// workgroups for a 1M-node cache takes about 9 us by itself). The cluster
+// pass uses demand_fill_block instead, which needs no per-node search.
 // `block` is the 256-thread block's index among the blocks doing this.
 constexpr int kPrefixNodes = 4;
 constexpr int64_t kPrefixBlockNodes = 256 * kPrefixNodes;   // nodes per 256-thread block
@@ -638,8 +638,10 @@ __global__ __launch_bounds__(256) void k_first_compare(AnchorIn in, HeadTable T,
 // segmented maximum across each wavefront, then one atomic per wavefront
 // and segment. The elements are written out as the refinement's (request,
 // length) pairs. flags[0] is raised if a segment is active, flags[1] if one
-// of them is one the second round takes. Extra blocks (ride) compute the
-// demand prefix P from the same order (sorted by last node first).
+// of them is one the second round takes. With ride.P set, the first
+// position of each last node's run also records P[c] and the node's bit in
+// ride.keyed (the order is sorted by last node first), for
+// demand_fill_block.
 __global__ __launch_bounds__(256) void k_first_groups(int32_t n, const AncElem* __restrict__ sd, AnchorIn in,
                                                       DeviceTree t, ClElem* __restrict__ el,
                                                       int32_t* __restrict__ nseg, int32_t* __restrict__ gsize,
@@ -745,7 +747,8 @@ __device__ __forceinline__ int32_t head_pos(int32_t s, int32_t d, int32_t size) 
 // compared with their segment's longest member, and get their keys in the
 // form the tail sorts by (hi = l << 33 | code, lo = request); the tail then
 // sorts and splits those segments without comparing again. Nothing to do
-// unless the first round left such a segment (flags_in[1]).
+// unless the first round left such a segment (flags_in[1]). Blocks from
+// ride.first_block on fill the demand prefix (demand_fill_block).
 __global__ __launch_bounds__(256) void k_refine_compare(const int32_t* __restrict__ tokens,
                                                         const int64_t* __restrict__ offsets, int32_t n,
                                                         ClElem* __restrict__ el, const int32_t* __restrict__ nseg,
