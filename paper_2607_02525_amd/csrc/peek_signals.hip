@@ -320,9 +320,7 @@ constexpr int kSegSortMax = 4096;
 __device__ __forceinline__ bool round_takes(int32_t size) { return size <= kSegSortMax; }
 
 __device__ __forceinline__ uint64_t tok_code(int32_t x) { return (uint64_t)((uint32_t)x ^ 0x80000000u) + 1; }
-__device__ __forceinline__ uint64_t lo_of(uint64_t code, uint32_t len) { return (code << 31) | (kLenMax - len); }
 __device__ __forceinline__ uint64_t code_of(uint64_t lo) { return lo >> 31; }
-__device__ __forceinline__ uint32_t ell_of(uint64_t hi) { return (uint32_t)hi; }
 // Depth of the lowest common ancestor of preorder nodes c1 < c2 that are
 // not ancestor-related: the minimum parent depth over (c1, c2], from the
 // in-block suffix/prefix minima and the sparse table over 64-node blocks.
