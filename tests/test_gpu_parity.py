@@ -759,3 +759,43 @@ def test_large_queue_big_sort_tiles():
     got = hp.results()
     assert np.array_equal(got["score"], s.clpm.score)
     assert np.array_equal(got["section"], s.clpm.section)
+
+
+def _pack(seqs):
+    off = np.zeros(len(seqs) + 1, dtype=np.int64)
+    np.cumsum([len(q) for q in seqs], out=off[1:])
+    tok = np.concatenate([np.asarray(q, dtype=np.int32) for q in seqs]) if seqs else np.zeros(0, np.int32)
+    return tok, off
+
+
+@pytest.mark.parametrize("case", ["root_only", "last_only", "every_node", "far_apart"])
+def test_demand_marks_and_fill(case):
+    """Demand in the cluster pass: run starts marked in the segment kernel,
+    the prefix filled across waves of 256 nodes. A star of 3000 children
+    (3001 nodes, several fill waves) with queues whose last nodes are only
+    the root, only the last node in preorder, every node, or a few nodes
+    far apart (long stretches of nodes no request ends at)."""
+    HotPath = _hot()
+    k = 3000
+    cache = [[1000 + i, 7] for i in range(k)]
+    rng = np.random.default_rng(7)
+    if case == "root_only":
+        queue = [[5, 6, int(x)] for x in rng.integers(0, 50, size=500)]
+    elif case == "last_only":
+        queue = [[1000 + k - 1, 7, int(x)] for x in rng.integers(0, 50, size=500)]
+    elif case == "every_node":
+        queue = [[1000 + i, 7, 99] for i in range(k)] + [[5, 6]]
+    else:
+        picks = [0, 1, 700, 1999, 2999]
+        queue = [[1000 + picks[int(j)], 7, int(x)] for j, x in zip(rng.integers(0, 5, size=800), rng.integers(0, 50, size=800))]
+    ct, co = _pack(cache)
+    qt, qo = _pack(queue)
+    print(f"[gpu] demand fill case={case} n={len(queue)}", flush=True)
+    hp = HotPath.from_sequences(ct, co)
+    hp.load_queue(qt, qo, 1, 2)
+    hp.step()
+    res = hp.results()
+    tree = O.Tree.from_sequences(ct, co)
+    r = O.lpm(tree, qt, qo, 1)
+    assert np.array_equal(res["last_node"], r.last_node)
+    assert np.array_equal(res["demand"], O.demand(tree, r.last_node))
