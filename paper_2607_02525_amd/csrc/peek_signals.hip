@@ -1756,6 +1756,15 @@ struct OffSource {
   }
 };
 
+// The pieces, one per thread, before they are sorted. Building them inside
+// the sort's tile pass (two per thread, each a chain of dependent range
+// searches) made that pass the longest of the sort; on their own they run
+// one chain per thread (offline order 4-6 us faster on the workload queues).
+__global__ __launch_bounds__(256) void k_off_make(OffSource src, OffElem* __restrict__ out, int64_t np) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < np) out[j] = src((size_t)j);
+}
+
 __device__ __forceinline__ int64_t off_size(const OffElem& e, int32_t n) {
   return e.node == INT32_MAX ? 0 : (e.k1 == 0 ? 1 : (int64_t)n + 1 - e.k1);
 }
@@ -2122,8 +2131,9 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
     int pc = 0;
     if (n >= 2) {
       const OffArgs oa{n, lcp, el, ix, ib2, st2, L.nb2, npar[0], start[0], rnode, roff};
-      const OffElem* sorted = msort::sort_from(OffSource{oa}, (OffElem*)(w + L.oel_a), (OffElem*)(w + L.oel_b),
-                                               L.onp, OffLess{}, st);
+      hipLaunchKernelGGL(k_off_make, dim3(blocks_for((int64_t)L.onp)), dim3(256), 0, st, OffSource{oa},
+                         (OffElem*)(w + L.oel_a), (int64_t)L.onp);
+      const OffElem* sorted = msort::sort((OffElem*)(w + L.oel_a), (OffElem*)(w + L.oel_b), L.onp, OffLess{}, st);
       const int32_t m2 = 2 * n;
       int64_t* olocal = (int64_t*)(w + L.olocal);
       int64_t* opart = (int64_t*)(w + L.opart);
