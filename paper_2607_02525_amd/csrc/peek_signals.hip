@@ -1988,6 +1988,8 @@ void launch_demand_from_sorted(const DeviceTree& t, Keys keys, int32_t n, int32_
 
 }  // namespace
 
+__global__ void k_zero_word(int32_t* p) { *p = 0; }
+
 peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, const int64_t* offsets,
                         const int32_t* last_node, const int32_t* match_len, int32_t threshold, int32_t* cid,
                         int32_t* csz, int32_t* demand, const ClpmRequest* clpm, const OfflineRequest* off,
@@ -2017,8 +2019,9 @@ peek_status run_signals(const peek_cache* c, int32_t n, const int32_t* tokens, c
   }
   if (!want_clusters) {
     // an empty queue shares nothing
+    // (a kernel rather than a memset, so that the call stays capturable)
     if (clpm != nullptr && clpm->has_sharing != nullptr)
-      PEEK_HIP_TRY(hipMemsetAsync(clpm->has_sharing, 0, sizeof(int32_t), st));
+      hipLaunchKernelGGL(k_zero_word, dim3(1), dim3(1), 0, st, clpm->has_sharing);
     PEEK_HIP_TRY(hipGetLastError());
     return PEEK_OK;
   }

@@ -799,3 +799,20 @@ def test_demand_marks_and_fill(case):
     r = O.lpm(tree, qt, qo, 1)
     assert np.array_equal(res["last_node"], r.last_node)
     assert np.array_equal(res["demand"], O.demand(tree, r.last_node))
+
+
+def test_clpm_empty_queue_clears_has_sharing():
+    """An empty queue shares nothing: has_sharing is written 0 even when it
+    held 1 from an earlier call (by a one-thread kernel, so that the call
+    stays capturable), and demand is all zero."""
+    HotPath = _hot()
+    ct, co = _pack([[3, 4, 5], [3, 4, 6], [9]])
+    hp = HotPath.from_sequences(ct, co)
+    print("[gpu] cLPM on an empty queue", flush=True)
+    hp.load_queue(np.zeros(0, np.int32), np.zeros(1, np.int64), 1, 1)
+    hp.lpm()
+    hp.d_sharing.fill_(1)
+    hp.clpm(0, 2)
+    res = hp.results()
+    assert res["has_sharing"] is False
+    assert np.array_equal(res["demand"], np.zeros(hp.num_nodes, np.int32))
